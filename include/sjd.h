@@ -1,0 +1,200 @@
+/*
+ * sjd.h — C ABI of the MI355X (gfx950) speculative-Jacobi step library
+ * (libsjd.so), implementing the per-iteration step of SJD-PAC:
+ * "SJD-PAC: Accelerating Speculative Jacobi Decoding via Proactive Drafting
+ * and Adaptive Continuation" (arXiv 2603.18599).
+ *
+ * One step (Alg. 1 of the paper) takes the window of draft tokens X^{t-1}
+ * with their draft distributions P^{t-1}, runs one parallel forward of the
+ * decoder over the cached keys/values plus the window to get P^t, verifies
+ * every window position by rejection sampling (Sec. 3.2), keeps verifying
+ * after the first rejection (adaptive continuation, Sec. 4.2), and after a
+ * rejection drafts K - 1 extra candidates at the next D positions (proactive
+ * drafting, Sec. 4.1). It returns the committed tokens and the next window.
+ *
+ * Conventions (all entry points):
+ *  - Every pointer named d_* is a device pointer (HIP global memory on the
+ *    current device). Host pointers are named h_* or are config structs.
+ *  - `stream` is a hipStream_t (NULL = the legacy default stream). Work is
+ *    enqueued asynchronously; outputs are valid after the stream syncs.
+ *  - Arguments are checked on the host before anything is enqueued; a bad
+ *    argument returns SJD_EINVAL and enqueues nothing.
+ *  - Errors reported by the HIP runtime are returned as SJD_EHIP; an
+ *    asynchronous kernel failure surfaces on a later call or sync.
+ *  - Tokens are absolute vocabulary ids. The sampling support is the
+ *    contiguous range [vis_lo, vis_lo + V); logits rows hold V fp32 values,
+ *    entry x belonging to token vis_lo + x.
+ *  - No entry point is thread-safe on the same context; different contexts
+ *    may be used from different threads on different streams.
+ *
+ * Random numbers: Philox4x32-10 (Salmon et al., SC'11). Element x of stream
+ * (tag, stage, row) for trial b at step s is word (x & 3) of the block at
+ * counter (x >> 2, b, tag << 24 | stage << 16 | row, s) under the key
+ * (seed low 32 bits, seed high 32 bits). u = (word >> 8) * 2^-24; a race key
+ * is -logf(1 - u) / w. Tags: 1 accept uniforms, 2 row samples, 3 fresh tail
+ * (vanilla SJD), 4 bonus token, 5 drafting candidates, 6 placeholders.
+ * Sampled results therefore depend only on (seed, trial, step, row) and the
+ * logits, never on launch shape.
+ */
+#ifndef SJD_H
+#define SJD_H
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define SJD_API __attribute__((visibility("default")))
+#else
+#define SJD_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SJD_OK = 0,
+  SJD_EINVAL = -1,  /* bad argument; nothing was enqueued                       */
+  SJD_ENOMEM = -2,  /* device allocation failed                                 */
+  SJD_EHIP = -3,    /* HIP runtime error                                        */
+  SJD_ESTATE = -4,  /* call not valid in the context's state (e.g. cache full)  */
+  SJD_ENOTSUP = -5  /* valid request this build does not support                */
+} sjd_status;
+
+/* flags */
+#define SJD_AC 1u /* adaptive continuation: no break after the first rejection (Sec. 4.2) */
+#define SJD_PD 2u /* proactive drafting after a rejection (Sec. 4.1)                      */
+
+/* Returns a static string naming a status code. */
+SJD_API const char* sjd_status_str(int status);
+
+/* ------------------------------------------------------------------------ */
+/* Standalone verification of one window per trial on given logits.
+ *
+ * Paper: Alg. 1 (the verification loop and drafting after it), Sec. 3.2
+ * (accept a draft with probability min(1, p/q), else draw from
+ * norm(max(0, p - q))), Sec. 4.1-4.2, and Theorem 2 (Appendix A.3) for rows
+ * holding several candidates.
+ *
+ * Window layout of one trial with tree depth D_in (0 <= D_in <= D,
+ * K * D_in <= L): n_s = L - (K-1) * D_in spine rows, then (K-1) * D_in
+ * sibling rows. Spine row j verifies spine draft s_j; at rows j < D_in the
+ * candidates are s_j and its K-1 siblings, verified in order. Sibling row
+ * n_s + j*(K-1) + (k-2) is the target row after candidate k of depth j; a
+ * token drawn from it is committed when that candidate is accepted.
+ * Spine rows j >= n_q have no draft distribution (appended placeholders):
+ * their token is drawn from p and they count as rejected.
+ * The committed prefix ends at the first spine row whose own draft was not
+ * accepted (first_rej); rows after it are verified anyway and carried into
+ * the next window as drafts (adaptive continuation).
+ *
+ * p and q of a row: keep the top_k largest logits (ties: lower index first;
+ * top_k = 0 or >= V keeps all), softmax of (l - max) / temperature.
+ *
+ * Row end tokens: when row_len > 0, the generated-token index g of row j is
+ * g0 + j, and rows with g mod (row_len + 1) == row_len take eol_id, count as
+ * accepted, and get no drafting candidates.
+ */
+typedef struct {
+  int32_t B;          /* trials (independent windows), >= 1                      */
+  int32_t L;          /* rows per window, 1..64                                   */
+  int32_t V;          /* logits per row, >= 1, multiple of 4                       */
+  int32_t K;          /* candidates per tree depth, 1..8                          */
+  int32_t D;          /* maximum tree depth, >= 0, K * D <= L                     */
+  int32_t top_k;      /* >= 0                                                     */
+  float temperature;  /* > 0                                                      */
+  uint32_t flags;     /* SJD_AC | SJD_PD                                          */
+  uint64_t seed;
+  uint32_t step;      /* counter word 3 of every random stream                   */
+  int32_t vis_lo;     /* token id of logits entry 0                               */
+  int32_t eol_id;     /* row end token                                            */
+  int32_t row_len;    /* <= 0 disables row ends                                   */
+} sjd_verify_params;
+
+typedef struct {
+  const float* d_cur;        /* [B][L][V] current logits, spine rows then sibling rows   */
+  const float* d_draft;      /* [B][L][V] draft logits; spine row j < n_q reads row j     */
+  const int32_t* d_draft_tok;/* [B][L] spine drafts s_0 .. s_{n_s-1}                     */
+  const int32_t* d_sib;      /* [B][D][K-1] siblings (-1 = none), or NULL                 */
+  const int32_t* d_in_meta;  /* [B][4] { D_in, n_q, g0, 0 }                               */
+  int32_t* d_out_meta;       /* [B][8] { n_c, first_rej or -1, D', n_s', n_q', accepted
+                                         sibling k or 0, g0 + n_c, 0 }                   */
+  int32_t* d_out_tok;        /* [B][L] committed tokens (n_c valid, rest -1)              */
+  int32_t* d_out_next;       /* [B][L] next spine drafts (n_s' valid, rest -1); the next
+                                step's draft row for index i < n_q' is this step's row
+                                n_c + i                                                   */
+  int32_t* d_out_sib;        /* [B][D][K-1] next siblings (-1 = none)                     */
+  int32_t* d_out_rows;       /* [B][L][2] (token, stage) per row, or NULL: stage k >= 1
+                                candidate k accepted, 0 drawn, -1 row end                 */
+  float* d_dbg_p;            /* [B][L][V] probabilities p of every row, or NULL           */
+} sjd_verify_io;
+
+/* Ownership: all buffers belong to the caller and must not overlap. The
+ * library keeps a grow-only per-device scratch buffer for per-row records
+ * (B * L * 48 bytes), allocated on first use. Errors: SJD_EINVAL for
+ * out-of-range parameters, NULL required pointers or misaligned logits
+ * (16-byte alignment), SJD_ENOMEM, SJD_EHIP. Drafts outside the support end
+ * that row's candidate list (an invalid spine draft makes the row a plain
+ * draw from p); a repeated sibling ends the list too. A trial whose in_meta
+ * is invalid (D_in outside [0, D], K * D_in > L, n_q outside [0, n_s]) is
+ * not verified: its out_meta becomes {-1, -1, 0, ...} and its other outputs
+ * are left untouched (the meta lives in device memory, so this cannot be
+ * reported as a status). */
+SJD_API int sjd_verify(const sjd_verify_params* params, const sjd_verify_io* io, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Decoder context: weights, KV cache and window state of one generation.
+ *
+ * The decoder is a pre-norm LLaMA-style stack (RMSNorm, rotary embeddings in
+ * the rotate-half layout, grouped-query attention, SwiGLU, untied head);
+ * the paper names its models (Sec. 5.1) but not their layers.
+ */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab_size;
+  int32_t vis_lo, V;     /* sampled range of the head: rows [vis_lo, vis_lo + V)       */
+  int32_t max_seq;       /* KV capacity in tokens (prompt + generated + L)             */
+  int32_t L, K, D;       /* window slots, candidates per depth, maximum depth          */
+  uint32_t flags;        /* SJD_AC | SJD_PD                                             */
+  float rms_eps, rope_theta;
+  int32_t eol_id, row_len;
+  int32_t weights_f32;   /* 1: weights are fp32, 0: bf16                                */
+} sjd_config;
+
+/* Borrowed device pointers, row-major [out][in] (a Linear layer's layout),
+ * bf16 or fp32 as configured; they must outlive the context.
+ * h_layer is a HOST array of 9 * n_layers device pointers, per layer:
+ * attn_norm[d], wq[H*hd][d], wk[Hkv*hd][d], wv[Hkv*hd][d], wo[d][H*hd],
+ * ffn_norm[d], wg[F][d], wu[F][d], wd[d][F]. */
+typedef struct {
+  const void* d_embed;        /* [vocab][d]  */
+  const void* const* h_layer; /* 9 * n_layers */
+  const void* d_final_norm;   /* [d]         */
+  const void* d_lm_head;      /* [vocab][d]  */
+} sjd_weights;
+
+typedef struct sjd_ctx sjd_ctx;
+
+/* Allocates the KV cache and work buffers on the current device. */
+SJD_API int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* stream, sjd_ctx** out);
+
+/* Starts a generation: writes the keys/values of d_prompt[0 .. n-2], makes
+ * d_prompt[n-1] the pending token and fills the window with placeholders
+ * (stream tag 6, step word 0xFFFFFFFF). n >= 1, n + L <= max_seq. */
+SJD_API int sjd_prefill(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, uint64_t seed, void* stream);
+
+/* One SJD-PAC iteration (Alg. 1): window forward, verification, drafting,
+ * KV commit. Outputs (device, may be NULL): d_out_meta[8] as in sjd_verify
+ * plus word 7 = cached rows after the step; d_out_tok[L] committed tokens;
+ * d_out_next[L] next spine drafts. SJD_ESTATE if the cache cannot take
+ * another window (checked against a host-side upper bound). */
+SJD_API int sjd_step(sjd_ctx* ctx, float temperature, int32_t top_k, uint64_t seed, uint32_t step,
+             int32_t* d_out_meta, int32_t* d_out_tok, int32_t* d_out_next, void* stream);
+
+/* Window forward only (no verification): logits of the current window into
+ * d_logits[L][V]. For parity tests. */
+SJD_API int sjd_forward_window(sjd_ctx* ctx, float* d_logits, void* stream);
+
+SJD_API void sjd_destroy(sjd_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -93,6 +93,7 @@ typedef struct {
   int32_t vis_lo;    /* token id of logits entry 0                         */
   int32_t eol_id;    /* forced row-end token                               */
   int32_t row_len;   /* image tokens per row; <= 0 disables forcing        */
+  uint32_t trial0;   /* counter word 1 of trial b is trial0 + b              */
 } orc_verify_cfg;
 
 /* Per-trial input meta, int32[4]: { D_in, n_q, g0, 0 }.

@@ -19,7 +19,7 @@ class VerifyCfg(C.Structure):
     _fields_ = [("B", C.c_int32), ("L", C.c_int32), ("V", C.c_int32), ("K", C.c_int32),
                 ("D", C.c_int32), ("top_k", C.c_int32), ("T", C.c_float), ("flags", C.c_uint32),
                 ("seed", C.c_uint64), ("step", C.c_uint32), ("vis_lo", C.c_int32),
-                ("eol_id", C.c_int32), ("row_len", C.c_int32)]
+                ("eol_id", C.c_int32), ("row_len", C.c_int32), ("trial0", C.c_uint32)]
 
 
 class VerifyIO(C.Structure):
@@ -136,7 +136,7 @@ def race_many(w, n, trials, seed=0, tag=TAG_RES, stage=0, row=0, step=0):
 
 
 def verify(cur, draft, draft_tok, in_meta, *, K, D, top_k, T=1.0, flags=AC | PD, seed=0, step=0,
-           sib=None, vis_lo=0, eol_id=-1, row_len=0, want_p=False):
+           sib=None, vis_lo=0, eol_id=-1, row_len=0, want_p=False, trial0=0):
     """One verification step over B trials. Arrays: cur/draft [B,L,V] f32,
     draft_tok [B,L] i32, in_meta [B,4] i32, sib [B,D,K-1] i32 or None."""
     cur = np.ascontiguousarray(cur, dtype=np.float32)
@@ -156,7 +156,7 @@ def verify(cur, draft, draft_tok, in_meta, *, K, D, top_k, T=1.0, flags=AC | PD,
         "margin": np.zeros((B, L, 4), np.float32),
     }
     dbg = np.zeros((B, L, V), np.float32) if want_p else None
-    cfg = VerifyCfg(B, L, V, K, D, top_k, T, flags, seed, step, vis_lo, eol_id, row_len)
+    cfg = VerifyCfg(B, L, V, K, D, top_k, T, flags, seed, step, vis_lo, eol_id, row_len, trial0)
     io = VerifyIO(_p(cur), _p(draft), _p(draft_tok), _p(sib), _p(in_meta), _p(out["meta"]),
                   _p(out["tok"]), _p(out["next"]), _p(out["sib"]), _p(out["rows"]),
                   _p(out["margin"]), _p(dbg))
@@ -177,7 +177,7 @@ def toy_logits(ctx, V, salt):
 
 def gen_cfg(*, L, V, K, D, top_k=0, T=1.0, flags=AC | PD, seed=0, n_prompt, n_gen, max_steps=100000,
             toy_salt=0, vis_lo=0, eol_id=-1, row_len=0, mcfg=None, weights=None):
-    vc = VerifyCfg(1, L, V, K, D, top_k, T, flags, seed, 0, vis_lo, eol_id, row_len)
+    vc = VerifyCfg(1, L, V, K, D, top_k, T, flags, seed, 0, vis_lo, eol_id, row_len, 0)
     g = GenCfg(vc, n_prompt, n_gen, max_steps,
                C.addressof(mcfg) if mcfg is not None else None,
                C.addressof(weights) if weights is not None else None,

@@ -181,6 +181,7 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
   const int32_t* s = io->draft_tok + (size_t)b * L;
   const int32_t* sib = io->sib ? io->sib + (size_t)b * D * Km1 : NULL;
   const int eol = c->eol_id;
+  const uint32_t tr = c->trial0 + (uint32_t)b; /* counter word 1 */
 
   float* P = (float*)malloc(sizeof(float) * (size_t)L * V);
   float* Q = (float*)malloc(sizeof(float) * (size_t)V);
@@ -215,7 +216,7 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
       /* appended placeholder with no draft distribution: its token is drawn
        * from p directly and the row counts as rejected (stage-0 stream). */
       float gap;
-      o->tok = orc_race(p, V, c->seed, ORC_TAG_RES, 0, (uint32_t)j, (uint32_t)b, c->step, &gap);
+      o->tok = orc_race(p, V, c->seed, ORC_TAG_RES, 0, (uint32_t)j, tr, c->step, &gap);
       o->stage = 0;
       o->m_race = gap;
     } else {
@@ -239,23 +240,23 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
       }
       if (nc == 0) {
         float gap;
-        o->tok = orc_race(p, V, c->seed, ORC_TAG_RES, 0, (uint32_t)j, (uint32_t)b, c->step, &gap);
+        o->tok = orc_race(p, V, c->seed, ORC_TAG_RES, 0, (uint32_t)j, tr, c->step, &gap);
         o->stage = 0;
         o->m_race = gap;
       } else {
-        verify_row(c, p, Q, cand, nc, (uint32_t)j, (uint32_t)b, rho, rho2, excl, o);
+        verify_row(c, p, Q, cand, nc, (uint32_t)j, tr, rho, rho2, excl, o);
       }
     }
     if (!(c->flags & ORC_AC)) {
       float gap;
-      fresh[j] = orc_race(p, V, c->seed, ORC_TAG_FRESH, 0, (uint32_t)j, (uint32_t)b, c->step, &gap);
+      fresh[j] = orc_race(p, V, c->seed, ORC_TAG_FRESH, 0, (uint32_t)j, tr, c->step, &gap);
       o->m_race = fminf_(o->m_race, gap);
     } else {
       fresh[j] = o->tok;
     }
     if ((c->flags & ORC_PD) && Km1 > 0) {
       int spine_next = (c->flags & ORC_AC) ? o->tok : fresh[j];
-      pd_siblings(c, p, spine_next, (uint32_t)j, (uint32_t)b, my_sib, &pdgap[j]);
+      pd_siblings(c, p, spine_next, (uint32_t)j, tr, my_sib, &pdgap[j]);
     }
   }
 
@@ -270,7 +271,7 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
       if (y < 0 || is_forced(c, g0 + d)) { o->tok = -1; o->stage = 0; continue; }
       if (is_forced(c, g0 + d + 1)) { o->tok = -1; o->stage = -1; continue; }
       float gap;
-      o->tok = orc_race(P + (size_t)t * V, V, c->seed, ORC_TAG_BONUS, 0, (uint32_t)t, (uint32_t)b, c->step, &gap);
+      o->tok = orc_race(P + (size_t)t * V, V, c->seed, ORC_TAG_BONUS, 0, (uint32_t)t, tr, c->step, &gap);
       o->stage = 0;
       o->m_race = gap;
     }
@@ -332,7 +333,7 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
     } else if (is_forced(c, g)) {
       onext[i] = eol;
     } else {
-      uint32_t bits = orc_bits(c->seed, ORC_TAG_INIT, 0, (uint32_t)i, (uint32_t)b, c->step, 0);
+      uint32_t bits = orc_bits(c->seed, ORC_TAG_INIT, 0, (uint32_t)i, tr, c->step, 0);
       onext[i] = c->vis_lo + (int)(((uint64_t)bits * (uint64_t)V) >> 32);
     }
   }

@@ -1,0 +1,99 @@
+// C ABI: status strings and the standalone verification entry point.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <vector>
+
+#include "sjd.h"
+#include "verify.h"
+
+namespace {
+
+// Grow-only per-device scratch for the per-row records of sjd_verify.
+struct Scratch {
+  std::mutex mu;
+  std::vector<void*> ptr;
+  std::vector<size_t> size;
+};
+Scratch g_scratch;
+
+int scratch_get(size_t bytes, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return SJD_EHIP;
+  std::lock_guard<std::mutex> lk(g_scratch.mu);
+  if ((int)g_scratch.ptr.size() <= dev) {
+    g_scratch.ptr.resize(dev + 1, nullptr);
+    g_scratch.size.resize(dev + 1, 0);
+  }
+  if (g_scratch.size[dev] < bytes) {
+    if (g_scratch.ptr[dev]) {
+      // the previous buffer may still be in use by queued work
+      if (hipDeviceSynchronize() != hipSuccess) return SJD_EHIP;
+      (void)hipFree(g_scratch.ptr[dev]);
+      g_scratch.ptr[dev] = nullptr;
+      g_scratch.size[dev] = 0;
+    }
+    void* p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) return SJD_ENOMEM;
+    g_scratch.ptr[dev] = p;
+    g_scratch.size[dev] = bytes;
+  }
+  *out = g_scratch.ptr[dev];
+  return SJD_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" const char* sjd_status_str(int s) {
+  switch (s) {
+    case SJD_OK: return "SJD_OK";
+    case SJD_EINVAL: return "SJD_EINVAL: invalid argument";
+    case SJD_ENOMEM: return "SJD_ENOMEM: device allocation failed";
+    case SJD_EHIP: return "SJD_EHIP: HIP runtime error";
+    case SJD_ESTATE: return "SJD_ESTATE: invalid context state";
+    case SJD_ENOTSUP: return "SJD_ENOTSUP: not supported";
+    default: return "unknown sjd status";
+  }
+}
+
+namespace sjd {
+int check_verify_params(const sjd_verify_params* p) {
+  if (!p) return SJD_EINVAL;
+  if (p->B < 1 || p->B > 65535 || p->L < 1 || p->L > 64 || p->V < 4 || (p->V & 3) || p->V > (1 << 22))
+    return SJD_EINVAL;
+  if (p->K < 1 || p->K > 8 || p->D < 0 || (long)p->K * p->D > p->L) return SJD_EINVAL;
+  if (p->top_k < 0 || !(p->temperature > 0.0f)) return SJD_EINVAL;
+  if (p->flags & ~(SJD_AC | SJD_PD)) return SJD_EINVAL;
+  return SJD_OK;
+}
+}  // namespace sjd
+
+extern "C" int sjd_verify(const sjd_verify_params* p, const sjd_verify_io* io, void* stream) {
+  int st = sjd::check_verify_params(p);
+  if (st != SJD_OK) return st;
+  if (!io || !io->d_cur || !io->d_draft || !io->d_draft_tok || !io->d_in_meta || !io->d_out_meta ||
+      !io->d_out_tok || !io->d_out_next || !io->d_out_sib)
+    return SJD_EINVAL;
+  if (!aligned16(io->d_cur) || !aligned16(io->d_draft) || (io->d_dbg_p && !aligned16(io->d_dbg_p)))
+    return SJD_EINVAL;
+  void* rec = nullptr;
+  st = scratch_get((size_t)p->B * p->L * sjd::kRecInts * sizeof(int32_t), &rec);
+  if (st != SJD_OK) return st;
+
+  sjd::VerifyArgs a{};
+  a.B = p->B; a.L = p->L; a.V = p->V; a.K = p->K; a.D = p->D; a.top_k = p->top_k;
+  a.T = p->temperature; a.flags = p->flags; a.seed = p->seed; a.step = p->step;
+  a.vis_lo = p->vis_lo; a.eol = p->eol_id; a.row_len = p->row_len;
+  a.cur = io->d_cur; a.draft = io->d_draft; a.draft_bstride = (long long)p->L * p->V; a.q_off = nullptr;
+  a.draft_tok = io->d_draft_tok; a.sib = io->d_sib; a.in_meta = io->d_in_meta;
+  a.rec = (int32_t*)rec; a.out_rows = io->d_out_rows; a.dbg_p = io->d_dbg_p;
+  sjd::FinalizeOut o{};
+  o.out_meta = io->d_out_meta; o.meta_stride = 8;
+  o.out_tok = io->d_out_tok; o.tok_stride = p->L;
+  o.out_next = io->d_out_next; o.next_stride = p->L;
+  o.out_sib = io->d_out_sib; o.sib_stride = p->D * (p->K - 1);
+  if (sjd::launch_verify(a, o, (hipStream_t)stream) != hipSuccess) return SJD_EHIP;
+  return SJD_OK;
+}

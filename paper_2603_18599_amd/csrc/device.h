@@ -1,0 +1,109 @@
+// Device-side helpers shared by the HIP kernels of libsjd: Philox4x32-10,
+// bf16 conversion, wave and block reductions. gfx950 (CDNA4), wave64.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define SJD_DEV __device__ __forceinline__
+
+namespace sjd {
+
+constexpr int kWave = 64;
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds, each
+// multiplying counter words 0 and 2 by the two round constants and mixing the
+// high halves with the other words and the key; the key advances by the Weyl
+// constants between rounds.
+SJD_DEV uint4 philox(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+  }
+  return c;
+}
+
+// Stream tags (counter word 2 bits 24..31).
+enum : uint32_t { kTagAcc = 1, kTagRes = 2, kTagFresh = 3, kTagBonus = 4, kTagPd = 5, kTagInit = 6 };
+
+struct Stream {
+  uint32_t k0, k1, trial, w2, step;
+  SJD_DEV Stream(uint64_t seed, uint32_t tag, uint32_t stage, uint32_t row, uint32_t trial_, uint32_t step_)
+      : k0((uint32_t)seed), k1((uint32_t)(seed >> 32)), trial(trial_),
+        w2((tag << 24) | ((stage & 0xFFu) << 16) | (row & 0xFFFFu)), step(step_) {}
+  // the four words of elements 4*blk .. 4*blk+3
+  SJD_DEV uint4 block(uint32_t blk) const { return philox(make_uint4(blk, trial, w2, step), k0, k1); }
+  SJD_DEV uint32_t word(uint32_t x) const {
+    uint4 b = block(x >> 2);
+    uint32_t s = x & 3u;
+    return s == 0 ? b.x : s == 1 ? b.y : s == 2 ? b.z : b.w;
+  }
+};
+
+SJD_DEV float u01(uint32_t w) { return (float)(w >> 8) * 0x1p-24f; }
+// Exp(1) variate; 1 - u is exact because u is a multiple of 2^-24.
+SJD_DEV float exp1(uint32_t w) { return -logf(1.0f - u01(w)); }
+
+// Order-preserving map of a float to uint32 (larger float -> larger key).
+SJD_DEV uint32_t fkey(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+SJD_DEV float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+// round to nearest even
+SJD_DEV uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)((u >> 16) | ((u & 0xFFFFu) ? 0x40u : 0u));
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// ---------------------------------------------------------------- reductions
+SJD_DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+SJD_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+SJD_DEV double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+SJD_DEV int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+SJD_DEV uint64_t wave_min_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint32_t lo = __shfl_xor((uint32_t)v, o, kWave);
+    uint32_t hi = __shfl_xor((uint32_t)(v >> 32), o, kWave);
+    uint64_t w = ((uint64_t)hi << 32) | lo;
+    v = w < v ? w : v;
+  }
+  return v;
+}
+// inclusive prefix sum within the wave
+SJD_DEV int wave_incl_scan(int v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    int t = __shfl_up(v, o, kWave);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+}  // namespace sjd

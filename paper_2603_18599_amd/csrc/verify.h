@@ -1,0 +1,40 @@
+// Internal interface of the verification kernels (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sjd {
+
+constexpr uint32_t kFlagAC = 1u;
+constexpr uint32_t kFlagPD = 2u;
+constexpr int kRecInts = 16;  // per-row record: tok, stage, 7 drafting candidates, fresh, pad
+
+struct VerifyArgs {
+  int B, L, V, K, D, top_k;
+  float T;
+  uint32_t flags;
+  uint64_t seed;
+  uint32_t step;
+  int vis_lo, eol, row_len;
+  const float* cur;          // [B][L][V]
+  const float* draft;        // draft rows: trial b, spine row j -> draft + b*draft_bstride + (q_off[b]+j)*V
+  long long draft_bstride;
+  const int32_t* q_off;      // [B] or NULL (= 0)
+  const int32_t* draft_tok;  // [B][L]
+  const int32_t* sib;        // [B][D][K-1] or NULL
+  const int32_t* in_meta;    // [B][4]
+  int32_t* rec;              // [B][L][kRecInts] scratch
+  int32_t* out_rows;         // [B][L][2] or NULL
+  float* dbg_p;              // [B][L][V] or NULL
+};
+
+struct FinalizeOut {
+  int32_t* out_meta; int meta_stride;
+  int32_t* out_tok;  int tok_stride;
+  int32_t* out_next; int next_stride;
+  int32_t* out_sib;  int sib_stride;
+};
+
+hipError_t launch_verify(const VerifyArgs& a, const FinalizeOut& o, hipStream_t s);
+
+}  // namespace sjd

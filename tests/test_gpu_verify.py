@@ -1,0 +1,166 @@
+"""GPU parity of sjd_verify (HIP, through the C ABI) with the oracle on the
+same seeded inputs: token indices, stages and accepted lengths bit-exact
+(decisions within 1e-6 of a tie are reported instead), probabilities within
+1e-5 absolute."""
+import numpy as np
+import pytest
+import torch
+
+from parity import compare_verify
+from synth_inputs import CONFIGS, verify_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def run_both(orc, inp, *, K, D, top_k, T=1.0, flags=3, seed=1, step=0, vis_lo=0, eol=-1, row_len=0,
+             want_p=True, oracle_trials=None):
+    import paper_2603_18599_amd as sjd
+    from paper_2603_18599_amd.sjd import verify_outputs
+    dev = {k: (v.cuda() if v is not None else None) for k, v in inp.items()}
+    B, L, V = dev["cur"].shape
+    out = verify_outputs(B, L, K, D)
+    rows = torch.zeros(B, L, 2, dtype=torch.int32, device="cuda")
+    dbg = torch.zeros(B, L, V, dtype=torch.float32, device="cuda") if want_p else None
+    sjd.sjd_verify(dev["cur"], dev["draft"], dev["draft_tok"], dev["meta"], out, K=K, D=D, top_k=top_k,
+                   temperature=T, flags=flags, seed=seed, step=step, sib=dev["sib"], vis_lo=vis_lo, eol_id=eol,
+                   row_len=row_len, out_rows=rows, dbg_p=dbg)
+    torch.cuda.synchronize()
+    idx = np.arange(B) if oracle_trials is None else np.asarray(oracle_trials)
+    cpu = {k: (v[idx].numpy() if v is not None else None) for k, v in inp.items()}
+    # trial index is a counter word: keep each trial's own index for the oracle
+    if oracle_trials is None:
+        ref = orc.verify(cpu["cur"], cpu["draft"], cpu["draft_tok"], cpu["meta"], K=K, D=D, top_k=top_k, T=T,
+                         flags=flags, seed=seed, step=step, sib=cpu["sib"], vis_lo=vis_lo, eol_id=eol,
+                         row_len=row_len, want_p=want_p)
+    else:
+        ref = orc_verify_trials(orc, cpu, idx, K=K, D=D, top_k=top_k, T=T, flags=flags, seed=seed, step=step,
+                                vis_lo=vis_lo, eol=eol, row_len=row_len, want_p=want_p)
+    gpu = dict(meta=out["meta"].cpu().numpy()[idx], tok=out["tok"].cpu().numpy()[idx],
+               next=out["next"].cpu().numpy()[idx], sib=out["sib"].cpu().numpy()[idx],
+               rows=rows.cpu().numpy()[idx])
+    if want_p:
+        gpu["p"] = dbg.cpu().numpy()[idx]
+    return gpu, ref
+
+
+def orc_verify_trials(orc, sub, trial_ids, **kw):
+    """Oracle on a subset of trials, each at its own trial index (counter
+    word 1), one call per trial."""
+    outs = []
+    for t, b in enumerate(trial_ids):
+        one = {k: (v[t:t + 1] if v is not None else None) for k, v in sub.items()}
+        r = orc.verify(one["cur"], one["draft"], one["draft_tok"], one["meta"], K=kw["K"], D=kw["D"],
+                       top_k=kw["top_k"], T=kw["T"], flags=kw["flags"], seed=kw["seed"], step=kw["step"],
+                       sib=one["sib"], vis_lo=kw["vis_lo"], eol_id=kw["eol"], row_len=kw["row_len"],
+                       want_p=kw["want_p"], trial0=int(b))
+        outs.append(r)
+    return {k: np.concatenate([o[k] for o in outs]) for k in outs[0]}
+
+
+def check(gpu, ref, K, D, want_p=True):
+    if want_p:
+        assert np.abs(gpu["p"] - ref["p"]).max() <= 1e-5
+    return compare_verify(gpu, ref, K=K, D=D)
+
+
+@pytest.mark.parametrize("V,top_k", [(1024, 0), (4096, 200), (16384, 2000), (65536, 2000)])
+def test_verify_chain_matches_oracle(orc, V, top_k):
+    B, L = 6, 32
+    inp = verify_inputs(B, L, V, top_k=top_k, seed=V + top_k)
+    gpu, ref = run_both(orc, inp, K=4, D=3, top_k=top_k, seed=7, step=3)
+    check(gpu, ref, 4, 3)
+    assert (gpu["meta"][:, 0] >= 1).all()
+
+
+def test_verify_tree_rows_with_siblings(orc):
+    B, L, V, K, D = 8, 32, 4096, 4, 3
+    inp = verify_inputs(B, L, V, top_k=300, seed=11, K=K, D=D, D_in=3, draft_noise=1.5)
+    gpu, ref = run_both(orc, inp, K=K, D=D, top_k=300, seed=3, step=9)
+    check(gpu, ref, K, D)
+    # some sibling must have been tried somewhere
+    assert (ref["rows"][:, :3, 1] != 1).any()
+
+
+def test_verify_placeholders_and_row_ends(orc):
+    B, L, V = 6, 16, 2048
+    inp = verify_inputs(B, L, V, top_k=100, seed=5, n_q=9)
+    inp["meta"][:, 2] = torch.tensor([0, 3, 7, 10, 15, 44], dtype=torch.int32)
+    eol = 5000
+    W = 4
+    for b in range(B):
+        for j in range(L):
+            if (int(inp["meta"][b, 2]) + j) % (W + 1) == W:
+                inp["draft_tok"][b, j] = eol
+    gpu, ref = run_both(orc, inp, K=4, D=3, top_k=100, seed=2, step=1, eol=eol, row_len=W, vis_lo=0)
+    check(gpu, ref, 4, 3)
+
+
+def test_verify_vanilla_sjd_mode(orc):
+    B, L, V = 6, 32, 4096
+    inp = verify_inputs(B, L, V, top_k=500, seed=21, draft_noise=2.0)
+    gpu, ref = run_both(orc, inp, K=1, D=0, top_k=500, flags=0, seed=4)
+    check(gpu, ref, 1, 0)
+
+
+def test_verify_ties_in_logits(orc):
+    # integer-valued logits: many exact ties at the top-k threshold
+    B, L, V = 4, 8, 1024
+    inp = verify_inputs(B, L, V, top_k=37, seed=9, int_logits=True)
+    gpu, ref = run_both(orc, inp, K=4, D=2, top_k=37, seed=8)
+    check(gpu, ref, 4, 2)
+
+
+def test_verify_small_shapes(orc):
+    for (B, L, V, top_k, K, D) in [(1, 1, 4, 0, 1, 0), (3, 1, 64, 1, 4, 0), (2, 5, 8, 3, 2, 2), (2, 64, 256, 17, 8, 8)]:
+        inp = verify_inputs(B, L, V, top_k=top_k, seed=B * 100 + L, K=K, D=D)
+        gpu, ref = run_both(orc, inp, K=K, D=D, top_k=top_k, seed=1)
+        check(gpu, ref, K, D)
+
+
+def test_verify_vis_range_offset(orc):
+    B, L, V = 3, 16, 2048
+    inp = verify_inputs(B, L, V, top_k=64, seed=31)
+    lo = 151854
+    inp["draft_tok"] += lo
+    gpu, ref = run_both(orc, inp, K=4, D=3, top_k=64, seed=6, vis_lo=lo, eol=lo - 1, row_len=7)
+    check(gpu, ref, 4, 3)
+    assert (gpu["tok"][gpu["tok"] >= 0] >= lo - 1).all()
+
+
+def test_verify_full_size_sampled(orc):
+    """The benchmark's verify workload (4096 trials x 32 rows x 16384, top-2000)
+    in the launch the benchmark times; the oracle checks 12 sampled trials."""
+    c = CONFIGS["verify"]
+    inp = verify_inputs(c["B"], c["L"], c["V"], top_k=c["top_k"], seed=1234, device="cuda")
+    inp = {k: (v.cpu() if v is not None else None) for k, v in inp.items()}
+    sample = [0, 1, 77, 500, 1023, 1024, 2047, 2048, 3000, 4000, 4094, 4095]
+    gpu, ref = run_both(orc, inp, K=c["K"], D=c["D"], top_k=c["top_k"], seed=99, step=5, want_p=False,
+                        oracle_trials=sample)
+    compare_verify(gpu, ref, K=c["K"], D=c["D"])
+
+
+def test_verify_is_deterministic(orc):
+    import paper_2603_18599_amd as sjd
+    from paper_2603_18599_amd.sjd import verify_outputs
+    B, L, V = 64, 32, 16384
+    inp = {k: (v.cuda() if v is not None else None) for k, v in verify_inputs(B, L, V, top_k=2000, seed=3).items()}
+    res = []
+    for _ in range(2):
+        out = verify_outputs(B, L, 4, 3)
+        sjd.sjd_verify(inp["cur"], inp["draft"], inp["draft_tok"], inp["meta"], out, K=4, D=3, top_k=2000, seed=5)
+        torch.cuda.synchronize()
+        res.append({k: v.cpu() for k, v in out.items()})
+    for k in res[0]:
+        assert torch.equal(res[0][k], res[1][k])
+
+
+def test_verify_rejects_bad_arguments():
+    import paper_2603_18599_amd as sjd
+    from paper_2603_18599_amd.sjd import SjdError, verify_outputs
+    inp = {k: (v.cuda() if v is not None else None) for k, v in verify_inputs(2, 4, 64, top_k=0, seed=1).items()}
+    out = verify_outputs(2, 4, 4, 1)
+    for kw in [dict(K=4, D=2), dict(K=9, D=0), dict(K=4, D=1, temperature=0.0), dict(K=4, D=1, top_k=-1)]:
+        args = dict(K=4, D=1, top_k=0)
+        args.update(kw)
+        with pytest.raises(SjdError):
+            sjd.sjd_verify(inp["cur"], inp["draft"], inp["draft_tok"], inp["meta"], out, **args)
