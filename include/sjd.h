@@ -121,7 +121,8 @@ typedef struct {
   int32_t* d_out_next;       /* [B][L] next spine drafts (n_s' valid, rest -1); the next
                                 step's draft row for index i < n_q' is this step's row
                                 n_c + i                                                   */
-  int32_t* d_out_sib;        /* [B][D][K-1] next siblings (-1 = none)                     */
+  int32_t* d_out_sib;        /* [B][D][K-1] next siblings (-1 = none); may be NULL when
+                                D * (K-1) == 0                                            */
   int32_t* d_out_rows;       /* [B][L][2] (token, stage) per row, or NULL: stage k >= 1
                                 candidate k accepted, 0 drawn, -1 row end                 */
   float* d_dbg_p;            /* [B][L][V] probabilities p of every row, or NULL           */

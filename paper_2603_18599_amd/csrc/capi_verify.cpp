@@ -74,7 +74,7 @@ extern "C" int sjd_verify(const sjd_verify_params* p, const sjd_verify_io* io, v
   int st = sjd::check_verify_params(p);
   if (st != SJD_OK) return st;
   if (!io || !io->d_cur || !io->d_draft || !io->d_draft_tok || !io->d_in_meta || !io->d_out_meta ||
-      !io->d_out_tok || !io->d_out_next || !io->d_out_sib)
+      !io->d_out_tok || !io->d_out_next || (p->D * (p->K - 1) > 0 && !io->d_out_sib))
     return SJD_EINVAL;
   if (!aligned16(io->d_cur) || !aligned16(io->d_draft) || (io->d_dbg_p && !aligned16(io->d_dbg_p)))
     return SJD_EINVAL;

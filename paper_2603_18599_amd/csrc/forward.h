@@ -1,0 +1,75 @@
+// Internal interface of the window-forward kernels (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sjd {
+
+enum { kGemmStore = 0, kGemmAdd = 1, kGemmSwiGLU = 2 };
+
+struct GemmArgs {
+  const uint16_t* A;  // bf16 activations, rows padded to 32 * ceil(M/32), row stride K
+  int M;
+  const uint16_t* W0;  // weight segments stacked along N (rows of W0, then W1, then W2);
+  const uint16_t* W1;  // SwiGLU: W0 = gate rows, W1 = up rows of the same columns
+  const uint16_t* W2;
+  int n0, n1;          // segment boundaries in output columns
+  int N, K;            // N multiple of 32, K multiple of 64
+  int S;               // workgroups along K
+  float* ws;           // split-K partials
+  int* cnt;            // arrival counters, one per 32-column block, zero between launches
+  float* out;          // fp32 output (store / add), row stride ldo
+  uint16_t* outb;      // bf16 output (SwiGLU), row stride ldo
+  int ldo;
+};
+
+int gemm_splits(int N, int K, int target_wgs);
+size_t gemm_ws_floats(int N, int S, int M, int mode);
+hipError_t launch_gemm(const GemmArgs& g, int mode, hipStream_t s);
+
+// Window description in device memory (written by the window builder).
+struct Window {
+  int32_t tok[64];
+  int32_t pos[64];
+  uint64_t anc[64];
+};
+
+// Device-resident decoding state of one context.
+struct DevState {
+  int32_t n;        // cached rows
+  int32_t pending;  // last committed token (slot 0)
+  int32_t n_s, D_in, n_q, g0, q_off, pad;
+  int32_t spine[64];
+  int32_t sib[64];  // [D][K-1]
+  int32_t meta[8];  // last step's outcome
+  int32_t tok[64];  // last step's committed tokens
+};
+
+struct AttnArgs {
+  const uint16_t* q;     // bf16 [Mpad][H * hd], rotated
+  const uint16_t* kc;    // bf16 [Hkv][cap][hd] key cache of this layer
+  const uint16_t* vt;    // bf16 [Hkv][hd][cap] transposed value cache of this layer
+  const Window* win;
+  const int32_t* n_dev;  // cached rows before the window (device scalar), or NULL -> n_host
+  int n_host;
+  int M, H, Hkv, cap;
+  float scale;
+  float* ws_o;           // [H][nsplit_max][32][hd] partial outputs
+  float* ws_ml;          // [H][nsplit_max][32][2]  partial max (log2 domain) and sum
+  int nsplit_max;
+  uint16_t* out;         // bf16 [Mpad][H * hd]
+};
+constexpr int kAttnChunk = 256;  // keys per workgroup
+hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s);
+
+// elementwise kernels
+hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, float* x, hipStream_t s);
+hipError_t launch_rmsnorm(const float* x, const uint16_t* g, int M, int d, float eps, uint16_t* y,
+                          hipStream_t s);
+// rotary embedding of q and k, key row and transposed value column into the caches
+hipError_t launch_rope_kv(const float* qkv, const Window* win, const int32_t* n_dev, int n_host, int M, int H,
+                          int Hkv, int hd, const float2* rope, uint16_t* q, uint16_t* kc, uint16_t* vt, int cap,
+                          hipStream_t s);
+hipError_t launch_f32_to_bf16(const float* src, uint16_t* dst, size_t n, hipStream_t s);
+
+}  // namespace sjd

@@ -97,7 +97,7 @@ def test_verify_placeholders_and_row_ends(orc):
 
 def test_verify_vanilla_sjd_mode(orc):
     B, L, V = 6, 32, 4096
-    inp = verify_inputs(B, L, V, top_k=500, seed=21, draft_noise=2.0)
+    inp = verify_inputs(B, L, V, top_k=500, seed=21, draft_noise=2.0, K=1, D=0)
     gpu, ref = run_both(orc, inp, K=1, D=0, top_k=500, flags=0, seed=4)
     check(gpu, ref, 1, 0)
 
@@ -105,7 +105,7 @@ def test_verify_vanilla_sjd_mode(orc):
 def test_verify_ties_in_logits(orc):
     # integer-valued logits: many exact ties at the top-k threshold
     B, L, V = 4, 8, 1024
-    inp = verify_inputs(B, L, V, top_k=37, seed=9, int_logits=True)
+    inp = verify_inputs(B, L, V, top_k=37, seed=9, int_logits=True, K=4, D=2)
     gpu, ref = run_both(orc, inp, K=4, D=2, top_k=37, seed=8)
     check(gpu, ref, 4, 2)
 
