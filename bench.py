@@ -1,8 +1,16 @@
 """Benchmark of the SJD-PAC step on one MI355X.
 
-python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload verify]
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 7b|8b|mid|tiny|verify]
 
 Prints ONE JSON line. Workloads (synthetic, seeded; see synth_inputs.py):
+  7b (default): one SJD-PAC iteration per step (window forward of L = 32
+           slots over the KV cache, verification, KV commit) of a 7B-shaped
+           decoder (32 layers, d = 4096, 32 heads x 128, SwiGLU 11008, vocab
+           65536, bf16 random-init weights), generating a 48x48 image with
+           row-end tokens after a 64-token random prompt; top-2000, T = 1,
+           K = 4, D = 3. value = committed image tokens per second. The same
+           line carries the verify workload's numbers under "verify".
+  8b, mid, tiny: the other decoder shapes.
   verify : sjd_verify over 4096 independent windows of 32 rows x 16384 logits
            (current logits N(0, 2^2), draft = current + N(0, 0.5^2), drafts
            drawn from top-2000 softmax of the draft logits), one launch per
@@ -30,7 +38,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="verify", choices=["verify"])
+    ap.add_argument("--workload", default="7b", choices=["7b", "8b", "mid", "tiny", "verify"])
+    ap.add_argument("--no-verify", action="store_true", help="skip the verify workload section")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
     return ap.parse_args()
@@ -122,6 +131,137 @@ def cpu_baseline_verify(args, inp, K, D, top_k, T, seed, B, L):
             "kind": "oracle", "sample": f"{len(idx)} of {B} windows (one verification step), {dt:.1f} s"}
 
 
+def step_bytes(cfg, n_mean):
+    """Algorithmic HBM bytes of one step: every weight streamed once (bf16),
+    the LM head rows of the sampled range only, the cached keys and values
+    read once (hi/lo bf16 planes, 4 bytes per element), the window's K/V
+    written, and the logits written and read back by the verification."""
+    d, H, Hkv, hd, F, V, L = (cfg[k] for k in ("d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim", "V", "L"))
+    per_layer = (H * hd * d + 2 * Hkv * hd * d + d * H * hd + 3 * F * d) * 2
+    weights = cfg["n_layers"] * per_layer + V * d * 2
+    kv = cfg["n_layers"] * 2 * Hkv * hd * 4 * (n_mean + L)
+    logits = 2 * L * V * 4 * 2  # written once, current + draft rows read once
+    return weights + kv + logits, weights, kv
+
+
+def bench_step(args):
+    import numpy as np
+    import torch
+
+    from paper_2603_18599_amd.sjd import Engine, SjdError
+    from synth_inputs import model_config, model_weights, prompt_tokens
+
+    cfg = model_config(args.workload)
+    seed = 11
+    w = model_weights(cfg, 1, device="cuda")
+    prompt = prompt_tokens(cfg, 2).cuda()
+    eng = Engine(cfg, w)
+    stream = torch.cuda.current_stream()
+    K, W = args.steps, args.warmup
+    metas = torch.zeros(W + K, 8, dtype=torch.int32, device="cuda")
+    eng.prefill(prompt, seed, stream=stream)
+    torch.cuda.synchronize()
+    t_pre = time.perf_counter()
+    eng.prefill(prompt, seed, stream=stream)
+    torch.cuda.synchronize()
+    prefill_ms = (time.perf_counter() - t_pre) * 1e3
+    restarts = 0
+
+    def one(t):
+        nonlocal restarts
+        try:
+            eng.step(cfg["temperature"], cfg["top_k"], seed, t, out_meta=metas[t], stream=stream)
+        except SjdError as e:
+            if e.code != -4:
+                raise
+            restarts += 1  # image complete: the cache is full, start the next image
+            eng.prefill(prompt, seed + restarts, stream=stream)
+            eng.step(cfg["temperature"], cfg["top_k"], seed, t, out_meta=metas[t], stream=stream)
+
+    for t in range(W):
+        one(t)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    t0 = time.perf_counter()
+    for i in range(K):
+        evs[i][0].record(stream)
+        one(W + i)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    m = metas.cpu().numpy()
+    ncs = m[W:, 0]
+    ns = m[W:, 7]
+    step_ms = [a.elapsed_time(b) for a, b in evs]
+    avg_ms = float(np.mean(step_ms))
+    n_mean = float(np.mean(ns - ncs))
+    total, weights, kv = step_bytes(cfg, n_mean)
+    achieved = total / (avg_ms * 1e-3) / 1e9
+    res = dict(metric="image tokens/sec on 1 MI355X; mean accept length/step; verify HBM GB/s",
+               value=float(ncs.sum()) / wall, unit="image tokens/s", n_gpus=1, steps=K, warmup=W,
+               ms_per_step=wall * 1e3 / K, higher_is_better=True, scaling="weak", vs_baseline=None, dtype="bf16",
+               data="synthetic (random-init weights, random prompt ids)",
+               config={"workload": f"{args.workload}-shaped decoder: {cfg['n_layers']} layers, d={cfg['d_model']}, "
+                                   f"{cfg['n_heads']}q/{cfg['n_kv_heads']}kv heads x {cfg['head_dim']}, "
+                                   f"SwiGLU {cfg['ffn_dim']}, vocab {cfg['vocab_size']} (sampled {cfg['V']}), "
+                                   f"L={cfg['L']} K={cfg['K']} D={cfg['D']}, top-{cfg['top_k']}, T=1, "
+                                   f"{cfg['n_prompt']}-token prompt, {cfg['n_gen']}-token image",
+                       "global_batch": 1, "seq_len": cfg["L"]},
+               mean_accept_length=float(ncs.mean()), step_latency_ms=avg_ms,
+               step_latency_p50_ms=float(np.percentile(step_ms, 50)),
+               step_latency_p99_ms=float(np.percentile(step_ms, 99)),
+               prefill_ms=prefill_ms, kv_rows_mean=n_mean, image_restarts=restarts,
+               roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                         "kernel": "sjd_step (window forward + verification + KV commit)",
+                         "bytes_per_launch": total, "weight_bytes": weights, "kv_bytes": kv,
+                         "avg_launch_ms": avg_ms,
+                         "mfma_tflops": 2.0 * weights / 2 * cfg["L"] / (avg_ms * 1e-3) / 1e12})
+    eng.close()
+    del w
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_step(args, cfg, seed)
+    return res
+
+
+def cpu_baseline_step(args, cfg, seed):
+    """The oracle (plain C, fp64 accumulation, OpenMP) on one SJD-PAC step of
+    the same model at the same start: weights regenerated from the same seed,
+    prompt prefilled untimed, then the first window's forward + verification
+    timed. Scaled to committed tokens per second."""
+    import numpy as np
+    import torch
+
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from model_util import oracle_model, oracle_prefill, placeholders, weights_numpy
+    from oracle import oracle as orc
+    from synth_inputs import model_weights, prompt_tokens
+
+    w = model_weights(cfg, 1, device="cuda")
+    w = dict(embed=w["embed"].cpu(), final_norm=w["final_norm"].cpu(), lm_head=w["lm_head"].cpu(),
+             layers=[{k: v.cpu() for k, v in l.items()} for l in w["layers"]])
+    prompt = prompt_tokens(cfg, 2).numpy().astype(np.int32)
+    m = oracle_model(orc, cfg, weights_numpy(w))
+    n = oracle_prefill(m, prompt)
+    L, V = cfg["L"], cfg["V"]
+    spine = placeholders(orc, cfg, seed)
+    t0 = time.perf_counter()
+    logits = m.forward(n, [int(prompt[-1])] + spine[:L - 1], [n + i for i in range(L)],
+                       [(1 << (a + 1)) - 1 for a in range(L)])
+    meta = np.array([[0, 0, 0, 0]], np.int32)
+    r = orc.verify(logits[None], logits[None], np.array([spine], np.int32), meta, K=cfg["K"], D=cfg["D"],
+                   top_k=cfg["top_k"], T=cfg["temperature"], seed=seed, step=0, vis_lo=cfg["vis_lo"],
+                   eol_id=cfg["eol_id"], row_len=cfg["row_len"])
+    dt = time.perf_counter() - t0
+    m.close()
+    n_c = int(r["meta"][0, 0])
+    return {"value": n_c / dt, "unit": "image tokens/s", "cores": int(os.environ.get("OMP_NUM_THREADS", cpu_cores())),
+            "kind": "oracle",
+            "sample": f"first SJD-PAC step after a {cfg['n_prompt']}-token prefill (prefill untimed): "
+                      f"{L}-slot window forward + verification, {dt:.1f} s, n_c={n_c}"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -129,6 +269,12 @@ def main():
         sys.exit(2)
     if args.workload == "verify":
         res = bench_verify(args)
+    else:
+        res = bench_step(args)
+        if not args.no_verify:
+            v = bench_verify(argparse.Namespace(steps=10, warmup=2, no_cpu_baseline=True, cpu_sample=0))
+            res["verify"] = {k: v[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length", "verify_GBps",
+                                               "roofline", "config")}
     print(json.dumps(res), flush=True)
 
 

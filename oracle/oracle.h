@@ -57,6 +57,9 @@ float orc_exp1(uint32_t bits);
  * the largest logit, Z = sum of w in fp64, p_x = (float)(w_x / Z); p_x = 0
  * off S. Returns 0, or -1 on bad arguments. */
 int orc_topk_softmax(const float* logits, int V, int top_k, float T, float* p);
+/* rank[x] = position of x among the kept (top-k) tokens in index order, -1
+ * for tokens outside the set. */
+int orc_topk_rank(const float* logits, int V, int top_k, int* rank);
 
 /* Exponential race: argmin over x with w_x > 0 of E_x / w_x (fp32 division),
  * E_x from stream (tag, stage, row); equal keys go to the smaller index.
@@ -64,6 +67,13 @@ int orc_topk_softmax(const float* logits, int V, int top_k, float T, float* p);
  * relative gap between the best and second-best keys (1 if only one). */
 int orc_race(const float* w, int V, uint64_t seed, uint32_t tag, uint32_t stage,
              uint32_t row, uint32_t trial, uint32_t step, float* gap);
+/* The same race with the exponential of token x taken from element rank[x]
+ * of the stream instead of element x (rank may be NULL: rank[x] = x). The
+ * verification step uses rank = position of x in the row's top-k set in
+ * index order, so the races of a row draw one stream element per kept
+ * token. */
+int orc_race_ranked(const float* w, const int* rank, int V, uint64_t seed, uint32_t tag,
+                    uint32_t stage, uint32_t row, uint32_t trial, uint32_t step, float* gap);
 
 /* The n smallest race keys (n <= 16) among tokens x != excl with w_x > 0, in
  * ascending key order, ties to the smaller index: a draw of n tokens without
@@ -73,6 +83,9 @@ int orc_race(const float* w, int V, uint64_t seed, uint32_t tag, uint32_t stage,
 int orc_race_topn(const float* w, int V, int n, int excl, uint64_t seed, uint32_t tag,
                   uint32_t stage, uint32_t row, uint32_t trial, uint32_t step, int* out,
                   float* gap);
+int orc_race_topn_ranked(const float* w, const int* rank, int V, int n, int excl, uint64_t seed,
+                         uint32_t tag, uint32_t stage, uint32_t row, uint32_t trial, uint32_t step,
+                         int* out, float* gap);
 /* trials independent races (trial b = counter word 1): out[trials] for n <= 1,
  * else the n smallest keys of each, out[trials][n]. */
 void orc_race_many(const float* w, int V, int n, uint64_t seed, uint32_t tag, uint32_t stage,

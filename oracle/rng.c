@@ -64,11 +64,17 @@ float orc_exp1(uint32_t bits) {
 
 int orc_race(const float* w, int V, uint64_t seed, uint32_t tag, uint32_t stage,
              uint32_t row, uint32_t trial, uint32_t step, float* gap) {
+  return orc_race_ranked(w, NULL, V, seed, tag, stage, row, trial, step, gap);
+}
+
+int orc_race_ranked(const float* w, const int* rank, int V, uint64_t seed, uint32_t tag, uint32_t stage,
+                    uint32_t row, uint32_t trial, uint32_t step, float* gap) {
   int best = -1;
   float best_key = INFINITY, second_key = INFINITY;
   for (int x = 0; x < V; ++x) {
     if (!(w[x] > 0.0f)) continue;
-    float e = orc_exp1(orc_bits(seed, tag, stage, row, trial, step, (uint32_t)x));
+    const uint32_t e_idx = rank ? (uint32_t)rank[x] : (uint32_t)x;
+    float e = orc_exp1(orc_bits(seed, tag, stage, row, trial, step, e_idx));
     float key = e / w[x];
     if (best < 0 || key < best_key) {
       second_key = best_key;
@@ -89,6 +95,12 @@ int orc_race(const float* w, int V, uint64_t seed, uint32_t tag, uint32_t stage,
 int orc_race_topn(const float* w, int V, int n, int excl, uint64_t seed, uint32_t tag,
                   uint32_t stage, uint32_t row, uint32_t trial, uint32_t step, int* out,
                   float* gap) {
+  return orc_race_topn_ranked(w, NULL, V, n, excl, seed, tag, stage, row, trial, step, out, gap);
+}
+
+int orc_race_topn_ranked(const float* w, const int* rank, int V, int n, int excl, uint64_t seed,
+                         uint32_t tag, uint32_t stage, uint32_t row, uint32_t trial, uint32_t step,
+                         int* out, float* gap) {
   /* keeps the n + 1 smallest (key, index) pairs, in ascending key order with
    * ties to the smaller index, by insertion */
   float keys[17];
@@ -98,7 +110,8 @@ int orc_race_topn(const float* w, int V, int n, int excl, uint64_t seed, uint32_
   const int cap = n + 1;
   for (int x = 0; x < V; ++x) {
     if (x == excl || !(w[x] > 0.0f)) continue;
-    float key = orc_exp1(orc_bits(seed, tag, stage, row, trial, step, (uint32_t)x)) / w[x];
+    const uint32_t e_idx = rank ? (uint32_t)rank[x] : (uint32_t)x;
+    float key = orc_exp1(orc_bits(seed, tag, stage, row, trial, step, e_idx)) / w[x];
     if (have == cap && !(key < keys[cap - 1])) continue;
     int pos = have < cap ? have : cap - 1;
     while (pos > 0 && key < keys[pos - 1]) {

@@ -50,16 +50,26 @@ static int cmp_desc(const void* a, const void* b) {
   return (x->idx > y->idx) - (x->idx < y->idx);
 }
 
-int orc_topk_softmax(const float* logits, int V, int top_k, float T, float* p) {
-  if (V < 1 || !(T > 0.0f) || top_k < 0) return -1;
+/* Marks the top-k set of a row: the k largest logits by (value descending,
+ * index ascending); k = V when top_k <= 0 or top_k >= V. */
+static int topk_members(const float* logits, int V, int top_k, uint8_t* in) {
   int k = (top_k <= 0 || top_k >= V) ? V : top_k;
   vi_t* s = (vi_t*)malloc(sizeof(vi_t) * (size_t)V);
-  uint8_t* in = (uint8_t*)calloc((size_t)V, 1);
-  if (!s || !in) { free(s); free(in); return -1; }
-  for (int x = 0; x < V; ++x) { s[x].val = logits[x]; s[x].idx = x; }
+  if (!s) return -1;
+  for (int x = 0; x < V; ++x) { s[x].val = logits[x]; s[x].idx = x; in[x] = 0; }
   qsort(s, (size_t)V, sizeof(vi_t), cmp_desc);
   for (int i = 0; i < k; ++i) in[s[i].idx] = 1;
-  float m = s[0].val;
+  free(s);
+  return 0;
+}
+
+int orc_topk_softmax(const float* logits, int V, int top_k, float T, float* p) {
+  if (V < 1 || !(T > 0.0f) || top_k < 0) return -1;
+  uint8_t* in = (uint8_t*)calloc((size_t)V, 1);
+  if (!in || topk_members(logits, V, top_k, in) != 0) { free(in); return -1; }
+  float m = -INFINITY;
+  for (int x = 0; x < V; ++x)
+    if (in[x] && logits[x] > m) m = logits[x];
   double Z = 0.0;
   for (int x = 0; x < V; ++x) {
     if (in[x]) {
@@ -74,7 +84,16 @@ int orc_topk_softmax(const float* logits, int V, int top_k, float T, float* p) {
   }
   for (int x = 0; x < V; ++x)
     if (in[x]) p[x] = (float)((double)p[x] / Z);
-  free(s);
+  free(in);
+  return 0;
+}
+
+int orc_topk_rank(const float* logits, int V, int top_k, int* rank) {
+  if (V < 1 || top_k < 0) return -1;
+  uint8_t* in = (uint8_t*)calloc((size_t)V, 1);
+  if (!in || topk_members(logits, V, top_k, in) != 0) { free(in); return -1; }
+  int r = 0;
+  for (int x = 0; x < V; ++x) rank[x] = in[x] ? r++ : -1;
   free(in);
   return 0;
 }
@@ -100,7 +119,7 @@ typedef struct {
 /* Verification of one spine row with candidate list cand[0..nc) (distinct,
  * in range) against target p and draft q (Theorem 2; K = 1 is the plain
  * single-draft test of Sec. 3.2). */
-static void verify_row(const orc_verify_cfg* c, const float* p, const float* q,
+static void verify_row(const orc_verify_cfg* c, const float* p, const float* q, const int* rank,
                        const int* cand, int ncand, uint32_t row, uint32_t trial,
                        float* rho, float* rho_new, uint8_t* excl, row_out* out) {
   const int V = c->V;
@@ -149,7 +168,7 @@ static void verify_row(const orc_verify_cfg* c, const float* p, const float* q,
     Nf = (float)Nd;
   }
   float gap;
-  int t = orc_race(rho, V, c->seed, ORC_TAG_RES, (uint32_t)tried, row, trial, c->step, &gap);
+  int t = orc_race_ranked(rho, rank, V, c->seed, ORC_TAG_RES, (uint32_t)tried, row, trial, c->step, &gap);
   out->tok = t;
   out->stage = 0;
   out->m_race = gap;
@@ -162,9 +181,10 @@ static void verify_row(const orc_verify_cfg* c, const float* p, const float* q,
 /* K - 1 siblings for the next window: the K - 1 smallest race keys of p over
  * its support without token excl_tok, ascending (a draw of K - 1 tokens
  * without replacement from p restricted to the other tokens). */
-static void pd_siblings(const orc_verify_cfg* c, const float* p, int excl_tok, uint32_t row,
+static void pd_siblings(const orc_verify_cfg* c, const float* p, const int* rank, int excl_tok, uint32_t row,
                         uint32_t trial, int* sib, float* m_gap) {
-  orc_race_topn(p, c->V, c->K - 1, excl_tok, c->seed, ORC_TAG_PD, 0, row, trial, c->step, sib, m_gap);
+  orc_race_topn_ranked(p, rank, c->V, c->K - 1, excl_tok, c->seed, ORC_TAG_PD, 0, row, trial, c->step, sib,
+                       m_gap);
 }
 
 static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b) {
@@ -192,17 +212,24 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
   int* fresh = (int*)malloc(sizeof(int) * (size_t)L);
   int* pds = (int*)malloc(sizeof(int) * (size_t)L * (Km1 > 0 ? Km1 : 1));
   float* pdgap = (float*)malloc(sizeof(float) * (size_t)L);
-  if (!P || !Q || !rho || !rho2 || !excl || !ro || !fresh || !pds || !pdgap) {
-    free(P); free(Q); free(rho); free(rho2); free(excl); free(ro); free(fresh); free(pds); free(pdgap);
+  int* R = (int*)malloc(sizeof(int) * (size_t)L * V);
+  if (!P || !Q || !rho || !rho2 || !excl || !ro || !fresh || !pds || !pdgap || !R) {
+    free(P); free(Q); free(rho); free(rho2); free(excl); free(ro); free(fresh); free(pds); free(pdgap); free(R);
     return -2;
   }
-  for (int j = 0; j < L; ++j) orc_topk_softmax(cur + (size_t)j * V, V, c->top_k, c->T, P + (size_t)j * V);
+  /* p of every row, and the rank of each kept token in its row's top-k set
+   * (index order): races of a row take the stream element of that rank */
+  for (int j = 0; j < L; ++j) {
+    orc_topk_softmax(cur + (size_t)j * V, V, c->top_k, c->T, P + (size_t)j * V);
+    orc_topk_rank(cur + (size_t)j * V, V, c->top_k, R + (size_t)j * V);
+  }
   if (io->dbg_p) memcpy(io->dbg_p + (size_t)b * L * V, P, sizeof(float) * (size_t)L * V);
 
   /* ---- spine rows: row j is the output of the slot that feeds the token
    * before s_j, i.e. p_j = P^t(. | X_{<j}) verifies draft s_j. */
   for (int j = 0; j < n_s; ++j) {
     const float* p = P + (size_t)j * V;
+    const int* rk = R + (size_t)j * V;
     row_out* o = &ro[j];
     o->m_acc = o->m_race = o->m_cond = INFINITY;
     int* my_sib = pds + (size_t)j * (Km1 > 0 ? Km1 : 1);
@@ -216,7 +243,7 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
       /* appended placeholder with no draft distribution: its token is drawn
        * from p directly and the row counts as rejected (stage-0 stream). */
       float gap;
-      o->tok = orc_race(p, V, c->seed, ORC_TAG_RES, 0, (uint32_t)j, tr, c->step, &gap);
+      o->tok = orc_race_ranked(p, rk, V, c->seed, ORC_TAG_RES, 0, (uint32_t)j, tr, c->step, &gap);
       o->stage = 0;
       o->m_race = gap;
     } else {
@@ -240,23 +267,23 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
       }
       if (nc == 0) {
         float gap;
-        o->tok = orc_race(p, V, c->seed, ORC_TAG_RES, 0, (uint32_t)j, tr, c->step, &gap);
+        o->tok = orc_race_ranked(p, rk, V, c->seed, ORC_TAG_RES, 0, (uint32_t)j, tr, c->step, &gap);
         o->stage = 0;
         o->m_race = gap;
       } else {
-        verify_row(c, p, Q, cand, nc, (uint32_t)j, tr, rho, rho2, excl, o);
+        verify_row(c, p, Q, rk, cand, nc, (uint32_t)j, tr, rho, rho2, excl, o);
       }
     }
     if (!(c->flags & ORC_AC)) {
       float gap;
-      fresh[j] = orc_race(p, V, c->seed, ORC_TAG_FRESH, 0, (uint32_t)j, tr, c->step, &gap);
+      fresh[j] = orc_race_ranked(p, rk, V, c->seed, ORC_TAG_FRESH, 0, (uint32_t)j, tr, c->step, &gap);
       o->m_race = fminf_(o->m_race, gap);
     } else {
       fresh[j] = o->tok;
     }
     if ((c->flags & ORC_PD) && Km1 > 0) {
       int spine_next = (c->flags & ORC_AC) ? o->tok : fresh[j];
-      pd_siblings(c, p, spine_next, (uint32_t)j, tr, my_sib, &pdgap[j]);
+      pd_siblings(c, p, rk, spine_next, (uint32_t)j, tr, my_sib, &pdgap[j]);
     }
   }
 
@@ -271,7 +298,8 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
       if (y < 0 || is_forced(c, g0 + d)) { o->tok = -1; o->stage = 0; continue; }
       if (is_forced(c, g0 + d + 1)) { o->tok = -1; o->stage = -1; continue; }
       float gap;
-      o->tok = orc_race(P + (size_t)t * V, V, c->seed, ORC_TAG_BONUS, 0, (uint32_t)t, tr, c->step, &gap);
+      o->tok = orc_race_ranked(P + (size_t)t * V, R + (size_t)t * V, V, c->seed, ORC_TAG_BONUS, 0, (uint32_t)t, tr,
+                               c->step, &gap);
       o->stage = 0;
       o->m_race = gap;
     }
@@ -367,7 +395,7 @@ static int verify_trial(const orc_verify_cfg* c, const orc_verify_io* io, int b)
     }
   }
 #undef TOKOF
-  free(P); free(Q); free(rho); free(rho2); free(excl); free(ro); free(fresh); free(pds); free(pdgap);
+  free(P); free(Q); free(rho); free(rho2); free(excl); free(ro); free(fresh); free(pds); free(pdgap); free(R);
   return 0;
 }
 

@@ -1,0 +1,228 @@
+// Window attention: M <= 32 query slots of one head against the cached keys
+// and values plus the window's own (tree-masked) keys, on bf16 MFMA.
+//
+// Layout choices (gfx950, wave64, v_mfma_f32_32x32x16_bf16):
+//  - scores are formed transposed, S^T = K . Q^T (rows = keys, columns =
+//    slots), so each lane owns one slot: the running max, sum and the output
+//    rescale of online softmax are lane-local (plus one exchange between the
+//    two lane halves);
+//  - the key rows fed to MFMA row i are key pi(i) (bits 2 and 3 of i
+//    swapped); then the score registers of a lane hold 16 keys in the order
+//    that O^T = V^T . P^T needs as its B operand, so P never leaves registers;
+//  - values are cached transposed ([kv head][dim][position]) so the V^T
+//    operand is one 16-byte load per lane;
+//  - a workgroup (4 waves x 64 keys) handles 256 keys of one head; the four
+//    waves merge in LDS and one partial (unnormalised output, max, sum) per
+//    workgroup is combined across chunks by a second kernel.
+// Scores use exp2 with the scale folded into log2(e) / sqrt(hd).
+// Precision: q, the cached keys and values, and P are each carried as a
+// pair of bf16 values (hi + lo); every product is formed as hi*hi + hi*lo +
+// lo*hi on MFMA (the lo*lo term is below fp32 accumulation noise).
+#include "device.h"
+#include "forward.h"
+
+namespace sjd {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+SJD_DEV bf16x8 to_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
+
+SJD_DEV int swap23(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
+
+template <int HD>
+struct AttnSmem {
+  float o[4][HD][32];
+  float m[4][32];
+  float l[4][32];
+};
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
+  constexpr int NQ = HD / 16;  // MFMAs per 32-key block for the scores
+  constexpr int ND = HD / 32;  // 32-dim output blocks
+  __shared__ AttnSmem<HD> sm;
+  const int h = blockIdx.x, sp = blockIdx.y;
+  const int n = a.n_dev ? *a.n_dev : a.n_host;
+  const int M = a.M, nk = n + M;
+  const int kbeg = sp * kAttnChunk;
+  if (kbeg >= nk) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r32 = lane & 31, half = lane >> 5;
+  const int kvh = h / (a.H / a.Hkv);
+  const int slot = r32;
+  const bool slot_ok = slot < M;
+  const uint64_t anc = slot_ok ? a.win->anc[slot] : 0ull;
+
+  // Q^T operand, held for the whole kernel: dims half*HD/2 + 8t + e of this slot
+  uint4 qv[NQ], qvl[NQ];
+  {
+    const size_t qo = (size_t)slot * a.H * HD + (size_t)h * HD + half * (HD / 2);
+    const uint4* qp = (const uint4*)(a.q + qo);
+    const uint4* qpl = (const uint4*)(a.q_lo + qo);
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+      qv[t] = slot_ok ? qp[t] : make_uint4(0, 0, 0, 0);
+      qvl[t] = slot_ok ? qpl[t] : make_uint4(0, 0, 0, 0);
+    }
+  }
+  const size_t kofs = (size_t)kvh * a.cap * HD;
+  const size_t vofs = (size_t)kvh * HD * a.cap;
+
+  f32x16 o[ND];
+#pragma unroll
+  for (int d = 0; d < ND; ++d)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[d][r] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  const int wbeg = kbeg + wave * 64;
+  for (int kb = wbeg; kb < wbeg + 64 && kb < nk; kb += 32) {
+    // ---- scores
+    const int krow = kb + swap23(r32);
+    const size_t ko = kofs + (size_t)krow * HD + half * (HD / 2);
+    const uint4* kp = (const uint4*)(a.kc + ko);
+    const uint4* kpl = (const uint4*)(a.kc_lo + ko);
+    f32x16 s;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+      const bf16x8 kh = to_bf16x8(kp[t]), kl = to_bf16x8(kpl[t]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, to_bf16x8(qv[t]), s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, to_bf16x8(qvl[t]), s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kl, to_bf16x8(qv[t]), s, 0, 0, 0);
+    }
+    // ---- mask, online softmax (register r = 8jj + e holds key kb + 16jj + 8half + e)
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = kb + 16 * (r >> 3) + 8 * half + (r & 7);
+      bool vis = slot_ok && key < nk;
+      if (vis && key >= n) vis = (anc >> (key - n)) & 1ull;
+      s[r] = vis ? s[r] * a.scale : -INFINITY;
+      mloc = fmaxf(mloc, s[r]);
+    }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, kWave));
+    const float m_new = fmaxf(m_run, mloc);
+    float lsum = 0.0f;
+    if (m_new == -INFINITY) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+    } else {
+      const float alpha = exp2f(m_run - m_new);  // m_run = -inf -> 0
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[r] = exp2f(s[r] - m_new);
+        lsum += s[r];
+      }
+#pragma unroll
+      for (int d = 0; d < ND; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+      l_run *= alpha;
+      m_run = m_new;
+    }
+    lsum += __shfl_xor(lsum, 32, kWave);
+    l_run += lsum;
+    // ---- P^T operand (hi / lo bf16) and O^T += V^T . P^T
+    uint4 pb[2], pbl[2];
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      uint32_t w[4], wl[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        uint16_t h0, l0, h1, l1;
+        split_bf16(s[8 * jj + 2 * e], h0, l0);
+        split_bf16(s[8 * jj + 2 * e + 1], h1, l1);
+        w[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        wl[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+      }
+      pb[jj] = make_uint4(w[0], w[1], w[2], w[3]);
+      pbl[jj] = make_uint4(wl[0], wl[1], wl[2], wl[3]);
+    }
+#pragma unroll
+    for (int d = 0; d < ND; ++d) {
+      const size_t vo = vofs + (size_t)(d * 32 + r32) * a.cap + kb + 8 * half;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const bf16x8 vh = to_bf16x8(*(const uint4*)(a.vt + vo + 16 * jj));
+        const bf16x8 vl = to_bf16x8(*(const uint4*)(a.vt_lo + vo + 16 * jj));
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vh, to_bf16x8(pb[jj]), o[d], 0, 0, 0);
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vh, to_bf16x8(pbl[jj]), o[d], 0, 0, 0);
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vl, to_bf16x8(pb[jj]), o[d], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- merge the four waves
+#pragma unroll
+  for (int d = 0; d < ND; ++d)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sm.o[wave][d * 32 + 8 * (r >> 2) + 4 * half + (r & 3)][slot] = o[d][r];
+  if (half == 0) {
+    sm.m[wave][slot] = m_run;
+    sm.l[wave][slot] = l_run;
+  }
+  __syncthreads();
+  float* wo = a.ws_o + ((size_t)h * a.nsplit_max + sp) * 32 * HD;
+  float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 32 * 2;
+  for (int idx = threadIdx.x; idx < 32 * HD; idx += 256) {
+    const int sl = idx / HD, dim = idx % HD;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, sm.m[w][sl]);
+    float acc = 0.0f, ls = 0.0f;
+    if (mx != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float f = exp2f(sm.m[w][sl] - mx);
+        acc += sm.o[w][dim][sl] * f;
+        ls += sm.l[w][sl] * f;
+      }
+    }
+    wo[(size_t)sl * HD + dim] = acc;
+    if (dim == 0) {
+      wml[sl * 2] = mx;
+      wml[sl * 2 + 1] = ls;
+    }
+  }
+}
+
+// out[slot][h*hd + dim] = bf16(sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m))
+template <int HD>
+__global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
+  const int slot = blockIdx.x, h = blockIdx.y, dim = threadIdx.x;
+  const int n = a.n_dev ? *a.n_dev : a.n_host;
+  const int nk = n + a.M;
+  const int ns = (nk + kAttnChunk - 1) / kAttnChunk;
+  const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * 64;
+  const float* wo = a.ws_o + (size_t)h * a.nsplit_max * 32 * HD;
+  float mx = -INFINITY;
+  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, wml[s * 64 + slot * 2]);
+  float acc = 0.0f, ls = 0.0f;
+  for (int s = 0; s < ns; ++s) {
+    const float ms = wml[s * 64 + slot * 2];
+    if (ms == -INFINITY) continue;
+    const float f = exp2f(ms - mx);
+    acc += wo[((size_t)s * 32 + slot) * HD + dim] * f;
+    ls += wml[s * 64 + slot * 2 + 1] * f;
+  }
+  const size_t oo = (size_t)slot * a.H * HD + (size_t)h * HD + dim;
+  split_bf16(acc / ls, a.out[oo], a.out_lo[oo]);
+}
+
+hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s) {
+  const dim3 g1(a.H, a.nsplit_max), g2(a.M, a.H);
+  if (hd == 128) {
+    hipLaunchKernelGGL(k_attn_partial<128>, g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_attn_combine<128>, g2, dim3(128), 0, s, a);
+  } else if (hd == 64) {
+    hipLaunchKernelGGL(k_attn_partial<64>, g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_attn_combine<64>, g2, dim3(64), 0, s, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sjd

@@ -64,6 +64,13 @@ SJD_DEV uint16_t f32_to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// v ~= hi + lo with hi = bf16(v), lo = bf16(v - hi): about 16 significant
+// bits carried in two bf16 MFMA operands.
+SJD_DEV void split_bf16(float v, uint16_t& hi, uint16_t& lo) {
+  hi = f32_to_bf16(v);
+  lo = f32_to_bf16(v - bf16_to_f32(hi));
+}
+
 // ---------------------------------------------------------------- reductions
 SJD_DEV float wave_max(float v) {
 #pragma unroll

@@ -18,8 +18,9 @@ hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, floa
   return hipGetLastError();
 }
 
-// y = bf16(x / sqrt(mean(x^2) + eps) * g), one workgroup per row
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* x, const uint16_t* g, int d, float eps, uint16_t* y) {
+// y = x / sqrt(mean(x^2) + eps) * g as hi / lo bf16 planes, one workgroup per row
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* x, const uint16_t* g, int d, float eps, uint16_t* y,
+                                                 uint16_t* y_lo) {
   __shared__ float red[4];
   const int m = blockIdx.x;
   const float* xr = x + (size_t)m * d;
@@ -30,20 +31,22 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* x, const uint16_t*
   __syncthreads();
   const float tot = red[0] + red[1] + red[2] + red[3];
   const float inv = rsqrtf(tot / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256) y[(size_t)m * d + i] = f32_to_bf16(xr[i] * inv * bf16_to_f32(g[i]));
+  for (int i = threadIdx.x; i < d; i += 256)
+    split_bf16(xr[i] * inv * bf16_to_f32(g[i]), y[(size_t)m * d + i], y_lo[(size_t)m * d + i]);
 }
 
-hipError_t launch_rmsnorm(const float* x, const uint16_t* g, int M, int d, float eps, uint16_t* y, hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, s, x, g, d, eps, y);
+hipError_t launch_rmsnorm(const float* x, const uint16_t* g, int M, int d, float eps, uint16_t* y, uint16_t* y_lo,
+                          hipStream_t s) {
+  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, s, x, g, d, eps, y, y_lo);
   return hipGetLastError();
 }
 
 // Rotate-half rotary embedding (pair i with i + hd/2 at angle pos * theta^(-2i/hd),
-// table rope[pos][i] = (cos, sin)), then: q -> q buffer (bf16), k -> key cache
-// row n + m, v -> column n + m of the transposed value cache.
-// grid (M, H + 2 * Hkv), block hd / 2
+// table rope[pos][i] = (cos, sin)), then: q -> q planes, k -> key cache row
+// n + m, v -> column n + m of the transposed value cache, all as hi / lo bf16
+// planes. grid (M, H + 2 * Hkv), block hd / 2
 __global__ void k_rope_kv(const float* qkv, const Window* win, const int32_t* n_dev, int n_host, int H, int Hkv,
-                          int hd, const float2* rope, uint16_t* q, uint16_t* kc, uint16_t* vt, int cap) {
+                          int hd, const float2* rope, KvPlanes o, int cap) {
   const int m = blockIdx.x, hh = blockIdx.y, i = threadIdx.x;
   const int half = hd / 2;
   const int n = n_dev ? *n_dev : n_host;
@@ -55,29 +58,28 @@ __global__ void k_rope_kv(const float* qkv, const Window* win, const int32_t* n_
     const float a = src[i], b = src[i + half];
     const float o0 = a * cs.x - b * cs.y;
     const float o1 = a * cs.y + b * cs.x;
+    size_t off;
+    uint16_t *dh, *dl;
     if (hh < H) {
-      uint16_t* dst = q + (size_t)m * H * hd + (size_t)hh * hd;
-      dst[i] = f32_to_bf16(o0);
-      dst[i + half] = f32_to_bf16(o1);
+      off = (size_t)m * H * hd + (size_t)hh * hd;
+      dh = o.q; dl = o.q_lo;
     } else {
-      const int kh = hh - H;
-      uint16_t* dst = kc + ((size_t)kh * cap + row) * hd;
-      dst[i] = f32_to_bf16(o0);
-      dst[i + half] = f32_to_bf16(o1);
+      off = ((size_t)(hh - H) * cap + row) * hd;
+      dh = o.kc; dl = o.kc_lo;
     }
+    split_bf16(o0, dh[off + i], dl[off + i]);
+    split_bf16(o1, dh[off + i + half], dl[off + i + half]);
   } else {
-    const int vh = hh - H - Hkv;
-    uint16_t* dst = vt + (size_t)vh * hd * cap;
-    dst[(size_t)i * cap + row] = f32_to_bf16(src[i]);
-    dst[(size_t)(i + half) * cap + row] = f32_to_bf16(src[i + half]);
+    const size_t base = (size_t)(hh - H - Hkv) * hd * cap + row;
+    split_bf16(src[i], o.vt[base + (size_t)i * cap], o.vt_lo[base + (size_t)i * cap]);
+    split_bf16(src[i + half], o.vt[base + (size_t)(i + half) * cap], o.vt_lo[base + (size_t)(i + half) * cap]);
   }
 }
 
 hipError_t launch_rope_kv(const float* qkv, const Window* win, const int32_t* n_dev, int n_host, int M, int H,
-                          int Hkv, int hd, const float2* rope, uint16_t* q, uint16_t* kc, uint16_t* vt, int cap,
-                          hipStream_t s) {
+                          int Hkv, int hd, const float2* rope, const KvPlanes& o, int cap, hipStream_t s) {
   hipLaunchKernelGGL(k_rope_kv, dim3(M, H + 2 * Hkv), dim3(hd / 2), 0, s, qkv, win, n_dev, n_host, H, Hkv, hd, rope,
-                     q, kc, vt, cap);
+                     o, cap);
   return hipGetLastError();
 }
 

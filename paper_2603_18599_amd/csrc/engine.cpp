@@ -1,20 +1,364 @@
-// Decoder context entry points (window forward + step). Filled in with the
-// forward kernels; until then they report SJD_ENOTSUP.
+// Decoder context: buffers, prefill and the SJD-PAC step (window forward,
+// verification, KV commit), all enqueued on the caller's stream. The host
+// never reads device state during a step except to keep a bound on the
+// cache fill (one 4-byte copy per step into pinned memory, polled without
+// blocking).
 #include <hip/hip_runtime.h>
 
-#include "sjd.h"
+#include <array>
+#include <cmath>
+#include <cstring>
+#include <vector>
 
-struct sjd_ctx {
-  int dummy;
+#include "forward.h"
+#include "sjd.h"
+#include "step.h"
+#include "verify.h"
+
+namespace {
+
+constexpr int kRing = 8;
+
+struct Ctx {
+  sjd_config c{};
+  int cap = 0;      // KV rows
+  int cap_pad = 0;  // row stride of the caches (multiple of the attention chunk)
+  int Mpad = 32;
+  const uint16_t* embed = nullptr;
+  const uint16_t* fnorm = nullptr;
+  const uint16_t* head = nullptr;
+  std::vector<std::array<const uint16_t*, 9>> lw;
+  std::vector<void*> owned;
+  // activations entering MFMAs are hi / lo bf16 plane pairs
+  float* x = nullptr;
+  uint16_t *xn = nullptr, *xn_lo = nullptr;
+  float* qkv = nullptr;
+  uint16_t *q = nullptr, *q_lo = nullptr;
+  uint16_t *att = nullptr, *att_lo = nullptr;
+  uint16_t *hbuf = nullptr, *hbuf_lo = nullptr;
+  uint16_t *kc = nullptr, *kc_lo = nullptr;
+  uint16_t *vt = nullptr, *vt_lo = nullptr;
+  float2* rope = nullptr;
+  float* logits[2] = {nullptr, nullptr};
+  float* attn_o = nullptr;
+  float* attn_ml = nullptr;
+  int nsplit_max = 0;
+  float* gws = nullptr;
+  int* gcnt = nullptr;
+  sjd::DevState* st = nullptr;
+  sjd::Window* win = nullptr;
+  int32_t* rec = nullptr;
+  int S_qkv = 1, S_o = 1, S_gu = 1, S_dn = 1, S_head = 1;
+  long long steps = 0;
+  bool prefilled = false;
+  // cache-fill bound
+  int32_t* h_n = nullptr;  // pinned ring
+  hipEvent_t ev[kRing];
+  long long ev_step[kRing];
+  long long known_step = -1;  // step after which known_n holds
+  int known_n = 0;
+  int n_events = 0;
 };
 
-extern "C" int sjd_init(const sjd_config*, const sjd_weights*, void*, sjd_ctx** out) {
-  if (out) *out = nullptr;
-  return SJD_ENOTSUP;
+template <class T>
+int dalloc(Ctx& x, T** p, size_t count) {
+  void* q = nullptr;
+  if (hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 16) != hipSuccess) return SJD_ENOMEM;
+  x.owned.push_back(q);
+  *p = (T*)q;
+  return SJD_OK;
 }
-extern "C" int sjd_prefill(sjd_ctx*, const int32_t*, int32_t, uint64_t, void*) { return SJD_ENOTSUP; }
-extern "C" int sjd_step(sjd_ctx*, float, int32_t, uint64_t, uint32_t, int32_t*, int32_t*, int32_t*, void*) {
-  return SJD_ENOTSUP;
+
+int check_config(const sjd_config* c) {
+  if (!c) return SJD_EINVAL;
+  if (c->n_layers < 1 || c->d_model < 64 || c->d_model % 64 || c->n_heads < 1 || c->n_kv_heads < 1 ||
+      c->n_heads % c->n_kv_heads)
+    return SJD_EINVAL;
+  if (c->head_dim != 64 && c->head_dim != 128) return SJD_ENOTSUP;
+  if ((c->n_heads * c->head_dim) % 64 || c->ffn_dim < 64 || c->ffn_dim % 64) return SJD_EINVAL;
+  if (c->vocab_size < 1 || c->V < 32 || c->V % 32 || c->vis_lo < 0 || c->vis_lo + c->V > c->vocab_size)
+    return SJD_EINVAL;
+  if (c->L < 1 || c->L > 64 || c->K < 1 || c->K > 8 || c->D < 0 || (long)c->K * c->D > c->L) return SJD_EINVAL;
+  if (c->L > 32) return SJD_ENOTSUP;
+  if (c->max_seq < c->L + 2) return SJD_EINVAL;
+  if (c->flags & ~(SJD_AC | SJD_PD)) return SJD_EINVAL;
+  if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
+  return SJD_OK;
 }
-extern "C" int sjd_forward_window(sjd_ctx*, float*, void*) { return SJD_ENOTSUP; }
-extern "C" void sjd_destroy(sjd_ctx*) {}
+
+#define TRY(e)                          \
+  do {                                  \
+    int _rc = (e);                      \
+    if (_rc != SJD_OK) return _rc;      \
+  } while (0)
+#define HIPTRY(e)                                \
+  do {                                           \
+    if ((e) != hipSuccess) return SJD_EHIP;      \
+  } while (0)
+
+int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, hipStream_t s) {
+  const sjd_config& c = x.c;
+  const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
+  const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv;
+  HIPTRY(sjd::launch_embed(x.embed, x.win, M, d, x.x, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const auto& w = x.lw[l];
+    const size_t lofs = (size_t)l * Hkv * x.cap_pad * hd;
+    sjd::KvPlanes kv{x.q, x.q_lo, x.kc + lofs, x.kc_lo + lofs, x.vt + lofs, x.vt_lo + lofs};
+    HIPTRY(sjd::launch_rmsnorm(x.x, w[0], M, d, c.rms_eps, x.xn, x.xn_lo, s));
+    sjd::GemmArgs g{};
+    g.A = x.xn; g.A_lo = x.xn_lo; g.M = M; g.W0 = w[1]; g.W1 = w[2]; g.W2 = w[3]; g.n0 = Nq; g.n1 = Nq + Nkv;
+    g.N = Nqkv; g.K = d; g.S = x.S_qkv; g.ws = x.gws; g.cnt = x.gcnt; g.out = x.qkv; g.ldo = Nqkv;
+    HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
+    HIPTRY(sjd::launch_rope_kv(x.qkv, x.win, n_dev, n_host, M, H, Hkv, hd, x.rope, kv, x.cap_pad, s));
+    sjd::AttnArgs a{};
+    a.q = x.q; a.q_lo = x.q_lo; a.kc = kv.kc; a.kc_lo = kv.kc_lo; a.vt = kv.vt; a.vt_lo = kv.vt_lo; a.win = x.win;
+    a.n_dev = n_dev; a.n_host = n_host; a.M = M; a.H = H; a.Hkv = Hkv; a.cap = x.cap_pad;
+    a.scale = (float)(1.4426950408889634 / std::sqrt((double)hd));
+    a.ws_o = x.attn_o; a.ws_ml = x.attn_ml; a.nsplit_max = x.nsplit_max; a.out = x.att; a.out_lo = x.att_lo;
+    HIPTRY(sjd::launch_attention(a, hd, s));
+    g = sjd::GemmArgs{};
+    g.A = x.att; g.A_lo = x.att_lo; g.M = M; g.W0 = w[4]; g.n0 = d; g.n1 = d; g.N = d; g.K = Nq; g.S = x.S_o;
+    g.ws = x.gws; g.cnt = x.gcnt; g.out = x.x; g.ldo = d;
+    HIPTRY(sjd::launch_gemm(g, sjd::kGemmAdd, s));
+    HIPTRY(sjd::launch_rmsnorm(x.x, w[5], M, d, c.rms_eps, x.xn, x.xn_lo, s));
+    g = sjd::GemmArgs{};
+    g.A = x.xn; g.A_lo = x.xn_lo; g.M = M; g.W0 = w[6]; g.W1 = w[7]; g.n0 = F; g.n1 = F; g.N = F; g.K = d;
+    g.S = x.S_gu; g.ws = x.gws; g.cnt = x.gcnt; g.outb = x.hbuf; g.outb_lo = x.hbuf_lo; g.ldo = F;
+    HIPTRY(sjd::launch_gemm(g, sjd::kGemmSwiGLU, s));
+    g = sjd::GemmArgs{};
+    g.A = x.hbuf; g.A_lo = x.hbuf_lo; g.M = M; g.W0 = w[8]; g.n0 = d; g.n1 = d; g.N = d; g.K = F; g.S = x.S_dn;
+    g.ws = x.gws; g.cnt = x.gcnt; g.out = x.x; g.ldo = d;
+    HIPTRY(sjd::launch_gemm(g, sjd::kGemmAdd, s));
+  }
+  if (logits) {
+    HIPTRY(sjd::launch_rmsnorm(x.x, x.fnorm, M, d, c.rms_eps, x.xn, x.xn_lo, s));
+    sjd::GemmArgs g{};
+    g.A = x.xn; g.A_lo = x.xn_lo; g.M = M; g.W0 = x.head + (size_t)c.vis_lo * d; g.n0 = c.V; g.n1 = c.V;
+    g.N = c.V; g.K = d; g.S = x.S_head; g.ws = x.gws; g.cnt = x.gcnt; g.out = logits; g.ldo = c.V;
+    HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
+  }
+  return SJD_OK;
+}
+
+// Refreshes the cache-fill bound from completed steps; blocks only when the
+// bound says the next window might not fit.
+int cache_check(Ctx& x) {
+  for (int i = 0; i < kRing; ++i) {
+    if (x.ev_step[i] > x.known_step && hipEventQuery(x.ev[i]) == hipSuccess) {
+      x.known_step = x.ev_step[i];
+      x.known_n = x.h_n[i];
+    }
+  }
+  long long pending = x.steps - 1 - x.known_step;
+  long long bound = (long long)x.known_n + pending * x.c.L;
+  if (bound + x.c.L <= x.cap) return SJD_OK;
+  // wait for the newest step and use its exact value
+  for (int i = 0; i < kRing; ++i) {
+    if (x.ev_step[i] == x.steps - 1) {
+      HIPTRY(hipEventSynchronize(x.ev[i]));
+      x.known_step = x.ev_step[i];
+      x.known_n = x.h_n[i];
+    }
+  }
+  if ((long long)x.known_n + x.c.L > x.cap) return SJD_ESTATE;
+  return SJD_OK;
+}
+
+}  // namespace
+
+struct sjd_ctx {
+  Ctx x;
+};
+
+extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* stream, sjd_ctx** out) {
+  if (!out) return SJD_EINVAL;
+  *out = nullptr;
+  TRY(check_config(cfg));
+  if (!w || !w->d_embed || !w->h_layer || !w->d_final_norm || !w->d_lm_head) return SJD_EINVAL;
+  for (int i = 0; i < 9 * cfg->n_layers; ++i)
+    if (!w->h_layer[i]) return SJD_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  sjd_ctx* h = new sjd_ctx();
+  Ctx& x = h->x;
+  x.c = *cfg;
+  const sjd_config& c = x.c;
+  auto fail = [&](int rc) {
+    sjd_destroy(h);
+    return rc;
+  };
+  const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
+  const int Nq = H * hd, Nkv = Hkv * hd;
+  x.cap = c.max_seq;
+  x.cap_pad = ((c.max_seq + sjd::kAttnChunk - 1) / sjd::kAttnChunk) * sjd::kAttnChunk;
+  x.nsplit_max = x.cap_pad / sjd::kAttnChunk;
+
+  // weights: borrowed bf16 pointers, or bf16 copies of fp32 weights
+  auto weight = [&](const void* p, size_t count, const uint16_t** dst) -> int {
+    if (!c.weights_f32) {
+      *dst = (const uint16_t*)p;
+      return SJD_OK;
+    }
+    uint16_t* b = nullptr;
+    int rc = dalloc(x, &b, count);
+    if (rc != SJD_OK) return rc;
+    if (sjd::launch_f32_to_bf16((const float*)p, b, count, s) != hipSuccess) return SJD_EHIP;
+    *dst = b;
+    return SJD_OK;
+  };
+  int rc = weight(w->d_embed, (size_t)c.vocab_size * d, &x.embed);
+  if (rc == SJD_OK) rc = weight(w->d_final_norm, d, &x.fnorm);
+  if (rc == SJD_OK) rc = weight(w->d_lm_head, (size_t)c.vocab_size * d, &x.head);
+  x.lw.resize(c.n_layers);
+  const size_t sizes[9] = {(size_t)d, (size_t)Nq * d, (size_t)Nkv * d, (size_t)Nkv * d, (size_t)d * Nq,
+                           (size_t)d, (size_t)F * d, (size_t)F * d, (size_t)d * F};
+  for (int l = 0; l < c.n_layers && rc == SJD_OK; ++l)
+    for (int i = 0; i < 9 && rc == SJD_OK; ++i) rc = weight(w->h_layer[9 * l + i], sizes[i], &x.lw[l][i]);
+  if (rc != SJD_OK) return fail(rc);
+
+  // work buffers
+  const int Mp = x.Mpad;
+  const size_t kv = (size_t)c.n_layers * Hkv * x.cap_pad * hd;
+  const size_t xnsz = (size_t)Mp * (d > F ? d : F);
+  if ((rc = dalloc(x, &x.x, (size_t)Mp * d)) || (rc = dalloc(x, &x.xn, xnsz)) || (rc = dalloc(x, &x.xn_lo, xnsz)) ||
+      (rc = dalloc(x, &x.qkv, (size_t)Mp * (Nq + 2 * Nkv))) || (rc = dalloc(x, &x.q, (size_t)Mp * Nq)) ||
+      (rc = dalloc(x, &x.q_lo, (size_t)Mp * Nq)) || (rc = dalloc(x, &x.att, (size_t)Mp * Nq)) ||
+      (rc = dalloc(x, &x.att_lo, (size_t)Mp * Nq)) || (rc = dalloc(x, &x.hbuf, (size_t)Mp * F)) ||
+      (rc = dalloc(x, &x.hbuf_lo, (size_t)Mp * F)) || (rc = dalloc(x, &x.kc, kv)) || (rc = dalloc(x, &x.kc_lo, kv)) ||
+      (rc = dalloc(x, &x.vt, kv)) || (rc = dalloc(x, &x.vt_lo, kv)) ||
+      (rc = dalloc(x, &x.rope, (size_t)x.cap_pad * (hd / 2))) ||
+      (rc = dalloc(x, &x.logits[0], (size_t)c.L * c.V)) || (rc = dalloc(x, &x.logits[1], (size_t)c.L * c.V)) ||
+      (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * 32 * hd)) ||
+      (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 64)) || (rc = dalloc(x, &x.st, 1)) ||
+      (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)c.L * sjd::kRecInts)))
+    return fail(rc);
+  // split-K plan: aim for two workgroups per compute unit
+  int ncu = 256;
+  {
+    int dev = 0;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess)
+      ncu = prop.multiProcessorCount;
+  }
+  const int target = 2 * ncu;
+  x.S_qkv = sjd::gemm_splits(Nq + 2 * Nkv, d, target);
+  x.S_o = sjd::gemm_splits(d, Nq, target);
+  x.S_gu = sjd::gemm_splits(F, d, target);
+  x.S_dn = sjd::gemm_splits(d, F, target);
+  x.S_head = sjd::gemm_splits(c.V, d, target);
+  size_t ws = 0, w1;
+  w1 = sjd::gemm_ws_floats(Nq + 2 * Nkv, x.S_qkv, Mp, sjd::kGemmStore); ws = ws > w1 ? ws : w1;
+  w1 = sjd::gemm_ws_floats(d, x.S_o, Mp, sjd::kGemmAdd); ws = ws > w1 ? ws : w1;
+  w1 = sjd::gemm_ws_floats(F, x.S_gu, Mp, sjd::kGemmSwiGLU); ws = ws > w1 ? ws : w1;
+  w1 = sjd::gemm_ws_floats(d, x.S_dn, Mp, sjd::kGemmAdd); ws = ws > w1 ? ws : w1;
+  w1 = sjd::gemm_ws_floats(c.V, x.S_head, Mp, sjd::kGemmStore); ws = ws > w1 ? ws : w1;
+  int maxN = Nq + 2 * Nkv;
+  if (F > maxN) maxN = F;
+  if (c.V > maxN) maxN = c.V;
+  if ((rc = dalloc(x, &x.gws, ws)) || (rc = dalloc(x, &x.gcnt, (size_t)maxN / 32))) return fail(rc);
+  // zero the caches (rows past the fill are read, masked, by the attention
+  // tiles) and the activation pad rows
+  void* zero[] = {x.kc, x.kc_lo, x.vt, x.vt_lo};
+  bool ok = hipMemsetAsync(x.gcnt, 0, sizeof(int) * (maxN / 32), s) == hipSuccess &&
+            hipMemsetAsync(x.st, 0, sizeof(sjd::DevState), s) == hipSuccess;
+  for (void* p : zero) ok = ok && hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess;
+  void* zero2[] = {x.xn, x.xn_lo};
+  for (void* p : zero2) ok = ok && hipMemsetAsync(p, 0, xnsz * 2, s) == hipSuccess;
+  void* zero3[] = {x.att, x.att_lo, x.q, x.q_lo};
+  for (void* p : zero3) ok = ok && hipMemsetAsync(p, 0, (size_t)Mp * Nq * 2, s) == hipSuccess;
+  void* zero4[] = {x.hbuf, x.hbuf_lo};
+  for (void* p : zero4) ok = ok && hipMemsetAsync(p, 0, (size_t)Mp * F * 2, s) == hipSuccess;
+  if (!ok) return fail(SJD_EHIP);
+  // rotary table in double precision: rope[pos][i] = (cos, sin)(pos * theta^(-2i/hd))
+  {
+    std::vector<float2> t((size_t)x.cap_pad * (hd / 2));
+    for (int p = 0; p < x.cap_pad; ++p)
+      for (int i = 0; i < hd / 2; ++i) {
+        const double ang = (double)p * std::pow((double)c.rope_theta, -2.0 * i / hd);
+        t[(size_t)p * (hd / 2) + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+      }
+    if (hipMemcpyAsync(x.rope, t.data(), t.size() * sizeof(float2), hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return fail(SJD_EHIP);
+  }
+  if (hipHostMalloc((void**)&x.h_n, sizeof(int32_t) * kRing, hipHostMallocDefault) != hipSuccess)
+    return fail(SJD_ENOMEM);
+  for (int i = 0; i < kRing; ++i) {
+    if (hipEventCreateWithFlags(&x.ev[i], hipEventDisableTiming) != hipSuccess) return fail(SJD_EHIP);
+    x.n_events = i + 1;
+    x.ev_step[i] = -1;
+  }
+  *out = h;
+  return SJD_OK;
+}
+
+extern "C" int sjd_prefill(sjd_ctx* h, const int32_t* d_prompt, int32_t n, uint64_t seed, void* stream) {
+  if (!h || !d_prompt || n < 1) return SJD_EINVAL;
+  Ctx& x = h->x;
+  if (n + x.c.L > x.cap) return SJD_ESTATE;
+  hipStream_t s = (hipStream_t)stream;
+  for (int start = 0; start < n - 1; start += x.Mpad) {
+    const int M = (n - 1 - start) < x.Mpad ? (n - 1 - start) : x.Mpad;
+    HIPTRY(sjd::launch_build_prefill(d_prompt, start, M, x.win, s));
+    TRY(forward(x, M, nullptr, start, nullptr, s));
+  }
+  HIPTRY(sjd::launch_state_init(x.st, d_prompt, n, x.c.L, x.c.V, x.c.vis_lo, x.c.eol_id, x.c.row_len, seed, s));
+  x.prefilled = true;
+  x.steps = 0;
+  x.known_n = n - 1;
+  x.known_step = -1;
+  for (int i = 0; i < kRing; ++i) x.ev_step[i] = -2;
+  return SJD_OK;
+}
+
+extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t seed, uint32_t step,
+                        int32_t* d_out_meta, int32_t* d_out_tok, int32_t* d_out_next, void* stream) {
+  if (!h || !(temperature > 0.0f) || top_k < 0) return SJD_EINVAL;
+  Ctx& x = h->x;
+  if (!x.prefilled) return SJD_ESTATE;
+  TRY(cache_check(x));
+  hipStream_t s = (hipStream_t)stream;
+  const sjd_config& c = x.c;
+  float* cur = x.logits[x.steps & 1];
+  float* prev = x.logits[(x.steps + 1) & 1];
+  HIPTRY(sjd::launch_build_window(x.st, x.win, c.L, c.K, c.vis_lo, s));
+  TRY(forward(x, c.L, &x.st->n, 0, cur, s));
+  sjd::VerifyArgs a{};
+  a.B = 1; a.L = c.L; a.V = c.V; a.K = c.K; a.D = c.D; a.top_k = top_k; a.T = temperature; a.flags = c.flags;
+  a.seed = seed; a.step = step; a.vis_lo = c.vis_lo; a.eol = c.eol_id; a.row_len = c.row_len;
+  a.cur = cur; a.draft = prev; a.draft_bstride = 0; a.q_off = &x.st->q_off; a.draft_tok = x.st->spine;
+  a.sib = x.st->sib; a.in_meta = &x.st->D_in; a.rec = x.rec;
+  sjd::FinalizeOut o{};
+  o.out_meta = x.st->meta; o.meta_stride = 8; o.out_tok = x.st->tok; o.tok_stride = c.L;
+  o.out_next = x.st->spine; o.next_stride = c.L; o.out_sib = x.st->sib; o.sib_stride = c.D * (c.K - 1);
+  HIPTRY(sjd::launch_verify(a, o, s));
+  sjd::KvPlanes all{nullptr, nullptr, x.kc, x.kc_lo, x.vt, x.vt_lo};
+  HIPTRY(sjd::launch_kv_move(x.st, all, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, s));
+  HIPTRY(sjd::launch_state_update(x.st, d_out_meta, d_out_tok, d_out_next, c.L, s));
+  const int slot = (int)(x.steps % kRing);
+  HIPTRY(hipMemcpyAsync(x.h_n + slot, &x.st->n, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HIPTRY(hipEventRecord(x.ev[slot], s));
+  x.ev_step[slot] = x.steps;
+  x.steps += 1;
+  return SJD_OK;
+}
+
+extern "C" int sjd_forward_window(sjd_ctx* h, float* d_logits, void* stream) {
+  if (!h || !d_logits) return SJD_EINVAL;
+  Ctx& x = h->x;
+  if (!x.prefilled) return SJD_ESTATE;
+  TRY(cache_check(x));
+  hipStream_t s = (hipStream_t)stream;
+  HIPTRY(sjd::launch_build_window(x.st, x.win, x.c.L, x.c.K, x.c.vis_lo, s));
+  return forward(x, x.c.L, &x.st->n, 0, d_logits, s);
+}
+
+extern "C" void sjd_destroy(sjd_ctx* h) {
+  if (!h) return;
+  Ctx& x = h->x;
+  (void)hipDeviceSynchronize();
+  for (void* p : x.owned) (void)hipFree(p);
+  if (x.h_n) (void)hipHostFree(x.h_n);
+  for (int i = 0; i < x.n_events; ++i) (void)hipEventDestroy(x.ev[i]);
+  delete h;
+}

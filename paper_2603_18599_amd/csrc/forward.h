@@ -8,7 +8,8 @@ namespace sjd {
 enum { kGemmStore = 0, kGemmAdd = 1, kGemmSwiGLU = 2 };
 
 struct GemmArgs {
-  const uint16_t* A;  // bf16 activations, rows padded to 32 * ceil(M/32), row stride K
+  const uint16_t* A;     // activations as two bf16 planes (A = hi + lo), rows padded to
+  const uint16_t* A_lo;  // 32 * ceil(M/32), row stride K
   int M;
   const uint16_t* W0;  // weight segments stacked along N (rows of W0, then W1, then W2);
   const uint16_t* W1;  // SwiGLU: W0 = gate rows, W1 = up rows of the same columns
@@ -19,7 +20,8 @@ struct GemmArgs {
   float* ws;           // split-K partials
   int* cnt;            // arrival counters, one per 32-column block, zero between launches
   float* out;          // fp32 output (store / add), row stride ldo
-  uint16_t* outb;      // bf16 output (SwiGLU), row stride ldo
+  uint16_t* outb;      // SwiGLU output as hi / lo bf16 planes, row stride ldo
+  uint16_t* outb_lo;
   int ldo;
 };
 
@@ -46,9 +48,13 @@ struct DevState {
 };
 
 struct AttnArgs {
-  const uint16_t* q;     // bf16 [Mpad][H * hd], rotated
-  const uint16_t* kc;    // bf16 [Hkv][cap][hd] key cache of this layer
-  const uint16_t* vt;    // bf16 [Hkv][hd][cap] transposed value cache of this layer
+  // every tensor below is a pair of bf16 planes (value = hi + lo)
+  const uint16_t* q;     // [Mpad][H * hd], rotated
+  const uint16_t* q_lo;
+  const uint16_t* kc;    // [Hkv][cap][hd] key cache of this layer
+  const uint16_t* kc_lo;
+  const uint16_t* vt;    // [Hkv][hd][cap] transposed value cache of this layer
+  const uint16_t* vt_lo;
   const Window* win;
   const int32_t* n_dev;  // cached rows before the window (device scalar), or NULL -> n_host
   int n_host;
@@ -57,7 +63,8 @@ struct AttnArgs {
   float* ws_o;           // [H][nsplit_max][32][hd] partial outputs
   float* ws_ml;          // [H][nsplit_max][32][2]  partial max (log2 domain) and sum
   int nsplit_max;
-  uint16_t* out;         // bf16 [Mpad][H * hd]
+  uint16_t* out;         // [Mpad][H * hd]
+  uint16_t* out_lo;
 };
 constexpr int kAttnChunk = 256;  // keys per workgroup
 hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s);
@@ -65,11 +72,13 @@ hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s);
 // elementwise kernels
 hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, float* x, hipStream_t s);
 hipError_t launch_rmsnorm(const float* x, const uint16_t* g, int M, int d, float eps, uint16_t* y,
-                          hipStream_t s);
+                          uint16_t* y_lo, hipStream_t s);
 // rotary embedding of q and k, key row and transposed value column into the caches
+struct KvPlanes {
+  uint16_t *q, *q_lo, *kc, *kc_lo, *vt, *vt_lo;
+};
 hipError_t launch_rope_kv(const float* qkv, const Window* win, const int32_t* n_dev, int n_host, int M, int H,
-                          int Hkv, int hd, const float2* rope, uint16_t* q, uint16_t* kc, uint16_t* vt, int cap,
-                          hipStream_t s);
+                          int Hkv, int hd, const float2* rope, const KvPlanes& o, int cap, hipStream_t s);
 hipError_t launch_f32_to_bf16(const float* src, uint16_t* dst, size_t n, hipStream_t s);
 
 }  // namespace sjd

@@ -15,7 +15,10 @@
 //    partials are summed in a fixed order by the last one to arrive
 //    (deterministic, no float atomics);
 //  - the next k-step's loads are issued before the current step's MFMAs.
-// Epilogues: store fp32, add into fp32 (residual), SwiGLU -> bf16.
+// Activations arrive as two bf16 planes (hi + lo, about 16 significant
+// bits): the weights are exact bf16, so two MFMAs per tile recover an
+// fp32-class product at no HBM cost (the MFMA units are otherwise idle).
+// Epilogues: store fp32, add into fp32 (residual), SwiGLU -> hi / lo planes.
 #include "device.h"
 #include "forward.h"
 
@@ -23,11 +26,12 @@ namespace sjd {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kGB = 256;
 constexpr int kGWaves = kGB / kWave;
 
-SJD_DEV bf16x8 as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
+SJD_DEV bf16x8 as_bf16x8(const u32x4& u) { return __builtin_bit_cast(bf16x8, u); }
 
 template <int MT, int NT>
 struct GemmSmem {
@@ -55,8 +59,12 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
                      : (r < g.n1 ? g.W1 + (size_t)(r - g.n0) * K : g.W2 + (size_t)(r - g.n1) * K);
   }
   const uint16_t* ap[MT];
+  const uint16_t* alp[MT];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) ap[mt] = g.A + (size_t)(mt * 32 + r32) * K;
+  for (int mt = 0; mt < MT; ++mt) {
+    ap[mt] = g.A + (size_t)(mt * 32 + r32) * K;
+    alp[mt] = g.A_lo + (size_t)(mt * 32 + r32) * K;
+  }
 
   const int T = K / 64;
   const int parts = g.S * kGWaves;
@@ -72,34 +80,41 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mt][t][r] = 0.0f;
 
-  uint4 wb[NT][4], ab[MT][4];
-  auto load = [&](int st, uint4 (&w)[NT][4], uint4 (&a)[MT][4]) {
+  u32x4 wb[NT][4], ab[MT][4], alb[MT][4];
+  auto load = [&](int st, u32x4 (&w)[NT][4], u32x4 (&a)[MT][4], u32x4 (&al)[MT][4]) {
     const int koff = st * 64 + half * 32;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      const uint4* p = (const uint4*)(wp[t] + koff);
+      const u32x4* p = (const u32x4*)(wp[t] + koff);
 #pragma unroll
       for (int i = 0; i < 4; ++i) w[t][i] = __builtin_nontemporal_load(p + i);
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const uint4* p = (const uint4*)(ap[mt] + koff);
+      const u32x4* p = (const u32x4*)(ap[mt] + koff);
+      const u32x4* pl = (const u32x4*)(alp[mt] + koff);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[mt][i] = p[i];
+      for (int i = 0; i < 4; ++i) {
+        a[mt][i] = p[i];
+        al[mt][i] = pl[i];
+      }
     }
   };
-  if (st0 < st1) load(st0, wb, ab);
+  if (st0 < st1) load(st0, wb, ab, alb);
   for (int st = st0; st < st1; ++st) {
-    uint4 wn[NT][4], an[MT][4];
-    if (st + 1 < st1) load(st + 1, wn, an);
+    u32x4 wn[NT][4], an[MT][4], aln[MT][4];
+    if (st + 1 < st1) load(st + 1, wn, an, aln);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
+        for (int t = 0; t < NT; ++t) {
           acc[mt][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ab[mt][i]), as_bf16x8(wb[t][i]),
                                                                acc[mt][t], 0, 0, 0);
+          acc[mt][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(alb[mt][i]), as_bf16x8(wb[t][i]),
+                                                               acc[mt][t], 0, 0, 0);
+        }
     if (st + 1 < st1) {
 #pragma unroll
       for (int t = 0; t < NT; ++t)
@@ -108,7 +123,10 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) ab[mt][i] = an[mt][i];
+        for (int i = 0; i < 4; ++i) {
+          ab[mt][i] = an[mt][i];
+          alb[mt][i] = aln[mt][i];
+        }
     }
   }
 
@@ -180,9 +198,15 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
     } else {
       const float gt = v[q][0], up = v[q][1];
       const float h = gt / (1.0f + expf(-gt)) * up;
-      g.outb[(size_t)m * g.ldo + n] = f32_to_bf16(h);
+      split_bf16(h, g.outb[(size_t)m * g.ldo + n], g.outb_lo[(size_t)m * g.ldo + n]);
     }
   }
+}
+
+size_t gemm_ws_floats(int N, int S, int M, int mode) {
+  const int MT = M > 32 ? 2 : 1;
+  const int NT = mode == kGemmSwiGLU ? 2 : 1;
+  return S > 1 ? (size_t)(N / 32) * S * NT * MT * 16 * kWave : 0;
 }
 
 int gemm_splits(int N, int K, int target_wgs) {

@@ -1,0 +1,148 @@
+// Step bookkeeping kernels: window layout from the device state, prefill
+// windows, state initialisation, KV commit (moving an accepted sibling's
+// key/value row) and the state update after verification. Everything stays
+// in device memory; the host only enqueues.
+//
+// Window layout (the paper fixes L verified positions per forward, Sec. 3.3,
+// and K candidates at each of the first D positions after a rejection,
+// Sec. 4.1): slot 0 holds the pending token (last committed, not yet cached)
+// at position n; slot i, 1 <= i < n_s, holds spine draft i-1 at n + i;
+// slot n_s + d(K-1) + k-2 holds sibling k of depth d at n + 1 + d and sees
+// slots 0..d and itself. A missing sibling slot is fed token vis_lo.
+#include "device.h"
+#include "forward.h"
+#include "step.h"
+
+namespace sjd {
+
+__global__ void k_build_window(const DevState* st, Window* w, int L, int K, int vis_lo) {
+  const int a = threadIdx.x;
+  if (a >= L) return;
+  const int n = st->n, n_s = st->n_s;
+  int tok, pos;
+  uint64_t anc;
+  if (a < n_s) {
+    tok = a == 0 ? st->pending : st->spine[a - 1];
+    pos = n + a;
+    anc = a == 63 ? ~0ull : ((1ull << (a + 1)) - 1ull);
+  } else {
+    const int t = a - n_s, d = t / (K - 1), k = t % (K - 1);
+    const int y = st->sib[d * (K - 1) + k];
+    tok = y >= 0 ? y : vis_lo;
+    pos = n + 1 + d;
+    anc = ((1ull << (d + 1)) - 1ull) | (1ull << a);
+  }
+  w->tok[a] = tok;
+  w->pos[a] = pos;
+  w->anc[a] = anc;
+}
+
+__global__ void k_build_prefill(const int32_t* prompt, int start, int M, Window* w) {
+  const int a = threadIdx.x;
+  if (a >= M) return;
+  w->tok[a] = prompt[start + a];
+  w->pos[a] = start + a;
+  w->anc[a] = a == 63 ? ~0ull : ((1ull << (a + 1)) - 1ull);
+}
+
+// Placeholders of the first window: uniform over the support (stream tag 6,
+// trial 0, step word 0xFFFFFFFF, row = window index), the row end token at
+// forced positions; no draft distributions, no siblings.
+__global__ void k_state_init(DevState* st, const int32_t* prompt, int n_p, int L, int V, int vis_lo, int eol,
+                             int row_len, uint64_t seed) {
+  const int i = threadIdx.x;
+  if (i == 0) {
+    st->n = n_p - 1;
+    st->pending = prompt[n_p - 1];
+    st->n_s = L;
+    st->D_in = 0;
+    st->n_q = 0;
+    st->g0 = 0;
+    st->q_off = 0;
+    st->pad = 0;
+    for (int t = 0; t < 8; ++t) st->meta[t] = 0;
+  }
+  if (i < 64) {
+    st->sib[i] = -1;
+    st->tok[i] = -1;
+    int t = -1;
+    if (i < L) {
+      const bool forced = row_len > 0 && (i % (row_len + 1)) == row_len;
+      if (forced) {
+        t = eol;
+      } else {
+        const Stream is(seed, kTagInit, 0, (uint32_t)i, 0u, 0xFFFFFFFFu);
+        t = vis_lo + (int)(((uint64_t)is.word(0) * (uint64_t)V) >> 32);
+      }
+    }
+    st->spine[i] = t;
+  }
+}
+
+// Accepted sibling (meta[5] = k >= 2 at first rejected row r): its key row
+// and value column move from cache row n + n_s + r(K-1) + k-2 to n + r + 1.
+// grid (layers, Hkv), block hd
+__global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int cap, int K) {
+  const int acc_k = st->meta[5];
+  if (acc_k < 2) return;
+  const int r = st->meta[1];
+  const int src = st->n + st->n_s + r * (K - 1) + (acc_k - 2);
+  const int dst = st->n + r + 1;
+  const int l = blockIdx.x, kh = blockIdx.y, i = threadIdx.x;
+  const size_t layer = (size_t)l * Hkv * cap * hd;
+  const size_t ko = layer + (size_t)kh * cap * hd;
+  c.kc[ko + (size_t)dst * hd + i] = c.kc[ko + (size_t)src * hd + i];
+  c.kc_lo[ko + (size_t)dst * hd + i] = c.kc_lo[ko + (size_t)src * hd + i];
+  const size_t vo = layer + (size_t)kh * hd * cap + (size_t)i * cap;
+  c.vt[vo + dst] = c.vt[vo + src];
+  c.vt_lo[vo + dst] = c.vt_lo[vo + src];
+}
+
+__global__ void k_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L) {
+  __shared__ int32_t sm[8];
+  const int i = threadIdx.x;
+  if (i < 8) sm[i] = st->meta[i];
+  __syncthreads();
+  const int n_c = sm[0];
+  const int n_new = st->n + (n_c > 0 ? n_c : 0);
+  if (out_tok && i < L) out_tok[i] = st->tok[i];
+  if (out_next && i < L) out_next[i] = st->spine[i];
+  if (out_meta && i < 8) out_meta[i] = i == 7 ? n_new : sm[i];
+  __syncthreads();
+  if (i == 0 && n_c > 0) {
+    st->pending = st->tok[n_c - 1];
+    st->n = n_new;
+    st->n_s = sm[3];
+    st->D_in = sm[2];
+    st->n_q = sm[4];
+    st->g0 = sm[6];
+    st->q_off = n_c;
+    st->meta[7] = n_new;
+  }
+}
+
+hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, hipStream_t s) {
+  hipLaunchKernelGGL(k_build_window, dim3(1), dim3(64), 0, s, st, w, L, K, vis_lo);
+  return hipGetLastError();
+}
+hipError_t launch_build_prefill(const int32_t* prompt, int start, int M, Window* w, hipStream_t s) {
+  hipLaunchKernelGGL(k_build_prefill, dim3(1), dim3(64), 0, s, prompt, start, M, w);
+  return hipGetLastError();
+}
+hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, int L, int V, int vis_lo, int eol,
+                             int row_len, uint64_t seed, hipStream_t s) {
+  hipLaunchKernelGGL(k_state_init, dim3(1), dim3(64), 0, s, st, prompt, n_p, L, V, vis_lo, eol, row_len, seed);
+  return hipGetLastError();
+}
+hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K,
+                          hipStream_t s) {
+  hipLaunchKernelGGL(k_kv_move, dim3(layers, Hkv), dim3(hd), 0, s, st, c, Hkv, hd, cap, K);
+  return hipGetLastError();
+}
+hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(k_state_update, dim3(1), dim3(64), 0, s, st, out_meta, out_tok, out_next, L);
+  return hipGetLastError();
+}
+
+}  // namespace sjd

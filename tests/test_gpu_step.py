@@ -1,0 +1,111 @@
+"""The full SJD-PAC step on the GPU (window forward + verification + KV
+commit, through the C ABI):
+- step invariants (committed counts, cache growth, valid tokens, row ends);
+- greedy decoding (top_k = 1) reaches the Jacobi fixed point, so the tokens
+  of a window engine equal those of a one-slot (plain autoregressive) engine
+  on the same weights (Sec. 3.3);
+- the acceptance statistics of GPU generations agree with the oracle's
+  generations on the same model (mean committed tokens per step).
+"""
+import numpy as np
+import pytest
+import torch
+
+from model_util import make_engine, setup, weights_device, weights_numpy
+from synth_inputs import model_config
+
+pytestmark = pytest.mark.gpu
+
+
+def generate(eng, cfg, prompt, *, seed, n_gen, top_k, T=1.0, max_steps=10_000):
+    meta = torch.zeros(8, dtype=torch.int32, device="cuda")
+    tok = torch.zeros(cfg["L"], dtype=torch.int32, device="cuda")
+    eng.prefill(prompt.cuda(), seed)
+    out, ncs, ns = [], [], []
+    step = 0
+    while len(out) < n_gen and step < max_steps:
+        eng.step(T, top_k, seed, step, out_meta=meta, out_tok=tok)
+        m = meta.cpu().numpy()
+        t = tok.cpu().numpy()
+        n_c = int(m[0])
+        assert 1 <= n_c <= cfg["L"], m
+        assert (t[:n_c] >= 0).all()
+        out.extend(t[:n_c].tolist())
+        ncs.append(n_c)
+        ns.append(int(m[7]))
+        step += 1
+    return out[:n_gen], ncs, ns
+
+
+def test_step_invariants_tiny():
+    cfg = model_config("tiny")
+    w, prompt = setup(cfg)
+    eng = make_engine(cfg, weights_device(w))
+    toks, ncs, ns = generate(eng, cfg, prompt, seed=3, n_gen=200, top_k=0)
+    eng.close()
+    assert len(toks) == 200
+    assert all(0 <= t < cfg["V"] for t in toks)
+    # cache rows grow by exactly the committed count
+    n0 = cfg["n_prompt"] - 1
+    assert ns == list(np.cumsum(ncs) + n0)
+    print("tiny: mean n_c", np.mean(ncs), "steps", len(ncs))
+
+
+def test_step_row_ends_and_vis_range():
+    cfg = model_config("8b", n_layers=1, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn_dim=512,
+                       row_len=5, n_prompt=8, n_gen=60)
+    w, prompt = setup(cfg)
+    eng = make_engine(cfg, weights_device(w))
+    toks, ncs, _ = generate(eng, cfg, prompt, seed=9, n_gen=60, top_k=50)
+    eng.close()
+    for g, t in enumerate(toks):
+        if g % 6 == 5:
+            assert t == cfg["eol_id"]
+        else:
+            assert cfg["vis_lo"] <= t < cfg["vis_lo"] + cfg["V"]
+
+
+@pytest.mark.parametrize("K,D,flags", [(4, 3, 3), (2, 2, 1), (1, 0, 0)])
+def test_greedy_window_equals_autoregressive(K, D, flags):
+    base = model_config("tiny", K=K, D=D, flags=flags)
+    w, prompt = setup(base, wseed=21, pseed=22)
+    wd = weights_device(w)
+    eng = make_engine(base, wd)
+    win, ncs, _ = generate(eng, base, prompt, seed=1, n_gen=96, top_k=1)
+    eng.close()
+    ar_cfg = model_config("tiny", L=1, K=1, D=0)
+    eng = make_engine(ar_cfg, wd)
+    ar, ar_ncs, _ = generate(eng, ar_cfg, prompt, seed=1, n_gen=96, top_k=1)
+    eng.close()
+    assert set(ar_ncs) == {1}
+    assert win == ar
+    assert np.mean(ncs) > 1.0  # the window actually ran ahead
+
+
+def test_acceptance_statistics_match_oracle(orc):
+    """Mean committed tokens per step of GPU and oracle generations of the
+    tiny model (same weights, different seeds of the same law); the logits
+    differ by the bf16 rounding of the GPU path, far below the sampling noise."""
+    cfg = model_config("tiny", n_gen=128)
+    w, prompt = setup(cfg, wseed=31, pseed=32)
+    eng = make_engine(cfg, weights_device(w))
+    gpu = []
+    for s in range(12):
+        _, ncs, _ = generate(eng, cfg, prompt, seed=100 + s, n_gen=128, top_k=0)
+        gpu += ncs
+    eng.close()
+    wn = weights_numpy(w)
+    m = orc.Model(cfg, wn, max_seq=cfg["max_seq"])
+    ocfg = orc.ModelCfg(cfg["n_layers"], cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"],
+                        cfg["ffn_dim"], cfg["vocab_size"], cfg["vis_lo"], cfg["V"], cfg["max_seq"], 1e-5, 1e4)
+    orc_nc = []
+    for s in range(12):
+        g = orc.gen_cfg(L=cfg["L"], V=cfg["V"], K=cfg["K"], D=cfg["D"], top_k=0, seed=200 + s,
+                        n_prompt=cfg["n_prompt"], n_gen=128, mcfg=ocfg, weights=m.w)
+        _, steps, hist = orc.generate(g, prompt.numpy().astype(np.int32))
+        orc_nc += sum(([i] * int(c) for i, c in enumerate(hist)), [])
+    m.close()
+    a, b = np.array(gpu, float), np.array(orc_nc, float)
+    se = np.sqrt(a.var() / a.size + b.var() / b.size)
+    print(f"mean n_c gpu {a.mean():.3f} ({a.size} steps) oracle {b.mean():.3f} ({b.size} steps) se {se:.3f}")
+    assert abs(a.mean() - b.mean()) < 4 * se + 0.02
