@@ -96,10 +96,11 @@ SJD_API const char* sjd_status_str(int status);
 typedef struct {
   int32_t B;          /* trials (independent windows), >= 1                      */
   int32_t L;          /* rows per window, 1..64                                   */
-  int32_t V;          /* logits per row, >= 1, multiple of 4                       */
+  int32_t V;          /* logits per row, 4..65536, multiple of 4                   */
   int32_t K;          /* candidates per tree depth, 1..8                          */
   int32_t D;          /* maximum tree depth, >= 0, K * D <= L                     */
-  int32_t top_k;      /* >= 0                                                     */
+  int32_t top_k;      /* >= 0; the kept set (top_k, or V when top_k is 0 or >= V)
+                         may hold at most 2048 tokens (SJD_ENOTSUP otherwise)    */
   float temperature;  /* > 0                                                      */
   uint32_t flags;     /* SJD_AC | SJD_PD                                          */
   uint64_t seed;
@@ -159,8 +160,10 @@ typedef struct {
   int32_t weights_f32;   /* 1: weights are fp32, 0: bf16                                */
 } sjd_config;
 
-/* Borrowed device pointers, row-major [out][in] (a Linear layer's layout),
- * bf16 or fp32 as configured; they must outlive the context.
+/* Device pointers, row-major [out][in] (a Linear layer's layout), bf16 or
+ * fp32 as configured. sjd_init copies them into library memory (matrices
+ * repacked into the GEMM tile layout, fp32 rounded to bf16), so the caller
+ * may release them once sjd_init returns.
  * h_layer is a HOST array of 9 * n_layers device pointers, per layer:
  * attn_norm[d], wq[H*hd][d], wk[Hkv*hd][d], wv[Hkv*hd][d], wo[d][H*hd],
  * ffn_norm[d], wg[F][d], wu[F][d], wd[d][F]. */
@@ -173,7 +176,8 @@ typedef struct {
 
 typedef struct sjd_ctx sjd_ctx;
 
-/* Allocates the KV cache and work buffers on the current device. */
+/* Allocates the weight copies, the KV cache and the work buffers on the
+ * current device; synchronises `stream` before returning. */
 SJD_API int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* stream, sjd_ctx** out);
 
 /* Starts a generation: writes the keys/values of d_prompt[0 .. n-2], makes

@@ -207,7 +207,7 @@ __global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
     acc += wo[((size_t)s * 32 + slot) * HD + dim] * f;
     ls += wml[s * 64 + slot * 2 + 1] * f;
   }
-  const size_t oo = (size_t)slot * a.H * HD + (size_t)h * HD + dim;
+  const size_t oo = (size_t)slot * a.ldo + (size_t)h * HD + dim;
   split_bf16(acc / ls, a.out[oo], a.out_lo[oo]);
 }
 

@@ -59,6 +59,15 @@ extern "C" const char* sjd_status_str(int s) {
 }
 
 namespace sjd {
+// The row kernel keeps one logits row in registers (V <= 65536) and the kept
+// (top-k) tokens in LDS (at most kVerifyMaxK of them unless V is that small).
+int check_verify_limits(int V, int top_k) {
+  if (V > kVerifyMaxV) return SJD_ENOTSUP;
+  const int k = (top_k <= 0 || top_k >= V) ? V : top_k;
+  if (k > kVerifyMaxK) return SJD_ENOTSUP;
+  return SJD_OK;
+}
+
 int check_verify_params(const sjd_verify_params* p) {
   if (!p) return SJD_EINVAL;
   if (p->B < 1 || p->B > 65535 || p->L < 1 || p->L > 64 || p->V < 4 || (p->V & 3) || p->V > (1 << 22))
@@ -66,7 +75,7 @@ int check_verify_params(const sjd_verify_params* p) {
   if (p->K < 1 || p->K > 8 || p->D < 0 || (long)p->K * p->D > p->L) return SJD_EINVAL;
   if (p->top_k < 0 || !(p->temperature > 0.0f)) return SJD_EINVAL;
   if (p->flags & ~(SJD_AC | SJD_PD)) return SJD_EINVAL;
-  return SJD_OK;
+  return check_verify_limits(p->V, p->top_k);
 }
 }  // namespace sjd
 

@@ -24,10 +24,13 @@ struct Ctx {
   int cap = 0;      // KV rows
   int cap_pad = 0;  // row stride of the caches (multiple of the attention chunk)
   int Mpad = 32;
+  // library-owned weights: embedding and norm gains as bf16 rows, matrices
+  // in the GEMM tile layout; lw[l] = {attn_norm, wqkv, -, -, wo, ffn_norm, wg, wu, wd}
   const uint16_t* embed = nullptr;
   const uint16_t* fnorm = nullptr;
   const uint16_t* head = nullptr;
   std::vector<std::array<const uint16_t*, 9>> lw;
+  int ld_d = 0, ld_q = 0, ld_f = 0;  // padded row strides of the activation planes
   std::vector<void*> owned;
   // activations entering MFMAs are hi / lo bf16 plane pairs
   float* x = nullptr;
@@ -43,8 +46,7 @@ struct Ctx {
   float* attn_o = nullptr;
   float* attn_ml = nullptr;
   int nsplit_max = 0;
-  float* gws = nullptr;
-  int* gcnt = nullptr;
+  float* rpart = nullptr;  // split-K partial planes of the O / down projections
   sjd::DevState* st = nullptr;
   sjd::Window* win = nullptr;
   int32_t* rec = nullptr;
@@ -79,7 +81,7 @@ int check_config(const sjd_config* c) {
   if (c->vocab_size < 1 || c->V < 32 || c->V % 32 || c->vis_lo < 0 || c->vis_lo + c->V > c->vocab_size)
     return SJD_EINVAL;
   if (c->L < 1 || c->L > 64 || c->K < 1 || c->K > 8 || c->D < 0 || (long)c->K * c->D > c->L) return SJD_EINVAL;
-  if (c->L > 32) return SJD_ENOTSUP;
+  if (c->L > 32 || c->V > 65536) return SJD_ENOTSUP;
   if (c->max_seq < c->L + 2) return SJD_EINVAL;
   if (c->flags & ~(SJD_AC | SJD_PD)) return SJD_EINVAL;
   if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
@@ -101,41 +103,46 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, hipS
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv;
   HIPTRY(sjd::launch_embed(x.embed, x.win, M, d, x.x, s));
+  const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d;
+  int pend = 0;  // partial planes of the last residual projection not yet added into x
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& w = x.lw[l];
     const size_t lofs = (size_t)l * Hkv * x.cap_pad * hd;
     sjd::KvPlanes kv{x.q, x.q_lo, x.kc + lofs, x.kc_lo + lofs, x.vt + lofs, x.vt_lo + lofs};
-    HIPTRY(sjd::launch_rmsnorm(x.x, w[0], M, d, c.rms_eps, x.xn, x.xn_lo, s));
+    HIPTRY(sjd::launch_rmsnorm(x.x, x.rpart, pend, rplane, w[0], M, d, c.rms_eps, x.xn, x.xn_lo, x.ld_d, s));
     sjd::GemmArgs g{};
-    g.A = x.xn; g.A_lo = x.xn_lo; g.M = M; g.W0 = w[1]; g.W1 = w[2]; g.W2 = w[3]; g.n0 = Nq; g.n1 = Nq + Nkv;
-    g.N = Nqkv; g.K = d; g.S = x.S_qkv; g.ws = x.gws; g.cnt = x.gcnt; g.out = x.qkv; g.ldo = Nqkv;
+    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W0 = w[1]; g.N = Nqkv; g.K = d; g.S = x.S_qkv;
+    g.out = x.qkv; g.plane = qplane; g.ldo = Nqkv;
     HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
-    HIPTRY(sjd::launch_rope_kv(x.qkv, x.win, n_dev, n_host, M, H, Hkv, hd, x.rope, kv, x.cap_pad, s));
+    HIPTRY(sjd::launch_rope_kv(x.qkv, x.S_qkv, qplane, x.win, n_dev, n_host, M, H, Hkv, hd, x.rope, kv, x.cap_pad,
+                               s));
     sjd::AttnArgs a{};
     a.q = x.q; a.q_lo = x.q_lo; a.kc = kv.kc; a.kc_lo = kv.kc_lo; a.vt = kv.vt; a.vt_lo = kv.vt_lo; a.win = x.win;
     a.n_dev = n_dev; a.n_host = n_host; a.M = M; a.H = H; a.Hkv = Hkv; a.cap = x.cap_pad;
     a.scale = (float)(1.4426950408889634 / std::sqrt((double)hd));
     a.ws_o = x.attn_o; a.ws_ml = x.attn_ml; a.nsplit_max = x.nsplit_max; a.out = x.att; a.out_lo = x.att_lo;
+    a.ldo = x.ld_q;
     HIPTRY(sjd::launch_attention(a, hd, s));
     g = sjd::GemmArgs{};
-    g.A = x.att; g.A_lo = x.att_lo; g.M = M; g.W0 = w[4]; g.n0 = d; g.n1 = d; g.N = d; g.K = Nq; g.S = x.S_o;
-    g.ws = x.gws; g.cnt = x.gcnt; g.out = x.x; g.ldo = d;
-    HIPTRY(sjd::launch_gemm(g, sjd::kGemmAdd, s));
-    HIPTRY(sjd::launch_rmsnorm(x.x, w[5], M, d, c.rms_eps, x.xn, x.xn_lo, s));
+    g.A = x.att; g.A_lo = x.att_lo; g.lda = x.ld_q; g.M = M; g.W0 = w[4]; g.N = d; g.K = Nq; g.S = x.S_o;
+    g.out = x.rpart; g.plane = rplane; g.ldo = d;
+    HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
+    HIPTRY(sjd::launch_rmsnorm(x.x, x.rpart, x.S_o, rplane, w[5], M, d, c.rms_eps, x.xn, x.xn_lo, x.ld_d, s));
     g = sjd::GemmArgs{};
-    g.A = x.xn; g.A_lo = x.xn_lo; g.M = M; g.W0 = w[6]; g.W1 = w[7]; g.n0 = F; g.n1 = F; g.N = F; g.K = d;
-    g.S = x.S_gu; g.ws = x.gws; g.cnt = x.gcnt; g.outb = x.hbuf; g.outb_lo = x.hbuf_lo; g.ldo = F;
+    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W0 = w[6]; g.W1 = w[7]; g.N = F; g.K = d; g.S = 1;
+    g.outb = x.hbuf; g.outb_lo = x.hbuf_lo; g.ldo = x.ld_f;
     HIPTRY(sjd::launch_gemm(g, sjd::kGemmSwiGLU, s));
     g = sjd::GemmArgs{};
-    g.A = x.hbuf; g.A_lo = x.hbuf_lo; g.M = M; g.W0 = w[8]; g.n0 = d; g.n1 = d; g.N = d; g.K = F; g.S = x.S_dn;
-    g.ws = x.gws; g.cnt = x.gcnt; g.out = x.x; g.ldo = d;
-    HIPTRY(sjd::launch_gemm(g, sjd::kGemmAdd, s));
+    g.A = x.hbuf; g.A_lo = x.hbuf_lo; g.lda = x.ld_f; g.M = M; g.W0 = w[8]; g.N = d; g.K = F; g.S = x.S_dn;
+    g.out = x.rpart; g.plane = rplane; g.ldo = d;
+    HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
+    pend = x.S_dn;
   }
   if (logits) {
-    HIPTRY(sjd::launch_rmsnorm(x.x, x.fnorm, M, d, c.rms_eps, x.xn, x.xn_lo, s));
+    HIPTRY(sjd::launch_rmsnorm(x.x, x.rpart, pend, rplane, x.fnorm, M, d, c.rms_eps, x.xn, x.xn_lo, x.ld_d, s));
     sjd::GemmArgs g{};
-    g.A = x.xn; g.A_lo = x.xn_lo; g.M = M; g.W0 = x.head + (size_t)c.vis_lo * d; g.n0 = c.V; g.n1 = c.V;
-    g.N = c.V; g.K = d; g.S = x.S_head; g.ws = x.gws; g.cnt = x.gcnt; g.out = logits; g.ldo = c.V;
+    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W0 = x.head; g.N = c.V; g.K = d; g.S = 1;
+    g.out = logits; g.plane = 0; g.ldo = c.V;
     HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
   }
   return SJD_OK;
@@ -193,38 +200,73 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   x.cap_pad = ((c.max_seq + sjd::kAttnChunk - 1) / sjd::kAttnChunk) * sjd::kAttnChunk;
   x.nsplit_max = x.cap_pad / sjd::kAttnChunk;
 
-  // weights: borrowed bf16 pointers, or bf16 copies of fp32 weights
-  auto weight = [&](const void* p, size_t count, const uint16_t** dst) -> int {
-    if (!c.weights_f32) {
-      *dst = (const uint16_t*)p;
-      return SJD_OK;
-    }
+  // weights: copied into library memory; matrices repacked into the GEMM
+  // tile layout (bf16), fp32 inputs rounded to nearest even
+  const int f32 = c.weights_f32 ? 1 : 0;
+  auto copy_rows = [&](const void* p, size_t count, const uint16_t** dst) -> int {
     uint16_t* b = nullptr;
     int rc = dalloc(x, &b, count);
     if (rc != SJD_OK) return rc;
-    if (sjd::launch_f32_to_bf16((const float*)p, b, count, s) != hipSuccess) return SJD_EHIP;
+    if (f32) {
+      if (sjd::launch_f32_to_bf16((const float*)p, b, count, s) != hipSuccess) return SJD_EHIP;
+    } else if (hipMemcpyAsync(b, p, count * 2, hipMemcpyDeviceToDevice, s) != hipSuccess) {
+      return SJD_EHIP;
+    }
     *dst = b;
     return SJD_OK;
   };
-  int rc = weight(w->d_embed, (size_t)c.vocab_size * d, &x.embed);
-  if (rc == SJD_OK) rc = weight(w->d_final_norm, d, &x.fnorm);
-  if (rc == SJD_OK) rc = weight(w->d_lm_head, (size_t)c.vocab_size * d, &x.head);
+  // tiles of rows [row0, row0 + N) of src ([*][K]) appended at dst + off
+  auto tile = [&](const void* p, size_t row0, int N, int K, uint16_t* dst) -> int {
+    return sjd::launch_tile_weights(p, f32, row0, N, K, dst, s) == hipSuccess ? SJD_OK : SJD_EHIP;
+  };
+  int rc = copy_rows(w->d_embed, (size_t)c.vocab_size * d, &x.embed);
+  if (rc == SJD_OK) rc = copy_rows(w->d_final_norm, d, &x.fnorm);
+  if (rc == SJD_OK) {
+    uint16_t* hp = nullptr;
+    rc = dalloc(x, &hp, (size_t)c.V * d);
+    if (rc == SJD_OK) rc = tile(w->d_lm_head, (size_t)c.vis_lo, c.V, d, hp);
+    x.head = hp;
+  }
   x.lw.resize(c.n_layers);
-  const size_t sizes[9] = {(size_t)d, (size_t)Nq * d, (size_t)Nkv * d, (size_t)Nkv * d, (size_t)d * Nq,
-                           (size_t)d, (size_t)F * d, (size_t)F * d, (size_t)d * F};
-  for (int l = 0; l < c.n_layers && rc == SJD_OK; ++l)
-    for (int i = 0; i < 9 && rc == SJD_OK; ++i) rc = weight(w->h_layer[9 * l + i], sizes[i], &x.lw[l][i]);
+  for (int l = 0; l < c.n_layers && rc == SJD_OK; ++l) {
+    const void* const* lp = w->h_layer + 9 * l;
+    auto& o = x.lw[l];
+    rc = copy_rows(lp[0], d, &o[0]);
+    if (rc == SJD_OK) rc = copy_rows(lp[5], d, &o[5]);
+    uint16_t *qkv = nullptr, *wo = nullptr, *wg = nullptr, *wu = nullptr, *wd = nullptr;
+    const size_t tq = (size_t)Nq * d, tkv = (size_t)Nkv * d;
+    if (rc == SJD_OK) rc = dalloc(x, &qkv, tq + 2 * tkv);
+    if (rc == SJD_OK) rc = tile(lp[1], 0, Nq, d, qkv);
+    if (rc == SJD_OK) rc = tile(lp[2], 0, Nkv, d, qkv + tq);
+    if (rc == SJD_OK) rc = tile(lp[3], 0, Nkv, d, qkv + tq + tkv);
+    if (rc == SJD_OK) rc = dalloc(x, &wo, (size_t)d * Nq);
+    if (rc == SJD_OK) rc = tile(lp[4], 0, d, Nq, wo);
+    if (rc == SJD_OK) rc = dalloc(x, &wg, (size_t)F * d);
+    if (rc == SJD_OK) rc = tile(lp[6], 0, F, d, wg);
+    if (rc == SJD_OK) rc = dalloc(x, &wu, (size_t)F * d);
+    if (rc == SJD_OK) rc = tile(lp[7], 0, F, d, wu);
+    if (rc == SJD_OK) rc = dalloc(x, &wd, (size_t)d * F);
+    if (rc == SJD_OK) rc = tile(lp[8], 0, d, F, wd);
+    o[1] = qkv; o[2] = nullptr; o[3] = nullptr; o[4] = wo; o[6] = wg; o[7] = wu; o[8] = wd;
+  }
   if (rc != SJD_OK) return fail(rc);
+  // the caller may release its weights once sjd_init returns
+  if (hipStreamSynchronize(s) != hipSuccess) return fail(SJD_EHIP);
 
   // work buffers
   const int Mp = x.Mpad;
   const size_t kv = (size_t)c.n_layers * Hkv * x.cap_pad * hd;
-  const size_t xnsz = (size_t)Mp * (d > F ? d : F);
+  // activation rows padded by 64 elements so that the 32 rows a wave reads per
+  // k-step spread over memory channels
+  x.ld_d = d + 64;
+  x.ld_q = Nq + 64;
+  x.ld_f = F + 64;
+  const size_t xnsz = (size_t)Mp * x.ld_d;
   if ((rc = dalloc(x, &x.x, (size_t)Mp * d)) || (rc = dalloc(x, &x.xn, xnsz)) || (rc = dalloc(x, &x.xn_lo, xnsz)) ||
-      (rc = dalloc(x, &x.qkv, (size_t)Mp * (Nq + 2 * Nkv))) || (rc = dalloc(x, &x.q, (size_t)Mp * Nq)) ||
-      (rc = dalloc(x, &x.q_lo, (size_t)Mp * Nq)) || (rc = dalloc(x, &x.att, (size_t)Mp * Nq)) ||
-      (rc = dalloc(x, &x.att_lo, (size_t)Mp * Nq)) || (rc = dalloc(x, &x.hbuf, (size_t)Mp * F)) ||
-      (rc = dalloc(x, &x.hbuf_lo, (size_t)Mp * F)) || (rc = dalloc(x, &x.kc, kv)) || (rc = dalloc(x, &x.kc_lo, kv)) ||
+      (rc = dalloc(x, &x.q, (size_t)Mp * Nq)) ||
+      (rc = dalloc(x, &x.q_lo, (size_t)Mp * Nq)) || (rc = dalloc(x, &x.att, (size_t)Mp * x.ld_q)) ||
+      (rc = dalloc(x, &x.att_lo, (size_t)Mp * x.ld_q)) || (rc = dalloc(x, &x.hbuf, (size_t)Mp * x.ld_f)) ||
+      (rc = dalloc(x, &x.hbuf_lo, (size_t)Mp * x.ld_f)) || (rc = dalloc(x, &x.kc, kv)) || (rc = dalloc(x, &x.kc_lo, kv)) ||
       (rc = dalloc(x, &x.vt, kv)) || (rc = dalloc(x, &x.vt_lo, kv)) ||
       (rc = dalloc(x, &x.rope, (size_t)x.cap_pad * (hd / 2))) ||
       (rc = dalloc(x, &x.logits[0], (size_t)c.L * c.V)) || (rc = dalloc(x, &x.logits[1], (size_t)c.L * c.V)) ||
@@ -243,31 +285,26 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   const int target = 2 * ncu;
   x.S_qkv = sjd::gemm_splits(Nq + 2 * Nkv, d, target);
   x.S_o = sjd::gemm_splits(d, Nq, target);
-  x.S_gu = sjd::gemm_splits(F, d, target);
+  x.S_gu = 1;
   x.S_dn = sjd::gemm_splits(d, F, target);
-  x.S_head = sjd::gemm_splits(c.V, d, target);
-  size_t ws = 0, w1;
-  w1 = sjd::gemm_ws_floats(Nq + 2 * Nkv, x.S_qkv, Mp, sjd::kGemmStore); ws = ws > w1 ? ws : w1;
-  w1 = sjd::gemm_ws_floats(d, x.S_o, Mp, sjd::kGemmAdd); ws = ws > w1 ? ws : w1;
-  w1 = sjd::gemm_ws_floats(F, x.S_gu, Mp, sjd::kGemmSwiGLU); ws = ws > w1 ? ws : w1;
-  w1 = sjd::gemm_ws_floats(d, x.S_dn, Mp, sjd::kGemmAdd); ws = ws > w1 ? ws : w1;
-  w1 = sjd::gemm_ws_floats(c.V, x.S_head, Mp, sjd::kGemmStore); ws = ws > w1 ? ws : w1;
-  int maxN = Nq + 2 * Nkv;
-  if (F > maxN) maxN = F;
-  if (c.V > maxN) maxN = c.V;
-  if ((rc = dalloc(x, &x.gws, ws)) || (rc = dalloc(x, &x.gcnt, (size_t)maxN / 32))) return fail(rc);
+  x.S_head = 1;
+  const int sr = x.S_o > x.S_dn ? x.S_o : x.S_dn;
+  if ((rc = dalloc(x, &x.qkv, (size_t)x.S_qkv * Mp * (Nq + 2 * Nkv))) ||
+      (rc = dalloc(x, &x.rpart, (size_t)sr * Mp * d)))
+    return fail(rc);
   // zero the caches (rows past the fill are read, masked, by the attention
   // tiles) and the activation pad rows
   void* zero[] = {x.kc, x.kc_lo, x.vt, x.vt_lo};
-  bool ok = hipMemsetAsync(x.gcnt, 0, sizeof(int) * (maxN / 32), s) == hipSuccess &&
-            hipMemsetAsync(x.st, 0, sizeof(sjd::DevState), s) == hipSuccess;
+  bool ok = hipMemsetAsync(x.st, 0, sizeof(sjd::DevState), s) == hipSuccess;
   for (void* p : zero) ok = ok && hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess;
   void* zero2[] = {x.xn, x.xn_lo};
   for (void* p : zero2) ok = ok && hipMemsetAsync(p, 0, xnsz * 2, s) == hipSuccess;
-  void* zero3[] = {x.att, x.att_lo, x.q, x.q_lo};
-  for (void* p : zero3) ok = ok && hipMemsetAsync(p, 0, (size_t)Mp * Nq * 2, s) == hipSuccess;
+  void* zero3[] = {x.att, x.att_lo};
+  for (void* p : zero3) ok = ok && hipMemsetAsync(p, 0, (size_t)Mp * x.ld_q * 2, s) == hipSuccess;
+  void* zero5[] = {x.q, x.q_lo};
+  for (void* p : zero5) ok = ok && hipMemsetAsync(p, 0, (size_t)Mp * Nq * 2, s) == hipSuccess;
   void* zero4[] = {x.hbuf, x.hbuf_lo};
-  for (void* p : zero4) ok = ok && hipMemsetAsync(p, 0, (size_t)Mp * F * 2, s) == hipSuccess;
+  for (void* p : zero4) ok = ok && hipMemsetAsync(p, 0, (size_t)Mp * x.ld_f * 2, s) == hipSuccess;
   if (!ok) return fail(SJD_EHIP);
   // rotary table in double precision: rope[pos][i] = (cos, sin)(pos * theta^(-2i/hd))
   {
@@ -311,9 +348,14 @@ extern "C" int sjd_prefill(sjd_ctx* h, const int32_t* d_prompt, int32_t n, uint6
   return SJD_OK;
 }
 
+namespace sjd {
+int check_verify_limits(int V, int top_k);
+}
+
 extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t seed, uint32_t step,
                         int32_t* d_out_meta, int32_t* d_out_tok, int32_t* d_out_next, void* stream) {
   if (!h || !(temperature > 0.0f) || top_k < 0) return SJD_EINVAL;
+  TRY(sjd::check_verify_limits(h->x.c.V, top_k));
   Ctx& x = h->x;
   if (!x.prefilled) return SJD_ESTATE;
   TRY(cache_check(x));

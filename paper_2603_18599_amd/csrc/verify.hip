@@ -1,20 +1,30 @@
 // Verification of SJD-PAC windows (Alg. 1 of the paper): per-row kernel and
 // per-trial finalize kernel.
 //
-// k_verify_rows: one 512-thread workgroup per (trial, row). The row's current
-// logits (and draft logits, when the row has a draft distribution) are read
-// once, coalesced as float4 per thread, and kept in registers for V <= 16384;
-// larger vocabularies re-read the row from L2 in each pass. On chip the
-// kernel finds the exact top-k threshold (radix select on order-preserving
-// keys), the softmax statistics, the accept test(s), the residual draw,
-// drafting candidates and the bonus draw, and writes one small record.
-//
+// k_verify_rows: one workgroup per (trial, row). The row is read once,
+// coalesced (float4 per thread), into registers; on chip the kernel finds
+// the exact top-k threshold, compacts the kept tokens into LDS in index
+// order, and then takes every decision on the compact list:
+//  - top-k threshold: one histogram over bins of the row's [min, max] range
+//    (well spread for real logits, so the LDS atomics rarely collide), then
+//    an exact (value desc, index asc) rank among the few entries of the
+//    threshold bin; a radix select over order-preserving keys is the
+//    fallback for degenerate rows (many equal values);
+//  - compaction: a bitmap of the kept set with per-word prefix popcounts
+//    gives each kept token its rank; that rank indexes the compact arrays
+//    and the random stream (four consecutive ranks share one Philox block);
+//  - the draft row (when the row has a draft distribution) is then read into
+//    the same registers; its own threshold and normaliser are found and its
+//    probabilities are scattered into the compact list;
+//  - accept tests, residual draws (Theorem 2's recursion for several
+//    candidates), drafting candidates and bonus draws run over the compact
+//    list only.
 // k_verify_finalize: one wave per trial. Finds the first rejected spine row,
 // the committed tokens, and assembles the next window.
 //
-// Arithmetic of every decision is fp32 with fp64 sums (the paper fixes no
-// precision); contraction into FMA is off in this file so the rounding of
-// each operation is the IEEE one.
+// Every decision is taken in fp32 with fp64 sums (the paper fixes no
+// precision); contraction into FMA is off in this file so each operation
+// rounds as IEEE specifies.
 #include "device.h"
 #include "verify.h"
 
@@ -22,85 +32,108 @@
 
 namespace sjd {
 
-constexpr int kVB = 512;            // threads per row workgroup
-constexpr int kVW = kVB / kWave;    // waves per row workgroup
 constexpr uint64_t kNoKey = ~0ull;
+constexpr int kKcap = kVerifyMaxK;   // kept tokens per row held on chip
+constexpr int kCandCap = 256;        // threshold-bin entries ranked exactly
+constexpr int kBins = 2048;
 
-struct VShared {
-  uint32_t hist[2048];
-  double red_d[kVW];
-  uint64_t red_u[kVW];
-  float red_f[kVW];
-  int red_i[kVW];
-  int bin, above;
+template <int BLOCK, int NC>
+struct VSh {
+  static constexpr int W = BLOCK / kWave;
+  static constexpr int NW = BLOCK * NC / 8;  // bitmap words (32 entries each)
+  uint32_t bm[NW];
+  int32_t pre[NW];
+  uint16_t sp_x[kKcap];
+  float sp_p[kKcap];
+  union {
+    float sp_q[kKcap];
+    uint32_t hist[kBins];
+  };
+  float cand_v[kCandCap];
+  int cand_x[kCandCap];
+  double red_d[W];
+  uint64_t red_u[W];
+  float red_f[2 * W];
+  int red_i[W];
+  float tau_v;
+  int tau_x, bin, above, ncand;
 };
 
 // ------------------------------------------------------------ block helpers
-SJD_DEV float block_max(float v, VShared& sh) {
-  v = wave_max(v);
+template <int W>
+SJD_DEV void block_maxmin(float& mx, float& mn, float* red) {
+  mx = wave_max(mx);
+  float t = -mn;
+  t = wave_max(t);
+  mn = -t;
   const int w = threadIdx.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) sh.red_f[w] = v;
   __syncthreads();
-  float r = sh.red_f[0];
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    red[w] = mx;
+    red[W + w] = mn;
+  }
+  __syncthreads();
+  mx = red[0];
+  mn = red[W];
 #pragma unroll
-  for (int i = 1; i < kVW; ++i) r = fmaxf(r, sh.red_f[i]);
+  for (int i = 1; i < W; ++i) {
+    mx = fmaxf(mx, red[i]);
+    mn = fminf(mn, red[W + i]);
+  }
   __syncthreads();
-  return r;
 }
-SJD_DEV double block_sum_d(double v, VShared& sh) {
+template <int W>
+SJD_DEV double block_sum_d(double v, double* red) {
   v = wave_sum_d(v);
   const int w = threadIdx.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) sh.red_d[w] = v;
+  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
   __syncthreads();
   double r = 0.0;
 #pragma unroll
-  for (int i = 0; i < kVW; ++i) r += sh.red_d[i];
+  for (int i = 0; i < W; ++i) r += red[i];
   __syncthreads();
   return r;
 }
-SJD_DEV uint64_t block_min_u64(uint64_t v, VShared& sh) {
+template <int W>
+SJD_DEV uint64_t block_min_u64(uint64_t v, uint64_t* red) {
   v = wave_min_u64(v);
   const int w = threadIdx.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) sh.red_u[w] = v;
+  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
   __syncthreads();
-  uint64_t r = sh.red_u[0];
+  uint64_t r = red[0];
 #pragma unroll
-  for (int i = 1; i < kVW; ++i) r = sh.red_u[i] < r ? sh.red_u[i] : r;
+  for (int i = 1; i < W; ++i) r = red[i] < r ? red[i] : r;
   __syncthreads();
   return r;
 }
 // exclusive prefix sum over the block (thread order)
-SJD_DEV int block_excl_scan(int v, VShared& sh) {
+template <int W>
+SJD_DEV int block_excl_scan(int v, int* red) {
   const int incl = wave_incl_scan(v);
   const int w = threadIdx.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == kWave - 1) sh.red_i[w] = incl;
+  if ((threadIdx.x & (kWave - 1)) == kWave - 1) red[w] = incl;
   __syncthreads();
   int base = 0;
-  for (int i = 0; i < w; ++i) base += sh.red_i[i];
+  for (int i = 0; i < w; ++i) base += red[i];
   __syncthreads();
   return base + incl - v;
 }
 
 SJD_DEV float comp(const float4& v, int e) { return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w; }
-SJD_DEV float& comp(float4& v, int e) { return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w; }
-
-SJD_DEV uint64_t pack_key(float key, int x) {
-  return ((uint64_t)__float_as_uint(key) << 32) | (uint32_t)x;
-}
+SJD_DEV uint32_t compu(const uint4& v, int e) { return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w; }
+SJD_DEV uint64_t pack_key(float key, int x) { return ((uint64_t)__float_as_uint(key) << 32) | (uint32_t)x; }
+// order-preserving key with -0 folded onto +0 (logits compare as floats)
+SJD_DEV uint32_t okey(float f) { return fkey(f + 0.0f); }
 
 // ---------------------------------------------------------- row statistics
 struct RowStats {
-  float m;        // largest logit
+  float m;       // largest logit
   float T;
-  uint32_t tau;   // key of the k-th largest logit
-  int itau;       // largest index taken among logits equal to tau
-  bool all;       // k >= V: every entry kept
-  double invZ;    // 1 / sum of weights
-  SJD_DEV bool in_set(float l, int x) const {
-    if (all) return true;
-    const uint32_t k = fkey(l);
-    return k > tau || (k == tau && x <= itau);
-  }
+  float tau_v;   // value of the k-th kept logit
+  int tau_x;     // its index: kept = l > tau_v or (l == tau_v and x <= tau_x)
+  bool all;      // every entry kept
+  double invZ;   // 1 / sum of kept weights
+  SJD_DEV bool in_set(float l, int x) const { return all || l > tau_v || (l == tau_v && x <= tau_x); }
   SJD_DEV float prob(float l, int x) const {
     if (!in_set(l, x)) return 0.0f;
     const float w = expf((l - m) / T);
@@ -108,81 +141,58 @@ struct RowStats {
   }
 };
 
-// Row data: NC > 0 keeps NC float4 chunks per thread in registers (chunk
-// c = tid + i * kVB holds entries 4c .. 4c+3); NC == 0 re-reads global memory.
-template <int NC>
-struct Row {
-  float4 v[NC];
-  int nchunk;
-  const float4* g;
-  SJD_DEV static constexpr int count(int) { return NC; }
-  SJD_DEV void load(const float* row, int V) {
-    g = (const float4*)row;
-    nchunk = V >> 2;
+// The row in registers: chunk c = tid + i * BLOCK holds entries 4c .. 4c+3.
+template <int BLOCK, int NC>
+SJD_DEV void load_row(float4 (&v)[NC], const float* row, int V) {
+  const float4* g = (const float4*)row;
+  const int nchunk = V >> 2;
 #pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = threadIdx.x + i * kVB;
-      v[i] = c < nchunk ? g[c] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-    }
+  for (int i = 0; i < NC; ++i) {
+    const int c = threadIdx.x + i * BLOCK;
+    v[i] = c < nchunk ? g[c] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
   }
-  SJD_DEV float4 get(int i) const { return v[i]; }
-};
-template <>
-struct Row<0> {
-  int nchunk;
-  const float4* g;
-  SJD_DEV int count(int) const { return (nchunk + kVB - 1) / kVB; }
-  SJD_DEV void load(const float* row, int V) {
-    g = (const float4*)row;
-    nchunk = V >> 2;
-  }
-  SJD_DEV float4 get(int i) const {
-    const int c = threadIdx.x + i * kVB;
-    return c < nchunk ? g[c] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-  }
-};
+}
 
-// Exact k-th largest under (value desc, index asc): radix select over the
-// order-preserving keys (11 + 11 + 10 bits), then, if the threshold value is
-// tied, over the indices of the tied entries (11 + 11 bits).
-template <int NC>
-SJD_DEV void topk_threshold(const Row<NC>& row, int V, int k, VShared& sh, RowStats& st) {
-  st.all = (k <= 0 || k >= V);
-  if (st.all) { st.tau = 0; st.itau = 0x7FFFFFFF; return; }
+// Radix select (fallback): k-th largest by (value desc, index asc) over
+// order-preserving keys (11 + 11 + 10 bits), then over the indices of the
+// entries tied at the threshold key (11 + 11 bits).
+template <int BLOCK, int NC>
+SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh, float& tau_v, int& tau_x) {
+  constexpr int W = BLOCK / kWave;
   const int tid = threadIdx.x;
-  const int cnt = row.count(V);
+  const int nchunk = V >> 2;
   uint32_t prefix = 0, pmask = 0;
-  int rem = k;
-  int last_bin = 0;
+  int rem = k, last_bin = 0;
   for (int pass = 0; pass < 3; ++pass) {
     const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
     const int nb = pass == 2 ? 1024 : 2048;
-    for (int b = tid; b < nb; b += kVB) sh.hist[b] = 0;
+    for (int b = tid; b < nb; b += BLOCK) sh.hist[b] = 0;
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < cnt; ++i) {
-      const int c = tid + i * kVB;
-      if (c < row.nchunk) {
-        const float4 v = row.get(i);
+    for (int i = 0; i < NC; ++i) {
+      const int c = tid + i * BLOCK;
+      if (c < nchunk) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const uint32_t key = fkey(comp(v, e));
+          const uint32_t key = okey(comp(v[i], e));
           if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & (uint32_t)(nb - 1)], 1u);
         }
       }
     }
     __syncthreads();
-    // bins in descending order: thread t owns reversed bins [t*per, t*per+per)
-    const int per = nb / kVB;
-    int cnts[4];
+    const int per = nb / BLOCK > 0 ? nb / BLOCK : 1;
     int s = 0;
-    for (int i = 0; i < per; ++i) {
-      cnts[i] = (int)sh.hist[nb - 1 - (tid * per + i)];
+    int cnts[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int bi = tid * per + i;
+      cnts[i] = (i < per && bi < nb) ? (int)sh.hist[nb - 1 - bi] : 0;
       s += cnts[i];
     }
-    int run = block_excl_scan(s, sh);
-    for (int i = 0; i < per; ++i) {
-      if (run < rem && run + cnts[i] >= rem) {
+    int run = block_excl_scan<W>(s, sh.red_i);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (i < per && run < rem && run + cnts[i] >= rem) {
         sh.bin = nb - 1 - (tid * per + i);
         sh.above = run;
       }
@@ -190,50 +200,52 @@ SJD_DEV void topk_threshold(const Row<NC>& row, int V, int k, VShared& sh, RowSt
     }
     __syncthreads();
     last_bin = sh.bin;
-    const int above = sh.above;
     prefix |= (uint32_t)last_bin << shift;
     pmask |= (uint32_t)(nb - 1) << shift;
-    rem -= above;
+    rem -= sh.above;
     __syncthreads();
   }
-  st.tau = prefix;
   const int eq = (int)sh.hist[last_bin];
   __syncthreads();
+  tau_v = 0.0f;
+  // value of the threshold key (any entry with that key)
+  {
+    const uint32_t u = (prefix & 0x80000000u) ? (prefix & 0x7FFFFFFFu) : ~prefix;
+    tau_v = __uint_as_float(u);
+  }
   if (rem >= eq) {
-    st.itau = 0x7FFFFFFF;
+    tau_x = 0x7FFFFFFF;
     return;
   }
-  // rem-th smallest index among entries whose key equals tau
   uint32_t ipre = 0, imask = 0;
   for (int pass = 0; pass < 2; ++pass) {
     const int shift = pass == 0 ? 11 : 0;
-    const int nb = 2048;
-    for (int b = tid; b < nb; b += kVB) sh.hist[b] = 0;
+    for (int b = tid; b < 2048; b += BLOCK) sh.hist[b] = 0;
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < cnt; ++i) {
-      const int c = tid + i * kVB;
-      if (c < row.nchunk) {
-        const float4 v = row.get(i);
+    for (int i = 0; i < NC; ++i) {
+      const int c = tid + i * BLOCK;
+      if (c < nchunk) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const uint32_t x = (uint32_t)(4 * c + e);
-          if (fkey(comp(v, e)) == prefix && (x & imask) == ipre)
-            atomicAdd(&sh.hist[(x >> shift) & 2047u], 1u);
+          if (okey(comp(v[i], e)) == prefix && (x & imask) == ipre) atomicAdd(&sh.hist[(x >> shift) & 2047u], 1u);
         }
       }
     }
     __syncthreads();
-    const int per = nb / kVB;
-    int cnts[4];
+    const int per = 2048 / BLOCK;
     int s = 0;
-    for (int i = 0; i < per; ++i) {
-      cnts[i] = (int)sh.hist[tid * per + i];
+    int cnts[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      cnts[i] = i < per ? (int)sh.hist[tid * per + i] : 0;
       s += cnts[i];
     }
-    int run = block_excl_scan(s, sh);
-    for (int i = 0; i < per; ++i) {
-      if (run < rem && run + cnts[i] >= rem) {
+    int run = block_excl_scan<W>(s, sh.red_i);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (i < per && run < rem && run + cnts[i] >= rem) {
         sh.bin = tid * per + i;
         sh.above = run;
       }
@@ -245,64 +257,190 @@ SJD_DEV void topk_threshold(const Row<NC>& row, int V, int k, VShared& sh, RowSt
     rem -= sh.above;
     __syncthreads();
   }
-  st.itau = (int)ipre;
+  tau_x = (int)ipre;
 }
 
-template <int NC>
-SJD_DEV void row_stats(Row<NC>& row, int V, int k, float T, VShared& sh, RowStats& st) {
+// Row statistics: max, exact top-k threshold, normaliser.
+template <int BLOCK, int NC>
+SJD_DEV void row_stats(const float4 (&v)[NC], int V, int top_k, float T, VSh<BLOCK, NC>& sh, RowStats& st) {
+  constexpr int W = BLOCK / kWave;
+  const int tid = threadIdx.x;
+  const int nchunk = V >> 2;
   st.T = T;
-  topk_threshold(row, V, k, sh, st);
-  const int cnt = row.count(V);
-  float mx = -INFINITY;
+  float mx = -INFINITY, mn = INFINITY;
 #pragma unroll
-  for (int i = 0; i < cnt; ++i) {
-    const float4 v = row.get(i);
-    mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+  for (int i = 0; i < NC; ++i) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float l = comp(v[i], e);
+      mx = fmaxf(mx, l);
+      if (l > -INFINITY) mn = fminf(mn, l);
+    }
   }
-  st.m = block_max(mx, sh);
+  block_maxmin<W>(mx, mn, sh.red_f);
+  st.m = mx;
+  const int k = (top_k <= 0 || top_k >= V) ? V : top_k;
+  st.all = (k >= V);
+  st.tau_v = -INFINITY;
+  st.tau_x = 0x7FFFFFFF;
+  if (!st.all) {
+    bool fast = (mx < INFINITY) && (mn < INFINITY) && (mx > mn);
+    const float scale = fast ? (float)kBins / (mx - mn) : 0.0f;
+    fast = fast && (scale < INFINITY) && (scale > 0.0f);
+    if (fast) {
+      for (int b = tid; b < kBins; b += BLOCK) sh.hist[b] = 0;
+      if (tid == 0) sh.ncand = 0;
+      __syncthreads();
+      auto binof = [&](float l) -> int {
+        if (!(l > mn)) return 0;
+        int b = (int)((l - mn) * scale);
+        return b < kBins - 1 ? b : kBins - 1;
+      };
+#pragma unroll
+      for (int i = 0; i < NC; ++i) {
+        const int c = tid + i * BLOCK;
+        if (c < nchunk) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) atomicAdd(&sh.hist[binof(comp(v[i], e))], 1u);
+        }
+      }
+      __syncthreads();
+      // bins from the top: thread t owns reversed bins [t*per, t*per+per)
+      constexpr int per = kBins / BLOCK;
+      int cnts[per];
+      int s = 0;
+#pragma unroll
+      for (int i = 0; i < per; ++i) {
+        cnts[i] = (int)sh.hist[kBins - 1 - (tid * per + i)];
+        s += cnts[i];
+      }
+      int run = block_excl_scan<W>(s, sh.red_i);
+#pragma unroll
+      for (int i = 0; i < per; ++i) {
+        if (run < k && run + cnts[i] >= k) {
+          sh.bin = kBins - 1 - (tid * per + i);
+          sh.above = run;
+        }
+        run += cnts[i];
+      }
+      __syncthreads();
+      const int bstar = sh.bin, rem = k - sh.above, c = (int)sh.hist[bstar];
+      if (c <= kCandCap) {
+#pragma unroll
+        for (int i = 0; i < NC; ++i) {
+          const int ch = tid + i * BLOCK;
+          if (ch < nchunk) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float l = comp(v[i], e);
+              if (binof(l) == bstar) {
+                const int p = atomicAdd(&sh.ncand, 1);
+                sh.cand_v[p] = l;
+                sh.cand_x[p] = 4 * ch + e;
+              }
+            }
+          }
+        }
+        __syncthreads();
+        for (int i = tid; i < c; i += BLOCK) {
+          const float vi = sh.cand_v[i];
+          const int xi = sh.cand_x[i];
+          int r = 0;
+          for (int j = 0; j < c; ++j) {
+            const float vj = sh.cand_v[j];
+            r += (vj > vi) || (vj == vi && sh.cand_x[j] < xi);
+          }
+          if (r == rem - 1) {
+            sh.tau_v = vi;
+            sh.tau_x = xi;
+          }
+        }
+        __syncthreads();
+        st.tau_v = sh.tau_v;
+        st.tau_x = sh.tau_x;
+        __syncthreads();
+      } else {
+        fast = false;
+      }
+    }
+    if (!fast) radix_topk<BLOCK, NC>(v, V, k, sh, st.tau_v, st.tau_x);
+  }
   double z = 0.0;
 #pragma unroll
-  for (int i = 0; i < cnt; ++i) {
-    const int c = threadIdx.x + i * kVB;
-    if (c < row.nchunk) {
-      const float4 v = row.get(i);
+  for (int i = 0; i < NC; ++i) {
+    const int c = tid + i * BLOCK;
+    if (c < nchunk) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float l = comp(v, e);
+        const float l = comp(v[i], e);
         if (st.in_set(l, 4 * c + e)) z += (double)expf((l - st.m) / T);
       }
     }
   }
-  st.invZ = 1.0 / block_sum_d(z, sh);
-  if constexpr (NC > 0) {
-    // keep probabilities instead of logits
+  st.invZ = 1.0 / block_sum_d<W>(z, sh.red_d);
+}
+
+// Bitmap of the kept set and its per-word prefix popcounts; returns the
+// number of kept entries.
+template <int BLOCK, int NC>
+SJD_DEV int build_rank(const float4 (&v)[NC], int V, const RowStats& st, VSh<BLOCK, NC>& sh) {
+  constexpr int W = BLOCK / kWave;
+  constexpr int NW = VSh<BLOCK, NC>::NW;
+  const int tid = threadIdx.x;
+  const int nchunk = V >> 2;
+  // word of chunk c is c >> 3: the eight chunks of a word belong to eight
+  // consecutive lanes, which OR their nibbles together
 #pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = threadIdx.x + i * kVB;
+  for (int i = 0; i < NC; ++i) {
+    const int c = tid + i * BLOCK;
+    uint32_t bits = 0;
+    if (c < nchunk) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) comp(row.v[i], e) = c < row.nchunk ? st.prob(comp(row.v[i], e), 4 * c + e) : 0.0f;
+      for (int e = 0; e < 4; ++e) bits |= (st.in_set(comp(v[i], e), 4 * c + e) ? 1u : 0u) << e;
     }
+    bits <<= 4 * (tid & 7);
+    bits |= __shfl_xor(bits, 1, kWave);
+    bits |= __shfl_xor(bits, 2, kWave);
+    bits |= __shfl_xor(bits, 4, kWave);
+    if ((tid & 7) == 0) sh.bm[(tid >> 3) + i * (BLOCK / 8)] = bits;
   }
+  __syncthreads();
+  constexpr int WPT = NW / BLOCK > 0 ? NW / BLOCK : 1;  // words per thread (contiguous)
+  int cnt[WPT];
+  int s = 0;
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int wi = tid * WPT + i;
+    cnt[i] = wi < NW ? __popc(sh.bm[wi]) : 0;
+    s += cnt[i];
+  }
+  int run = block_excl_scan<W>(s, sh.red_i);
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int wi = tid * WPT + i;
+    if (wi < NW) sh.pre[wi] = run;
+    run += cnt[i];
+  }
+  if (tid == BLOCK - 1) sh.ncand = run;
+  __syncthreads();
+  const int total = sh.ncand;
+  __syncthreads();
+  return total;
 }
 
-// probability of entry 4c+e given the chunk read from the row
-template <int NC>
-SJD_DEV float prob_of(const RowStats& st, const float4& v, int c, int e) {
-  if constexpr (NC > 0) return comp(v, e);
-  else return st.prob(comp(v, e), 4 * c + e);
-}
-
-// probability of one entry (any thread; reads global memory)
-SJD_DEV float prob_scalar(const RowStats& st, const float* row, int x) {
-  return st.prob(row[x], x);
+template <int BLOCK, int NC>
+SJD_DEV bool kept(const VSh<BLOCK, NC>& sh, int x) { return (sh.bm[x >> 5] >> (x & 31)) & 1u; }
+template <int BLOCK, int NC>
+SJD_DEV int rank_of(const VSh<BLOCK, NC>& sh, int x) {
+  return sh.pre[x >> 5] + __popc(sh.bm[x >> 5] & ((1u << (x & 31)) - 1u));
 }
 
 struct Stages {
-  int n;             // stages whose residual has been formed
+  int n;        // stages whose residual has been formed
   int cand[8];
-  float Nf[8];       // normaliser of p^(s)
-  float den[8];      // 1 - q mass of candidates rejected before stage s
-  // rho^(n+1)(y): the unnormalised residual after n rejected stages. Loops
+  float Nf[8];  // normaliser of p^(s)
+  float den[8]; // 1 - q mass of candidates rejected before stage s
+  // rho^(n+1)(y): the unnormalised residual after n rejected stages; loops
   // have fixed trip counts so every array index is a compile-time constant.
   SJD_DEV float rho(float py, float qy, int y) const {
     float r = py;
@@ -322,13 +460,40 @@ struct Stages {
   }
 };
 
+// Race over the compact list: argmin over kept entries with weight w(e) > 0
+// of Exp(1) / w, the exponential of entry e being stream element e.
+template <int BLOCK, int NC, class Wfn>
+SJD_DEV int race_compact(const VSh<BLOCK, NC>& shc, VSh<BLOCK, NC>& sh, int nk, const Stream& rs, Wfn wfn) {
+  constexpr int W = BLOCK / kWave;
+  uint64_t best = kNoKey;
+  for (int j = threadIdx.x; 4 * j < nk; j += BLOCK) {
+    const uint4 wd = rs.block((uint32_t)j);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int ent = 4 * j + e;
+      if (ent < nk) {
+        const float w = wfn(ent);
+        if (w > 0.0f) {
+          const uint64_t pk = pack_key(exp1(compu(wd, e)) / w, (int)shc.sp_x[ent]);
+          best = pk < best ? pk : best;
+        }
+      }
+    }
+  }
+  best = block_min_u64<W>(best, sh.red_u);
+  return best == kNoKey ? -1 : (int)(uint32_t)best;
+}
+
 // ------------------------------------------------------------ row kernel
-template <int NC>
-__global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
-  __shared__ VShared sh;
+template <int BLOCK, int NC>
+__global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
+  constexpr int W = BLOCK / kWave;
+  __shared__ VSh<BLOCK, NC> sh;
+  const int tid = threadIdx.x;
   const int j = blockIdx.x;
   const int b = blockIdx.y;
   const int L = a.L, V = a.V, K = a.K, Km1 = a.K - 1;
+  const int nchunk = V >> 2;
   const int32_t* meta = a.in_meta + 4 * (size_t)b;
   const int D_in = meta[0], n_q = meta[1];
   const long g0 = meta[2];
@@ -340,45 +505,65 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
   auto forced = [&](long g) -> bool { return a.row_len > 0 && g >= 0 && (g % (a.row_len + 1)) == a.row_len; };
 
   // ---- classify the row (uniform over the block)
-  bool spine = j < n_s;
+  const bool spine = j < n_s;
   bool is_forced = false, need_p = true, has_q = false;
   int sib_d = -1, sib_k = 0, sib_tok = -1;
   if (spine) {
     is_forced = forced(g0 + j);
     has_q = !is_forced && j < n_q;
+    if (is_forced) need_p = false;
   } else {
     sib_d = (j - n_s) / Km1;
     sib_k = (j - n_s) % Km1 + 2;
     sib_tok = a.sib ? a.sib[((size_t)b * a.D + sib_d) * Km1 + (sib_k - 2)] : -1;
     is_forced = forced(g0 + sib_d + 1);
-    if (sib_tok < 0 || forced(g0 + sib_d)) need_p = false;
-    else if (is_forced) need_p = false;
+    if (sib_tok < 0 || forced(g0 + sib_d) || is_forced) need_p = false;
   }
-  if (is_forced && spine) need_p = false;
   if (a.dbg_p) need_p = true;
 
   const float* cur_row = a.cur + ((size_t)b * L + j) * V;
-  Row<NC> P;
+  float4 v[NC];
   RowStats ps{};
+  int nk = 0;
   if (need_p) {
-    P.load(cur_row, V);
-    row_stats(P, V, a.top_k, a.T, sh, ps);
+    load_row<BLOCK, NC>(v, cur_row, V);
+    row_stats<BLOCK, NC>(v, V, a.top_k, a.T, sh, ps);
+    nk = build_rank<BLOCK, NC>(v, V, ps, sh);
+    // compact the kept entries (index order) with their probabilities
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = tid + i * BLOCK;
+      if (c < nchunk) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int x = 4 * c + e;
+          const float l = comp(v[i], e);
+          if (ps.in_set(l, x)) {
+            const int r = rank_of(sh, x);
+            sh.sp_x[r] = (uint16_t)x;
+            sh.sp_p[r] = ps.prob(l, x);
+          }
+        }
+      }
+    }
     if (a.dbg_p) {
       float4* dst = (float4*)(a.dbg_p + ((size_t)b * L + j) * V);
-      const int cnt = P.count(V);
 #pragma unroll
-      for (int i = 0; i < cnt; ++i) {
-        const int c = threadIdx.x + i * kVB;
-        if (c < P.nchunk) {
-          const float4 v = P.get(i);
+      for (int i = 0; i < NC; ++i) {
+        const int c = tid + i * BLOCK;
+        if (c < nchunk) {
           float4 o;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) comp(o, e) = prob_of<NC>(ps, v, c, e);
+          o.x = ps.prob(v[i].x, 4 * c);
+          o.y = ps.prob(v[i].y, 4 * c + 1);
+          o.z = ps.prob(v[i].z, 4 * c + 2);
+          o.w = ps.prob(v[i].w, 4 * c + 3);
           dst[c] = o;
         }
       }
     }
+    __syncthreads();
   }
+  auto prow = [&](int ent) -> float { return sh.sp_p[ent]; };
 
   // ---- sibling rows: bonus draw from the sibling's own output row
   if (!spine) {
@@ -389,29 +574,9 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
       tok = -1; stage = -1;
     } else {
       const Stream rs(a.seed, kTagBonus, 0, (uint32_t)j, (uint32_t)b, a.step);
-      uint64_t best = kNoKey;
-      const int cnt = P.count(V);
-#pragma unroll
-      for (int i = 0; i < cnt; ++i) {
-        const int c = threadIdx.x + i * kVB;
-        if (c < P.nchunk) {
-          const float4 v = P.get(i);
-          const uint4 w = rs.block((uint32_t)c);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float pw = prob_of<NC>(ps, v, c, e);
-            if (pw > 0.0f) {
-              const uint32_t wd = e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
-              const uint64_t pk = pack_key(exp1(wd) / pw, 4 * c + e);
-              best = pk < best ? pk : best;
-            }
-          }
-        }
-      }
-      best = block_min_u64(best, sh);
-      tok = best == kNoKey ? -1 : (int)(uint32_t)best;
+      tok = race_compact<BLOCK, NC>(sh, sh, nk, rs, prow);
     }
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
       rec[0] = tok; rec[1] = stage;
       for (int t = 0; t < 7; ++t) rec[2 + t] = -1;
       rec[9] = tok;
@@ -426,7 +591,7 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
 
   // ---- spine rows
   if (is_forced) {
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
       rec[0] = -1; rec[1] = -1;
       for (int t = 0; t < 7; ++t) rec[2 + t] = -1;
       rec[9] = -1;
@@ -471,23 +636,35 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
 
   int out_tok = -1, out_stage = 0;
   if (ncand > 0) {
+    // draft row: statistics, then its probabilities at the kept entries
     const size_t qrow = (size_t)b * a.draft_bstride + (size_t)((a.q_off ? a.q_off[b] : 0) + j) * V;
     const float* draft_row = a.draft + qrow;
-    Row<NC> Q;
     RowStats qs{};
-    Q.load(draft_row, V);
-    row_stats(Q, V, a.top_k, a.T, sh, qs);
+    load_row<BLOCK, NC>(v, draft_row, V);
+    row_stats<BLOCK, NC>(v, V, a.top_k, a.T, sh, qs);  // the histogram aliases sp_q: written after
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = tid + i * BLOCK;
+      if (c < nchunk) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int x = 4 * c + e;
+          if (kept(sh, x)) sh.sp_q[rank_of(sh, x)] = qs.prob(comp(v[i], e), x);
+        }
+      }
+    }
+    __syncthreads();
+    auto qrow_c = [&](int ent) -> float { return sh.sp_q[ent]; };
 
     float Qsum = 0.0f;
     float Nf = 1.0f;
-    bool done = false;
-    for (int k = 1; k <= ncand && !done; ++k) {
+    for (int k = 1; k <= ncand; ++k) {
       int x = stg.cand[0];
 #pragma unroll
       for (int t = 1; t < 8; ++t) x = (t == k - 1) ? stg.cand[t] : x;
       const float den = 1.0f - Qsum;
-      const float px = prob_scalar(ps, cur_row, x);
-      const float qx = prob_scalar(qs, draft_row, x);
+      const float px = kept(sh, x) ? sh.sp_p[rank_of(sh, x)] : 0.0f;
+      const float qx = qs.prob(draft_row[x], x);
       const float pk = stg.rho(px, qx, x) / Nf;
       const float qk = den > 0.0f ? qx / den : 0.0f;
       const Stream us(a.seed, kTagAcc, (uint32_t)(k - 1), (uint32_t)j, (uint32_t)b, a.step);
@@ -496,7 +673,6 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
       if (acc) {
         out_tok = x;
         out_stage = k;
-        done = true;
         break;
       }
       // residual of this stage
@@ -505,18 +681,9 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
         if (t == stg.n) { stg.Nf[t] = Nf; stg.den[t] = den; }
       stg.n += 1;
       double nd = 0.0;
-      const int cnt = P.count(V);
-#pragma unroll
-      for (int i = 0; i < cnt; ++i) {
-        const int c = threadIdx.x + i * kVB;
-        if (c < P.nchunk) {
-          const float4 pv = P.get(i), qv = Q.get(i);
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            nd += (double)stg.rho(prob_of<NC>(ps, pv, c, e), prob_of<NC>(qs, qv, c, e), 4 * c + e);
-        }
-      }
-      nd = block_sum_d(nd, sh);
+      for (int ent = tid; ent < nk; ent += BLOCK)
+        nd += (double)stg.rho(sh.sp_p[ent], sh.sp_q[ent], (int)sh.sp_x[ent]);
+      nd = block_sum_d<W>(nd, sh.red_d);
       Qsum = Qsum + qx;
       if (!(nd > 0.0)) {
         stg.n -= 1;  // no residual mass: draw from p^(k) itself
@@ -524,59 +691,20 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
       }
       Nf = (float)nd;
     }
-    // draw from the last residual (stage number = candidates tried)
     if (out_stage == 0) {
       // candidates tried: all of them unless the loop left through the
       // zero-mass exit, in which case that stage was tried too
       const int tried = stg.n + (stg.n < ncand ? 1 : 0);
       const Stream rs(a.seed, kTagRes, (uint32_t)tried, (uint32_t)j, (uint32_t)b, a.step);
-      uint64_t best = kNoKey;
-      const int cnt = P.count(V);
-#pragma unroll
-      for (int i = 0; i < cnt; ++i) {
-        const int c = threadIdx.x + i * kVB;
-        if (c < P.nchunk) {
-          const float4 pv = P.get(i), qv = Q.get(i);
-          const uint4 w = rs.block((uint32_t)c);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float r = stg.rho(prob_of<NC>(ps, pv, c, e), prob_of<NC>(qs, qv, c, e), 4 * c + e);
-            if (r > 0.0f) {
-              const uint32_t wd = e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
-              const uint64_t pk = pack_key(exp1(wd) / r, 4 * c + e);
-              best = pk < best ? pk : best;
-            }
-          }
-        }
-      }
-      best = block_min_u64(best, sh);
-      out_tok = best == kNoKey ? -1 : (int)(uint32_t)best;
+      out_tok = race_compact<BLOCK, NC>(sh, sh, nk, rs, [&](int ent) -> float {
+        return stg.rho(sh.sp_p[ent], qrow_c(ent), (int)sh.sp_x[ent]);
+      });
     }
   } else {
     // no draft distribution (appended placeholder) or no valid candidate:
     // a plain draw from p, counted as a rejection
     const Stream rs(a.seed, kTagRes, 0, (uint32_t)j, (uint32_t)b, a.step);
-    uint64_t best = kNoKey;
-    const int cnt = P.count(V);
-#pragma unroll
-    for (int i = 0; i < cnt; ++i) {
-      const int c = threadIdx.x + i * kVB;
-      if (c < P.nchunk) {
-        const float4 v = P.get(i);
-        const uint4 w = rs.block((uint32_t)c);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float pw = prob_of<NC>(ps, v, c, e);
-          if (pw > 0.0f) {
-            const uint32_t wd = e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
-            const uint64_t pk = pack_key(exp1(wd) / pw, 4 * c + e);
-            best = pk < best ? pk : best;
-          }
-        }
-      }
-    }
-    best = block_min_u64(best, sh);
-    out_tok = best == kNoKey ? -1 : (int)(uint32_t)best;
+    out_tok = race_compact<BLOCK, NC>(sh, sh, nk, rs, prow);
     out_stage = 0;
   }
 
@@ -584,27 +712,7 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
   int fresh = out_tok;
   if (!ac) {
     const Stream rs(a.seed, kTagFresh, 0, (uint32_t)j, (uint32_t)b, a.step);
-    uint64_t best = kNoKey;
-    const int cnt = P.count(V);
-#pragma unroll
-    for (int i = 0; i < cnt; ++i) {
-      const int c = threadIdx.x + i * kVB;
-      if (c < P.nchunk) {
-        const float4 v = P.get(i);
-        const uint4 w = rs.block((uint32_t)c);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float pw = prob_of<NC>(ps, v, c, e);
-          if (pw > 0.0f) {
-            const uint32_t wd = e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
-            const uint64_t pk = pack_key(exp1(wd) / pw, 4 * c + e);
-            best = pk < best ? pk : best;
-          }
-        }
-      }
-    }
-    best = block_min_u64(best, sh);
-    fresh = best == kNoKey ? -1 : (int)(uint32_t)best;
+    fresh = race_compact<BLOCK, NC>(sh, sh, nk, rs, prow);
   }
 
   // proactive drafting: K-1 draws without replacement from p, excluding the
@@ -616,21 +724,16 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
     uint64_t loc[7];
 #pragma unroll
     for (int t = 0; t < 7; ++t) loc[t] = kNoKey;
-    const int cnt = P.count(V);
+    for (int jj = tid; 4 * jj < nk; jj += BLOCK) {
+      const uint4 wd = rs.block((uint32_t)jj);
 #pragma unroll
-    for (int i = 0; i < cnt; ++i) {
-      const int c = threadIdx.x + i * kVB;
-      if (c < P.nchunk) {
-        const float4 v = P.get(i);
-        const uint4 w = rs.block((uint32_t)c);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int x = 4 * c + e;
-          const float pw = prob_of<NC>(ps, v, c, e);
+      for (int e = 0; e < 4; ++e) {
+        const int ent = 4 * jj + e;
+        if (ent < nk) {
+          const int x = (int)sh.sp_x[ent];
+          const float pw = sh.sp_p[ent];
           if (pw > 0.0f && x != excl) {
-            const uint32_t wd = e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
-            uint64_t pk = pack_key(exp1(wd) / pw, x);
-            // insert into the thread's ascending list of the Km1 smallest
+            uint64_t pk = pack_key(exp1(compu(wd, e)) / pw, x);
 #pragma unroll
             for (int t = 0; t < 7; ++t) {
               if (t < Km1 && pk < loc[t]) {
@@ -646,7 +749,7 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
 #pragma unroll
     for (int t = 0; t < 7; ++t) {
       if (t < Km1) {
-        const uint64_t best = block_min_u64(loc[0], sh);
+        const uint64_t best = block_min_u64<W>(loc[0], sh.red_u);
         if (best != kNoKey) {
           pds[t] = (int)(uint32_t)best;
           if (loc[0] == best) {
@@ -659,7 +762,7 @@ __global__ __launch_bounds__(kVB) void k_verify_rows(VerifyArgs a) {
     }
   }
 
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     rec[0] = out_tok;
     rec[1] = out_stage;
     for (int t = 0; t < 7; ++t) rec[2 + t] = pds[t];
@@ -772,14 +875,21 @@ __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, Finaliz
 }
 
 // ------------------------------------------------------------ launch
+int verify_block_for(int V) {
+  if (V <= 4096) return 256;
+  if (V <= 16384) return 256;
+  if (V <= 32768) return 512;
+  if (V <= 65536) return 1024;
+  return 0;
+}
+
 hipError_t launch_verify(const VerifyArgs& a, const FinalizeOut& o, hipStream_t s) {
   const dim3 grid(a.L, a.B);
-  const int nchunk = a.V / 4;
-  if (nchunk <= kVB) hipLaunchKernelGGL(k_verify_rows<1>, grid, dim3(kVB), 0, s, a);
-  else if (nchunk <= 2 * kVB) hipLaunchKernelGGL(k_verify_rows<2>, grid, dim3(kVB), 0, s, a);
-  else if (nchunk <= 4 * kVB) hipLaunchKernelGGL(k_verify_rows<4>, grid, dim3(kVB), 0, s, a);
-  else if (nchunk <= 8 * kVB) hipLaunchKernelGGL(k_verify_rows<8>, grid, dim3(kVB), 0, s, a);
-  else hipLaunchKernelGGL(k_verify_rows<0>, grid, dim3(kVB), 0, s, a);
+  if (a.V <= 4096) hipLaunchKernelGGL((k_verify_rows<256, 4>), grid, dim3(256), 0, s, a);
+  else if (a.V <= 16384) hipLaunchKernelGGL((k_verify_rows<256, 16>), grid, dim3(256), 0, s, a);
+  else if (a.V <= 32768) hipLaunchKernelGGL((k_verify_rows<512, 16>), grid, dim3(512), 0, s, a);
+  else if (a.V <= 65536) hipLaunchKernelGGL((k_verify_rows<1024, 16>), grid, dim3(1024), 0, s, a);
+  else return hipErrorInvalidValue;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_verify_finalize, dim3(a.B), dim3(kWave), 0, s, a, o);

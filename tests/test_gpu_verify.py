@@ -111,7 +111,8 @@ def test_verify_ties_in_logits(orc):
 
 
 def test_verify_small_shapes(orc):
-    for (B, L, V, top_k, K, D) in [(1, 1, 4, 0, 1, 0), (3, 1, 64, 1, 4, 0), (2, 5, 8, 3, 2, 2), (2, 64, 256, 17, 8, 8)]:
+    for (B, L, V, top_k, K, D) in [(1, 1, 4, 0, 1, 0), (3, 1, 64, 1, 4, 0), (2, 5, 8, 3, 2, 2), (2, 64, 256, 17, 8, 8),
+                                   (2, 3, 2048, 0, 2, 1), (2, 4, 20000, 2048, 4, 1), (1, 2, 40000, 1, 1, 0)]:
         inp = verify_inputs(B, L, V, top_k=top_k, seed=B * 100 + L, K=K, D=D)
         gpu, ref = run_both(orc, inp, K=K, D=D, top_k=top_k, seed=1)
         check(gpu, ref, K, D)
