@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="7b", choices=["7b", "8b", "mid", "tiny", "verify"])
     ap.add_argument("--no-verify", action="store_true", help="skip the verify workload section")
+    ap.add_argument("--context", default="mid", choices=["mid", "start"],
+                    help="mid: time the steps half-way through an image (prompt + n_gen/2 tokens cached); "
+                         "start: right after the prompt")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
     return ap.parse_args()
@@ -149,12 +152,15 @@ def bench_step(args):
     import torch
 
     from paper_2603_18599_amd.sjd import Engine, SjdError
-    from synth_inputs import model_config, model_weights, prompt_tokens
+    from synth_inputs import image_history, model_config, model_weights, prompt_tokens
 
     cfg = model_config(args.workload)
     seed = 11
     w = model_weights(cfg, 1, device="cuda")
-    prompt = prompt_tokens(cfg, 2).cuda()
+    prompt = prompt_tokens(cfg, 2)
+    if args.context == "mid":
+        prompt = torch.cat([prompt, image_history(cfg, cfg["n_gen"] // 2, 3)])
+    prompt = prompt.cuda()
     eng = Engine(cfg, w)
     stream = torch.cuda.current_stream()
     K, W = args.steps, args.warmup
@@ -205,7 +211,8 @@ def bench_step(args):
                                    f"{cfg['n_heads']}q/{cfg['n_kv_heads']}kv heads x {cfg['head_dim']}, "
                                    f"SwiGLU {cfg['ffn_dim']}, vocab {cfg['vocab_size']} (sampled {cfg['V']}), "
                                    f"L={cfg['L']} K={cfg['K']} D={cfg['D']}, top-{cfg['top_k']}, T=1, "
-                                   f"{cfg['n_prompt']}-token prompt, {cfg['n_gen']}-token image",
+                                   f"{cfg['n_prompt']}-token prompt, {cfg['n_gen']}-token image, "
+                                   f"steps timed from KV length {prompt.numel() - 1}",
                        "global_batch": 1, "seq_len": cfg["L"]},
                mean_accept_length=float(ncs.mean()), step_latency_ms=avg_ms,
                step_latency_p50_ms=float(np.percentile(step_ms, 50)),

@@ -3,17 +3,17 @@
 //
 // Layout choices (gfx950, wave64, v_mfma_f32_32x32x16_bf16):
 //  - scores are formed transposed, S^T = K . Q^T (rows = keys, columns =
-//    slots), so each lane owns one slot: the running max, sum and the output
-//    rescale of online softmax are lane-local (plus one exchange between the
-//    two lane halves);
-//  - the key rows fed to MFMA row i are key pi(i) (bits 2 and 3 of i
-//    swapped); then the score registers of a lane hold 16 keys in the order
-//    that O^T = V^T . P^T needs as its B operand, so P never leaves registers;
-//  - values are cached transposed ([kv head][dim][position]) so the V^T
-//    operand is one 16-byte load per lane;
-//  - a workgroup (4 waves x 64 keys) handles 256 keys of one head; the four
-//    waves merge in LDS and one partial (unnormalised output, max, sum) per
-//    workgroup is combined across chunks by a second kernel.
+//    slots), so each lane owns one slot: the max, sum and output scaling of
+//    the softmax are lane-local (plus one exchange between the two lane
+//    halves);
+//  - the key rows fed to MFMA row i are key swap23(i); then the score
+//    registers of a lane hold 16 keys in the order that O^T = V^T . P^T
+//    needs as its B operand, so P never leaves registers;
+//  - the caches are tiled in exactly these operand orders (forward.h), so
+//    every key or value load is one contiguous 1 KB per wave;
+//  - a workgroup handles kAttnChunk = 128 keys of one head, 32 per wave; the
+//    four waves merge in LDS and one partial (unnormalised output, max, sum)
+//    per workgroup is combined across chunks by a second kernel.
 // Scores use exp2 with the scale folded into log2(e) / sqrt(hd).
 // Precision: q, the cached keys and values, and P are each carried as a
 // pair of bf16 values (hi + lo); every product is formed as hi*hi + hi*lo +
@@ -28,11 +28,9 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 SJD_DEV bf16x8 to_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
 
-SJD_DEV int swap23(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
-
 template <int HD>
 struct AttnSmem {
-  float o[4][HD][32];
+  float o[4][32][HD + 1];  // [wave][slot][dim], padded against bank conflicts
   float m[4][32];
   float l[4][32];
 };
@@ -41,6 +39,7 @@ template <int HD>
 __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   constexpr int NQ = HD / 16;  // MFMAs per 32-key block for the scores
   constexpr int ND = HD / 32;  // 32-dim output blocks
+  static_assert(kAttnChunk == 4 * 32, "one 32-key block per wave");
   __shared__ AttnSmem<HD> sm;
   const int h = blockIdx.x, sp = blockIdx.y;
   const int n = a.n_dev ? *a.n_dev : a.n_host;
@@ -51,9 +50,22 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   const int kvh = h / (a.H / a.Hkv);
   const int slot = r32;
   const bool slot_ok = slot < M;
-  const uint64_t anc = slot_ok ? a.win->anc[slot] : 0ull;
+  const int kb = kbeg + wave * 32;  // this wave's key block
+  const bool has = kb < nk;
+  const size_t tofs = (size_t)kvh * a.cap * HD + (size_t)kb * HD + (size_t)lane * 8;
 
-  // Q^T operand, held for the whole kernel: dims half*HD/2 + 8t + e of this slot
+  // key tile first (the longest dependency), then q
+  uint4 kh[NQ], kl[NQ];
+  if (has) {
+    const uint4* kp = (const uint4*)(a.kc + tofs);
+    const uint4* kpl = (const uint4*)(a.kc_lo + tofs);
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+      kh[t] = kp[t * 64];
+      kl[t] = kpl[t * 64];
+    }
+  }
+  // Q^T operand: dims half*HD/2 + 8t + e of this slot
   uint4 qv[NQ], qvl[NQ];
   {
     const size_t qo = (size_t)slot * a.H * HD + (size_t)h * HD + half * (HD / 2);
@@ -65,66 +77,69 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
       qvl[t] = slot_ok ? qpl[t] : make_uint4(0, 0, 0, 0);
     }
   }
-  const size_t kofs = (size_t)kvh * a.cap * HD;
-  const size_t vofs = (size_t)kvh * HD * a.cap;
 
   f32x16 o[ND];
 #pragma unroll
   for (int d = 0; d < ND; ++d)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[d][r] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
-
-  const int wbeg = kbeg + wave * 64;
-  for (int kb = wbeg; kb < wbeg + 64 && kb < nk; kb += 32) {
-    // ---- scores
-    const int krow = kb + swap23(r32);
-    const size_t ko = kofs + (size_t)krow * HD + half * (HD / 2);
-    const uint4* kp = (const uint4*)(a.kc + ko);
-    const uint4* kpl = (const uint4*)(a.kc_lo + ko);
+  float m_w = -INFINITY, l_w = 0.0f;
+  if (has) {
     f32x16 s;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = 0.0f;
 #pragma unroll
     for (int t = 0; t < NQ; ++t) {
-      const bf16x8 kh = to_bf16x8(kp[t]), kl = to_bf16x8(kpl[t]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, to_bf16x8(qv[t]), s, 0, 0, 0);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, to_bf16x8(qvl[t]), s, 0, 0, 0);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kl, to_bf16x8(qv[t]), s, 0, 0, 0);
+      const bf16x8 khb = to_bf16x8(kh[t]), klb = to_bf16x8(kl[t]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, to_bf16x8(qv[t]), s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, to_bf16x8(qvl[t]), s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(klb, to_bf16x8(qv[t]), s, 0, 0, 0);
     }
-    // ---- mask, online softmax (register r = 8jj + e holds key kb + 16jj + 8half + e)
-    float mloc = -INFINITY;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = kb + 16 * (r >> 3) + 8 * half + (r & 7);
-      bool vis = slot_ok && key < nk;
-      if (vis && key >= n) vis = (anc >> (key - n)) & 1ull;
-      s[r] = vis ? s[r] * a.scale : -INFINITY;
-      mloc = fmaxf(mloc, s[r]);
-    }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, kWave));
-    const float m_new = fmaxf(m_run, mloc);
-    float lsum = 0.0f;
-    if (m_new == -INFINITY) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
-    } else {
-      const float alpha = exp2f(m_run - m_new);  // m_run = -inf -> 0
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = exp2f(s[r] - m_new);
-        lsum += s[r];
-      }
+    // value tile loads overlap the softmax
+    uint4 vh[ND][2], vl[ND][2];
+    {
+      const uint4* vp = (const uint4*)(a.vt + tofs);
+      const uint4* vpl = (const uint4*)(a.vt_lo + tofs);
 #pragma unroll
       for (int d = 0; d < ND; ++d)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
-      l_run *= alpha;
-      m_run = m_new;
+        for (int jj = 0; jj < 2; ++jj) {
+          vh[d][jj] = vp[(d * 2 + jj) * 64];
+          vl[d][jj] = vpl[(d * 2 + jj) * 64];
+        }
     }
-    lsum += __shfl_xor(lsum, 32, kWave);
-    l_run += lsum;
-    // ---- P^T operand (hi / lo bf16) and O^T += V^T . P^T
+    // mask (register r = 8jj + e holds key kb + 16jj + 8half + e): cached
+    // keys are visible to every slot, window keys by the ancestor mask
+    if (kb + 32 <= n) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = slot_ok ? s[r] * a.scale : -INFINITY;
+    } else {
+      const uint64_t anc = slot_ok ? a.win->anc[slot] : 0ull;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + 16 * (r >> 3) + 8 * half + (r & 7);
+        bool vis = slot_ok && key < nk;
+        if (vis && key >= n) vis = (anc >> (key - n)) & 1ull;
+        s[r] = vis ? s[r] * a.scale : -INFINITY;
+      }
+    }
+    float mloc = s[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[r]);
+    m_w = fmaxf(mloc, __shfl_xor(mloc, 32, kWave));
+    float lsum = 0.0f;
+    if (m_w != -INFINITY) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[r] = exp2f(s[r] - m_w);
+        lsum += s[r];
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+    }
+    l_w = lsum + __shfl_xor(lsum, 32, kWave);
+    // P^T operand (hi / lo bf16; P is finite, in [0, 1]) and O^T = V^T . P^T
     uint4 pb[2], pbl[2];
 #pragma unroll
     for (int jj = 0; jj < 2; ++jj) {
@@ -132,8 +147,8 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         uint16_t h0, l0, h1, l1;
-        split_bf16(s[8 * jj + 2 * e], h0, l0);
-        split_bf16(s[8 * jj + 2 * e + 1], h1, l1);
+        split_bf16_finite(s[8 * jj + 2 * e], h0, l0);
+        split_bf16_finite(s[8 * jj + 2 * e + 1], h1, l1);
         w[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
         wl[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
       }
@@ -141,50 +156,57 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
       pbl[jj] = make_uint4(wl[0], wl[1], wl[2], wl[3]);
     }
 #pragma unroll
-    for (int d = 0; d < ND; ++d) {
-      const size_t vo = vofs + (size_t)(d * 32 + r32) * a.cap + kb + 8 * half;
+    for (int d = 0; d < ND; ++d)
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj) {
-        const bf16x8 vh = to_bf16x8(*(const uint4*)(a.vt + vo + 16 * jj));
-        const bf16x8 vl = to_bf16x8(*(const uint4*)(a.vt_lo + vo + 16 * jj));
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vh, to_bf16x8(pb[jj]), o[d], 0, 0, 0);
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vh, to_bf16x8(pbl[jj]), o[d], 0, 0, 0);
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vl, to_bf16x8(pb[jj]), o[d], 0, 0, 0);
+        const bf16x8 vhb = to_bf16x8(vh[d][jj]), vlb = to_bf16x8(vl[d][jj]);
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vhb, to_bf16x8(pb[jj]), o[d], 0, 0, 0);
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vhb, to_bf16x8(pbl[jj]), o[d], 0, 0, 0);
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vlb, to_bf16x8(pb[jj]), o[d], 0, 0, 0);
       }
-    }
   }
 
-  // ---- merge the four waves
+  // ---- merge the four waves: output register r of block d holds dim
+  // d*32 + 8(r/4) + 4half + r%4 of this lane's slot
 #pragma unroll
   for (int d = 0; d < ND; ++d)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sm.o[wave][d * 32 + 8 * (r >> 2) + 4 * half + (r & 3)][slot] = o[d][r];
+    for (int r = 0; r < 16; ++r) sm.o[wave][slot][d * 32 + 8 * (r >> 2) + 4 * half + (r & 3)] = o[d][r];
   if (half == 0) {
-    sm.m[wave][slot] = m_run;
-    sm.l[wave][slot] = l_run;
+    sm.m[wave][slot] = m_w;
+    sm.l[wave][slot] = l_w;
   }
   __syncthreads();
-  float* wo = a.ws_o + ((size_t)h * a.nsplit_max + sp) * 32 * HD;
-  float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 32 * 2;
-  for (int idx = threadIdx.x; idx < 32 * HD; idx += 256) {
-    const int sl = idx / HD, dim = idx % HD;
-    float mx = -INFINITY;
+  // thread -> (slot, HD/8 consecutive dims)
+  constexpr int DPT = HD / 8;
+  const int sl = threadIdx.x >> 3, d0 = (threadIdx.x & 7) * DPT;
+  float mx = sm.m[0][sl];
 #pragma unroll
-    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, sm.m[w][sl]);
-    float acc = 0.0f, ls = 0.0f;
-    if (mx != -INFINITY) {
+  for (int w = 1; w < 4; ++w) mx = fmaxf(mx, sm.m[w][sl]);
+  float f[4], ls = 0.0f;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float f = exp2f(sm.m[w][sl] - mx);
-        acc += sm.o[w][dim][sl] * f;
-        ls += sm.l[w][sl] * f;
-      }
-    }
-    wo[(size_t)sl * HD + dim] = acc;
-    if (dim == 0) {
-      wml[sl * 2] = mx;
-      wml[sl * 2 + 1] = ls;
-    }
+  for (int w = 0; w < 4; ++w) {
+    f[w] = mx == -INFINITY ? 0.0f : exp2f(sm.m[w][sl] - mx);
+    ls += sm.l[w][sl] * f[w];
+  }
+  float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * 32 + sl) * HD + d0;
+#pragma unroll
+  for (int i = 0; i < DPT; i += 4) {
+    float4 v;
+    v.x = sm.o[0][sl][d0 + i] * f[0] + sm.o[1][sl][d0 + i] * f[1] + sm.o[2][sl][d0 + i] * f[2] +
+          sm.o[3][sl][d0 + i] * f[3];
+    v.y = sm.o[0][sl][d0 + i + 1] * f[0] + sm.o[1][sl][d0 + i + 1] * f[1] + sm.o[2][sl][d0 + i + 1] * f[2] +
+          sm.o[3][sl][d0 + i + 1] * f[3];
+    v.z = sm.o[0][sl][d0 + i + 2] * f[0] + sm.o[1][sl][d0 + i + 2] * f[1] + sm.o[2][sl][d0 + i + 2] * f[2] +
+          sm.o[3][sl][d0 + i + 2] * f[3];
+    v.w = sm.o[0][sl][d0 + i + 3] * f[0] + sm.o[1][sl][d0 + i + 3] * f[1] + sm.o[2][sl][d0 + i + 3] * f[2] +
+          sm.o[3][sl][d0 + i + 3] * f[3];
+    *(float4*)(wo + i) = v;
+  }
+  if ((threadIdx.x & 7) == 0) {
+    float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 32 * 2;
+    wml[sl * 2] = mx;
+    wml[sl * 2 + 1] = ls;
   }
 }
 

@@ -71,6 +71,15 @@ SJD_DEV void split_bf16(float v, uint16_t& hi, uint16_t& lo) {
   lo = f32_to_bf16(v - bf16_to_f32(hi));
 }
 
+// split_bf16 for values known to be finite (no NaN / Inf handling)
+SJD_DEV void split_bf16_finite(float v, uint16_t& hi, uint16_t& lo) {
+  const uint32_t u = __float_as_uint(v);
+  hi = (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+  const float r = v - __uint_as_float((uint32_t)hi << 16);
+  const uint32_t ur = __float_as_uint(r);
+  lo = (uint16_t)((ur + 0x7FFFu + ((ur >> 16) & 1u)) >> 16);
+}
+
 // ---------------------------------------------------------------- reductions
 SJD_DEV float wave_max(float v) {
 #pragma unroll

@@ -19,40 +19,52 @@ hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, floa
 }
 
 // x += sum_s part[s] (split-K partial planes of the projection that feeds
-// the residual, fixed order), then y = x / sqrt(mean(x^2) + eps) * g as hi /
-// lo bf16 planes; one workgroup per row
-__global__ __launch_bounds__(256) void k_rmsnorm(float* x, const float* part, int S, size_t plane,
-                                                 const uint16_t* g, int d, float eps, uint16_t* y, uint16_t* y_lo,
-                                                 int ldy) {
-  __shared__ float red[4];
-  const int m = blockIdx.x;
-  float* xr = x + (size_t)m * d;
-  float ss = 0.0f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float v = xr[i];
-    for (int s = 0; s < S; ++s) v += part[(size_t)s * plane + (size_t)m * d + i];
-    if (S > 0) xr[i] = v;
-    ss += v * v;
+// the residual, fixed order), y = x * g as hi / lo bf16 planes, ss[m][c] =
+// sum of x^2 over the 256 elements of chunk c. grid (chunks, M), one wave.
+__global__ __launch_bounds__(64) void k_resid_norm(float* x, const float* part, int S, size_t plane,
+                                                   const uint16_t* g, int d, uint16_t* y, uint16_t* y_lo, int ldy,
+                                                   float* ss) {
+  const int c = blockIdx.x, m = blockIdx.y, lane = threadIdx.x;
+  const int i0 = c * 256 + lane * 4;
+  float ssq = 0.0f;
+  if (i0 < d) {  // d is a multiple of 64, so a lane's 4 elements are all in range
+    float* xr = x + (size_t)m * d + i0;
+    float4 v = *(const float4*)xr;
+    const float* pr = part + (size_t)m * d + i0;
+#pragma unroll 4
+    for (int s = 0; s < S; ++s) {
+      const float4 p = *(const float4*)(pr + (size_t)s * plane);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+    if (S > 0) *(float4*)xr = v;
+    ssq = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    const ushort4 gg = *(const ushort4*)(g + i0);
+    ushort4 h, l;
+    split_bf16(v.x * bf16_to_f32(gg.x), h.x, l.x);
+    split_bf16(v.y * bf16_to_f32(gg.y), h.y, l.y);
+    split_bf16(v.z * bf16_to_f32(gg.z), h.z, l.z);
+    split_bf16(v.w * bf16_to_f32(gg.w), h.w, l.w);
+    *(ushort4*)(y + (size_t)m * ldy + i0) = h;
+    *(ushort4*)(y_lo + (size_t)m * ldy + i0) = l;
   }
-  ss = wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
-  const float inv = rsqrtf(tot / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256)
-    split_bf16(xr[i] * inv * bf16_to_f32(g[i]), y[(size_t)m * ldy + i], y_lo[(size_t)m * ldy + i]);
+  ssq = wave_sum(ssq);
+  if (lane == 0) ss[(size_t)m * gridDim.x + c] = ssq;
 }
 
-hipError_t launch_rmsnorm(float* x, const float* part, int S, size_t plane, const uint16_t* g, int M, int d,
-                          float eps, uint16_t* y, uint16_t* y_lo, int ldy, hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, s, x, part, S, plane, g, d, eps, y, y_lo, ldy);
+hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, const uint16_t* g, int M, int d,
+                             uint16_t* y, uint16_t* y_lo, int ldy, float* ss, hipStream_t s) {
+  hipLaunchKernelGGL(k_resid_norm, dim3(norm_chunks(d), M), dim3(64), 0, s, x, part, S, plane, g, d, y, y_lo, ldy,
+                     ss);
   return hipGetLastError();
 }
 
 // Rotate-half rotary embedding (pair i with i + hd/2 at angle pos * theta^(-2i/hd),
-// table rope[pos][i] = (cos, sin)), then: q -> q planes, k -> key cache row
-// n + m, v -> column n + m of the transposed value cache, all as hi / lo bf16
-// planes. grid (M, H + 2 * Hkv), block hd / 2
+// table rope[pos][i] = (cos, sin)), then: q -> q planes, k and v -> cache
+// position n + m (tiled layout), all as hi / lo bf16 planes.
+// grid (M, H + 2 * Hkv), block hd / 2
 __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,
                           int H, int Hkv, int hd, const float2* rope, KvPlanes o, int cap) {
   const int m = blockIdx.x, hh = blockIdx.y, i = threadIdx.x;
@@ -70,21 +82,21 @@ __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* w
     const float2 cs = rope[(size_t)win->pos[m] * half + i];
     const float o0 = a * cs.x - b * cs.y;
     const float o1 = a * cs.y + b * cs.x;
-    size_t off;
-    uint16_t *dh, *dl;
     if (hh < H) {
-      off = (size_t)m * H * hd + (size_t)hh * hd;
-      dh = o.q; dl = o.q_lo;
+      const size_t off = (size_t)m * H * hd + (size_t)hh * hd;
+      split_bf16(o0, o.q[off + i], o.q_lo[off + i]);
+      split_bf16(o1, o.q[off + i + half], o.q_lo[off + i + half]);
     } else {
-      off = ((size_t)(hh - H) * cap + row) * hd;
-      dh = o.kc; dl = o.kc_lo;
+      const size_t base = (size_t)(hh - H) * cap * hd;
+      const size_t k0 = base + kv_key_off(row, i, hd), k1 = base + kv_key_off(row, i + half, hd);
+      split_bf16(o0, o.kc[k0], o.kc_lo[k0]);
+      split_bf16(o1, o.kc[k1], o.kc_lo[k1]);
     }
-    split_bf16(o0, dh[off + i], dl[off + i]);
-    split_bf16(o1, dh[off + i + half], dl[off + i + half]);
   } else {
-    const size_t base = (size_t)(hh - H - Hkv) * hd * cap + row;
-    split_bf16(a, o.vt[base + (size_t)i * cap], o.vt_lo[base + (size_t)i * cap]);
-    split_bf16(b, o.vt[base + (size_t)(i + half) * cap], o.vt_lo[base + (size_t)(i + half) * cap]);
+    const size_t base = (size_t)(hh - H - Hkv) * cap * hd;
+    const size_t v0 = base + kv_val_off(row, i, hd), v1 = base + kv_val_off(row, i + half, hd);
+    split_bf16(a, o.vt[v0], o.vt_lo[v0]);
+    split_bf16(b, o.vt[v1], o.vt_lo[v1]);
   }
 }
 
@@ -93,6 +105,37 @@ hipError_t launch_rope_kv(const float* qkv, int S, size_t plane, const Window* w
                           hipStream_t s) {
   hipLaunchKernelGGL(k_rope_kv, dim3(M, H + 2 * Hkv), dim3(hd / 2), 0, s, qkv, S, plane, win, n_dev, n_host, H, Hkv,
                      hd, rope, o, cap);
+  return hipGetLastError();
+}
+
+// h[m][n] = silu(g) * u with g, u the plane sums of columns n and F + n.
+// grid (chunks of 256 columns, M), one wave, 4 columns per lane.
+__global__ __launch_bounds__(64) void k_swiglu(const float* P, int S, size_t plane, int F, uint16_t* h,
+                                               uint16_t* h_lo, int ldh) {
+  const int m = blockIdx.y;
+  const int n0 = blockIdx.x * 256 + threadIdx.x * 4;
+  if (n0 >= F) return;  // F is a multiple of 64: a lane's 4 columns are all in range
+  const float* pg = P + (size_t)m * 2 * F + n0;
+  float4 gs = make_float4(0.f, 0.f, 0.f, 0.f), us = gs;
+#pragma unroll 4
+  for (int s = 0; s < S; ++s) {
+    const float4 a = *(const float4*)(pg + (size_t)s * plane);
+    const float4 b = *(const float4*)(pg + (size_t)s * plane + F);
+    gs.x += a.x; gs.y += a.y; gs.z += a.z; gs.w += a.w;
+    us.x += b.x; us.y += b.y; us.z += b.z; us.w += b.w;
+  }
+  ushort4 hi, lo;
+  split_bf16(gs.x / (1.0f + expf(-gs.x)) * us.x, hi.x, lo.x);
+  split_bf16(gs.y / (1.0f + expf(-gs.y)) * us.y, hi.y, lo.y);
+  split_bf16(gs.z / (1.0f + expf(-gs.z)) * us.z, hi.z, lo.z);
+  split_bf16(gs.w / (1.0f + expf(-gs.w)) * us.w, hi.w, lo.w);
+  *(ushort4*)(h + (size_t)m * ldh + n0) = hi;
+  *(ushort4*)(h_lo + (size_t)m * ldh + n0) = lo;
+}
+
+hipError_t launch_swiglu(const float* P, int S, size_t plane, int M, int F, uint16_t* h, uint16_t* h_lo, int ldh,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(k_swiglu, dim3((F + 255) / 256, M), dim3(64), 0, s, P, S, plane, F, h, h_lo, ldh);
   return hipGetLastError();
 }
 

@@ -25,7 +25,7 @@ struct Ctx {
   int cap_pad = 0;  // row stride of the caches (multiple of the attention chunk)
   int Mpad = 32;
   // library-owned weights: embedding and norm gains as bf16 rows, matrices
-  // in the GEMM tile layout; lw[l] = {attn_norm, wqkv, -, -, wo, ffn_norm, wg, wu, wd}
+  // in the GEMM tile layout; lw[l] = {attn_norm, wqkv, -, -, wo, ffn_norm, wgu, -, wd}
   const uint16_t* embed = nullptr;
   const uint16_t* fnorm = nullptr;
   const uint16_t* head = nullptr;
@@ -47,6 +47,8 @@ struct Ctx {
   float* attn_ml = nullptr;
   int nsplit_max = 0;
   float* rpart = nullptr;  // split-K partial planes of the O / down projections
+  float* gup = nullptr;    // split-K partial planes of the gate / up projection [S_gu][Mpad][2F]
+  float* ss = nullptr;     // RMSNorm chunk sums of squares [Mpad][norm_chunks(d)]
   sjd::DevState* st = nullptr;
   sjd::Window* win = nullptr;
   int32_t* rec = nullptr;
@@ -103,17 +105,22 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, hipS
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv;
   HIPTRY(sjd::launch_embed(x.embed, x.win, M, d, x.x, s));
-  const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d;
+  const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d, guplane = (size_t)x.Mpad * 2 * F;
   int pend = 0;  // partial planes of the last residual projection not yet added into x
+  sjd::GemmArgs normed{};  // GEMM arguments that apply the RMSNorm row scale
+  normed.ss = x.ss;
+  normed.ss_n = sjd::norm_chunks(d);
+  normed.inv_d = 1.0f / (float)d;
+  normed.eps = c.rms_eps;
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& w = x.lw[l];
     const size_t lofs = (size_t)l * Hkv * x.cap_pad * hd;
     sjd::KvPlanes kv{x.q, x.q_lo, x.kc + lofs, x.kc_lo + lofs, x.vt + lofs, x.vt_lo + lofs};
-    HIPTRY(sjd::launch_rmsnorm(x.x, x.rpart, pend, rplane, w[0], M, d, c.rms_eps, x.xn, x.xn_lo, x.ld_d, s));
-    sjd::GemmArgs g{};
-    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W0 = w[1]; g.N = Nqkv; g.K = d; g.S = x.S_qkv;
+    HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, pend, rplane, w[0], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
+    sjd::GemmArgs g = normed;
+    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = w[1]; g.N = Nqkv; g.K = d; g.S = x.S_qkv;
     g.out = x.qkv; g.plane = qplane; g.ldo = Nqkv;
-    HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
+    HIPTRY(sjd::launch_gemm(g, s));
     HIPTRY(sjd::launch_rope_kv(x.qkv, x.S_qkv, qplane, x.win, n_dev, n_host, M, H, Hkv, hd, x.rope, kv, x.cap_pad,
                                s));
     sjd::AttnArgs a{};
@@ -124,26 +131,27 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, hipS
     a.ldo = x.ld_q;
     HIPTRY(sjd::launch_attention(a, hd, s));
     g = sjd::GemmArgs{};
-    g.A = x.att; g.A_lo = x.att_lo; g.lda = x.ld_q; g.M = M; g.W0 = w[4]; g.N = d; g.K = Nq; g.S = x.S_o;
+    g.A = x.att; g.A_lo = x.att_lo; g.lda = x.ld_q; g.M = M; g.W = w[4]; g.N = d; g.K = Nq; g.S = x.S_o;
     g.out = x.rpart; g.plane = rplane; g.ldo = d;
-    HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
-    HIPTRY(sjd::launch_rmsnorm(x.x, x.rpart, x.S_o, rplane, w[5], M, d, c.rms_eps, x.xn, x.xn_lo, x.ld_d, s));
+    HIPTRY(sjd::launch_gemm(g, s));
+    HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, x.S_o, rplane, w[5], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
+    g = normed;
+    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = w[6]; g.N = 2 * F; g.K = d; g.S = x.S_gu;
+    g.out = x.gup; g.plane = guplane; g.ldo = 2 * F;
+    HIPTRY(sjd::launch_gemm(g, s));
+    HIPTRY(sjd::launch_swiglu(x.gup, x.S_gu, guplane, M, F, x.hbuf, x.hbuf_lo, x.ld_f, s));
     g = sjd::GemmArgs{};
-    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W0 = w[6]; g.W1 = w[7]; g.N = F; g.K = d; g.S = 1;
-    g.outb = x.hbuf; g.outb_lo = x.hbuf_lo; g.ldo = x.ld_f;
-    HIPTRY(sjd::launch_gemm(g, sjd::kGemmSwiGLU, s));
-    g = sjd::GemmArgs{};
-    g.A = x.hbuf; g.A_lo = x.hbuf_lo; g.lda = x.ld_f; g.M = M; g.W0 = w[8]; g.N = d; g.K = F; g.S = x.S_dn;
+    g.A = x.hbuf; g.A_lo = x.hbuf_lo; g.lda = x.ld_f; g.M = M; g.W = w[8]; g.N = d; g.K = F; g.S = x.S_dn;
     g.out = x.rpart; g.plane = rplane; g.ldo = d;
-    HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
+    HIPTRY(sjd::launch_gemm(g, s));
     pend = x.S_dn;
   }
   if (logits) {
-    HIPTRY(sjd::launch_rmsnorm(x.x, x.rpart, pend, rplane, x.fnorm, M, d, c.rms_eps, x.xn, x.xn_lo, x.ld_d, s));
-    sjd::GemmArgs g{};
-    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W0 = x.head; g.N = c.V; g.K = d; g.S = 1;
+    HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, pend, rplane, x.fnorm, M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
+    sjd::GemmArgs g = normed;
+    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = x.head; g.N = c.V; g.K = d; g.S = 1;
     g.out = logits; g.plane = 0; g.ldo = c.V;
-    HIPTRY(sjd::launch_gemm(g, sjd::kGemmStore, s));
+    HIPTRY(sjd::launch_gemm(g, s));
   }
   return SJD_OK;
 }
@@ -233,7 +241,7 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     auto& o = x.lw[l];
     rc = copy_rows(lp[0], d, &o[0]);
     if (rc == SJD_OK) rc = copy_rows(lp[5], d, &o[5]);
-    uint16_t *qkv = nullptr, *wo = nullptr, *wg = nullptr, *wu = nullptr, *wd = nullptr;
+    uint16_t *qkv = nullptr, *wo = nullptr, *wgu = nullptr, *wd = nullptr;
     const size_t tq = (size_t)Nq * d, tkv = (size_t)Nkv * d;
     if (rc == SJD_OK) rc = dalloc(x, &qkv, tq + 2 * tkv);
     if (rc == SJD_OK) rc = tile(lp[1], 0, Nq, d, qkv);
@@ -241,13 +249,12 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     if (rc == SJD_OK) rc = tile(lp[3], 0, Nkv, d, qkv + tq + tkv);
     if (rc == SJD_OK) rc = dalloc(x, &wo, (size_t)d * Nq);
     if (rc == SJD_OK) rc = tile(lp[4], 0, d, Nq, wo);
-    if (rc == SJD_OK) rc = dalloc(x, &wg, (size_t)F * d);
-    if (rc == SJD_OK) rc = tile(lp[6], 0, F, d, wg);
-    if (rc == SJD_OK) rc = dalloc(x, &wu, (size_t)F * d);
-    if (rc == SJD_OK) rc = tile(lp[7], 0, F, d, wu);
+    if (rc == SJD_OK) rc = dalloc(x, &wgu, (size_t)2 * F * d);
+    if (rc == SJD_OK) rc = tile(lp[6], 0, F, d, wgu);
+    if (rc == SJD_OK) rc = tile(lp[7], 0, F, d, wgu + (size_t)F * d);
     if (rc == SJD_OK) rc = dalloc(x, &wd, (size_t)d * F);
     if (rc == SJD_OK) rc = tile(lp[8], 0, d, F, wd);
-    o[1] = qkv; o[2] = nullptr; o[3] = nullptr; o[4] = wo; o[6] = wg; o[7] = wu; o[8] = wd;
+    o[1] = qkv; o[2] = nullptr; o[3] = nullptr; o[4] = wo; o[6] = wgu; o[7] = nullptr; o[8] = wd;
   }
   if (rc != SJD_OK) return fail(rc);
   // the caller may release its weights once sjd_init returns
@@ -285,12 +292,14 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   const int target = 2 * ncu;
   x.S_qkv = sjd::gemm_splits(Nq + 2 * Nkv, d, target);
   x.S_o = sjd::gemm_splits(d, Nq, target);
-  x.S_gu = 1;
+  x.S_gu = sjd::gemm_splits(2 * F, d, target);
   x.S_dn = sjd::gemm_splits(d, F, target);
   x.S_head = 1;
   const int sr = x.S_o > x.S_dn ? x.S_o : x.S_dn;
   if ((rc = dalloc(x, &x.qkv, (size_t)x.S_qkv * Mp * (Nq + 2 * Nkv))) ||
-      (rc = dalloc(x, &x.rpart, (size_t)sr * Mp * d)))
+      (rc = dalloc(x, &x.rpart, (size_t)sr * Mp * d)) ||
+      (rc = dalloc(x, &x.gup, (size_t)x.S_gu * Mp * 2 * F)) ||
+      (rc = dalloc(x, &x.ss, (size_t)Mp * sjd::norm_chunks(d))))
     return fail(rc);
   // zero the caches (rows past the fill are read, masked, by the attention
   // tiles) and the activation pad rows

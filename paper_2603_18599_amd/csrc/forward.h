@@ -5,31 +5,34 @@
 
 namespace sjd {
 
-enum { kGemmStore = 0, kGemmSwiGLU = 2 };
+constexpr int kGemmMaxSplits = 32;
 
 // Weights are repacked at init into 32-row x 64-column tiles (4 KB, bf16):
 // tile (nb, kb) of a [N][K] matrix starts at element (nb * (K/64) + kb) *
 // 2048 and holds, for i = 0..3 and lane l = 0..63, the 8 elements of row
 // nb*32 + l%32, columns kb*64 + (l/32)*32 + i*8 .. +8 at (i*64 + l) * 8. A wave
-// then reads one tile as four contiguous 1 KB loads.
+// then reads one tile as four contiguous 1 KB loads. Matrices that share an
+// input (q, k, v; gate, up) are tiled one after the other into one [N][K].
 struct GemmArgs {
-  const uint16_t* A;     // activations as two bf16 planes (A = hi + lo), rows padded to
-  const uint16_t* A_lo;  // 32 * ceil(M/32), row stride lda
+  const uint16_t* A;     // activations as two bf16 planes (A = hi + lo), 32 rows
+  const uint16_t* A_lo;  // (rows >= M zero), row stride lda
   int lda;
-  int M;
-  const uint16_t* W0;  // tiled weights [N][K]; SwiGLU: W0 = gate, W1 = up (same columns)
-  const uint16_t* W1;
+  int M;               // 1..32
+  const uint16_t* W;   // tiled weights [N][K]
   int N, K;            // N multiple of 32, K multiple of 64
-  int S;               // workgroups along K (SwiGLU: 1)
-  float* out;          // store: fp32 partial plane sp at out + sp * plane, row stride ldo
+  int S;               // workgroups along K = fp32 partial planes (1..kGemmMaxSplits)
+  float* out;          // plane sp at out + sp * plane, row stride ldo
   size_t plane;
-  uint16_t* outb;      // SwiGLU output as hi / lo bf16 planes, row stride ldo
-  uint16_t* outb_lo;
   int ldo;
+  // optional RMS scale of row m (fused RMSNorm): rsqrt(sum_c ss[m * ss_n + c] *
+  // inv_d + eps) multiplies the row of the product before the store
+  const float* ss;
+  int ss_n;
+  float inv_d, eps;
 };
 
 int gemm_splits(int N, int K, int target_wgs);
-hipError_t launch_gemm(const GemmArgs& g, int mode, hipStream_t s);
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 
 // Repacks rows [row0, row0 + N) of a row-major [*][K] bf16 (or fp32, then
 // rounded to nearest even) matrix into the tile layout above.
@@ -54,13 +57,34 @@ struct DevState {
   int32_t tok[64];  // last step's committed tokens
 };
 
+// Key / value cache layout. Per layer and kv head, positions are grouped in
+// tiles of 32 (32 * hd elements each) stored in the register order of the
+// attention MFMAs, so that every load of a tile is a contiguous 1 KB per
+// wave: key (position p, dim j) is element (t * 64 + lane) * 8 + e of tile
+// p / 32, with lane = swap23(p % 32) + 32 * (j / (hd / 2)), t = (j % (hd / 2)) / 8,
+// e = j % 8 (swap23 exchanges bits 2 and 3: the key-row order of the score
+// MFMA); value (p, j) is element ((j / 32) * 2 + i / 16) * 512 + lane * 8 + i % 8
+// with i = p % 32, lane = j % 32 + 32 * ((i / 8) % 2) (the transposed-value
+// operand of the output MFMA).
+__host__ __device__ inline int swap23(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
+__host__ __device__ inline size_t kv_key_off(int p, int j, int hd) {
+  const int i = p & 31, h2 = hd / 2;
+  const int lane = swap23(i) + 32 * (j / h2), t = (j % h2) >> 3;
+  return (size_t)(p >> 5) * 32 * hd + (size_t)(t * 64 + lane) * 8 + (j & 7);
+}
+__host__ __device__ inline size_t kv_val_off(int p, int j, int hd) {
+  const int i = p & 31;
+  const int lane = (j & 31) + 32 * ((i >> 3) & 1);
+  return (size_t)(p >> 5) * 32 * hd + (size_t)(((j >> 5) * 2 + (i >> 4)) * 64 + lane) * 8 + (i & 7);
+}
+
 struct AttnArgs {
   // every tensor below is a pair of bf16 planes (value = hi + lo)
   const uint16_t* q;     // [Mpad][H * hd], rotated
   const uint16_t* q_lo;
-  const uint16_t* kc;    // [Hkv][cap][hd] key cache of this layer
+  const uint16_t* kc;    // [Hkv][cap * hd] key cache of this layer (tiled, see above)
   const uint16_t* kc_lo;
-  const uint16_t* vt;    // [Hkv][hd][cap] transposed value cache of this layer
+  const uint16_t* vt;    // [Hkv][cap * hd] value cache of this layer (tiled)
   const uint16_t* vt_lo;
   const Window* win;
   const int32_t* n_dev;  // cached rows before the window (device scalar), or NULL -> n_host
@@ -74,15 +98,18 @@ struct AttnArgs {
   uint16_t* out_lo;
   int ldo;
 };
-constexpr int kAttnChunk = 256;  // keys per workgroup
+constexpr int kAttnChunk = 128;  // keys per workgroup (4 waves x 32)
 hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s);
 
 // elementwise kernels
 hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, float* x, hipStream_t s);
-// x += sum of S fp32 partial planes (fixed order; S may be 0), then
-// y = x / sqrt(mean(x^2) + eps) * g as hi / lo bf16 planes (row stride ldy)
-hipError_t launch_rmsnorm(float* x, const float* part, int S, size_t plane, const uint16_t* g, int M, int d,
-                          float eps, uint16_t* y, uint16_t* y_lo, int ldy, hipStream_t s);
+// RMSNorm split in two: x += sum of S fp32 partial planes (fixed order; S
+// may be 0), y = x * g as hi / lo bf16 planes (row stride ldy) and the
+// sums of squares of x over 256-element chunks, ss[m][c] (c < norm_chunks(d));
+// the GEMM that consumes y applies the row scale 1 / sqrt(mean(x^2) + eps).
+inline int norm_chunks(int d) { return (d + 255) / 256; }
+hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, const uint16_t* g, int M, int d,
+                             uint16_t* y, uint16_t* y_lo, int ldy, float* ss, hipStream_t s);
 // rotary embedding of q and k, key row and transposed value column into the caches
 struct KvPlanes {
   uint16_t *q, *q_lo, *kc, *kc_lo, *vt, *vt_lo;
@@ -91,6 +118,11 @@ struct KvPlanes {
 hipError_t launch_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,
                           int M, int H, int Hkv, int hd, const float2* rope, const KvPlanes& o, int cap,
                           hipStream_t s);
+// h = silu(gate) * up as hi / lo bf16 planes (row stride ldh), gate = sum of
+// the S fp32 partial planes at columns [0, F), up = at columns [F, 2F)
+// (row stride 2F)
+hipError_t launch_swiglu(const float* P, int S, size_t plane, int M, int F, uint16_t* h, uint16_t* h_lo, int ldh,
+                         hipStream_t s);
 hipError_t launch_f32_to_bf16(const float* src, uint16_t* dst, size_t n, hipStream_t s);
 
 }  // namespace sjd

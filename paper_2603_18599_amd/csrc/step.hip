@@ -79,8 +79,8 @@ __global__ void k_state_init(DevState* st, const int32_t* prompt, int n_p, int L
   }
 }
 
-// Accepted sibling (meta[5] = k >= 2 at first rejected row r): its key row
-// and value column move from cache row n + n_s + r(K-1) + k-2 to n + r + 1.
+// Accepted sibling (meta[5] = k >= 2 at first rejected row r): its key and
+// value move from cache position n + n_s + r(K-1) + k-2 to n + r + 1.
 // grid (layers, Hkv), block hd
 __global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int cap, int K) {
   const int acc_k = st->meta[5];
@@ -88,14 +88,14 @@ __global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int c
   const int r = st->meta[1];
   const int src = st->n + st->n_s + r * (K - 1) + (acc_k - 2);
   const int dst = st->n + r + 1;
-  const int l = blockIdx.x, kh = blockIdx.y, i = threadIdx.x;
-  const size_t layer = (size_t)l * Hkv * cap * hd;
-  const size_t ko = layer + (size_t)kh * cap * hd;
-  c.kc[ko + (size_t)dst * hd + i] = c.kc[ko + (size_t)src * hd + i];
-  c.kc_lo[ko + (size_t)dst * hd + i] = c.kc_lo[ko + (size_t)src * hd + i];
-  const size_t vo = layer + (size_t)kh * hd * cap + (size_t)i * cap;
-  c.vt[vo + dst] = c.vt[vo + src];
-  c.vt_lo[vo + dst] = c.vt_lo[vo + src];
+  const int l = blockIdx.x, kh = blockIdx.y, j = threadIdx.x;
+  const size_t base = ((size_t)l * Hkv + kh) * cap * hd;
+  const size_t ks = base + kv_key_off(src, j, hd), kd = base + kv_key_off(dst, j, hd);
+  const size_t vs = base + kv_val_off(src, j, hd), vd = base + kv_val_off(dst, j, hd);
+  c.kc[kd] = c.kc[ks];
+  c.kc_lo[kd] = c.kc_lo[ks];
+  c.vt[vd] = c.vt[vs];
+  c.vt_lo[vd] = c.vt_lo[vs];
 }
 
 __global__ void k_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L) {

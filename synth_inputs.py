@@ -102,3 +102,16 @@ def prompt_tokens(cfg, seed, device="cpu"):
     model carry no meaning)."""
     g = torch.Generator(device=device).manual_seed(seed)
     return torch.randint(0, cfg["vocab_size"], (cfg["n_prompt"],), generator=g, device=device, dtype=torch.int32)
+
+
+def image_history(cfg, n, seed, device="cpu"):
+    """n already-generated image tokens: random visual ids in [vis_lo, vis_lo
+    + V), the row-end id at every (row_len + 1)-th position (Lumina-mGPT and
+    Emu3 end each image row with a row-end token). Stands in for the first part
+    of an image so that a step can be timed at a mid-image cache length."""
+    g = torch.Generator(device=device).manual_seed(seed)
+    t = torch.randint(cfg["vis_lo"], cfg["vis_lo"] + cfg["V"], (n,), generator=g, device=device, dtype=torch.int32)
+    if cfg.get("row_len", 0) > 0:
+        t[cfg["row_len"]::cfg["row_len"] + 1] = cfg["eol_id"]
+    return t
+
