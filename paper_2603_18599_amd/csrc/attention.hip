@@ -210,37 +210,53 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   }
 }
 
-// out[slot][h*hd + dim] = bf16(sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m))
+// out[slot][h*hd + dim] = sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m).
+// grid (H, HD / 32), block 256: thread -> (slot, 4 consecutive dims); the
+// split loop is unrolled so that its loads are in flight together.
 template <int HD>
-__global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
-  const int slot = blockIdx.x, h = blockIdx.y, dim = threadIdx.x;
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
+  const int h = blockIdx.x, t = threadIdx.x;
+  const int slot = t >> 3, dim0 = blockIdx.y * 32 + (t & 7) * 4;
+  if (slot >= a.M) return;
   const int n = a.n_dev ? *a.n_dev : a.n_host;
   const int nk = n + a.M;
   const int ns = (nk + kAttnChunk - 1) / kAttnChunk;
-  const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * 64;
-  const float* wo = a.ws_o + (size_t)h * a.nsplit_max * 32 * HD;
+  const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * 64 + slot * 2;
+  const float* wo = a.ws_o + ((size_t)h * a.nsplit_max * 32 + slot) * HD + dim0;
   float mx = -INFINITY;
-  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, wml[s * 64 + slot * 2]);
-  float acc = 0.0f, ls = 0.0f;
+#pragma unroll 8
+  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, wml[s * 64]);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float ls = 0.0f;
+#pragma unroll 8
   for (int s = 0; s < ns; ++s) {
-    const float ms = wml[s * 64 + slot * 2];
-    if (ms == -INFINITY) continue;
-    const float f = exp2f(ms - mx);
-    acc += wo[((size_t)s * 32 + slot) * HD + dim] * f;
-    ls += wml[s * 64 + slot * 2 + 1] * f;
+    const float2 ml = *(const float2*)(wml + s * 64);
+    const float4 v = *(const float4*)(wo + (size_t)s * 32 * HD);
+    const float f = ml.x == -INFINITY ? 0.0f : exp2f(ml.x - mx);
+    ls += ml.y * f;
+    acc.x += v.x * f;
+    acc.y += v.y * f;
+    acc.z += v.z * f;
+    acc.w += v.w * f;
   }
-  const size_t oo = (size_t)slot * a.ldo + (size_t)h * HD + dim;
-  split_bf16(acc / ls, a.out[oo], a.out_lo[oo]);
+  const size_t oo = (size_t)slot * a.ldo + (size_t)h * HD + dim0;
+  ushort4 hi, lo;
+  split_bf16(acc.x / ls, hi.x, lo.x);
+  split_bf16(acc.y / ls, hi.y, lo.y);
+  split_bf16(acc.z / ls, hi.z, lo.z);
+  split_bf16(acc.w / ls, hi.w, lo.w);
+  *(ushort4*)(a.out + oo) = hi;
+  *(ushort4*)(a.out_lo + oo) = lo;
 }
 
 hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s) {
-  const dim3 g1(a.H, a.nsplit_max), g2(a.M, a.H);
+  const dim3 g1(a.H, a.nsplit_max), g2(a.H, hd / 32);
   if (hd == 128) {
     hipLaunchKernelGGL(k_attn_partial<128>, g1, dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_attn_combine<128>, g2, dim3(128), 0, s, a);
+    hipLaunchKernelGGL(k_attn_combine<128>, g2, dim3(256), 0, s, a);
   } else if (hd == 64) {
     hipLaunchKernelGGL(k_attn_partial<64>, g1, dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_attn_combine<64>, g2, dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_attn_combine<64>, g2, dim3(256), 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }

@@ -131,13 +131,29 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   }
 }
 
+// Split count along K. Splits that divide the K steps evenly are preferred
+// (an uneven split leaves a tail of workgroups one step longer); among them
+// the one whose workgroup count is nearest the target (by ratio), if within
+// a factor of two, else ceil(target / groups).
 int gemm_splits(int N, int K, int target_wgs) {
   const int groups = (N / 32 + kGWaves - 1) / kGWaves;
   const int T = K / 64;
+  int smax = T / 2 > 0 ? T / 2 : 1;  // at least two k-steps per workgroup
+  if (smax > kGemmMaxSplits) smax = kGemmMaxSplits;
+  int best = 0;
+  double best_r = 0.0;
+  for (int S = 1; S <= smax; ++S) {
+    if (T % S) continue;
+    const double w = (double)groups * S;
+    const double r = w > target_wgs ? w / target_wgs : target_wgs / w;
+    if (best == 0 || r < best_r) {
+      best = S;
+      best_r = r;
+    }
+  }
+  if (best > 0 && best_r <= 2.0) return best;
   int S = (target_wgs + groups - 1) / groups;
-  const int smax = T / 2 > 0 ? T / 2 : 1;  // at least two k-steps per workgroup
   if (S > smax) S = smax;
-  if (S > kGemmMaxSplits) S = kGemmMaxSplits;
   if (S < 1) S = 1;
   return S;
 }
