@@ -2,20 +2,22 @@
 // per-trial finalize kernel.
 //
 // k_verify_rows: one workgroup per (trial, row). The row is read once,
-// coalesced (float4 per thread), into registers; on chip the kernel finds
-// the exact top-k threshold, compacts the kept tokens into LDS in index
-// order, and then takes every decision on the compact list:
-//  - top-k threshold: one histogram over bins of the row's [min, max] range
-//    (well spread for real logits, so the LDS atomics rarely collide), then
-//    an exact (value desc, index asc) rank among the few entries of the
-//    threshold bin; a radix select over order-preserving keys is the
-//    fallback for degenerate rows (many equal values);
-//  - compaction: a bitmap of the kept set with per-word prefix popcounts
-//    gives each kept token its rank; that rank indexes the compact arrays
-//    and the random stream (four consecutive ranks share one Philox block);
-//  - the draft row (when the row has a draft distribution) is then read into
-//    the same registers; its own threshold and normaliser are found and its
-//    probabilities are scattered into the compact list;
+// coalesced (float4 per thread), into registers. Every full-row pass is kept
+// to a few instructions per logit; the exponentials, normalisers and all
+// decisions run over the compact list of kept tokens (at most 2048):
+//  - top-k selection: one histogram over bins of the row's [min, max] range
+//    (well spread for real logits, so the LDS atomics rarely collide); one
+//    pass then marks every entry of a bin above the threshold bin in a
+//    bitmap of the kept set and collects the threshold bin's entries, whose
+//    exact (value desc, index asc) rank decides which of them join it; a
+//    radix select over order-preserving keys is the fallback for degenerate
+//    rows (many equal values);
+//  - compaction: per-word prefix popcounts of the bitmap give each kept token
+//    its rank, which indexes the compact arrays and the random stream (four
+//    consecutive ranks share one Philox block);
+//  - the draft row (when the row has a draft distribution) goes through the
+//    same selection into a second bitmap; one pass stores its logits at the
+//    target's kept entries and at its own kept entries (for its normaliser);
 //  - accept tests, residual draws (Theorem 2's recursion for several
 //    candidates), drafting candidates and bonus draws run over the compact
 //    list only.
@@ -41,13 +43,16 @@ template <int BLOCK, int NC>
 struct VSh {
   static constexpr int W = BLOCK / kWave;
   static constexpr int NW = BLOCK * NC / 8;  // bitmap words (32 entries each)
-  uint32_t bm[NW];
-  int32_t pre[NW];
-  uint16_t sp_x[kKcap];
-  float sp_p[kKcap];
+  uint32_t bm[NW];    // kept set of the target row
+  int32_t pre[NW];    // its per-word prefix popcounts
+  uint32_t bmq[NW];   // kept set of the draft row
+  int32_t preq[NW];
+  uint16_t sp_x[kKcap];  // compact list: token index,
+  float sp_p[kKcap];     //   target probability,
+  float sp_q[kKcap];     //   draft probability
   union {
-    float sp_q[kKcap];
     uint32_t hist[kBins];
+    float qc[kKcap];  // draft row's kept weights (its normaliser)
   };
   float cand_v[kCandCap];
   int cand_x[kCandCap];
@@ -58,6 +63,7 @@ struct VSh {
   float tau_v;
   int tau_x, bin, above, ncand;
 };
+static_assert(kBins == kKcap, "the draft weights reuse the histogram");
 
 // ------------------------------------------------------------ block helpers
 template <int W>
@@ -260,29 +266,76 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
   tau_x = (int)ipre;
 }
 
-// Row statistics: max, exact top-k threshold, normaliser.
+// Loads a row into registers (chunk c = tid + i * BLOCK holds entries
+// 4c .. 4c+3) and returns, block-wide, its largest value and its smallest
+// value above -inf.
 template <int BLOCK, int NC>
-SJD_DEV void row_stats(const float4 (&v)[NC], int V, int top_k, float T, VSh<BLOCK, NC>& sh, RowStats& st) {
+SJD_DEV void load_row_maxmin(float4 (&v)[NC], const float* row, int V, VSh<BLOCK, NC>& sh, float& mx, float& mn) {
   constexpr int W = BLOCK / kWave;
-  const int tid = threadIdx.x;
-  const int nchunk = V >> 2;
-  st.T = T;
-  float mx = -INFINITY, mn = INFINITY;
+  load_row<BLOCK, NC>(v, row, V);
+  mx = -INFINITY;
+  mn = INFINITY;
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float l = comp(v[i], e);
-      mx = fmaxf(mx, l);
-      if (l > -INFINITY) mn = fminf(mn, l);
-    }
+    mx = fmaxf(mx, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
+    mn = fminf(mn, fminf(fminf(v[i].x, v[i].y), fminf(v[i].z, v[i].w)));
   }
   block_maxmin<W>(mx, mn, sh.red_f);
-  st.m = mx;
+  if (mn == -INFINITY) {
+    // rows with -inf entries (padding, masked tokens): minimum over the rest
+    mn = INFINITY;
+    float t = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float l = comp(v[i], e);
+        if (l > -INFINITY) mn = fminf(mn, l);
+      }
+    }
+    block_maxmin<W>(t, mn, sh.red_f);
+  }
+}
+
+// Bitmap of a kept set given by the threshold (tau_v, tau_x); the eight
+// chunks of a bitmap word belong to eight consecutive lanes, which OR their
+// nibbles together.
+template <int BLOCK, int NC>
+SJD_DEV void bitmap_from_tau(const float4 (&v)[NC], int V, const RowStats& st, uint32_t* bm) {
+  const int tid = threadIdx.x;
+  const int nchunk = V >> 2;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int c = tid + i * BLOCK;
+    uint32_t bits = 0;
+    if (c < nchunk) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bits |= (st.in_set(comp(v[i], e), 4 * c + e) ? 1u : 0u) << e;
+    }
+    bits <<= 4 * (tid & 7);
+    bits |= __shfl_xor(bits, 1, kWave);
+    bits |= __shfl_xor(bits, 2, kWave);
+    bits |= __shfl_xor(bits, 4, kWave);
+    if ((tid & 7) == 0) bm[(tid >> 3) + i * (BLOCK / 8)] = bits;
+  }
+}
+
+// Exact top-k selection of the row in registers: fills the bitmap bm of the
+// kept set and its prefix popcounts pre, sets st.all / tau_v / tau_x (the
+// k-th kept entry: kept = l > tau_v or (l == tau_v and x <= tau_x)) and
+// returns the number of kept entries.
+template <int BLOCK, int NC>
+SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float mn, VSh<BLOCK, NC>& sh,
+                        uint32_t* bm, int32_t* pre, RowStats& st) {
+  constexpr int W = BLOCK / kWave;
+  constexpr int NW = VSh<BLOCK, NC>::NW;
+  const int tid = threadIdx.x;
+  const int nchunk = V >> 2;
   const int k = (top_k <= 0 || top_k >= V) ? V : top_k;
   st.all = (k >= V);
   st.tau_v = -INFINITY;
   st.tau_x = 0x7FFFFFFF;
+  bool have_bitmap = false;
   if (!st.all) {
     bool fast = (mx < INFINITY) && (mn < INFINITY) && (mx > mn);
     const float scale = fast ? (float)kBins / (mx - mn) : 0.0f;
@@ -291,10 +344,13 @@ SJD_DEV void row_stats(const float4 (&v)[NC], int V, int top_k, float T, VSh<BLO
       for (int b = tid; b < kBins; b += BLOCK) sh.hist[b] = 0;
       if (tid == 0) sh.ncand = 0;
       __syncthreads();
+      // bin of a value: (l - mn) * scale rounded once (fma), truncated,
+      // clamped; monotone in l, so every entry of a higher bin outranks
+      // every entry of a lower one (-inf converts to INT_MIN, clamped to 0)
+      const float off = -mn * scale;
       auto binof = [&](float l) -> int {
-        if (!(l > mn)) return 0;
-        int b = (int)((l - mn) * scale);
-        return b < kBins - 1 ? b : kBins - 1;
+        const int b = __float2int_rz(__builtin_fmaf(l, scale, off));
+        return min(max(b, 0), kBins - 1);
       };
 #pragma unroll
       for (int i = 0; i < NC; ++i) {
@@ -326,22 +382,32 @@ SJD_DEV void row_stats(const float4 (&v)[NC], int V, int top_k, float T, VSh<BLO
       __syncthreads();
       const int bstar = sh.bin, rem = k - sh.above, c = (int)sh.hist[bstar];
       if (c <= kCandCap) {
+        // entries of higher bins are kept; the threshold bin's are collected
 #pragma unroll
         for (int i = 0; i < NC; ++i) {
           const int ch = tid + i * BLOCK;
+          uint32_t bits = 0;
           if (ch < nchunk) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const float l = comp(v[i], e);
-              if (binof(l) == bstar) {
+              const int b = binof(l);
+              bits |= (b > bstar ? 1u : 0u) << e;
+              if (b == bstar) {
                 const int p = atomicAdd(&sh.ncand, 1);
                 sh.cand_v[p] = l;
                 sh.cand_x[p] = 4 * ch + e;
               }
             }
           }
+          bits <<= 4 * (tid & 7);
+          bits |= __shfl_xor(bits, 1, kWave);
+          bits |= __shfl_xor(bits, 2, kWave);
+          bits |= __shfl_xor(bits, 4, kWave);
+          if ((tid & 7) == 0) bm[(tid >> 3) + i * (BLOCK / 8)] = bits;
         }
         __syncthreads();
+        // exact rank inside the threshold bin; the first rem join the set
         for (int i = tid; i < c; i += BLOCK) {
           const float vi = sh.cand_v[i];
           const int xi = sh.cand_x[i];
@@ -350,6 +416,7 @@ SJD_DEV void row_stats(const float4 (&v)[NC], int V, int top_k, float T, VSh<BLO
             const float vj = sh.cand_v[j];
             r += (vj > vi) || (vj == vi && sh.cand_x[j] < xi);
           }
+          if (r < rem) atomicOr(&bm[xi >> 5], 1u << (xi & 31));
           if (r == rem - 1) {
             sh.tau_v = vi;
             sh.tau_x = xi;
@@ -358,67 +425,32 @@ SJD_DEV void row_stats(const float4 (&v)[NC], int V, int top_k, float T, VSh<BLO
         __syncthreads();
         st.tau_v = sh.tau_v;
         st.tau_x = sh.tau_x;
-        __syncthreads();
+        have_bitmap = true;
       } else {
         fast = false;
       }
     }
     if (!fast) radix_topk<BLOCK, NC>(v, V, k, sh, st.tau_v, st.tau_x);
   }
-  double z = 0.0;
-#pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int c = tid + i * BLOCK;
-    if (c < nchunk) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float l = comp(v[i], e);
-        if (st.in_set(l, 4 * c + e)) z += (double)expf((l - st.m) / T);
-      }
-    }
+  if (!have_bitmap) {
+    bitmap_from_tau<BLOCK, NC>(v, V, st, bm);
+    __syncthreads();
   }
-  st.invZ = 1.0 / block_sum_d<W>(z, sh.red_d);
-}
-
-// Bitmap of the kept set and its per-word prefix popcounts; returns the
-// number of kept entries.
-template <int BLOCK, int NC>
-SJD_DEV int build_rank(const float4 (&v)[NC], int V, const RowStats& st, VSh<BLOCK, NC>& sh) {
-  constexpr int W = BLOCK / kWave;
-  constexpr int NW = VSh<BLOCK, NC>::NW;
-  const int tid = threadIdx.x;
-  const int nchunk = V >> 2;
-  // word of chunk c is c >> 3: the eight chunks of a word belong to eight
-  // consecutive lanes, which OR their nibbles together
-#pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int c = tid + i * BLOCK;
-    uint32_t bits = 0;
-    if (c < nchunk) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) bits |= (st.in_set(comp(v[i], e), 4 * c + e) ? 1u : 0u) << e;
-    }
-    bits <<= 4 * (tid & 7);
-    bits |= __shfl_xor(bits, 1, kWave);
-    bits |= __shfl_xor(bits, 2, kWave);
-    bits |= __shfl_xor(bits, 4, kWave);
-    if ((tid & 7) == 0) sh.bm[(tid >> 3) + i * (BLOCK / 8)] = bits;
-  }
-  __syncthreads();
-  constexpr int WPT = NW / BLOCK > 0 ? NW / BLOCK : 1;  // words per thread (contiguous)
+  // per-word prefix popcounts (words contiguous per thread)
+  constexpr int WPT = NW / BLOCK > 0 ? NW / BLOCK : 1;
   int cnt[WPT];
   int s = 0;
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
     const int wi = tid * WPT + i;
-    cnt[i] = wi < NW ? __popc(sh.bm[wi]) : 0;
+    cnt[i] = wi < NW ? __popc(bm[wi]) : 0;
     s += cnt[i];
   }
   int run = block_excl_scan<W>(s, sh.red_i);
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
     const int wi = tid * WPT + i;
-    if (wi < NW) sh.pre[wi] = run;
+    if (wi < NW) pre[wi] = run;
     run += cnt[i];
   }
   if (tid == BLOCK - 1) sh.ncand = run;
@@ -426,6 +458,48 @@ SJD_DEV int build_rank(const float4 (&v)[NC], int V, const RowStats& st, VSh<BLO
   const int total = sh.ncand;
   __syncthreads();
   return total;
+}
+
+// Kept entries of the row in registers, by rank: ox[r] = index (if ox),
+// ol[r] = value.
+template <int BLOCK, int NC>
+SJD_DEV void compact_row(const float4 (&v)[NC], int V, const uint32_t* bm, const int32_t* pre, uint16_t* ox,
+                         float* ol) {
+  const int nchunk = V >> 2;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int c = threadIdx.x + i * BLOCK;
+    if (c < nchunk) {
+      const uint32_t word = bm[c >> 3];
+      const int sh4 = 4 * (c & 7);
+      const uint32_t nib = (word >> sh4) & 15u;
+      if (nib) {
+        int r = pre[c >> 3] + __popc(word & ((1u << sh4) - 1u));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if ((nib >> e) & 1u) {
+            if (ox) ox[r] = (uint16_t)(4 * c + e);
+            ol[r] = comp(v[i], e);
+            ++r;
+          }
+        }
+      }
+    }
+  }
+}
+
+// Softmax weights over a compact list of logits: w[i] = expf((w[i] - m) / T)
+// in place; returns 1 / sum (fp64, fixed order).
+template <int BLOCK, int NC>
+SJD_DEV double softmax_weights(float* w, int n, float m, float T, VSh<BLOCK, NC>& sh) {
+  constexpr int W = BLOCK / kWave;
+  double z = 0.0;
+  for (int i = threadIdx.x; i < n; i += BLOCK) {
+    const float e = expf((w[i] - m) / T);
+    w[i] = e;
+    z += (double)e;
+  }
+  return 1.0 / block_sum_d<W>(z, sh.red_d);
 }
 
 template <int BLOCK, int NC>
@@ -526,26 +600,15 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
   RowStats ps{};
   int nk = 0;
   if (need_p) {
-    load_row<BLOCK, NC>(v, cur_row, V);
-    row_stats<BLOCK, NC>(v, V, a.top_k, a.T, sh, ps);
-    nk = build_rank<BLOCK, NC>(v, V, ps, sh);
-    // compact the kept entries (index order) with their probabilities
-#pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = tid + i * BLOCK;
-      if (c < nchunk) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int x = 4 * c + e;
-          const float l = comp(v[i], e);
-          if (ps.in_set(l, x)) {
-            const int r = rank_of(sh, x);
-            sh.sp_x[r] = (uint16_t)x;
-            sh.sp_p[r] = ps.prob(l, x);
-          }
-        }
-      }
-    }
+    float mx, mn;
+    load_row_maxmin<BLOCK, NC>(v, cur_row, V, sh, mx, mn);
+    ps.m = mx;
+    ps.T = a.T;
+    nk = select_kept<BLOCK, NC>(v, V, a.top_k, mx, mn, sh, sh.bm, sh.pre, ps);
+    compact_row<BLOCK, NC>(v, V, sh.bm, sh.pre, sh.sp_x, sh.sp_p);
+    __syncthreads();
+    ps.invZ = softmax_weights<BLOCK, NC>(sh.sp_p, nk, ps.m, a.T, sh);
+    for (int i = tid; i < nk; i += BLOCK) sh.sp_p[i] = (float)((double)sh.sp_p[i] * ps.invZ);
     if (a.dbg_p) {
       float4* dst = (float4*)(a.dbg_p + ((size_t)b * L + j) * V);
 #pragma unroll
@@ -640,18 +703,38 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
     const size_t qrow = (size_t)b * a.draft_bstride + (size_t)((a.q_off ? a.q_off[b] : 0) + j) * V;
     const float* draft_row = a.draft + qrow;
     RowStats qs{};
-    load_row<BLOCK, NC>(v, draft_row, V);
-    row_stats<BLOCK, NC>(v, V, a.top_k, a.T, sh, qs);  // the histogram aliases sp_q: written after
+    float qmx, qmn;
+    load_row_maxmin<BLOCK, NC>(v, draft_row, V, sh, qmx, qmn);
+    qs.m = qmx;
+    qs.T = a.T;
+    const int nq = select_kept<BLOCK, NC>(v, V, a.top_k, qmx, qmn, sh, sh.bmq, sh.preq, qs);
+    // draft logits at the target's kept entries (by target rank) and at its
+    // own kept entries (by draft rank, for its normaliser)
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
       const int c = tid + i * BLOCK;
       if (c < nchunk) {
+        const int sh4 = 4 * (c & 7);
+        const uint32_t wp = sh.bm[c >> 3], wq = sh.bmq[c >> 3];
+        const uint32_t np = (wp >> sh4) & 15u, nqb = (wq >> sh4) & 15u;
+        if (np | nqb) {
+          int rp = sh.pre[c >> 3] + __popc(wp & ((1u << sh4) - 1u));
+          int rq = sh.preq[c >> 3] + __popc(wq & ((1u << sh4) - 1u));
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int x = 4 * c + e;
-          if (kept(sh, x)) sh.sp_q[rank_of(sh, x)] = qs.prob(comp(v[i], e), x);
+          for (int e = 0; e < 4; ++e) {
+            const float l = comp(v[i], e);
+            if ((np >> e) & 1u) sh.sp_q[rp++] = l;
+            if ((nqb >> e) & 1u) sh.qc[rq++] = l;
+          }
         }
       }
+    }
+    __syncthreads();
+    qs.invZ = softmax_weights<BLOCK, NC>(sh.qc, nq, qs.m, a.T, sh);
+    for (int i = tid; i < nk; i += BLOCK) {
+      const int x = (int)sh.sp_x[i];
+      const bool in_q = (sh.bmq[x >> 5] >> (x & 31)) & 1u;
+      sh.sp_q[i] = in_q ? (float)((double)expf((sh.sp_q[i] - qs.m) / a.T) * qs.invZ) : 0.0f;
     }
     __syncthreads();
     auto qrow_c = [&](int ent) -> float { return sh.sp_q[ent]; };
@@ -877,7 +960,7 @@ __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, Finaliz
 // ------------------------------------------------------------ launch
 int verify_block_for(int V) {
   if (V <= 4096) return 256;
-  if (V <= 16384) return 256;
+  if (V <= 16384) return 512;
   if (V <= 32768) return 512;
   if (V <= 65536) return 1024;
   return 0;
@@ -886,7 +969,7 @@ int verify_block_for(int V) {
 hipError_t launch_verify(const VerifyArgs& a, const FinalizeOut& o, hipStream_t s) {
   const dim3 grid(a.L, a.B);
   if (a.V <= 4096) hipLaunchKernelGGL((k_verify_rows<256, 4>), grid, dim3(256), 0, s, a);
-  else if (a.V <= 16384) hipLaunchKernelGGL((k_verify_rows<256, 16>), grid, dim3(256), 0, s, a);
+  else if (a.V <= 16384) hipLaunchKernelGGL((k_verify_rows<512, 8>), grid, dim3(512), 0, s, a);
   else if (a.V <= 32768) hipLaunchKernelGGL((k_verify_rows<512, 16>), grid, dim3(512), 0, s, a);
   else if (a.V <= 65536) hipLaunchKernelGGL((k_verify_rows<1024, 16>), grid, dim3(1024), 0, s, a);
   else return hipErrorInvalidValue;
