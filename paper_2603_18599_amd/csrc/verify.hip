@@ -266,13 +266,11 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
   tau_x = (int)ipre;
 }
 
-// Loads a row into registers (chunk c = tid + i * BLOCK holds entries
-// 4c .. 4c+3) and returns, block-wide, its largest value and its smallest
-// value above -inf.
+// Block-wide largest value of the row in registers and its smallest value
+// above -inf.
 template <int BLOCK, int NC>
-SJD_DEV void load_row_maxmin(float4 (&v)[NC], const float* row, int V, VSh<BLOCK, NC>& sh, float& mx, float& mn) {
+SJD_DEV void row_maxmin(const float4 (&v)[NC], VSh<BLOCK, NC>& sh, float& mx, float& mn) {
   constexpr int W = BLOCK / kWave;
-  load_row<BLOCK, NC>(v, row, V);
   mx = -INFINITY;
   mn = INFINITY;
 #pragma unroll
@@ -559,49 +557,79 @@ SJD_DEV int race_compact(const VSh<BLOCK, NC>& shc, VSh<BLOCK, NC>& sh, int nk, 
 }
 
 // ------------------------------------------------------------ row kernel
-template <int BLOCK, int NC>
-__global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
-  constexpr int W = BLOCK / kWave;
-  __shared__ VSh<BLOCK, NC> sh;
-  const int tid = threadIdx.x;
-  const int j = blockIdx.x;
-  const int b = blockIdx.y;
-  const int L = a.L, V = a.V, K = a.K, Km1 = a.K - 1;
-  const int nchunk = V >> 2;
+// What a row needs from memory (uniform over the workgroup).
+struct RowLoad {
+  bool valid;   // the trial's window description is well formed
+  bool need_p;  // the row's own logits are used
+  bool need_q;  // its draft row is read (a spine row with a valid draft token)
+  const float* cur;
+  const float* draft;
+};
+
+SJD_DEV bool forced_pos(const VerifyArgs& a, long g) {
+  return a.row_len > 0 && g >= 0 && (g % (a.row_len + 1)) == a.row_len;
+}
+
+SJD_DEV RowLoad plan_load(const VerifyArgs& a, int row) {
+  RowLoad r;
+  const int b = row / a.L, j = row % a.L;
+  const int Km1 = a.K - 1;
   const int32_t* meta = a.in_meta + 4 * (size_t)b;
   const int D_in = meta[0], n_q = meta[1];
   const long g0 = meta[2];
+  const int n_s = a.L - Km1 * D_in;
+  r.valid = !(D_in < 0 || D_in > a.D || a.K * D_in > a.L || n_q < 0 || n_q > n_s);
+  r.need_p = false;
+  r.need_q = false;
+  r.cur = a.cur + ((size_t)b * a.L + j) * a.V;
+  r.draft = nullptr;
+  if (!r.valid) return r;
+  if (j < n_s) {
+    const bool is_forced = forced_pos(a, g0 + j);
+    r.need_p = !is_forced;
+    if (!is_forced && j < n_q) {
+      const int x0 = a.draft_tok[(size_t)b * a.L + j] - a.vis_lo;
+      if (x0 >= 0 && x0 < a.V) {
+        r.need_q = true;
+        r.draft = a.draft + (size_t)b * a.draft_bstride + (size_t)((a.q_off ? a.q_off[b] : 0) + j) * a.V;
+      }
+    }
+  } else {
+    const int sib_d = (j - n_s) / Km1, sib_k = (j - n_s) % Km1 + 2;
+    const int sib_tok = a.sib ? a.sib[((size_t)b * a.D + sib_d) * Km1 + (sib_k - 2)] : -1;
+    r.need_p = !(sib_tok < 0 || forced_pos(a, g0 + sib_d) || forced_pos(a, g0 + sib_d + 1));
+  }
+  if (a.dbg_p) r.need_p = true;
+  return r;
+}
+
+// One row. With PF, v already holds the row's logits (if ld.need_p) and vq
+// its draft row (if ld.need_q), both loaded at kernel start so that the two
+// reads overlap; without PF, vq is v and each row is loaded when needed.
+template <int BLOCK, int NC, bool PF>
+SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const RowLoad& ld, float4 (&v)[NC],
+                        float4 (&vq)[NC]) {
+  constexpr int W = BLOCK / kWave;
+  const int tid = threadIdx.x;
+  const int b = row / a.L, j = row % a.L;
+  const int L = a.L, V = a.V, Km1 = a.K - 1;
+  const int nchunk = V >> 2;
+  if (!ld.valid) return;  // finalize flags the trial
+  const int32_t* meta = a.in_meta + 4 * (size_t)b;
+  const int D_in = meta[0];
+  const long g0 = meta[2];
   const int n_s = L - Km1 * D_in;
   int32_t* rec = a.rec + ((size_t)b * L + j) * kRecInts;
-  if (D_in < 0 || D_in > a.D || K * D_in > L || n_q < 0 || n_q > n_s) return;  // finalize flags the trial
   const bool ac = (a.flags & kFlagAC) != 0;
   const bool pd = (a.flags & kFlagPD) != 0 && Km1 > 0;
-  auto forced = [&](long g) -> bool { return a.row_len > 0 && g >= 0 && (g % (a.row_len + 1)) == a.row_len; };
-
-  // ---- classify the row (uniform over the block)
   const bool spine = j < n_s;
-  bool is_forced = false, need_p = true, has_q = false;
-  int sib_d = -1, sib_k = 0, sib_tok = -1;
-  if (spine) {
-    is_forced = forced(g0 + j);
-    has_q = !is_forced && j < n_q;
-    if (is_forced) need_p = false;
-  } else {
-    sib_d = (j - n_s) / Km1;
-    sib_k = (j - n_s) % Km1 + 2;
-    sib_tok = a.sib ? a.sib[((size_t)b * a.D + sib_d) * Km1 + (sib_k - 2)] : -1;
-    is_forced = forced(g0 + sib_d + 1);
-    if (sib_tok < 0 || forced(g0 + sib_d) || is_forced) need_p = false;
-  }
-  if (a.dbg_p) need_p = true;
 
-  const float* cur_row = a.cur + ((size_t)b * L + j) * V;
-  float4 v[NC];
   RowStats ps{};
   int nk = 0;
-  if (need_p) {
+  if (ld.need_p) {
+    if (!PF) load_row<BLOCK, NC>(v, ld.cur, V);
     float mx, mn;
-    load_row_maxmin<BLOCK, NC>(v, cur_row, V, sh, mx, mn);
+    row_maxmin<BLOCK, NC>(v, sh, mx, mn);
     ps.m = mx;
     ps.T = a.T;
     nk = select_kept<BLOCK, NC>(v, V, a.top_k, mx, mn, sh, sh.bm, sh.pre, ps);
@@ -630,10 +658,12 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
 
   // ---- sibling rows: bonus draw from the sibling's own output row
   if (!spine) {
+    const int sib_d = (j - n_s) / Km1, sib_k = (j - n_s) % Km1 + 2;
+    const int sib_tok = a.sib ? a.sib[((size_t)b * a.D + sib_d) * Km1 + (sib_k - 2)] : -1;
     int tok = -1, stage = 0;
-    if (sib_tok < 0 || forced(g0 + sib_d)) {
+    if (sib_tok < 0 || forced_pos(a, g0 + sib_d)) {
       tok = -1; stage = 0;
-    } else if (is_forced) {
+    } else if (forced_pos(a, g0 + sib_d + 1)) {
       tok = -1; stage = -1;
     } else {
       const Stream rs(a.seed, kTagBonus, 0, (uint32_t)j, (uint32_t)b, a.step);
@@ -653,7 +683,19 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
   }
 
   // ---- spine rows
-  if (is_forced) {
+  if (!ld.need_p && !a.dbg_p) {  // row-end position: the token is forced
+    if (tid == 0) {
+      rec[0] = -1; rec[1] = -1;
+      for (int t = 0; t < 7; ++t) rec[2 + t] = -1;
+      rec[9] = -1;
+      if (a.out_rows) {
+        int32_t* o = a.out_rows + ((size_t)b * L + j) * 2;
+        o[0] = a.eol; o[1] = -1;
+      }
+    }
+    return;
+  }
+  if (forced_pos(a, g0 + j)) {  // (debug output requested on a forced row)
     if (tid == 0) {
       rec[0] = -1; rec[1] = -1;
       for (int t = 0; t < 7; ++t) rec[2 + t] = -1;
@@ -673,25 +715,22 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
 #pragma unroll
   for (int t = 0; t < 8; ++t) { stg.cand[t] = -1; stg.Nf[t] = 1.0f; stg.den[t] = 1.0f; }
   int ncand = 0;
-  if (has_q) {
-    const int x0 = a.draft_tok[(size_t)b * L + j] - a.vis_lo;
-    if (x0 >= 0 && x0 < V) {
-      stg.cand[0] = x0;
-      ncand = 1;
-      if (j < D_in && a.sib) {
-        bool open = true;
+  if (ld.need_q) {
+    stg.cand[0] = a.draft_tok[(size_t)b * L + j] - a.vis_lo;
+    ncand = 1;
+    if (j < D_in && a.sib) {
+      bool open = true;
 #pragma unroll
-        for (int k = 0; k < 7; ++k) {
-          if (open && k < Km1) {
-            int y = a.sib[((size_t)b * a.D + j) * Km1 + k];
-            bool stop = y < 0;
-            y -= a.vis_lo;
-            stop |= (y < 0 || y >= V);
+      for (int k = 0; k < 7; ++k) {
+        if (open && k < Km1) {
+          int y = a.sib[((size_t)b * a.D + j) * Km1 + k];
+          bool stop = y < 0;
+          y -= a.vis_lo;
+          stop |= (y < 0 || y >= V);
 #pragma unroll
-            for (int t = 0; t < 8; ++t) stop |= (t <= k) && (stg.cand[t] == y);
-            if (stop) open = false;
-            else { stg.cand[k + 1] = y; ncand = k + 2; }
-          }
+          for (int t = 0; t < 8; ++t) stop |= (t <= k) && (stg.cand[t] == y);
+          if (stop) open = false;
+          else { stg.cand[k + 1] = y; ncand = k + 2; }
         }
       }
     }
@@ -699,15 +738,15 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
 
   int out_tok = -1, out_stage = 0;
   if (ncand > 0) {
-    // draft row: statistics, then its probabilities at the kept entries
-    const size_t qrow = (size_t)b * a.draft_bstride + (size_t)((a.q_off ? a.q_off[b] : 0) + j) * V;
-    const float* draft_row = a.draft + qrow;
+    // draft row: selection, then its logits at the kept entries
+    const float* draft_row = ld.draft;
+    if (!PF) load_row<BLOCK, NC>(vq, draft_row, V);
     RowStats qs{};
     float qmx, qmn;
-    load_row_maxmin<BLOCK, NC>(v, draft_row, V, sh, qmx, qmn);
+    row_maxmin<BLOCK, NC>(vq, sh, qmx, qmn);
     qs.m = qmx;
     qs.T = a.T;
-    const int nq = select_kept<BLOCK, NC>(v, V, a.top_k, qmx, qmn, sh, sh.bmq, sh.preq, qs);
+    const int nq = select_kept<BLOCK, NC>(vq, V, a.top_k, qmx, qmn, sh, sh.bmq, sh.preq, qs);
     // draft logits at the target's kept entries (by target rank) and at its
     // own kept entries (by draft rank, for its normaliser)
 #pragma unroll
@@ -722,7 +761,7 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
           int rq = sh.preq[c >> 3] + __popc(wq & ((1u << sh4) - 1u));
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float l = comp(v[i], e);
+            const float l = comp(vq[i], e);
             if ((np >> e) & 1u) sh.sp_q[rp++] = l;
             if ((nqb >> e) & 1u) sh.qc[rq++] = l;
           }
@@ -858,6 +897,26 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
   }
 }
 
+// Persistent over rows: workgroup w takes rows w, w + grid, ... With PF the
+// first row's data is loaded before the loop and each later row's while the
+// previous one finishes.
+// One workgroup per row (row = trial * L + window row).
+template <int BLOCK, int NC, bool PF>
+__global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
+  __shared__ VSh<BLOCK, NC> sh;
+  const int row = blockIdx.x;
+  const RowLoad ld = plan_load(a, row);
+  float4 v[NC];
+  if constexpr (PF) {
+    float4 vq[NC];
+    if (ld.need_q) load_row<BLOCK, NC>(vq, ld.draft, a.V);
+    if (ld.need_p) load_row<BLOCK, NC>(v, ld.cur, a.V);
+    verify_row<BLOCK, NC, true>(a, sh, row, ld, v, vq);
+  } else {
+    verify_row<BLOCK, NC, false>(a, sh, row, ld, v, v);
+  }
+}
+
 // ------------------------------------------------------------ finalize
 __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, FinalizeOut o) {
   const int b = blockIdx.x;
@@ -958,20 +1017,14 @@ __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, Finaliz
 }
 
 // ------------------------------------------------------------ launch
-int verify_block_for(int V) {
-  if (V <= 4096) return 256;
-  if (V <= 16384) return 512;
-  if (V <= 32768) return 512;
-  if (V <= 65536) return 1024;
-  return 0;
-}
-
 hipError_t launch_verify(const VerifyArgs& a, const FinalizeOut& o, hipStream_t s) {
-  const dim3 grid(a.L, a.B);
-  if (a.V <= 4096) hipLaunchKernelGGL((k_verify_rows<256, 4>), grid, dim3(256), 0, s, a);
-  else if (a.V <= 16384) hipLaunchKernelGGL((k_verify_rows<512, 8>), grid, dim3(512), 0, s, a);
-  else if (a.V <= 32768) hipLaunchKernelGGL((k_verify_rows<512, 16>), grid, dim3(512), 0, s, a);
-  else if (a.V <= 65536) hipLaunchKernelGGL((k_verify_rows<1024, 16>), grid, dim3(1024), 0, s, a);
+  const long rows = (long)a.B * a.L;
+  if (rows < 1 || rows > 0x7FFFFFFFL) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)rows);
+  if (a.V <= 4096) hipLaunchKernelGGL((k_verify_rows<256, 4, true>), grid, dim3(256), 0, s, a);
+  else if (a.V <= 16384) hipLaunchKernelGGL((k_verify_rows<512, 8, true>), grid, dim3(512), 0, s, a);
+  else if (a.V <= 32768) hipLaunchKernelGGL((k_verify_rows<1024, 8, true>), grid, dim3(1024), 0, s, a);
+  else if (a.V <= 65536) hipLaunchKernelGGL((k_verify_rows<1024, 16, false>), grid, dim3(1024), 0, s, a);
   else return hipErrorInvalidValue;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
