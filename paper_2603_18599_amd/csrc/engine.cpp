@@ -281,7 +281,7 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 64)) || (rc = dalloc(x, &x.st, 1)) ||
       (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)c.L * sjd::kRecInts)))
     return fail(rc);
-  // split-K plan: aim for two workgroups per compute unit
+  // split-K plan: aim for two to three workgroups per compute unit
   int ncu = 256;
   {
     int dev = 0;
@@ -289,7 +289,7 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess)
       ncu = prop.multiProcessorCount;
   }
-  const int target = 2 * ncu;
+  const int target = 5 * ncu / 2;
   x.S_qkv = sjd::gemm_splits(Nq + 2 * Nkv, d, target);
   x.S_o = sjd::gemm_splits(d, Nq, target);
   x.S_gu = sjd::gemm_splits(2 * F, d, target);

@@ -5,7 +5,7 @@
 // weight byte per slot: 64 flop/B at M = 32, far below the MFMA ridge), so
 // the kernel is laid out for the weight stream:
 //  - weights are pre-tiled (see forward.h): a wave reads one 32-row x 64-k
-//    tile per k-step as four contiguous 1 KB loads, kDepth k-steps in flight;
+//    tile per k-step as four contiguous 1 KB loads, the next k-step in flight;
 //  - the activation tile of a k-step (32 rows x 64 k, hi and lo planes, 8 KB)
 //    is staged once per workgroup into LDS (double buffered) and shared by
 //    the four waves, each of which owns a different 32-column block. Loading
@@ -34,7 +34,9 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kGB = 256;
 constexpr int kGWaves = kGB / kWave;
-constexpr int kDepth = 3;  // weight k-steps in flight per wave
+// k-steps held per wave (the current one plus one in flight): deeper rings
+// help a lone workgroup but lose once every compute unit holds several
+constexpr int kRingDepth = 2;
 
 SJD_DEV bf16x8 as_bf16x8(const u32x4& u) { return __builtin_bit_cast(bf16x8, u); }
 
@@ -43,6 +45,14 @@ struct GemmSmem {
   float inv[32];
 };
 
+// The main loop is straight-line code: vector loads return in issue order
+// and the wait before a use covers everything issued earlier, so no load is
+// ever consumed in the step that issued it, loads are never conditional
+// (a branch makes the compiler's wait counts conservative), and within a
+// step the activation chunk is issued before the weight tile. The step count
+// is padded to a multiple of the ring: padded steps reload the last real
+// tile and stage a zero activation tile, so they add nothing.
+template <int kRing>
 __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   __shared__ GemmSmem sm;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
@@ -52,6 +62,8 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   const bool active = nb < nblk;
   const int sp = blockIdx.y;
   const int st0 = (int)((long)T * sp / g.S), st1 = (int)((long)T * (sp + 1) / g.S);
+  const int n = st1 - st0;
+  const int npad = (n + kRing - 1) / kRing * kRing;
 
   // fused RMSNorm: row scale from the chunk sums of squares (loads issued
   // ahead of the weight stream, consumed after it)
@@ -70,52 +82,44 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   f32x16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
-  u32x4 w[kDepth][4];
-  auto load_w = [&](int st, int j) {
-    if (!active) return;
+  u32x4 w[kRing][4], ra[kRing], ral[kRing];
+  // step t of this workgroup's range, clamped to the last real step
+  auto kstep = [&](int t) { return st0 + (t < n ? t : n - 1); };
+  // steps past the range read 4 KB of the (cache-resident, finite) A plane
+  // in place of a weight tile: they are multiplied by a zero tile
+  const uint16_t* wpad = g.A + (size_t)lane * 8;
+  auto issue = [&](int t, int slot) {
+    const int st = kstep(t);
+    ra[slot] = *(const u32x4*)(sap + st * 64);
+    ral[slot] = *(const u32x4*)(salp + st * 64);
+    const uint16_t* src = t < n ? wp + (size_t)st * 2048 : wpad;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      w[j][i] = __builtin_nontemporal_load((const u32x4*)(wp + (size_t)st * 2048 + i * 512));
+    for (int i = 0; i < 4; ++i) w[slot][i] = __builtin_nontemporal_load((const u32x4*)(src + i * 512));
+  };
+  auto stage = [&](int t, int slot, int buf) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    sm.a[buf][0][wave][lane] = t < n ? ra[slot] : z;
+    sm.a[buf][1][wave][lane] = t < n ? ral[slot] : z;
   };
 
-  u32x4 ra, ral;
-  if (st0 < st1) {
-    ra = *(const u32x4*)(sap + st0 * 64);
-    ral = *(const u32x4*)(salp + st0 * 64);
-  }
+  if (n > 0) {
 #pragma unroll
-  for (int p = 0; p < kDepth - 1; ++p)
-    if (st0 + p < st1) load_w(st0 + p, p);
-  if (st0 < st1) {
-    sm.a[0][0][wave][lane] = ra;
-    sm.a[0][1][wave][lane] = ral;
+    for (int t = 0; t < kRing - 1; ++t) issue(t, t);
+    stage(0, 0, 0);
   }
   __syncthreads();
-  for (int st = st0; st < st1; st += kDepth) {
+  for (int t0 = 0; t0 < npad; t0 += kRing) {
 #pragma unroll
-    for (int j = 0; j < kDepth; ++j) {
-      const int cur = st + j;
-      if (cur < st1) {  // uniform over the workgroup
-        const int buf = (cur - st0) & 1;
-        if (cur + kDepth - 1 < st1) load_w(cur + kDepth - 1, (j + kDepth - 1) % kDepth);
-        if (cur + 1 < st1) {
-          ra = *(const u32x4*)(sap + (cur + 1) * 64);
-          ral = *(const u32x4*)(salp + (cur + 1) * 64);
-        }
-        if (active) {
+    for (int u = 0; u < kRing; ++u) {
+      issue(t0 + u + kRing - 1, (u + kRing - 1) % kRing);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const u32x4 ah = sm.a[buf][0][i][lane], al = sm.a[buf][1][i][lane];
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ah), as_bf16x8(w[j][i]), acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(al), as_bf16x8(w[j][i]), acc, 0, 0, 0);
-          }
-        }
-        if (cur + 1 < st1) {
-          sm.a[buf ^ 1][0][wave][lane] = ra;
-          sm.a[buf ^ 1][1][wave][lane] = ral;
-        }
-        __syncthreads();
+      for (int i = 0; i < 4; ++i) {
+        const u32x4 ah = sm.a[u & 1][0][i][lane], al = sm.a[u & 1][1][i][lane];
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ah), as_bf16x8(w[u][i]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(al), as_bf16x8(w[u][i]), acc, 0, 0, 0);
       }
+      stage(t0 + u + 1, (u + 1) % kRing, (u + 1) & 1);
+      __syncthreads();
     }
   }
 
@@ -134,7 +138,7 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
 // Split count along K. Splits that divide the K steps evenly are preferred
 // (an uneven split leaves a tail of workgroups one step longer); among them
 // the one whose workgroup count is nearest the target (by ratio), if within
-// a factor of two, else ceil(target / groups).
+// a factor of two, else ceil(0.8 target / groups).
 int gemm_splits(int N, int K, int target_wgs) {
   const int groups = (N / 32 + kGWaves - 1) / kGWaves;
   const int T = K / 64;
@@ -152,7 +156,9 @@ int gemm_splits(int N, int K, int target_wgs) {
     }
   }
   if (best > 0 && best_r <= 2.0) return best;
-  int S = (target_wgs + groups - 1) / groups;
+  // no even split near the target: stay below it (uneven splits add a tail)
+  const int t2 = target_wgs * 4 / 5;
+  int S = (t2 + groups - 1) / groups;
   if (S > smax) S = smax;
   if (S < 1) S = 1;
   return S;
@@ -161,7 +167,7 @@ int gemm_splits(int N, int K, int target_wgs) {
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M < 1 || g.M > 32 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
   const dim3 grid((g.N / 32 + kGWaves - 1) / kGWaves, g.S);
-  hipLaunchKernelGGL(k_gemm, grid, dim3(kGB), 0, s, g);
+  hipLaunchKernelGGL(k_gemm<kRingDepth>, grid, dim3(kGB), 0, s, g);
   return hipGetLastError();
 }
 
