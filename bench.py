@@ -45,7 +45,159 @@ def parse():
                          "start: right after the prompt")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one 256 MiB device-to-device copy before the timed region (the reference kernel "
+                         "of known size for HBM counter runs) and mark copy + timed region as the profiler's "
+                         "selected region (rocprofv3 --selected-regions)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="read two rocprofv3 --pmc output directories (FETCH_SIZE, WRITE_SIZE) of a "
+                         "--calibrate-copy run of this workload and record the measured HBM bytes per launch "
+                         "in profiles/traffic_<workload>.txt")
     return ap.parse_args()
+
+
+CALIB_BYTES = 256 << 20
+
+
+def kernel_source_hash():
+    """sha256 over the HIP/C++ sources of the library: a recorded traffic
+    figure is reported only while the kernels it was measured on are
+    unchanged."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2603_18599_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".cpp", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+
+
+def recorded_traffic(workload):
+    """Measured HBM bytes per launch (FETCH + WRITE) from the counter record,
+    or None if there is none or the kernels changed since."""
+    try:
+        with open(traffic_file(workload)) as fh:
+            rec = dict(l.strip().split("=", 1) for l in fh if "=" in l and not l.startswith("#"))
+    except OSError:
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(rec["fetch_bytes_per_launch"]) + float(rec["write_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def profiler_region(on):
+    """Resume (on) or pause the profiler's collection (rocprofv3
+    --selected-regions); a no-op when the ROCtx library is absent."""
+    import ctypes
+    for name in ("librocprofiler-sdk-roctx.so.1", "librocprofiler-sdk-roctx.so"):
+        try:
+            lib = ctypes.CDLL(name)
+        except OSError:
+            continue
+        fn = lib.roctxProfilerResume if on else lib.roctxProfilerPause
+        fn.argtypes = [ctypes.c_uint64]
+        fn(0)
+        return
+
+
+def calibration_copy():
+    import torch
+    a = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
+
+
+def read_counter(dirname, counter):
+    """{dispatch id: (kernel name, summed value)} from a rocprofv3 counter_collection.csv"""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(dirname, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {dirname}")
+    out = {}
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                d = int(r["Dispatch_Id"])
+                name, v = out.get(d, (r["Kernel_Name"], 0.0))
+                out[d] = (name, v + float(r["Counter_Value"]))
+    return out
+
+
+def traffic_from(args):
+    """Per-launch HBM bytes from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
+    each scaled by the counter's reading on the calibration copy of known
+    size; written to profiles/traffic_<workload>.txt."""
+    per = {}
+    facs = {}
+    for counter, d in (("FETCH_SIZE", args.traffic_from[0]), ("WRITE_SIZE", args.traffic_from[1])):
+        c = read_counter(d, counter)
+        ids = sorted(c)
+        # the calibration copy is the last large device-to-device copy before
+        # the timed launches (the model set-up may copy earlier)
+        copies = [i for i in ids if "copyBuffer" in c[i][0] and c[i][1] * 1024.0 >= CALIB_BYTES / 8]
+        if args.workload == "verify":
+            launches_all = [i for i in ids if "k_verify_rows" in c[i][0]]
+        else:
+            launches_all = [i for i in ids if "k_build_window" in c[i][0]]
+        copies = [i for i in copies if any(j > i for j in launches_all)]
+        if not copies:
+            raise SystemExit(f"{counter}: no calibration copy found (run with --calibrate-copy)")
+        cal = max(copies)
+        fac = CALIB_BYTES / (c[cal][1] * 1024.0)
+        facs[counter] = fac
+        if args.workload == "verify":
+            launches = [i for i in ids if "k_verify_rows" in c[i][0] and i > cal]
+            tot = []
+            for i in launches:
+                fin = [j for j in ids if j > i and "k_verify_finalize" in c[j][0]]
+                tot.append(c[i][1] + (c[fin[0]][1] if fin else 0.0))
+        else:
+            starts = [i for i in ids if "k_build_window" in c[i][0] and i > cal]
+            tot = []
+            for a, b in zip(starts, starts[1:]):
+                tot.append(sum(c[j][1] for j in ids if a <= j < b))
+        if not tot:
+            raise SystemExit(f"{counter}: no launches of the {args.workload} workload found")
+        per[counter] = sum(tot) / len(tot) * 1024.0 * fac
+    wl = "" if args.workload == "7b" else f" --workload {args.workload}"
+    run = (f"python3 bench.py{wl} --steps 3 --warmup 1 --no-cpu-baseline --no-verify --calibrate-copy"
+           if args.workload != "verify" else "python3 bench.py --workload verify --steps 2 --warmup 1 "
+                                              "--no-cpu-baseline --calibrate-copy")
+    lines = ["# Measured HBM traffic per launch (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE; KiB per dispatch",
+             "# summed over the dispatches of one launch, scaled by the counter's reading on a 256 MiB",
+             "# device-to-device copy in the same run). Reported by bench.py while source_hash matches.",
+             "# Commands (repository root; cd /tmp && export TMPDIR=/tmp first):",
+             f"#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <fetch_dir> -- {run}",
+             f"#   rocprofv3 --pmc WRITE_SIZE --output-format csv -d <write_dir> -- {run}",
+             f"#   python3 bench.py{' --workload ' + args.workload} --traffic-from <fetch_dir> <write_dir>",
+             f"workload={args.workload}",
+             f"source_hash={kernel_source_hash()}",
+             f"fetch_bytes_per_launch={per['FETCH_SIZE']:.0f}",
+             f"write_bytes_per_launch={per['WRITE_SIZE']:.0f}",
+             f"fetch_calibration={facs['FETCH_SIZE']:.4f}",
+             f"write_calibration={facs['WRITE_SIZE']:.4f}"]
+    with open(traffic_file(args.workload), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def progress(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def cpu_cores():
@@ -79,6 +231,9 @@ def bench_verify(args):
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
+    if getattr(args, "calibrate_copy", False):
+        profiler_region(True)
+        calibration_copy()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     nc_sum = torch.zeros((), dtype=torch.int64, device="cuda")
     t0 = time.perf_counter()
@@ -89,6 +244,8 @@ def bench_verify(args):
         nc_sum += out["meta"][:, 0].sum()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    if getattr(args, "calibrate_copy", False):
+        profiler_region(False)
     kern_ms = [a.elapsed_time(b) for a, b in evs]
     avg_ms = sum(kern_ms) / len(kern_ms)
     total_nc = int(nc_sum.item())
@@ -108,7 +265,7 @@ def bench_verify(args):
                        "global_batch": B, "seq_len": L},
                mean_accept_length=mean_nc, verify_GBps=achieved,
                roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                         "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                         "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic("verify"),
                          "kernel": "k_verify_rows + k_verify_finalize", "bytes_per_launch": bytes_per_launch,
                          "avg_launch_ms": avg_ms})
     if not args.no_cpu_baseline:
@@ -165,8 +322,10 @@ def bench_step(args):
     stream = torch.cuda.current_stream()
     K, W = args.steps, args.warmup
     metas = torch.zeros(W + K, 8, dtype=torch.int32, device="cuda")
-    eng.prefill(prompt, seed, stream=stream)
+    if not args.calibrate_copy:  # (counter runs: one prefill only, each dispatch is slow there)
+        eng.prefill(prompt, seed, stream=stream)
     torch.cuda.synchronize()
+    progress(f"model ready; prefill of {prompt.numel()} tokens")
     t_pre = time.perf_counter()
     eng.prefill(prompt, seed, stream=stream)
     torch.cuda.synchronize()
@@ -184,9 +343,14 @@ def bench_step(args):
             eng.prefill(prompt, seed + restarts, stream=stream)
             eng.step(cfg["temperature"], cfg["top_k"], seed, t, out_meta=metas[t], stream=stream)
 
+    progress("prefill done")
     for t in range(W):
         one(t)
     torch.cuda.synchronize()
+    progress("warmup done")
+    if args.calibrate_copy:
+        profiler_region(True)
+        calibration_copy()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
     t0 = time.perf_counter()
     for i in range(K):
@@ -195,6 +359,8 @@ def bench_step(args):
         evs[i][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    if args.calibrate_copy:
+        profiler_region(False)
     m = metas.cpu().numpy()
     ncs = m[W:, 0]
     ns = m[W:, 7]
@@ -219,7 +385,7 @@ def bench_step(args):
                step_latency_p99_ms=float(np.percentile(step_ms, 99)),
                prefill_ms=prefill_ms, kv_rows_mean=n_mean, image_restarts=restarts,
                roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                         "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                         "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic(args.workload),
                          "kernel": "sjd_step (window forward + verification + KV commit)",
                          "bytes_per_launch": total, "weight_bytes": weights, "kv_bytes": kv,
                          "avg_launch_ms": avg_ms,
@@ -271,6 +437,9 @@ def cpu_baseline_step(args, cfg, seed):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        traffic_from(args)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -279,7 +448,8 @@ def main():
     else:
         res = bench_step(args)
         if not args.no_verify:
-            v = bench_verify(argparse.Namespace(steps=10, warmup=2, no_cpu_baseline=True, cpu_sample=0))
+            v = bench_verify(argparse.Namespace(steps=10, warmup=2, no_cpu_baseline=True, cpu_sample=0,
+                                                calibrate_copy=False))
             res["verify"] = {k: v[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length", "verify_GBps",
                                                "roofline", "config")}
     print(json.dumps(res), flush=True)
