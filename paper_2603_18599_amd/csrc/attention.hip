@@ -13,7 +13,12 @@
 //    every key or value load is one contiguous 1 KB per wave;
 //  - a workgroup handles kAttnChunk = 128 keys of one head, 32 per wave; the
 //    four waves merge in LDS and one partial (unnormalised output, max, sum)
-//    per workgroup is combined across chunks by a second kernel.
+//    per workgroup is combined across chunks by a second kernel;
+//  - each wave issues its q chunk, then all of its key and value loads before
+//    any arithmetic (the loads are the critical path); q is shared by the
+//    four waves through LDS (the same LDS later holds the merge).
+// (One wave per workgroup with no merge balances better across compute
+// units but writes four times the partials; measured slower.)
 // Scores use exp2 with the scale folded into log2(e) / sqrt(hd).
 // Precision: q, the cached keys and values, and P are each carried as a
 // pair of bf16 values (hi + lo); every product is formed as hi*hi + hi*lo +
@@ -30,7 +35,10 @@ SJD_DEV bf16x8 to_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8, u);
 
 template <int HD>
 struct AttnSmem {
-  float o[4][32][HD + 1];  // [wave][slot][dim], padded against bank conflicts
+  union {
+    uint4 q[2][HD / 16][kWave];  // Q^T operand (hi, lo) in register order, loaded once per workgroup
+    float o[4][32][HD + 1];      // merge: [wave][slot][dim], padded against bank conflicts
+  };
   float m[4][32];
   float l[4][32];
 };
@@ -54,8 +62,21 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   const bool has = kb < nk;
   const size_t tofs = (size_t)kvh * a.cap * HD + (size_t)kb * HD + (size_t)lane * 8;
 
-  // key tile first (the longest dependency), then q
-  uint4 kh[NQ], kl[NQ];
+  // q first (small, cache-resident; the four waves share it through LDS),
+  // then the key and value tiles (the long dependencies)
+  uint4 qs[2][(NQ + 3) / 4];
+  {
+    const size_t qo = (size_t)slot * a.H * HD + (size_t)h * HD + half * (HD / 2);
+    const uint4* qp = (const uint4*)(a.q + qo);
+    const uint4* qpl = (const uint4*)(a.q_lo + qo);
+#pragma unroll
+    for (int i = 0; i < (NQ + 3) / 4; ++i) {
+      const int t = wave + 4 * i;
+      qs[0][i] = (slot_ok && t < NQ) ? qp[t] : make_uint4(0, 0, 0, 0);
+      qs[1][i] = (slot_ok && t < NQ) ? qpl[t] : make_uint4(0, 0, 0, 0);
+    }
+  }
+  uint4 kh[NQ], kl[NQ], vh[ND][2], vl[ND][2];
   if (has) {
     const uint4* kp = (const uint4*)(a.kc + tofs);
     const uint4* kpl = (const uint4*)(a.kc_lo + tofs);
@@ -64,19 +85,27 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
       kh[t] = kp[t * 64];
       kl[t] = kpl[t * 64];
     }
-  }
-  // Q^T operand: dims half*HD/2 + 8t + e of this slot
-  uint4 qv[NQ], qvl[NQ];
-  {
-    const size_t qo = (size_t)slot * a.H * HD + (size_t)h * HD + half * (HD / 2);
-    const uint4* qp = (const uint4*)(a.q + qo);
-    const uint4* qpl = (const uint4*)(a.q_lo + qo);
+    const uint4* vp = (const uint4*)(a.vt + tofs);
+    const uint4* vpl = (const uint4*)(a.vt_lo + tofs);
 #pragma unroll
-    for (int t = 0; t < NQ; ++t) {
-      qv[t] = slot_ok ? qp[t] : make_uint4(0, 0, 0, 0);
-      qvl[t] = slot_ok ? qpl[t] : make_uint4(0, 0, 0, 0);
+    for (int d = 0; d < ND; ++d)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        vh[d][jj] = vp[(d * 2 + jj) * 64];
+        vl[d][jj] = vpl[(d * 2 + jj) * 64];
+      }
+  }
+  // Q^T operand: lane (slot, half) holds dims half*HD/2 + 8t + e of its
+  // slot; wave w staged chunks t = w, w + 4, ...
+#pragma unroll
+  for (int i = 0; i < (NQ + 3) / 4; ++i) {
+    const int t = wave + 4 * i;
+    if (t < NQ) {
+      sm.q[0][t][lane] = qs[0][i];
+      sm.q[1][t][lane] = qs[1][i];
     }
   }
+  __syncthreads();
 
   f32x16 o[ND];
 #pragma unroll
@@ -91,22 +120,10 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < NQ; ++t) {
       const bf16x8 khb = to_bf16x8(kh[t]), klb = to_bf16x8(kl[t]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, to_bf16x8(qv[t]), s, 0, 0, 0);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, to_bf16x8(qvl[t]), s, 0, 0, 0);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(klb, to_bf16x8(qv[t]), s, 0, 0, 0);
-    }
-    // value tile loads overlap the softmax
-    uint4 vh[ND][2], vl[ND][2];
-    {
-      const uint4* vp = (const uint4*)(a.vt + tofs);
-      const uint4* vpl = (const uint4*)(a.vt_lo + tofs);
-#pragma unroll
-      for (int d = 0; d < ND; ++d)
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          vh[d][jj] = vp[(d * 2 + jj) * 64];
-          vl[d][jj] = vpl[(d * 2 + jj) * 64];
-        }
+      const bf16x8 qh = to_bf16x8(sm.q[0][t][lane]), ql = to_bf16x8(sm.q[1][t][lane]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, qh, s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, ql, s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(klb, qh, s, 0, 0, 0);
     }
     // mask (register r = 8jj + e holds key kb + 16jj + 8half + e): cached
     // keys are visible to every slot, window keys by the ancestor mask
@@ -166,8 +183,10 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
       }
   }
 
-  // ---- merge the four waves: output register r of block d holds dim
+  // ---- merge the four waves (the merge buffer overlays q: wait for every
+  // wave's scores first). Output register r of block d holds dim
   // d*32 + 8(r/4) + 4half + r%4 of this lane's slot
+  __syncthreads();
 #pragma unroll
   for (int d = 0; d < ND; ++d)
 #pragma unroll
