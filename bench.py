@@ -43,6 +43,12 @@ def parse():
     ap.add_argument("--context", default="mid", choices=["mid", "start"],
                     help="mid: time the steps half-way through an image (prompt + n_gen/2 tokens cached); "
                          "start: right after the prompt")
+    ap.add_argument("--mode", default="sjd-pac", choices=["sjd-pac", "sjd", "ac", "pd"],
+                    help="verification mode (Sec. 5.3 ablation): both adaptive continuation and proactive "
+                         "drafting, vanilla SJD, AC only, PD only")
+    ap.add_argument("--L", type=int, default=0, help="window slots (0 = the workload's)")
+    ap.add_argument("--K", type=int, default=0, help="drafting candidates per tree row (0 = the workload's)")
+    ap.add_argument("--D", type=int, default=-1, help="tree depth (-1 = the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -311,7 +317,16 @@ def bench_step(args):
     from paper_2603_18599_amd.sjd import Engine, SjdError
     from synth_inputs import image_history, model_config, model_weights, prompt_tokens
 
-    cfg = model_config(args.workload)
+    over = {"flags": {"sjd-pac": 3, "sjd": 0, "ac": 1, "pd": 2}[args.mode]}
+    if args.L > 0:
+        over["L"] = args.L
+    if args.K > 0:
+        over["K"] = args.K
+    if args.D >= 0:
+        over["D"] = args.D
+    if args.mode in ("sjd", "ac") and args.K <= 0:
+        over["K"], over["D"] = 1, 0  # no drafting tree without PD
+    cfg = model_config(args.workload, **over)
     seed = 11
     w = model_weights(cfg, 1, device="cuda")
     prompt = prompt_tokens(cfg, 2)
@@ -376,7 +391,8 @@ def bench_step(args):
                config={"workload": f"{args.workload}-shaped decoder: {cfg['n_layers']} layers, d={cfg['d_model']}, "
                                    f"{cfg['n_heads']}q/{cfg['n_kv_heads']}kv heads x {cfg['head_dim']}, "
                                    f"SwiGLU {cfg['ffn_dim']}, vocab {cfg['vocab_size']} (sampled {cfg['V']}), "
-                                   f"L={cfg['L']} K={cfg['K']} D={cfg['D']}, top-{cfg['top_k']}, T=1, "
+                                   f"L={cfg['L']} K={cfg['K']} D={cfg['D']}, mode {args.mode}, "
+                                   f"top-{cfg['top_k']}, T=1, "
                                    f"{cfg['n_prompt']}-token prompt, {cfg['n_gen']}-token image, "
                                    f"steps timed from KV length {prompt.numel() - 1}",
                        "global_batch": 1, "seq_len": cfg["L"]},
@@ -424,7 +440,8 @@ def cpu_baseline_step(args, cfg, seed):
                        [(1 << (a + 1)) - 1 for a in range(L)])
     meta = np.array([[0, 0, 0, 0]], np.int32)
     r = orc.verify(logits[None], logits[None], np.array([spine], np.int32), meta, K=cfg["K"], D=cfg["D"],
-                   top_k=cfg["top_k"], T=cfg["temperature"], seed=seed, step=0, vis_lo=cfg["vis_lo"],
+                   top_k=cfg["top_k"], T=cfg["temperature"], flags=cfg.get("flags", 3), seed=seed, step=0,
+                   vis_lo=cfg["vis_lo"],
                    eol_id=cfg["eol_id"], row_len=cfg["row_len"])
     dt = time.perf_counter() - t0
     m.close()

@@ -82,11 +82,14 @@ def test_greedy_window_equals_autoregressive(K, D, flags):
     assert np.mean(ncs) > 1.0  # the window actually ran ahead
 
 
-def test_acceptance_statistics_match_oracle(orc):
+@pytest.mark.parametrize("mode,flags,K,D", [("sjd-pac", 3, 4, 3), ("ac", 1, 1, 0), ("pd", 2, 4, 3), ("sjd", 0, 1, 0)])
+def test_acceptance_statistics_match_oracle(orc, mode, flags, K, D):
     """Mean committed tokens per step of GPU and oracle generations of the
-    tiny model (same weights, different seeds of the same law); the logits
-    differ by the bf16 rounding of the GPU path, far below the sampling noise."""
-    cfg = model_config("tiny", n_gen=128)
+    tiny model (same weights, different seeds of the same law), for each of
+    the paper's ablation modes (vanilla SJD, adaptive continuation only,
+    proactive drafting only, both; Sec. 5.3); the logits differ by the bf16
+    rounding of the GPU path, far below the sampling noise."""
+    cfg = model_config("tiny", n_gen=128, K=K, D=D, flags=flags)
     w, prompt = setup(cfg, wseed=31, pseed=32)
     eng = make_engine(cfg, weights_device(w))
     gpu = []
@@ -100,12 +103,12 @@ def test_acceptance_statistics_match_oracle(orc):
                         cfg["ffn_dim"], cfg["vocab_size"], cfg["vis_lo"], cfg["V"], cfg["max_seq"], 1e-5, 1e4)
     orc_nc = []
     for s in range(12):
-        g = orc.gen_cfg(L=cfg["L"], V=cfg["V"], K=cfg["K"], D=cfg["D"], top_k=0, seed=200 + s,
+        g = orc.gen_cfg(L=cfg["L"], V=cfg["V"], K=cfg["K"], D=cfg["D"], top_k=0, seed=200 + s, flags=flags,
                         n_prompt=cfg["n_prompt"], n_gen=128, mcfg=ocfg, weights=m.w)
         _, steps, hist = orc.generate(g, prompt.numpy().astype(np.int32))
         orc_nc += sum(([i] * int(c) for i, c in enumerate(hist)), [])
     m.close()
     a, b = np.array(gpu, float), np.array(orc_nc, float)
     se = np.sqrt(a.var() / a.size + b.var() / b.size)
-    print(f"mean n_c gpu {a.mean():.3f} ({a.size} steps) oracle {b.mean():.3f} ({b.size} steps) se {se:.3f}")
+    print(f"{mode}: mean n_c gpu {a.mean():.3f} ({a.size} steps) oracle {b.mean():.3f} ({b.size} steps) se {se:.3f}")
     assert abs(a.mean() - b.mean()) < 4 * se + 0.02
