@@ -153,8 +153,8 @@ typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab_size;
   int32_t vis_lo, V;     /* sampled range of the head: rows [vis_lo, vis_lo + V)       */
   int32_t max_seq;       /* KV capacity in tokens (prompt + generated + L)             */
-  int32_t L, K, D;       /* window slots, candidates per depth, maximum depth          */
-  uint32_t flags;        /* SJD_AC | SJD_PD                                             */
+  int32_t L, K, D;       /* window slots (1..64), candidates per depth (1..8), depth   */
+  uint32_t flags;        /* SJD_AC | SJD_PD (0 = vanilla SJD; Sec. 5.3's ablation)     */
   float rms_eps, rope_theta;
   int32_t eol_id, row_len;
   int32_t weights_f32;   /* 1: weights are fp32, 0: bf16                                */
@@ -177,7 +177,8 @@ typedef struct {
 typedef struct sjd_ctx sjd_ctx;
 
 /* Allocates the weight copies, the KV cache and the work buffers on the
- * current device; synchronises `stream` before returning. */
+ * current device; synchronises `stream` before returning. SJD_ENOTSUP for
+ * head_dim other than 64 or 128, or V > 65536. */
 SJD_API int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* stream, sjd_ctx** out);
 
 /* Starts a generation: writes the keys/values of d_prompt[0 .. n-2], makes

@@ -1,4 +1,4 @@
-// Window attention: M <= 32 query slots of one head against the cached keys
+// Window attention: M <= 64 query slots of one head against the cached keys
 // and values plus the window's own (tree-masked) keys, on bf16 MFMA.
 //
 // Layout choices (gfx950, wave64, v_mfma_f32_32x32x16_bf16):
@@ -11,7 +11,8 @@
 //    needs as its B operand, so P never leaves registers;
 //  - the caches are tiled in exactly these operand orders (forward.h), so
 //    every key or value load is one contiguous 1 KB per wave;
-//  - a workgroup handles kAttnChunk = 128 keys of one head, 32 per wave; the
+//  - a workgroup handles kAttnChunk = 128 keys of one head for 32 query slots
+//    (grid z: slots 0-31, 32-63), 32 keys per wave; the
 //    four waves merge in LDS and one partial (unnormalised output, max, sum)
 //    per workgroup is combined across chunks by a second kernel;
 //  - each wave issues its q chunk, then all of its key and value loads before
@@ -56,8 +57,10 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   if (kbeg >= nk) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r32 = lane & 31, half = lane >> 5;
   const int kvh = h / (a.H / a.Hkv);
-  const int slot = r32;
-  const bool slot_ok = slot < M;
+  const int zs = blockIdx.z * 32;  // this workgroup's 32 query slots start here
+  const int slot = r32;            // local slot (MFMA column)
+  const int gslot = zs + slot;
+  const bool slot_ok = gslot < M;
   const int kb = kbeg + wave * 32;  // this wave's key block
   const bool has = kb < nk;
   const size_t tofs = (size_t)kvh * a.cap * HD + (size_t)kb * HD + (size_t)lane * 8;
@@ -66,7 +69,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   // then the key and value tiles (the long dependencies)
   uint4 qs[2][(NQ + 3) / 4];
   {
-    const size_t qo = (size_t)slot * a.H * HD + (size_t)h * HD + half * (HD / 2);
+    const size_t qo = (size_t)(slot_ok ? gslot : 0) * a.H * HD + (size_t)h * HD + half * (HD / 2);
     const uint4* qp = (const uint4*)(a.q + qo);
     const uint4* qpl = (const uint4*)(a.q_lo + qo);
 #pragma unroll
@@ -131,7 +134,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = slot_ok ? s[r] * a.scale : -INFINITY;
     } else {
-      const uint64_t anc = slot_ok ? a.win->anc[slot] : 0ull;
+      const uint64_t anc = slot_ok ? a.win->anc[gslot] : 0ull;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = kb + 16 * (r >> 3) + 8 * half + (r & 7);
@@ -208,7 +211,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
     f[w] = mx == -INFINITY ? 0.0f : exp2f(sm.m[w][sl] - mx);
     ls += sm.l[w][sl] * f[w];
   }
-  float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * 32 + sl) * HD + d0;
+  float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * 64 + zs + sl) * HD + d0;
 #pragma unroll
   for (int i = 0; i < DPT; i += 4) {
     float4 v;
@@ -223,34 +226,34 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
     *(float4*)(wo + i) = v;
   }
   if ((threadIdx.x & 7) == 0) {
-    float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 32 * 2;
-    wml[sl * 2] = mx;
-    wml[sl * 2 + 1] = ls;
+    float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 64 * 2 + (size_t)(zs + sl) * 2;
+    wml[0] = mx;
+    wml[1] = ls;
   }
 }
 
 // out[slot][h*hd + dim] = sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m).
-// grid (H, HD / 32), block 256: thread -> (slot, 4 consecutive dims); the
+// grid (H, HD / 32, slot halves), block 256: thread -> (slot, 4 consecutive dims); the
 // split loop is unrolled so that its loads are in flight together.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   const int h = blockIdx.x, t = threadIdx.x;
-  const int slot = t >> 3, dim0 = blockIdx.y * 32 + (t & 7) * 4;
+  const int slot = blockIdx.z * 32 + (t >> 3), dim0 = blockIdx.y * 32 + (t & 7) * 4;
   if (slot >= a.M) return;
   const int n = a.n_dev ? *a.n_dev : a.n_host;
   const int nk = n + a.M;
   const int ns = (nk + kAttnChunk - 1) / kAttnChunk;
-  const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * 64 + slot * 2;
-  const float* wo = a.ws_o + ((size_t)h * a.nsplit_max * 32 + slot) * HD + dim0;
+  const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * 128 + slot * 2;
+  const float* wo = a.ws_o + ((size_t)h * a.nsplit_max * 64 + slot) * HD + dim0;
   float mx = -INFINITY;
 #pragma unroll 8
-  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, wml[s * 64]);
+  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, wml[s * 128]);
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float ls = 0.0f;
 #pragma unroll 8
   for (int s = 0; s < ns; ++s) {
-    const float2 ml = *(const float2*)(wml + s * 64);
-    const float4 v = *(const float4*)(wo + (size_t)s * 32 * HD);
+    const float2 ml = *(const float2*)(wml + s * 128);
+    const float4 v = *(const float4*)(wo + (size_t)s * 64 * HD);
     const float f = ml.x == -INFINITY ? 0.0f : exp2f(ml.x - mx);
     ls += ml.y * f;
     acc.x += v.x * f;
@@ -269,7 +272,9 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
 }
 
 hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s) {
-  const dim3 g1(a.H, a.nsplit_max), g2(a.H, hd / 32);
+  if (a.M < 1 || a.M > 64) return hipErrorInvalidValue;
+  const unsigned zh = (unsigned)(a.M + 31) / 32;  // 32-slot halves
+  const dim3 g1(a.H, a.nsplit_max, zh), g2(a.H, hd / 32, zh);
   if (hd == 128) {
     hipLaunchKernelGGL(k_attn_partial<128>, g1, dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_attn_combine<128>, g2, dim3(256), 0, s, a);

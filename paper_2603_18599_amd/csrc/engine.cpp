@@ -23,7 +23,7 @@ struct Ctx {
   sjd_config c{};
   int cap = 0;      // KV rows
   int cap_pad = 0;  // row stride of the caches (multiple of the attention chunk)
-  int Mpad = 32;
+  int Mpad = 64;  // activation rows (window slots <= 64; prefill windows of 64 tokens)
   // library-owned weights: embedding and norm gains as bf16 rows, matrices
   // in the GEMM tile layout; lw[l] = {attn_norm, wqkv, -, -, wo, ffn_norm, wgu, -, wd}
   const uint16_t* embed = nullptr;
@@ -83,7 +83,7 @@ int check_config(const sjd_config* c) {
   if (c->vocab_size < 1 || c->V < 32 || c->V % 32 || c->vis_lo < 0 || c->vis_lo + c->V > c->vocab_size)
     return SJD_EINVAL;
   if (c->L < 1 || c->L > 64 || c->K < 1 || c->K > 8 || c->D < 0 || (long)c->K * c->D > c->L) return SJD_EINVAL;
-  if (c->L > 32 || c->V > 65536) return SJD_ENOTSUP;
+  if (c->V > 65536) return SJD_ENOTSUP;
   if (c->max_seq < c->L + 2) return SJD_EINVAL;
   if (c->flags & ~(SJD_AC | SJD_PD)) return SJD_EINVAL;
   if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
@@ -277,8 +277,8 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       (rc = dalloc(x, &x.vt, kv)) || (rc = dalloc(x, &x.vt_lo, kv)) ||
       (rc = dalloc(x, &x.rope, (size_t)x.cap_pad * (hd / 2))) ||
       (rc = dalloc(x, &x.logits[0], (size_t)c.L * c.V)) || (rc = dalloc(x, &x.logits[1], (size_t)c.L * c.V)) ||
-      (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * 32 * hd)) ||
-      (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 64)) || (rc = dalloc(x, &x.st, 1)) ||
+      (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * 64 * hd)) ||
+      (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 128)) || (rc = dalloc(x, &x.st, 1)) ||
       (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)c.L * sjd::kRecInts)))
     return fail(rc);
   // split-K plan: aim for two to three workgroups per compute unit

@@ -15,9 +15,9 @@ constexpr int kGemmMaxSplits = 32;
 // input (q, k, v; gate, up) are tiled one after the other into one [N][K].
 struct GemmArgs {
   const uint16_t* A;     // activations as two bf16 planes (A = hi + lo), 32 rows
-  const uint16_t* A_lo;  // (rows >= M zero), row stride lda
+  const uint16_t* A_lo;  // (64 if M > 32; rows >= M finite), row stride lda
   int lda;
-  int M;               // 1..32
+  int M;               // 1..64
   const uint16_t* W;   // tiled weights [N][K]
   int N, K;            // N multiple of 32, K multiple of 64
   int S;               // workgroups along K = fp32 partial planes (1..kGemmMaxSplits)
@@ -91,8 +91,8 @@ struct AttnArgs {
   int n_host;
   int M, H, Hkv, cap;
   float scale;
-  float* ws_o;           // [H][nsplit_max][32][hd] partial outputs
-  float* ws_ml;          // [H][nsplit_max][32][2]  partial max (log2 domain) and sum
+  float* ws_o;           // [H][nsplit_max][64][hd] partial outputs (per query slot)
+  float* ws_ml;          // [H][nsplit_max][64][2]  partial max (log2 domain) and sum
   int nsplit_max;
   uint16_t* out;         // [Mpad][ldo]
   uint16_t* out_lo;

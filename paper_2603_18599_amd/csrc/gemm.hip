@@ -1,5 +1,5 @@
 // Skinny bf16 GEMM for the window forward: C[M x N] = A[M x K] . W[N x K]^T
-// with M <= 32 window slots, on gfx950 MFMA (v_mfma_f32_32x32x16_bf16).
+// with M <= 64 window slots, on gfx950 MFMA (v_mfma_f32_32x32x16_bf16).
 //
 // The window forward is bound by streaming the weights from HBM (2 flop per
 // weight byte per slot: 64 flop/B at M = 32, far below the MFMA ridge), so
@@ -40,9 +40,10 @@ constexpr int kRingDepth = 2;
 
 SJD_DEV bf16x8 as_bf16x8(const u32x4& u) { return __builtin_bit_cast(bf16x8, u); }
 
+template <int MT>
 struct GemmSmem {
-  u32x4 a[2][2][4][kWave];  // [buffer][hi / lo][16-byte chunk][lane]: one A tile in MFMA operand order
-  float inv[32];
+  u32x4 a[2][2][MT][4][kWave];  // [buffer][hi / lo][row tile][16-byte chunk][lane]: A tiles in MFMA operand order
+  float inv[32 * MT];
 };
 
 // The main loop is straight-line code: vector loads return in issue order
@@ -52,9 +53,10 @@ struct GemmSmem {
 // step the activation chunk is issued before the weight tile. The step count
 // is padded to a multiple of the ring: padded steps reload the last real
 // tile and stage a zero activation tile, so they add nothing.
-template <int kRing>
+// MT = 32-row tiles of A (M <= 32 MT).
+template <int kRing, int MT>
 __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
-  __shared__ GemmSmem sm;
+  __shared__ GemmSmem<MT> sm;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
   const int r32 = lane & 31, half = lane >> 5;
   const int T = g.K / 64, nblk = g.N / 32;
@@ -72,17 +74,20 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   if (has_ss)
     for (int c = 0; c < g.ss_n; ++c) ssum += g.ss[(size_t)threadIdx.x * g.ss_n + c];
 
-  // element (row r32, k = kb*64 + half*32 + i*8 + e) of a tile sits in chunk
-  // i of lane r32 + 32*half; wave w stages chunk w of every lane
+  // element (row mt*32 + r32, k = kb*64 + half*32 + i*8 + e) of a tile sits
+  // in chunk i of lane r32 + 32*half of row tile mt; wave w stages chunk w
   const uint16_t* wp = g.W + (size_t)(active ? nb : 0) * T * 2048 + (size_t)lane * 8;
   const size_t aofs = (size_t)r32 * g.lda + half * 32 + wave * 8;
+  const size_t tstride = (size_t)32 * g.lda;  // next row tile
   const uint16_t* sap = g.A + aofs;
   const uint16_t* salp = g.A_lo + aofs;
 
-  f32x16 acc;
+  f32x16 acc[MT];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
-  u32x4 w[kRing][4], ra[kRing], ral[kRing];
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+  u32x4 w[kRing][4], ra[kRing][MT], ral[kRing][MT];
   // step t of this workgroup's range, clamped to the last real step
   auto kstep = [&](int t) { return st0 + (t < n ? t : n - 1); };
   // steps past the range read 4 KB of the (cache-resident, finite) A plane
@@ -90,16 +95,22 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   const uint16_t* wpad = g.A + (size_t)lane * 8;
   auto issue = [&](int t, int slot) {
     const int st = kstep(t);
-    ra[slot] = *(const u32x4*)(sap + st * 64);
-    ral[slot] = *(const u32x4*)(salp + st * 64);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      ra[slot][mt] = *(const u32x4*)(sap + mt * tstride + st * 64);
+      ral[slot][mt] = *(const u32x4*)(salp + mt * tstride + st * 64);
+    }
     const uint16_t* src = t < n ? wp + (size_t)st * 2048 : wpad;
 #pragma unroll
     for (int i = 0; i < 4; ++i) w[slot][i] = __builtin_nontemporal_load((const u32x4*)(src + i * 512));
   };
   auto stage = [&](int t, int slot, int buf) {
     const u32x4 z = {0u, 0u, 0u, 0u};
-    sm.a[buf][0][wave][lane] = t < n ? ra[slot] : z;
-    sm.a[buf][1][wave][lane] = t < n ? ral[slot] : z;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      sm.a[buf][0][mt][wave][lane] = t < n ? ra[slot][mt] : z;
+      sm.a[buf][1][mt][wave][lane] = t < n ? ral[slot][mt] : z;
+    }
   };
 
   if (n > 0) {
@@ -113,26 +124,31 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
     for (int u = 0; u < kRing; ++u) {
       issue(t0 + u + kRing - 1, (u + kRing - 1) % kRing);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const u32x4 ah = sm.a[u & 1][0][i][lane], al = sm.a[u & 1][1][i][lane];
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ah), as_bf16x8(w[u][i]), acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(al), as_bf16x8(w[u][i]), acc, 0, 0, 0);
-      }
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const u32x4 ah = sm.a[u & 1][0][mt][i][lane], al = sm.a[u & 1][1][mt][i][lane];
+          acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ah), as_bf16x8(w[u][i]), acc[mt], 0, 0, 0);
+          acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(al), as_bf16x8(w[u][i]), acc[mt], 0, 0, 0);
+        }
       stage(t0 + u + 1, (u + 1) % kRing, (u + 1) & 1);
       __syncthreads();
     }
   }
 
-  if (threadIdx.x < 32) sm.inv[threadIdx.x] = has_ss ? rsqrtf(ssum * g.inv_d + g.eps) : 1.0f;
+  if (threadIdx.x < 32 * MT) sm.inv[threadIdx.x] = has_ss ? rsqrtf(ssum * g.inv_d + g.eps) : 1.0f;
   __syncthreads();
   if (!active) return;
-  // accumulator register r of lane l holds row 8(r/4) + 4(l/32) + r%4, column l%32
+  // accumulator register r of lane l holds row 8(r/4) + 4(l/32) + r%4 of
+  // its row tile, column l%32
   float* out = g.out + (size_t)sp * g.plane + (size_t)nb * 32 + r32;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int m = 8 * (r / 4) + 4 * half + (r % 4);
-    if (m < g.M) out[(size_t)m * g.ldo] = acc[r] * sm.inv[m];
-  }
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = mt * 32 + 8 * (r / 4) + 4 * half + (r % 4);
+      if (m < g.M) out[(size_t)m * g.ldo] = acc[mt][r] * sm.inv[m];
+    }
 }
 
 // Split count along K. Splits that divide the K steps evenly are preferred
@@ -165,9 +181,10 @@ int gemm_splits(int N, int K, int target_wgs) {
 }
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
-  if (g.M < 1 || g.M > 32 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
+  if (g.M < 1 || g.M > 64 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
   const dim3 grid((g.N / 32 + kGWaves - 1) / kGWaves, g.S);
-  hipLaunchKernelGGL(k_gemm<kRingDepth>, grid, dim3(kGB), 0, s, g);
+  if (g.M <= 32) hipLaunchKernelGGL((k_gemm<kRingDepth, 1>), grid, dim3(kGB), 0, s, g);
+  else hipLaunchKernelGGL((k_gemm<kRingDepth, 2>), grid, dim3(kGB), 0, s, g);
   return hipGetLastError();
 }
 

@@ -22,6 +22,11 @@ CASES = [
     ("tiny", {"L": 7, "K": 2, "D": 3, "n_prompt": 1}),
     ("mid", {}),
     ("7b", {"n_prompt": 16}),
+    # windows of up to 64 slots: two 32-row GEMM tiles, two attention slot
+    # halves; prompts longer than one 64-token prefill window
+    ("tiny", {"L": 64, "n_prompt": 100}),
+    ("7b", {"n_layers": 2, "L": 64, "n_prompt": 70}),
+    ("8b", {"n_layers": 2, "L": 48, "n_prompt": 40}),
 ]
 
 

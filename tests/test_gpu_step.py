@@ -65,9 +65,9 @@ def test_step_row_ends_and_vis_range():
             assert cfg["vis_lo"] <= t < cfg["vis_lo"] + cfg["V"]
 
 
-@pytest.mark.parametrize("K,D,flags", [(4, 3, 3), (2, 2, 1), (1, 0, 0)])
-def test_greedy_window_equals_autoregressive(K, D, flags):
-    base = model_config("tiny", K=K, D=D, flags=flags)
+@pytest.mark.parametrize("K,D,flags,L", [(4, 3, 3, 16), (2, 2, 1, 16), (1, 0, 0, 16), (4, 3, 3, 64)])
+def test_greedy_window_equals_autoregressive(K, D, flags, L):
+    base = model_config("tiny", K=K, D=D, flags=flags, L=L)
     w, prompt = setup(base, wseed=21, pseed=22)
     wd = weights_device(w)
     eng = make_engine(base, wd)
@@ -82,14 +82,15 @@ def test_greedy_window_equals_autoregressive(K, D, flags):
     assert np.mean(ncs) > 1.0  # the window actually ran ahead
 
 
-@pytest.mark.parametrize("mode,flags,K,D", [("sjd-pac", 3, 4, 3), ("ac", 1, 1, 0), ("pd", 2, 4, 3), ("sjd", 0, 1, 0)])
-def test_acceptance_statistics_match_oracle(orc, mode, flags, K, D):
+@pytest.mark.parametrize("mode,flags,K,D,L", [("sjd-pac", 3, 4, 3, 16), ("ac", 1, 1, 0, 16), ("pd", 2, 4, 3, 16),
+                                              ("sjd", 0, 1, 0, 16), ("sjd-pac", 3, 4, 3, 64)])
+def test_acceptance_statistics_match_oracle(orc, mode, flags, K, D, L):
     """Mean committed tokens per step of GPU and oracle generations of the
     tiny model (same weights, different seeds of the same law), for each of
     the paper's ablation modes (vanilla SJD, adaptive continuation only,
     proactive drafting only, both; Sec. 5.3); the logits differ by the bf16
     rounding of the GPU path, far below the sampling noise."""
-    cfg = model_config("tiny", n_gen=128, K=K, D=D, flags=flags)
+    cfg = model_config("tiny", n_gen=128, K=K, D=D, flags=flags, L=L)
     w, prompt = setup(cfg, wseed=31, pseed=32)
     eng = make_engine(cfg, weights_device(w))
     gpu = []
@@ -110,5 +111,5 @@ def test_acceptance_statistics_match_oracle(orc, mode, flags, K, D):
     m.close()
     a, b = np.array(gpu, float), np.array(orc_nc, float)
     se = np.sqrt(a.var() / a.size + b.var() / b.size)
-    print(f"{mode}: mean n_c gpu {a.mean():.3f} ({a.size} steps) oracle {b.mean():.3f} ({b.size} steps) se {se:.3f}")
+    print(f"{mode} L={L}: mean n_c gpu {a.mean():.3f} ({a.size} steps) oracle {b.mean():.3f} ({b.size} steps) se {se:.3f}")
     assert abs(a.mean() - b.mean()) < 4 * se + 0.02
