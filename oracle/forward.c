@@ -218,3 +218,9 @@ int orc_forward(const orc_model_cfg* c, const orc_weights* w, orc_kv* kv, int n,
   free(x); free(xn); free(q); free(kk); free(vv); free(att); free(tmp); free(g); free(u);
   return 0;
 }
+
+/* Classifier-free guidance (Sec. 5.1): l = l_u + w (l_c - l_u), fp64. */
+void orc_cfg_combine(const float* l_c, const float* l_u, float w, long n, float* out) {
+  for (long i = 0; i < n; ++i) out[i] = (float)((double)l_u[i] + (double)w * ((double)l_c[i] - (double)l_u[i]));
+}
+

@@ -52,6 +52,10 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
   if (!cfg->mcfg && (cfg->toy_V != V || vc->vis_lo != 0)) return -1;
   const int cap = np + cfg->n_gen + 2 * L + 2;
   if (cfg->mcfg && cfg->mcfg->max_seq < cap) return -1;
+  const int cfg_on = cfg->cfg_w != 0.0f;
+  const int nu = cfg_on ? cfg->n_uncond : 0;
+  if (cfg_on && (!cfg->mcfg || !cfg->uncond || nu < 1 || cfg->mcfg->max_seq < nu + cfg->n_gen + 2 * L + 2))
+    return -1;
   int32_t* hist = (int32_t*)calloc((size_t)cap, sizeof(int32_t));
   float* cur = (float*)malloc(sizeof(float) * (size_t)L * V);
   float* prev = (float*)malloc(sizeof(float) * (size_t)L * V);
@@ -62,8 +66,12 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
   int32_t* sib = (int32_t*)malloc(sizeof(int32_t) * (size_t)(D * Km1 + 1));
   int32_t* osib = (int32_t*)malloc(sizeof(int32_t) * (size_t)(D * Km1 + 1));
   orc_kv* kv = cfg->mcfg ? orc_kv_new(cfg->mcfg) : NULL;
+  orc_kv* kvu = cfg_on ? orc_kv_new(cfg->mcfg) : NULL;          /* unconditional stream */
+  float* curu = cfg_on ? (float*)malloc(sizeof(float) * (size_t)L * V) : NULL;
+  int32_t upos[64];
   int ret = -1;
-  if (!hist || !cur || !prev || !dr || !ctx || !sib || !osib || (cfg->mcfg && !kv)) goto done;
+  if (!hist || !cur || !prev || !dr || !ctx || !sib || !osib || (cfg->mcfg && !kv) || (cfg_on && (!kvu || !curu)))
+    goto done;
 
   memcpy(hist, prompt, sizeof(int32_t) * (size_t)np);
   int n = np - 1; /* cached rows; hist[n] is the pending token */
@@ -76,6 +84,21 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
         anc[a] = (a == 63) ? ~0ull : ((1ull << (a + 1)) - 1ull);
       }
       if (orc_forward(cfg->mcfg, cfg->w, kv, s0, stok, spos, anc, M, NULL) != 0) goto done;
+    }
+  }
+  /* unconditional stream: its own prompt, its own rows; nu_c = its cached
+   * rows, pend_u its pending token until the first step commits */
+  int nu_c = nu - 1;
+  int32_t pend_u = cfg_on ? cfg->uncond[nu - 1] : 0;
+  if (cfg_on) {
+    for (int s0 = 0; s0 < nu_c; s0 += 64) {
+      int M = nu_c - s0 < 64 ? nu_c - s0 : 64;
+      for (int a = 0; a < M; ++a) {
+        stok[a] = cfg->uncond[s0 + a];
+        spos[a] = s0 + a;
+        anc[a] = (a == 63) ? ~0ull : ((1ull << (a + 1)) - 1ull);
+      }
+      if (orc_forward(cfg->mcfg, cfg->w, kvu, s0, stok, spos, anc, M, NULL) != 0) goto done;
     }
   }
   /* initial window: all placeholders without a draft distribution */
@@ -106,6 +129,15 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
     }
     if (kv) {
       if (orc_forward(cfg->mcfg, cfg->w, kv, n, stok, spos, anc, L, cur) != 0) goto done;
+      if (cfg_on) {
+        /* same window, unconditional context and positions */
+        const int32_t t0 = stok[0];
+        stok[0] = pend_u;
+        for (int a = 0; a < L; ++a) upos[a] = spos[a] - n + nu_c;
+        if (orc_forward(cfg->mcfg, cfg->w, kvu, nu_c, stok, upos, anc, L, curu) != 0) goto done;
+        stok[0] = t0;
+        orc_cfg_combine(cur, curu, cfg->cfg_w, (long)L * V, cur);
+      }
     } else {
       for (int a = 0; a < L; ++a) {
         int len = 0;
@@ -127,8 +159,13 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
     if (orc_verify(&c1, &io) != 0) goto done;
     const int n_c = ometa[0], r = ometa[1], acc_k = ometa[5];
     if (kv && acc_k >= 2) orc_kv_move(kv, n + n_s + r * Km1 + (acc_k - 2), n + r + 1);
+    if (cfg_on && acc_k >= 2) orc_kv_move(kvu, nu_c + n_s + r * Km1 + (acc_k - 2), nu_c + r + 1);
     for (int i = 0; i < n_c; ++i) hist[n + 1 + i] = otok[i];
     n += n_c;
+    if (cfg_on && n_c > 0) {
+      nu_c += n_c;
+      pend_u = otok[n_c - 1];
+    }
     gen += n_c;
     if (nc_hist) nc_hist[n_c] += 1;
     memcpy(spine, onext, sizeof(int32_t) * (size_t)L);
@@ -142,8 +179,9 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
   if (steps_out) *steps_out = step;
   ret = gen;
 done:
-  free(hist); free(cur); free(prev); free(dr); free(ctx); free(sib); free(osib);
+  free(hist); free(cur); free(prev); free(dr); free(ctx); free(sib); free(osib); free(curu);
   orc_kv_free(kv);
+  orc_kv_free(kvu);
   return ret;
 }
 

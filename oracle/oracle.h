@@ -169,6 +169,14 @@ int orc_forward(const orc_model_cfg* cfg, const orc_weights* w, orc_kv* kv, int 
                 const int32_t* tok, const int32_t* pos, const uint64_t* anc, int M,
                 float* logits);
 
+/* ---------- classifier-free guidance ----------------------------------------
+ * The paper samples with a CFG weight of 3 (Sec. 5.1). Reading: the standard
+ * logit-space guidance of autoregressive image models, l = l_u + w (l_c - l_u)
+ * with l_c the logits under the text prompt and l_u under the unconditional
+ * prompt, evaluated in fp64 and rounded once; the guided logits are what is
+ * sampled and what the next step's drafts are verified against. */
+void orc_cfg_combine(const float* l_c, const float* l_u, float w, long n, float* out);
+
 /* ---------- generation driver (prefill + repeated steps) ------------------- */
 
 /* Tabular toy model over V tokens: the logits of a slot are a hash of its
@@ -184,6 +192,13 @@ typedef struct {
   /* model: exactly one of these */
   const orc_model_cfg* mcfg; const orc_weights* w;   /* transformer */
   int32_t toy_V; uint64_t toy_salt;                  /* toy model (mcfg NULL) */
+  /* classifier-free guidance (transformer only): weight cfg_w != 0 enables
+   * a second, unconditional stream with its own cache, prefilled from
+   * uncond[0..n_uncond); its window holds the same tokens (its first
+   * pending token is uncond[n_uncond-1]) at its own positions. */
+  float cfg_w;
+  const int32_t* uncond;
+  int32_t n_uncond;
 } orc_gen_cfg;
 
 /* Generates up to n_gen tokens after prompt[0..n_prompt). out_tok receives

@@ -44,7 +44,8 @@ class Weights(C.Structure):
 class GenCfg(C.Structure):
     _fields_ = [("v", VerifyCfg), ("n_prompt", C.c_int32), ("n_gen", C.c_int32),
                 ("max_steps", C.c_int32), ("mcfg", C.c_void_p), ("w", C.c_void_p),
-                ("toy_V", C.c_int32), ("toy_salt", C.c_uint64)]
+                ("toy_V", C.c_int32), ("toy_salt", C.c_uint64),
+                ("cfg_w", C.c_float), ("uncond", C.c_void_p), ("n_uncond", C.c_int32)]
 
 
 _lib = None
@@ -72,6 +73,7 @@ def lib():
         _lib.orc_verify.argtypes = [C.POINTER(VerifyCfg), C.POINTER(VerifyIO)]
         _lib.orc_kv_new.restype = C.c_void_p
         _lib.orc_kv_new.argtypes = [C.POINTER(ModelCfg)]
+        _lib.orc_cfg_combine.argtypes = [C.c_void_p, C.c_void_p, C.c_float, C.c_long, C.c_void_p]
         _lib.orc_kv_free.argtypes = [C.c_void_p]
         _lib.orc_kv_move.argtypes = [C.c_void_p, C.c_int, C.c_int]
         _lib.orc_forward.argtypes = [C.POINTER(ModelCfg), C.POINTER(Weights), C.c_void_p, C.c_int,
@@ -175,13 +177,28 @@ def toy_logits(ctx, V, salt):
     return out
 
 
+def cfg_combine(l_c, l_u, w):
+    """Classifier-free guidance l_u + w (l_c - l_u) (Sec. 5.1), fp64 rounded once."""
+    l_c = np.ascontiguousarray(l_c, dtype=np.float32)
+    l_u = np.ascontiguousarray(l_u, dtype=np.float32)
+    assert l_c.shape == l_u.shape
+    out = np.empty_like(l_c)
+    lib().orc_cfg_combine(_p(l_c), _p(l_u), w, l_c.size, _p(out))
+    return out
+
+
 def gen_cfg(*, L, V, K, D, top_k=0, T=1.0, flags=AC | PD, seed=0, n_prompt, n_gen, max_steps=100000,
-            toy_salt=0, vis_lo=0, eol_id=-1, row_len=0, mcfg=None, weights=None):
+            toy_salt=0, vis_lo=0, eol_id=-1, row_len=0, mcfg=None, weights=None, cfg_w=0.0, uncond=None):
+    """Generation config. With cfg_w != 0 (transformer only), `uncond` is the
+    unconditional prompt (kept alive on the returned object)."""
     vc = VerifyCfg(1, L, V, K, D, top_k, T, flags, seed, 0, vis_lo, eol_id, row_len, 0)
+    u = None if uncond is None else np.ascontiguousarray(uncond, dtype=np.int32)
     g = GenCfg(vc, n_prompt, n_gen, max_steps,
                C.addressof(mcfg) if mcfg is not None else None,
                C.addressof(weights) if weights is not None else None,
-               V if mcfg is None else 0, toy_salt)
+               V if mcfg is None else 0, toy_salt, cfg_w, _p(u) if u is not None else None,
+               0 if u is None else u.size)
+    g._uncond = u
     return g
 
 
