@@ -158,6 +158,10 @@ typedef struct {
   float rms_eps, rope_theta;
   int32_t eol_id, row_len;
   int32_t weights_f32;   /* 1: weights are fp32, 0: bf16                                */
+  float cfg_w;           /* classifier-free guidance weight w (Sec. 5.1 uses 3); 0 = off.
+                            On: the context keeps a second (unconditional) stream,
+                            prefilled by sjd_prefill_cfg, and every step samples from
+                            l_u + w (l_c - l_u); needs L <= 32 (SJD_ENOTSUP otherwise) */
 } sjd_config;
 
 /* Device pointers, row-major [out][in] (a Linear layer's layout), bf16 or
@@ -186,6 +190,15 @@ SJD_API int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* stream, 
  * (stream tag 6, step word 0xFFFFFFFF). n >= 1, n + L <= max_seq. */
 SJD_API int sjd_prefill(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, uint64_t seed, void* stream);
 
+/* sjd_prefill for a guided context (cfg_w != 0; SJD_EINVAL otherwise, and
+ * sjd_prefill is SJD_EINVAL on a guided context): d_prompt[0..n) is the
+ * text prompt, d_uncond[0..n_u) the unconditional prompt, prefilled into the
+ * second stream's cache. Both streams then receive the same window tokens
+ * (the second stream's first pending token is d_uncond[n_u-1]) at their own
+ * positions. n, n_u >= 1; n + L <= max_seq and n_u + L <= max_seq. */
+SJD_API int sjd_prefill_cfg(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, const int32_t* d_uncond,
+                            int32_t n_u, uint64_t seed, void* stream);
+
 /* One SJD-PAC iteration (Alg. 1): window forward, verification, drafting,
  * KV commit. Outputs (device, may be NULL): d_out_meta[8] as in sjd_verify
  * plus word 7 = cached rows after the step; d_out_tok[L] committed tokens;
@@ -195,7 +208,7 @@ SJD_API int sjd_step(sjd_ctx* ctx, float temperature, int32_t top_k, uint64_t se
              int32_t* d_out_meta, int32_t* d_out_tok, int32_t* d_out_next, void* stream);
 
 /* Window forward only (no verification): logits of the current window into
- * d_logits[L][V]. For parity tests. */
+ * d_logits[L][V] (a guided context: the guided logits). For parity tests. */
 SJD_API int sjd_forward_window(sjd_ctx* ctx, float* d_logits, void* stream);
 
 SJD_API void sjd_destroy(sjd_ctx* ctx);

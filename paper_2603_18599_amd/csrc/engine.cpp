@@ -8,6 +8,7 @@
 #include <array>
 #include <cmath>
 #include <cstring>
+#include <utility>
 #include <vector>
 
 #include "forward.h"
@@ -41,6 +42,11 @@ struct Ctx {
   uint16_t *hbuf = nullptr, *hbuf_lo = nullptr;
   uint16_t *kc = nullptr, *kc_lo = nullptr;
   uint16_t *vt = nullptr, *vt_lo = nullptr;
+  // guided contexts: the unconditional stream's caches, and its position
+  // offset from the text stream (n_uncond - n_prompt)
+  bool guided = false;
+  uint16_t *kc2 = nullptr, *kc2_lo = nullptr, *vt2 = nullptr, *vt2_lo = nullptr;
+  int delta = 0;
   float2* rope = nullptr;
   float* logits[2] = {nullptr, nullptr};
   float* attn_o = nullptr;
@@ -87,6 +93,8 @@ int check_config(const sjd_config* c) {
   if (c->max_seq < c->L + 2) return SJD_EINVAL;
   if (c->flags & ~(SJD_AC | SJD_PD)) return SJD_EINVAL;
   if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
+  if (!std::isfinite(c->cfg_w)) return SJD_EINVAL;
+  if (c->cfg_w != 0.0f && c->L > 32) return SJD_ENOTSUP;  // two streams of L rows in 64
   return SJD_OK;
 }
 
@@ -100,7 +108,11 @@ int check_config(const sjd_config* c) {
     if ((e) != hipSuccess) return SJD_EHIP;      \
   } while (0)
 
-int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, hipStream_t s) {
+// Window forward of M rows. sm.cfg: a guided window (two streams, see
+// Streams); otherwise one stream on the main caches, or on the unconditional
+// stream's caches with second (its prefill).
+int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, const sjd::Streams& sm, bool second,
+            hipStream_t s) {
   const sjd_config& c = x.c;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv;
@@ -115,16 +127,25 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, hipS
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& w = x.lw[l];
     const size_t lofs = (size_t)l * Hkv * x.cap_pad * hd;
-    sjd::KvPlanes kv{x.q, x.q_lo, x.kc + lofs, x.kc_lo + lofs, x.vt + lofs, x.vt_lo + lofs};
+    sjd::KvPlanes kv{x.q, x.q_lo, x.kc + lofs, x.kc_lo + lofs, x.vt + lofs, x.vt_lo + lofs,
+                     nullptr, nullptr, nullptr, nullptr};
+    if (x.guided) {
+      kv.kc2 = x.kc2 + lofs; kv.kc2_lo = x.kc2_lo + lofs; kv.vt2 = x.vt2 + lofs; kv.vt2_lo = x.vt2_lo + lofs;
+      if (second) {
+        std::swap(kv.kc, kv.kc2); std::swap(kv.kc_lo, kv.kc2_lo);
+        std::swap(kv.vt, kv.vt2); std::swap(kv.vt_lo, kv.vt2_lo);
+      }
+    }
     HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, pend, rplane, w[0], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
     sjd::GemmArgs g = normed;
     g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = w[1]; g.N = Nqkv; g.K = d; g.S = x.S_qkv;
     g.out = x.qkv; g.plane = qplane; g.ldo = Nqkv;
     HIPTRY(sjd::launch_gemm(g, s));
     HIPTRY(sjd::launch_rope_kv(x.qkv, x.S_qkv, qplane, x.win, n_dev, n_host, M, H, Hkv, hd, x.rope, kv, x.cap_pad,
-                               s));
+                               sm, s));
     sjd::AttnArgs a{};
     a.q = x.q; a.q_lo = x.q_lo; a.kc = kv.kc; a.kc_lo = kv.kc_lo; a.vt = kv.vt; a.vt_lo = kv.vt_lo; a.win = x.win;
+    a.kc2 = kv.kc2; a.kc2_lo = kv.kc2_lo; a.vt2 = kv.vt2; a.vt2_lo = kv.vt2_lo; a.st = sm;
     a.n_dev = n_dev; a.n_host = n_host; a.M = M; a.H = H; a.Hkv = Hkv; a.cap = x.cap_pad;
     a.scale = (float)(1.4426950408889634 / std::sqrt((double)hd));
     a.ws_o = x.attn_o; a.ws_ml = x.attn_ml; a.nsplit_max = x.nsplit_max; a.out = x.att; a.out_lo = x.att_lo;
@@ -151,6 +172,10 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, hipS
     sjd::GemmArgs g = normed;
     g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = x.head; g.N = c.V; g.K = d; g.S = 1;
     g.out = logits; g.plane = 0; g.ldo = c.V;
+    if (sm.cfg) {  // rows [0, L) of the output: guided logits
+      g.cfg_rows = sm.L;
+      g.cfg_w = c.cfg_w;
+    }
     HIPTRY(sjd::launch_gemm(g, s));
   }
   return SJD_OK;
@@ -166,7 +191,8 @@ int cache_check(Ctx& x) {
     }
   }
   long long pending = x.steps - 1 - x.known_step;
-  long long bound = (long long)x.known_n + pending * x.c.L;
+  const int ahead = x.delta > 0 ? x.delta : 0;  // the unconditional stream runs ahead by delta
+  long long bound = (long long)x.known_n + ahead + pending * x.c.L;
   if (bound + x.c.L <= x.cap) return SJD_OK;
   // wait for the newest step and use its exact value
   for (int i = 0; i < kRing; ++i) {
@@ -176,7 +202,7 @@ int cache_check(Ctx& x) {
       x.known_n = x.h_n[i];
     }
   }
-  if ((long long)x.known_n + x.c.L > x.cap) return SJD_ESTATE;
+  if ((long long)x.known_n + ahead + x.c.L > x.cap) return SJD_ESTATE;
   return SJD_OK;
 }
 
@@ -198,6 +224,7 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   Ctx& x = h->x;
   x.c = *cfg;
   const sjd_config& c = x.c;
+  x.guided = c.cfg_w != 0.0f;
   auto fail = [&](int rc) {
     sjd_destroy(h);
     return rc;
@@ -275,6 +302,8 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       (rc = dalloc(x, &x.att_lo, (size_t)Mp * x.ld_q)) || (rc = dalloc(x, &x.hbuf, (size_t)Mp * x.ld_f)) ||
       (rc = dalloc(x, &x.hbuf_lo, (size_t)Mp * x.ld_f)) || (rc = dalloc(x, &x.kc, kv)) || (rc = dalloc(x, &x.kc_lo, kv)) ||
       (rc = dalloc(x, &x.vt, kv)) || (rc = dalloc(x, &x.vt_lo, kv)) ||
+      (x.guided && ((rc = dalloc(x, &x.kc2, kv)) || (rc = dalloc(x, &x.kc2_lo, kv)) ||
+                    (rc = dalloc(x, &x.vt2, kv)) || (rc = dalloc(x, &x.vt2_lo, kv)))) ||
       (rc = dalloc(x, &x.rope, (size_t)x.cap_pad * (hd / 2))) ||
       (rc = dalloc(x, &x.logits[0], (size_t)c.L * c.V)) || (rc = dalloc(x, &x.logits[1], (size_t)c.L * c.V)) ||
       (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * 64 * hd)) ||
@@ -303,9 +332,9 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     return fail(rc);
   // zero the caches (rows past the fill are read, masked, by the attention
   // tiles) and the activation pad rows
-  void* zero[] = {x.kc, x.kc_lo, x.vt, x.vt_lo};
+  void* zero[] = {x.kc, x.kc_lo, x.vt, x.vt_lo, x.kc2, x.kc2_lo, x.vt2, x.vt2_lo};
   bool ok = hipMemsetAsync(x.st, 0, sizeof(sjd::DevState), s) == hipSuccess;
-  for (void* p : zero) ok = ok && hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess;
+  for (void* p : zero) ok = ok && (!p || hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess);
   void* zero2[] = {x.xn, x.xn_lo};
   for (void* p : zero2) ok = ok && hipMemsetAsync(p, 0, xnsz * 2, s) == hipSuccess;
   void* zero3[] = {x.att, x.att_lo};
@@ -338,23 +367,59 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   return SJD_OK;
 }
 
-extern "C" int sjd_prefill(sjd_ctx* h, const int32_t* d_prompt, int32_t n, uint64_t seed, void* stream) {
-  if (!h || !d_prompt || n < 1) return SJD_EINVAL;
-  Ctx& x = h->x;
-  if (n + x.c.L > x.cap) return SJD_ESTATE;
-  hipStream_t s = (hipStream_t)stream;
+namespace {
+
+// Caches the first n - 1 prompt tokens (windows of Mpad rows) into one
+// stream's caches.
+int prefill_stream(Ctx& x, const int32_t* d_prompt, int n, bool second, hipStream_t s) {
+  const sjd::Streams one{0, 0, 0};
   for (int start = 0; start < n - 1; start += x.Mpad) {
     const int M = (n - 1 - start) < x.Mpad ? (n - 1 - start) : x.Mpad;
     HIPTRY(sjd::launch_build_prefill(d_prompt, start, M, x.win, s));
-    TRY(forward(x, M, nullptr, start, nullptr, s));
+    TRY(forward(x, M, nullptr, start, nullptr, one, second, s));
   }
-  HIPTRY(sjd::launch_state_init(x.st, d_prompt, n, x.c.L, x.c.V, x.c.vis_lo, x.c.eol_id, x.c.row_len, seed, s));
+  return SJD_OK;
+}
+
+int prefill(Ctx& x, const int32_t* d_prompt, int n, const int32_t* d_uncond, int n_u, uint64_t seed, hipStream_t s) {
+  x.prefilled = false;
+  TRY(prefill_stream(x, d_prompt, n, false, s));
+  if (d_uncond) TRY(prefill_stream(x, d_uncond, n_u, true, s));
+  HIPTRY(sjd::launch_state_init(x.st, d_prompt, n, d_uncond, n_u, x.c.L, x.c.V, x.c.vis_lo, x.c.eol_id,
+                                x.c.row_len, seed, s));
+  x.delta = d_uncond ? n_u - n : 0;
   x.prefilled = true;
   x.steps = 0;
   x.known_n = n - 1;
   x.known_step = -1;
   for (int i = 0; i < kRing; ++i) x.ev_step[i] = -2;
   return SJD_OK;
+}
+
+sjd::Streams window_streams(const Ctx& x) {
+  return x.guided ? sjd::Streams{1, x.c.L, x.delta} : sjd::Streams{0, 0, 0};
+}
+
+// window rows: one stream of L, or two streams in rows [0, L) and [32, 32 + L)
+int window_rows(const Ctx& x) { return x.guided ? 32 + x.c.L : x.c.L; }
+
+}  // namespace
+
+extern "C" int sjd_prefill(sjd_ctx* h, const int32_t* d_prompt, int32_t n, uint64_t seed, void* stream) {
+  if (!h || !d_prompt || n < 1) return SJD_EINVAL;
+  Ctx& x = h->x;
+  if (x.guided) return SJD_EINVAL;
+  if (n + x.c.L > x.cap) return SJD_ESTATE;
+  return prefill(x, d_prompt, n, nullptr, 0, seed, (hipStream_t)stream);
+}
+
+extern "C" int sjd_prefill_cfg(sjd_ctx* h, const int32_t* d_prompt, int32_t n, const int32_t* d_uncond,
+                               int32_t n_u, uint64_t seed, void* stream) {
+  if (!h || !d_prompt || n < 1 || !d_uncond || n_u < 1) return SJD_EINVAL;
+  Ctx& x = h->x;
+  if (!x.guided) return SJD_EINVAL;
+  if (n + x.c.L > x.cap || n_u + x.c.L > x.cap) return SJD_ESTATE;
+  return prefill(x, d_prompt, n, d_uncond, n_u, seed, (hipStream_t)stream);
 }
 
 namespace sjd {
@@ -372,8 +437,9 @@ extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t s
   const sjd_config& c = x.c;
   float* cur = x.logits[x.steps & 1];
   float* prev = x.logits[(x.steps + 1) & 1];
-  HIPTRY(sjd::launch_build_window(x.st, x.win, c.L, c.K, c.vis_lo, s));
-  TRY(forward(x, c.L, &x.st->n, 0, cur, s));
+  const sjd::Streams sm = window_streams(x);
+  HIPTRY(sjd::launch_build_window(x.st, x.win, c.L, c.K, c.vis_lo, sm, s));
+  TRY(forward(x, window_rows(x), &x.st->n, 0, cur, sm, false, s));
   sjd::VerifyArgs a{};
   a.B = 1; a.L = c.L; a.V = c.V; a.K = c.K; a.D = c.D; a.top_k = top_k; a.T = temperature; a.flags = c.flags;
   a.seed = seed; a.step = step; a.vis_lo = c.vis_lo; a.eol = c.eol_id; a.row_len = c.row_len;
@@ -383,8 +449,12 @@ extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t s
   o.out_meta = x.st->meta; o.meta_stride = 8; o.out_tok = x.st->tok; o.tok_stride = c.L;
   o.out_next = x.st->spine; o.next_stride = c.L; o.out_sib = x.st->sib; o.sib_stride = c.D * (c.K - 1);
   HIPTRY(sjd::launch_verify(a, o, s));
-  sjd::KvPlanes all{nullptr, nullptr, x.kc, x.kc_lo, x.vt, x.vt_lo};
-  HIPTRY(sjd::launch_kv_move(x.st, all, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, s));
+  sjd::KvPlanes all{nullptr, nullptr, x.kc, x.kc_lo, x.vt, x.vt_lo, nullptr, nullptr, nullptr, nullptr};
+  HIPTRY(sjd::launch_kv_move(x.st, all, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, 0, s));
+  if (x.guided) {
+    sjd::KvPlanes u{nullptr, nullptr, x.kc2, x.kc2_lo, x.vt2, x.vt2_lo, nullptr, nullptr, nullptr, nullptr};
+    HIPTRY(sjd::launch_kv_move(x.st, u, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, x.delta, s));
+  }
   HIPTRY(sjd::launch_state_update(x.st, d_out_meta, d_out_tok, d_out_next, c.L, s));
   const int slot = (int)(x.steps % kRing);
   HIPTRY(hipMemcpyAsync(x.h_n + slot, &x.st->n, sizeof(int32_t), hipMemcpyDeviceToHost, s));
@@ -400,8 +470,9 @@ extern "C" int sjd_forward_window(sjd_ctx* h, float* d_logits, void* stream) {
   if (!x.prefilled) return SJD_ESTATE;
   TRY(cache_check(x));
   hipStream_t s = (hipStream_t)stream;
-  HIPTRY(sjd::launch_build_window(x.st, x.win, x.c.L, x.c.K, x.c.vis_lo, s));
-  return forward(x, x.c.L, &x.st->n, 0, d_logits, s);
+  const sjd::Streams sm = window_streams(x);
+  HIPTRY(sjd::launch_build_window(x.st, x.win, x.c.L, x.c.K, x.c.vis_lo, sm, s));
+  return forward(x, window_rows(x), &x.st->n, 0, d_logits, sm, false, s);
 }
 
 extern "C" void sjd_destroy(sjd_ctx* h) {

@@ -29,6 +29,10 @@ struct GemmArgs {
   const float* ss;
   int ss_n;
   float inv_d, eps;
+  // guided head (M > 32 only): rows m < cfg_rows of the output are
+  // u + cfg_w (c - u) with c = product row m, u = product row 32 + m
+  int cfg_rows;
+  float cfg_w;
 };
 
 int gemm_splits(int N, int K, int target_wgs);
@@ -55,6 +59,18 @@ struct DevState {
   int32_t sib[64];  // [D][K-1]
   int32_t meta[8];  // last step's outcome
   int32_t tok[64];  // last step's committed tokens
+  int32_t pending_u;  // guided contexts: pending token of the unconditional stream
+  int32_t pad2[3];
+};
+
+// Guided (classifier-free guidance) windows run two streams in one forward:
+// rows [0, L) are the text-prompt stream, rows [32, 32 + L) the
+// unconditional stream (same tokens, positions shifted by delta, its own
+// cache); the other rows are padding. Off: rows [0, M) are one stream.
+struct Streams {
+  int cfg;    // 1: two streams as above
+  int L;      // window rows per stream
+  int delta;  // unconditional stream position = text-stream position + delta
 };
 
 // Key / value cache layout. Per layer and kv head, positions are grouped in
@@ -86,6 +102,8 @@ struct AttnArgs {
   const uint16_t* kc_lo;
   const uint16_t* vt;    // [Hkv][cap * hd] value cache of this layer (tiled)
   const uint16_t* vt_lo;
+  const uint16_t *kc2, *kc2_lo, *vt2, *vt2_lo;  // unconditional stream's caches (guided only)
+  Streams st;
   const Window* win;
   const int32_t* n_dev;  // cached rows before the window (device scalar), or NULL -> n_host
   int n_host;
@@ -113,11 +131,12 @@ hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, c
 // rotary embedding of q and k, key row and transposed value column into the caches
 struct KvPlanes {
   uint16_t *q, *q_lo, *kc, *kc_lo, *vt, *vt_lo;
+  uint16_t *kc2, *kc2_lo, *vt2, *vt2_lo;  // unconditional stream (guided only)
 };
 // qkv: S fp32 partial planes [S][plane] summed in order
 hipError_t launch_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,
                           int M, int H, int Hkv, int hd, const float2* rope, const KvPlanes& o, int cap,
-                          hipStream_t s);
+                          const Streams& st, hipStream_t s);
 // h = silu(gate) * up as hi / lo bf16 planes (row stride ldh), gate = sum of
 // the S fp32 partial planes at columns [0, F), up = at columns [F, 2F)
 // (row stride 2F)

@@ -22,7 +22,8 @@
 // bits): the weights are exact bf16, so two MFMAs per tile recover an
 // fp32-class product at no HBM cost (the MFMA units are otherwise idle).
 // Epilogue: optional per-row RMS scale (the normalisation of a preceding
-// RMSNorm, whose gain is already folded into A), then store fp32 to plane sp.
+// RMSNorm, whose gain is already folded into A), then store fp32 to plane sp;
+// for a guided head, the guidance combine of row pairs (m, 32 + m).
 #include "device.h"
 #include "forward.h"
 
@@ -142,6 +143,15 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   // accumulator register r of lane l holds row 8(r/4) + 4(l/32) + r%4 of
   // its row tile, column l%32
   float* out = g.out + (size_t)sp * g.plane + (size_t)nb * 32 + r32;
+  if (MT == 2 && g.cfg_rows > 0) {  // guided head: rows m and 32 + m share lane and register
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = 8 * (r / 4) + 4 * half + (r % 4);
+      const float c = acc[0][r] * sm.inv[m], u = acc[MT - 1][r] * sm.inv[32 + m];
+      if (m < g.cfg_rows) out[(size_t)m * g.ldo] = u + g.cfg_w * (c - u);
+    }
+    return;
+  }
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -182,6 +192,7 @@ int gemm_splits(int N, int K, int target_wgs) {
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M < 1 || g.M > 64 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
+  if (g.cfg_rows < 0 || g.cfg_rows > 32 || (g.cfg_rows > 0 && g.M < 32 + g.cfg_rows)) return hipErrorInvalidValue;
   const dim3 grid((g.N / 32 + kGWaves - 1) / kGWaves, g.S);
   if (g.M <= 32) hipLaunchKernelGGL((k_gemm<kRingDepth, 1>), grid, dim3(kGB), 0, s, g);
   else hipLaunchKernelGGL((k_gemm<kRingDepth, 2>), grid, dim3(kGB), 0, s, g);

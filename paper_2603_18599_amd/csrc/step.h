@@ -6,12 +6,16 @@
 #include "forward.h"
 
 namespace sjd {
-hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, hipStream_t s);
+hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, const Streams& sm,
+                               hipStream_t s);
 hipError_t launch_build_prefill(const int32_t* prompt, int start, int M, Window* w, hipStream_t s);
-hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, int L, int V, int vis_lo, int eol,
-                             int row_len, uint64_t seed, hipStream_t s);
-// c.kc / c.vt hold the whole caches ([layers][Hkv][...]); q planes unused
-hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K,
+// uncond: the unconditional prompt of a guided context (its last token is
+// that stream's first pending token), or NULL
+hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, const int32_t* uncond, int n_u, int L,
+                             int V, int vis_lo, int eol, int row_len, uint64_t seed, hipStream_t s);
+// c.kc / c.vt hold the whole caches ([layers][Hkv][...]); q planes unused;
+// cache positions are shifted by off (the unconditional stream's delta)
+hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K, int off,
                           hipStream_t s);
 hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L,
                                hipStream_t s);

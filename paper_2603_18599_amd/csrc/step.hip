@@ -15,25 +15,34 @@
 
 namespace sjd {
 
-__global__ void k_build_window(const DevState* st, Window* w, int L, int K, int vis_lo) {
+__global__ void k_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, Streams sm) {
   const int a = threadIdx.x;
-  if (a >= L) return;
+  const int loc = sm.cfg ? (a & 31) : a;  // window row within its stream
+  const bool second = sm.cfg && a >= 32;
+  if (loc >= L) {  // padding row of a guided window: never read, never cached
+    if (sm.cfg && a < 64) {
+      w->tok[a] = vis_lo;
+      w->pos[a] = st->n;
+      w->anc[a] = 0ull;
+    }
+    return;
+  }
   const int n = st->n, n_s = st->n_s;
   int tok, pos;
   uint64_t anc;
-  if (a < n_s) {
-    tok = a == 0 ? st->pending : st->spine[a - 1];
-    pos = n + a;
-    anc = a == 63 ? ~0ull : ((1ull << (a + 1)) - 1ull);
+  if (loc < n_s) {
+    tok = loc == 0 ? (second ? st->pending_u : st->pending) : st->spine[loc - 1];
+    pos = n + loc;
+    anc = loc == 63 ? ~0ull : ((1ull << (loc + 1)) - 1ull);
   } else {
-    const int t = a - n_s, d = t / (K - 1), k = t % (K - 1);
+    const int t = loc - n_s, d = t / (K - 1), k = t % (K - 1);
     const int y = st->sib[d * (K - 1) + k];
     tok = y >= 0 ? y : vis_lo;
     pos = n + 1 + d;
-    anc = ((1ull << (d + 1)) - 1ull) | (1ull << a);
+    anc = ((1ull << (d + 1)) - 1ull) | (1ull << loc);
   }
   w->tok[a] = tok;
-  w->pos[a] = pos;
+  w->pos[a] = second ? pos + sm.delta : pos;
   w->anc[a] = anc;
 }
 
@@ -48,12 +57,14 @@ __global__ void k_build_prefill(const int32_t* prompt, int start, int M, Window*
 // Placeholders of the first window: uniform over the support (stream tag 6,
 // trial 0, step word 0xFFFFFFFF, row = window index), the row end token at
 // forced positions; no draft distributions, no siblings.
-__global__ void k_state_init(DevState* st, const int32_t* prompt, int n_p, int L, int V, int vis_lo, int eol,
-                             int row_len, uint64_t seed) {
+__global__ void k_state_init(DevState* st, const int32_t* prompt, int n_p, const int32_t* uncond, int n_u, int L,
+                             int V, int vis_lo, int eol, int row_len, uint64_t seed) {
   const int i = threadIdx.x;
   if (i == 0) {
     st->n = n_p - 1;
     st->pending = prompt[n_p - 1];
+    st->pending_u = uncond ? uncond[n_u - 1] : prompt[n_p - 1];
+    st->pad2[0] = st->pad2[1] = st->pad2[2] = 0;
     st->n_s = L;
     st->D_in = 0;
     st->n_q = 0;
@@ -82,12 +93,12 @@ __global__ void k_state_init(DevState* st, const int32_t* prompt, int n_p, int L
 // Accepted sibling (meta[5] = k >= 2 at first rejected row r): its key and
 // value move from cache position n + n_s + r(K-1) + k-2 to n + r + 1.
 // grid (layers, Hkv), block hd
-__global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int cap, int K) {
+__global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int cap, int K, int off) {
   const int acc_k = st->meta[5];
   if (acc_k < 2) return;
   const int r = st->meta[1];
-  const int src = st->n + st->n_s + r * (K - 1) + (acc_k - 2);
-  const int dst = st->n + r + 1;
+  const int src = st->n + off + st->n_s + r * (K - 1) + (acc_k - 2);
+  const int dst = st->n + off + r + 1;
   const int l = blockIdx.x, kh = blockIdx.y, j = threadIdx.x;
   const size_t base = ((size_t)l * Hkv + kh) * cap * hd;
   const size_t ks = base + kv_key_off(src, j, hd), kd = base + kv_key_off(dst, j, hd);
@@ -111,6 +122,7 @@ __global__ void k_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok
   __syncthreads();
   if (i == 0 && n_c > 0) {
     st->pending = st->tok[n_c - 1];
+    st->pending_u = st->tok[n_c - 1];
     st->n = n_new;
     st->n_s = sm[3];
     st->D_in = sm[2];
@@ -121,22 +133,24 @@ __global__ void k_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok
   }
 }
 
-hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, hipStream_t s) {
-  hipLaunchKernelGGL(k_build_window, dim3(1), dim3(64), 0, s, st, w, L, K, vis_lo);
+hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, const Streams& sm,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(k_build_window, dim3(1), dim3(64), 0, s, st, w, L, K, vis_lo, sm);
   return hipGetLastError();
 }
 hipError_t launch_build_prefill(const int32_t* prompt, int start, int M, Window* w, hipStream_t s) {
   hipLaunchKernelGGL(k_build_prefill, dim3(1), dim3(64), 0, s, prompt, start, M, w);
   return hipGetLastError();
 }
-hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, int L, int V, int vis_lo, int eol,
-                             int row_len, uint64_t seed, hipStream_t s) {
-  hipLaunchKernelGGL(k_state_init, dim3(1), dim3(64), 0, s, st, prompt, n_p, L, V, vis_lo, eol, row_len, seed);
+hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, const int32_t* uncond, int n_u, int L,
+                             int V, int vis_lo, int eol, int row_len, uint64_t seed, hipStream_t s) {
+  hipLaunchKernelGGL(k_state_init, dim3(1), dim3(64), 0, s, st, prompt, n_p, uncond, n_u, L, V, vis_lo, eol, row_len,
+                     seed);
   return hipGetLastError();
 }
-hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K,
+hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K, int off,
                           hipStream_t s) {
-  hipLaunchKernelGGL(k_kv_move, dim3(layers, Hkv), dim3(hd), 0, s, st, c, Hkv, hd, cap, K);
+  hipLaunchKernelGGL(k_kv_move, dim3(layers, Hkv), dim3(hd), 0, s, st, c, Hkv, hd, cap, K, off);
   return hipGetLastError();
 }
 hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L,
