@@ -157,7 +157,8 @@ hipError_t launch_swiglu(const float* P, int S, size_t plane, int M, int F, uint
 }
 
 // one thread per 8-element chunk of the tiled layout
-__global__ void k_tile_weights(const void* src, int is_f32, size_t row0, int N, int K, uint16_t* dst) {
+__global__ void k_tile_weights(const void* src, int is_f32, size_t row0, int N, int K, uint16_t* dst,
+                               int nblk_total, int nb0) {
   const size_t T = (size_t)K / 64;
   const size_t nchunks = (size_t)N / 32 * T * 256;
   for (size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x; q < nchunks; q += (size_t)gridDim.x * blockDim.x) {
@@ -176,18 +177,19 @@ __global__ void k_tile_weights(const void* src, int is_f32, size_t row0, int N, 
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = p[e];
     }
-    uint16_t* d = dst + q * 8;
+    uint16_t* d = dst + ((kb * nblk_total + nb0 + nb) * 256 + within) * 8;
 #pragma unroll
     for (int e = 0; e < 8; ++e) d[e] = v[e];
   }
 }
 
 hipError_t launch_tile_weights(const void* src, int is_f32, size_t row0, int N, int K, uint16_t* dst,
-                               hipStream_t s) {
+                               int nblk_total, int nb0, hipStream_t s) {
   size_t n = (size_t)N / 32 * (K / 64) * 256;
   size_t blocks = (n + 255) / 256;
   if (blocks > 65535 * 8) blocks = 65535 * 8;
-  hipLaunchKernelGGL(k_tile_weights, dim3((unsigned)blocks), dim3(256), 0, s, src, is_f32, row0, N, K, dst);
+  hipLaunchKernelGGL(k_tile_weights, dim3((unsigned)blocks), dim3(256), 0, s, src, is_f32, row0, N, K, dst,
+                     nblk_total, nb0);
   return hipGetLastError();
 }
 

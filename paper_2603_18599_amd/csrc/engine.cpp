@@ -250,16 +250,18 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     *dst = b;
     return SJD_OK;
   };
-  // tiles of rows [row0, row0 + N) of src ([*][K]) appended at dst + off
-  auto tile = [&](const void* p, size_t row0, int N, int K, uint16_t* dst) -> int {
-    return sjd::launch_tile_weights(p, f32, row0, N, K, dst, s) == hipSuccess ? SJD_OK : SJD_EHIP;
+  // rows [row0, row0 + N) of src ([*][K]) as row blocks [nb0, nb0 + N/32) of
+  // a tiled matrix of Ntot rows at dst
+  auto tile = [&](const void* p, size_t row0, int N, int K, uint16_t* dst, int Ntot, int nb0) -> int {
+    return sjd::launch_tile_weights(p, f32, row0, N, K, dst, Ntot / 32, nb0, s) == hipSuccess ? SJD_OK
+                                                                                             : SJD_EHIP;
   };
   int rc = copy_rows(w->d_embed, (size_t)c.vocab_size * d, &x.embed);
   if (rc == SJD_OK) rc = copy_rows(w->d_final_norm, d, &x.fnorm);
   if (rc == SJD_OK) {
     uint16_t* hp = nullptr;
     rc = dalloc(x, &hp, (size_t)c.V * d);
-    if (rc == SJD_OK) rc = tile(w->d_lm_head, (size_t)c.vis_lo, c.V, d, hp);
+    if (rc == SJD_OK) rc = tile(w->d_lm_head, (size_t)c.vis_lo, c.V, d, hp, c.V, 0);
     x.head = hp;
   }
   x.lw.resize(c.n_layers);
@@ -271,16 +273,17 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     uint16_t *qkv = nullptr, *wo = nullptr, *wgu = nullptr, *wd = nullptr;
     const size_t tq = (size_t)Nq * d, tkv = (size_t)Nkv * d;
     if (rc == SJD_OK) rc = dalloc(x, &qkv, tq + 2 * tkv);
-    if (rc == SJD_OK) rc = tile(lp[1], 0, Nq, d, qkv);
-    if (rc == SJD_OK) rc = tile(lp[2], 0, Nkv, d, qkv + tq);
-    if (rc == SJD_OK) rc = tile(lp[3], 0, Nkv, d, qkv + tq + tkv);
+    const int Nqkv = Nq + 2 * Nkv;
+    if (rc == SJD_OK) rc = tile(lp[1], 0, Nq, d, qkv, Nqkv, 0);
+    if (rc == SJD_OK) rc = tile(lp[2], 0, Nkv, d, qkv, Nqkv, Nq / 32);
+    if (rc == SJD_OK) rc = tile(lp[3], 0, Nkv, d, qkv, Nqkv, (Nq + Nkv) / 32);
     if (rc == SJD_OK) rc = dalloc(x, &wo, (size_t)d * Nq);
-    if (rc == SJD_OK) rc = tile(lp[4], 0, d, Nq, wo);
+    if (rc == SJD_OK) rc = tile(lp[4], 0, d, Nq, wo, d, 0);
     if (rc == SJD_OK) rc = dalloc(x, &wgu, (size_t)2 * F * d);
-    if (rc == SJD_OK) rc = tile(lp[6], 0, F, d, wgu);
-    if (rc == SJD_OK) rc = tile(lp[7], 0, F, d, wgu + (size_t)F * d);
+    if (rc == SJD_OK) rc = tile(lp[6], 0, F, d, wgu, 2 * F, 0);
+    if (rc == SJD_OK) rc = tile(lp[7], 0, F, d, wgu, 2 * F, F / 32);
     if (rc == SJD_OK) rc = dalloc(x, &wd, (size_t)d * F);
-    if (rc == SJD_OK) rc = tile(lp[8], 0, d, F, wd);
+    if (rc == SJD_OK) rc = tile(lp[8], 0, d, F, wd, d, 0);
     o[1] = qkv; o[2] = nullptr; o[3] = nullptr; o[4] = wo; o[6] = wgu; o[7] = nullptr; o[8] = wd;
   }
   if (rc != SJD_OK) return fail(rc);

@@ -5,7 +5,8 @@
 // weight byte per slot: 64 flop/B at M = 32, far below the MFMA ridge), so
 // the kernel is laid out for the weight stream:
 //  - weights are pre-tiled (see forward.h): a wave reads one 32-row x 64-k
-//    tile per k-step as four contiguous 1 KB loads, the next k-step in flight;
+//    tile per k-step as four contiguous 1 KB loads, the next k-step in flight,
+//    and the column blocks' tiles of a k-step form one contiguous stripe;
 //  - the activation tile of a k-step (32 rows x 64 k, hi and lo planes, 8 KB)
 //    is staged once per workgroup into LDS (double buffered) and shared by
 //    the four waves, each of which owns a different 32-column block. Loading
@@ -38,6 +39,8 @@ constexpr int kGWaves = kGB / kWave;
 // k-steps held per wave (the current one plus one in flight): deeper rings
 // help a lone workgroup but lose once every compute unit holds several
 constexpr int kRingDepth = 2;
+// RMSNorm chunk sums held in registers (d <= 4096; larger d reads the rest late)
+constexpr int kSsRegs = 16;
 
 SJD_DEV bf16x8 as_bf16x8(const u32x4& u) { return __builtin_bit_cast(bf16x8, u); }
 
@@ -68,16 +71,20 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   const int n = st1 - st0;
   const int npad = (n + kRing - 1) / kRing * kRing;
 
-  // fused RMSNorm: row scale from the chunk sums of squares (loads issued
-  // ahead of the weight stream, consumed after it)
-  float ssum = 0.0f;
-  const bool has_ss = g.ss != nullptr && (int)threadIdx.x < g.M;
+  // fused RMSNorm: row scale from the chunk sums of squares. The loads go
+  // into registers ahead of the weight stream and are summed after it (a sum
+  // here would wait for them before the first weight load is issued).
+  const bool has_ss = g.ss != nullptr && (int)threadIdx.x < 32 * MT;
+  const float* ssr = has_ss ? g.ss + (size_t)((int)threadIdx.x < g.M ? threadIdx.x : 0) * g.ss_n : nullptr;
+  float ssv[kSsRegs];
   if (has_ss)
-    for (int c = 0; c < g.ss_n; ++c) ssum += g.ss[(size_t)threadIdx.x * g.ss_n + c];
+#pragma unroll
+    for (int c = 0; c < kSsRegs; ++c) ssv[c] = ssr[c < g.ss_n ? c : 0];
 
   // element (row mt*32 + r32, k = kb*64 + half*32 + i*8 + e) of a tile sits
   // in chunk i of lane r32 + 32*half of row tile mt; wave w stages chunk w
-  const uint16_t* wp = g.W + (size_t)(active ? nb : 0) * T * 2048 + (size_t)lane * 8;
+  const uint16_t* wp = g.W + (size_t)(active ? nb : 0) * 2048 + (size_t)lane * 8;
+  const size_t wstep = (size_t)nblk * 2048;  // next k-step of the same column block
   const size_t aofs = (size_t)r32 * g.lda + half * 32 + wave * 8;
   const size_t tstride = (size_t)32 * g.lda;  // next row tile
   const uint16_t* sap = g.A + aofs;
@@ -101,7 +108,7 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
       ra[slot][mt] = *(const u32x4*)(sap + mt * tstride + st * 64);
       ral[slot][mt] = *(const u32x4*)(salp + mt * tstride + st * 64);
     }
-    const uint16_t* src = t < n ? wp + (size_t)st * 2048 : wpad;
+    const uint16_t* src = t < n ? wp + (size_t)st * wstep : wpad;
 #pragma unroll
     for (int i = 0; i < 4; ++i) w[slot][i] = __builtin_nontemporal_load((const u32x4*)(src + i * 512));
   };
@@ -137,7 +144,15 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
     }
   }
 
-  if (threadIdx.x < 32 * MT) sm.inv[threadIdx.x] = has_ss ? rsqrtf(ssum * g.inv_d + g.eps) : 1.0f;
+  if (threadIdx.x < 32 * MT) {
+    float ssum = 0.0f;
+    if (has_ss) {
+#pragma unroll
+      for (int c = 0; c < kSsRegs; ++c) ssum += c < g.ss_n ? ssv[c] : 0.0f;
+      for (int c = kSsRegs; c < g.ss_n; ++c) ssum += ssr[c];
+    }
+    sm.inv[threadIdx.x] = has_ss ? rsqrtf(ssum * g.inv_d + g.eps) : 1.0f;
+  }
   __syncthreads();
   if (!active) return;
   // accumulator register r of lane l holds row 8(r/4) + 4(l/32) + r%4 of
