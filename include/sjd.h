@@ -162,6 +162,13 @@ typedef struct {
                             On: the context keeps a second (unconditional) stream,
                             prefilled by sjd_prefill_cfg, and every step samples from
                             l_u + w (l_c - l_u); needs L <= 32 (SJD_ENOTSUP otherwise) */
+  int32_t batch;         /* images generated together, 1 (0 reads as 1) or 2. With 2,
+                            every step runs both images' windows in one forward (one
+                            pass over the weights), each image with its own cache,
+                            state and prompt (sjd_prefill_image), drawing from Philox
+                            trial b; needs L <= 32 and cfg_w = 0 (SJD_ENOTSUP). The
+                            paper decodes one image at a time; batching serves
+                            several requests per weight pass. */
 } sjd_config;
 
 /* Device pointers, row-major [out][in] (a Linear layer's layout), bf16 or
@@ -187,8 +194,16 @@ SJD_API int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* stream, 
 
 /* Starts a generation: writes the keys/values of d_prompt[0 .. n-2], makes
  * d_prompt[n-1] the pending token and fills the window with placeholders
- * (stream tag 6, step word 0xFFFFFFFF). n >= 1, n + L <= max_seq. */
+ * (stream tag 6, step word 0xFFFFFFFF). n >= 1, n + L <= max_seq.
+ * sjd_prefill is sjd_prefill_image for image 0. */
 SJD_API int sjd_prefill(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, uint64_t seed, void* stream);
+
+/* sjd_prefill for image `image` (0 .. batch-1) of a batched context; the
+ * other image's generation is left as it is (an image can be restarted while
+ * the other one continues). Every image must have been prefilled before
+ * sjd_step (SJD_ESTATE otherwise). SJD_EINVAL on a guided context. */
+SJD_API int sjd_prefill_image(sjd_ctx* ctx, int32_t image, const int32_t* d_prompt, int32_t n, uint64_t seed,
+                              void* stream);
 
 /* sjd_prefill for a guided context (cfg_w != 0; SJD_EINVAL otherwise, and
  * sjd_prefill is SJD_EINVAL on a guided context): d_prompt[0..n) is the
@@ -202,13 +217,15 @@ SJD_API int sjd_prefill_cfg(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, co
 /* One SJD-PAC iteration (Alg. 1): window forward, verification, drafting,
  * KV commit. Outputs (device, may be NULL): d_out_meta[8] as in sjd_verify
  * plus word 7 = cached rows after the step; d_out_tok[L] committed tokens;
- * d_out_next[L] next spine drafts. SJD_ESTATE if the cache cannot take
- * another window (checked against a host-side upper bound). */
+ * d_out_next[L] next spine drafts; a batched context writes one such block
+ * per image ([batch][8], [batch][L], [batch][L]). SJD_ESTATE if a cache
+ * cannot take another window (checked against a host-side upper bound). */
 SJD_API int sjd_step(sjd_ctx* ctx, float temperature, int32_t top_k, uint64_t seed, uint32_t step,
              int32_t* d_out_meta, int32_t* d_out_tok, int32_t* d_out_next, void* stream);
 
 /* Window forward only (no verification): logits of the current window into
- * d_logits[L][V] (a guided context: the guided logits). For parity tests. */
+ * d_logits[L][V] (a guided context: the guided logits; a batched context:
+ * d_logits[32 + L][V], image b's rows from row 32 b). For parity tests. */
 SJD_API int sjd_forward_window(sjd_ctx* ctx, float* d_logits, void* stream);
 
 SJD_API void sjd_destroy(sjd_ctx* ctx);

@@ -51,11 +51,12 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   static_assert(kAttnChunk == 4 * 32, "one 32-key block per wave");
   __shared__ AttnSmem<HD> sm;
   const int h = blockIdx.x, sp = blockIdx.y;
-  // guided windows: slot half z is stream z (its own cache and positions,
-  // L slots each); otherwise the M slots are one stream
-  const bool second = a.st.cfg && blockIdx.z == 1;
-  const int n = (a.n_dev ? *a.n_dev : a.n_host) + (second ? a.st.delta : 0);
-  const int Ms = a.st.cfg ? a.st.L : a.M, nk = n + Ms;
+  // two-stream windows: slot half z is stream z (its own cache and
+  // positions, L slots each); otherwise the M slots are one stream
+  const bool two = a.st.mode != kStreamsOne;
+  const bool second = two && blockIdx.z == 1;
+  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, second);
+  const int Ms = two ? a.st.L : a.M, nk = n + Ms;
   const int kbeg = sp * kAttnChunk;
   if (kbeg >= nk) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r32 = lane & 31, half = lane >> 5;
@@ -63,11 +64,12 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   const int zs = blockIdx.z * 32;  // this workgroup's 32 query slots start here
   const int slot = r32;            // local slot (MFMA column)
   const int gslot = zs + slot;
-  const bool slot_ok = a.st.cfg ? slot < Ms : gslot < Ms;
-  const uint16_t* kc = second ? a.kc2 : a.kc;
-  const uint16_t* kc_lo = second ? a.kc2_lo : a.kc_lo;
-  const uint16_t* vt = second ? a.vt2 : a.vt;
-  const uint16_t* vt_lo = second ? a.vt2_lo : a.vt_lo;
+  const bool slot_ok = two ? slot < Ms : gslot < Ms;
+  const size_t so = second ? a.sstride : 0;
+  const uint16_t* kc = a.kc + so;
+  const uint16_t* kc_lo = a.kc_lo + so;
+  const uint16_t* vt = a.vt + so;
+  const uint16_t* vt_lo = a.vt_lo + so;
   const int kb = kbeg + wave * 32;  // this wave's key block
   const bool has = kb < nk;
   const size_t tofs = (size_t)kvh * a.cap * HD + (size_t)kb * HD + (size_t)lane * 8;
@@ -248,13 +250,14 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   const int slot = blockIdx.z * 32 + (t >> 3), dim0 = blockIdx.y * 32 + (t & 7) * 4;
   if (slot >= a.M) return;
   const size_t oo = (size_t)slot * a.ldo + (size_t)h * HD + dim0;
-  if (a.st.cfg && (slot & 31) >= a.st.L) {  // padding row of a guided window: finite zeros
+  const bool two = a.st.mode != kStreamsOne;
+  if (two && (slot & 31) >= a.st.L) {  // padding row of a two-stream window: finite zeros
     *(ushort4*)(a.out + oo) = make_ushort4(0, 0, 0, 0);
     *(ushort4*)(a.out_lo + oo) = make_ushort4(0, 0, 0, 0);
     return;
   }
-  const int n = (a.n_dev ? *a.n_dev : a.n_host) + (a.st.cfg && slot >= 32 ? a.st.delta : 0);
-  const int nk = n + (a.st.cfg ? a.st.L : a.M);
+  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, two && slot >= 32);
+  const int nk = n + (two ? a.st.L : a.M);
   const int ns = (nk + kAttnChunk - 1) / kAttnChunk;
   const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * 128 + slot * 2;
   const float* wo = a.ws_o + ((size_t)h * a.nsplit_max * 64 + slot) * HD + dim0;

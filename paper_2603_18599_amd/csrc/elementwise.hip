@@ -63,30 +63,31 @@ hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, c
 
 // Rotate-half rotary embedding (pair i with i + hd/2 at angle pos * theta^(-2i/hd),
 // table rope[pos][i] = (cos, sin)), then: q -> q planes, k and v -> cache
-// position n + m (tiled layout), all as hi / lo bf16 planes. Guided windows:
-// row m is slot m & 31 of stream m >> 5, cached at that stream's own
-// position in its own cache; padding rows get a zero q and no cache write.
+// position n + m (tiled layout), all as hi / lo bf16 planes. Two-stream
+// windows: row m is slot m & 31 of stream m >> 5, cached at that stream's
+// own position in its own cache; padding rows get a zero q and no cache write.
 // grid (M, H + 2 * Hkv), block hd / 2
 __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,
                           int H, int Hkv, int hd, const float2* rope, KvPlanes o, int cap, Streams sm) {
   const int m = blockIdx.x, hh = blockIdx.y, i = threadIdx.x;
   const int half = hd / 2;
-  const bool second = sm.cfg && m >= 32;
-  const int loc = sm.cfg ? (m & 31) : m;
-  if (sm.cfg && loc >= sm.L) {
+  const bool two = sm.mode != kStreamsOne;
+  const bool second = two && m >= 32;
+  const int loc = two ? (m & 31) : m;
+  if (two && loc >= sm.L) {
     if (hh < H) {
       const size_t off = (size_t)m * H * hd + (size_t)hh * hd;
       o.q[off + i] = o.q_lo[off + i] = o.q[off + i + half] = o.q_lo[off + i + half] = 0;
     }
     return;
   }
-  const int n = (n_dev ? *n_dev : n_host) + (second ? sm.delta : 0);
+  const int n = stream_rows(sm, n_dev ? *n_dev : n_host, second);
   const int row = n + loc;
   if (second) {
-    o.kc = o.kc2;
-    o.kc_lo = o.kc2_lo;
-    o.vt = o.vt2;
-    o.vt_lo = o.vt2_lo;
+    o.kc += o.sstride;
+    o.kc_lo += o.sstride;
+    o.vt += o.sstride;
+    o.vt_lo += o.sstride;
   }
   const int ld = (H + 2 * Hkv) * hd;
   const float* src = qkv + (size_t)m * ld + (size_t)hh * hd;

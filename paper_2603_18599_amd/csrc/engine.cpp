@@ -42,10 +42,14 @@ struct Ctx {
   uint16_t *hbuf = nullptr, *hbuf_lo = nullptr;
   uint16_t *kc = nullptr, *kc_lo = nullptr;
   uint16_t *vt = nullptr, *vt_lo = nullptr;
-  // guided contexts: the unconditional stream's caches, and its position
-  // offset from the text stream (n_uncond - n_prompt)
+  // streams: 1, or 2 for a guided context (text prompt + unconditional
+  // stream) or a batch of two images; stream z's caches start z * kv_elems
+  // elements into kc.. (the guided stream's positions are the text stream's
+  // plus delta = n_uncond - n_prompt)
   bool guided = false;
-  uint16_t *kc2 = nullptr, *kc2_lo = nullptr, *vt2 = nullptr, *vt2_lo = nullptr;
+  int B = 1;         // images per step
+  int nstreams = 1;
+  size_t kv_elems = 0;
   int delta = 0;
   float2* rope = nullptr;
   float* logits[2] = {nullptr, nullptr};
@@ -60,13 +64,16 @@ struct Ctx {
   int32_t* rec = nullptr;
   int S_qkv = 1, S_o = 1, S_gu = 1, S_dn = 1, S_head = 1;
   long long steps = 0;
-  bool prefilled = false;
-  // cache-fill bound
-  int32_t* h_n = nullptr;  // pinned ring
+  unsigned prefilled = 0;  // bit b: image b prefilled
+  // cache-fill bound, per image: cached rows after step ev_step[i] are
+  // written by the step's last kernel into h_n[i * B + b] (pinned host ring)
+  int32_t* h_n = nullptr;
+  int32_t* h_n_dev = nullptr;  // its device-side address
   hipEvent_t ev[kRing];
   long long ev_step[kRing];
-  long long known_step = -1;  // step after which known_n holds
-  int known_n = 0;
+  long long known_step[2] = {-1, -1};  // step after which known_n holds
+  long long img_step0[2] = {0, 0};     // first step of the image's current generation
+  int known_n[2] = {0, 0};
   int n_events = 0;
 };
 
@@ -78,6 +85,10 @@ int dalloc(Ctx& x, T** p, size_t count) {
   *p = (T*)q;
   return SJD_OK;
 }
+
+// rows of a step's logits buffer: the window rows that carry logits (two
+// batched images: rows [0, L) and [32, 32 + L))
+int logit_rows(const Ctx& x) { return x.B == 2 ? 32 + x.c.L : x.c.L; }
 
 int check_config(const sjd_config* c) {
   if (!c) return SJD_EINVAL;
@@ -94,7 +105,11 @@ int check_config(const sjd_config* c) {
   if (c->flags & ~(SJD_AC | SJD_PD)) return SJD_EINVAL;
   if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
   if (!std::isfinite(c->cfg_w)) return SJD_EINVAL;
-  if (c->cfg_w != 0.0f && c->L > 32) return SJD_ENOTSUP;  // two streams of L rows in 64
+  if (c->batch < 0) return SJD_EINVAL;
+  if (c->batch > 2) return SJD_ENOTSUP;
+  const bool two = c->cfg_w != 0.0f || c->batch == 2;
+  if (c->cfg_w != 0.0f && c->batch == 2) return SJD_ENOTSUP;  // four streams
+  if (two && c->L > 32) return SJD_ENOTSUP;                   // two streams of L rows in 64
   return SJD_OK;
 }
 
@@ -108,10 +123,9 @@ int check_config(const sjd_config* c) {
     if ((e) != hipSuccess) return SJD_EHIP;      \
   } while (0)
 
-// Window forward of M rows. sm.cfg: a guided window (two streams, see
-// Streams); otherwise one stream on the main caches, or on the unconditional
-// stream's caches with second (its prefill).
-int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, const sjd::Streams& sm, bool second,
+// Window forward of M rows: two streams (sm.mode != kStreamsOne, see
+// Streams), or one stream on the caches of stream `cache` (a prefill).
+int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, const sjd::Streams& sm, int cache,
             hipStream_t s) {
   const sjd_config& c = x.c;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
@@ -126,16 +140,8 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
   normed.eps = c.rms_eps;
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& w = x.lw[l];
-    const size_t lofs = (size_t)l * Hkv * x.cap_pad * hd;
-    sjd::KvPlanes kv{x.q, x.q_lo, x.kc + lofs, x.kc_lo + lofs, x.vt + lofs, x.vt_lo + lofs,
-                     nullptr, nullptr, nullptr, nullptr};
-    if (x.guided) {
-      kv.kc2 = x.kc2 + lofs; kv.kc2_lo = x.kc2_lo + lofs; kv.vt2 = x.vt2 + lofs; kv.vt2_lo = x.vt2_lo + lofs;
-      if (second) {
-        std::swap(kv.kc, kv.kc2); std::swap(kv.kc_lo, kv.kc2_lo);
-        std::swap(kv.vt, kv.vt2); std::swap(kv.vt_lo, kv.vt2_lo);
-      }
-    }
+    const size_t lofs = (size_t)l * Hkv * x.cap_pad * hd + (size_t)cache * x.kv_elems;
+    sjd::KvPlanes kv{x.q, x.q_lo, x.kc + lofs, x.kc_lo + lofs, x.vt + lofs, x.vt_lo + lofs, x.kv_elems};
     HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, pend, rplane, w[0], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
     sjd::GemmArgs g = normed;
     g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = w[1]; g.N = Nqkv; g.K = d; g.S = x.S_qkv;
@@ -145,7 +151,7 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
                                sm, s));
     sjd::AttnArgs a{};
     a.q = x.q; a.q_lo = x.q_lo; a.kc = kv.kc; a.kc_lo = kv.kc_lo; a.vt = kv.vt; a.vt_lo = kv.vt_lo; a.win = x.win;
-    a.kc2 = kv.kc2; a.kc2_lo = kv.kc2_lo; a.vt2 = kv.vt2; a.vt2_lo = kv.vt2_lo; a.st = sm;
+    a.sstride = kv.sstride; a.st = sm;
     a.n_dev = n_dev; a.n_host = n_host; a.M = M; a.H = H; a.Hkv = Hkv; a.cap = x.cap_pad;
     a.scale = (float)(1.4426950408889634 / std::sqrt((double)hd));
     a.ws_o = x.attn_o; a.ws_ml = x.attn_ml; a.nsplit_max = x.nsplit_max; a.out = x.att; a.out_lo = x.att_lo;
@@ -172,7 +178,7 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
     sjd::GemmArgs g = normed;
     g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = x.head; g.N = c.V; g.K = d; g.S = 1;
     g.out = logits; g.plane = 0; g.ldo = c.V;
-    if (sm.cfg) {  // rows [0, L) of the output: guided logits
+    if (sm.mode == sjd::kStreamsGuided) {  // rows [0, L) of the output: guided logits
       g.cfg_rows = sm.L;
       g.cfg_w = c.cfg_w;
     }
@@ -181,28 +187,29 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
   return SJD_OK;
 }
 
-// Refreshes the cache-fill bound from completed steps; blocks only when the
-// bound says the next window might not fit.
+// Refreshes the cache-fill bound of every image from completed steps;
+// blocks only when the bound says the next window might not fit.
 int cache_check(Ctx& x) {
-  for (int i = 0; i < kRing; ++i) {
-    if (x.ev_step[i] > x.known_step && hipEventQuery(x.ev[i]) == hipSuccess) {
-      x.known_step = x.ev_step[i];
-      x.known_n = x.h_n[i];
-    }
-  }
-  long long pending = x.steps - 1 - x.known_step;
   const int ahead = x.delta > 0 ? x.delta : 0;  // the unconditional stream runs ahead by delta
-  long long bound = (long long)x.known_n + ahead + pending * x.c.L;
-  if (bound + x.c.L <= x.cap) return SJD_OK;
-  // wait for the newest step and use its exact value
-  for (int i = 0; i < kRing; ++i) {
-    if (x.ev_step[i] == x.steps - 1) {
-      HIPTRY(hipEventSynchronize(x.ev[i]));
-      x.known_step = x.ev_step[i];
-      x.known_n = x.h_n[i];
-    }
+  for (int b = 0; b < x.B; ++b) {
+    auto refresh = [&](bool wait) -> int {
+      for (int i = 0; i < kRing; ++i) {
+        if (x.ev_step[i] <= x.known_step[b] || x.ev_step[i] < x.img_step0[b]) continue;
+        if (wait && x.ev_step[i] == x.steps - 1) HIPTRY(hipEventSynchronize(x.ev[i]));
+        if (hipEventQuery(x.ev[i]) == hipSuccess) {
+          x.known_step[b] = x.ev_step[i];
+          x.known_n[b] = x.h_n[i * x.B + b];
+        }
+      }
+      return SJD_OK;
+    };
+    TRY(refresh(false));
+    long long pending = x.steps - 1 - x.known_step[b];
+    if ((long long)x.known_n[b] + ahead + pending * x.c.L + x.c.L <= x.cap) continue;
+    TRY(refresh(true));  // wait for the newest step and use its exact value
+    pending = x.steps - 1 - x.known_step[b];
+    if ((long long)x.known_n[b] + ahead + pending * x.c.L + x.c.L > x.cap) return SJD_ESTATE;
   }
-  if ((long long)x.known_n + ahead + x.c.L > x.cap) return SJD_ESTATE;
   return SJD_OK;
 }
 
@@ -225,6 +232,8 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   x.c = *cfg;
   const sjd_config& c = x.c;
   x.guided = c.cfg_w != 0.0f;
+  x.B = c.batch == 2 ? 2 : 1;
+  x.nstreams = x.guided || x.B == 2 ? 2 : 1;
   auto fail = [&](int rc) {
     sjd_destroy(h);
     return rc;
@@ -292,7 +301,8 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
 
   // work buffers
   const int Mp = x.Mpad;
-  const size_t kv = (size_t)c.n_layers * Hkv * x.cap_pad * hd;
+  x.kv_elems = (size_t)c.n_layers * Hkv * x.cap_pad * hd;
+  const size_t kv = x.kv_elems * x.nstreams;  // every stream's caches
   // activation rows padded by 64 elements so that the 32 rows a wave reads per
   // k-step spread over memory channels
   x.ld_d = d + 64;
@@ -305,13 +315,12 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       (rc = dalloc(x, &x.att_lo, (size_t)Mp * x.ld_q)) || (rc = dalloc(x, &x.hbuf, (size_t)Mp * x.ld_f)) ||
       (rc = dalloc(x, &x.hbuf_lo, (size_t)Mp * x.ld_f)) || (rc = dalloc(x, &x.kc, kv)) || (rc = dalloc(x, &x.kc_lo, kv)) ||
       (rc = dalloc(x, &x.vt, kv)) || (rc = dalloc(x, &x.vt_lo, kv)) ||
-      (x.guided && ((rc = dalloc(x, &x.kc2, kv)) || (rc = dalloc(x, &x.kc2_lo, kv)) ||
-                    (rc = dalloc(x, &x.vt2, kv)) || (rc = dalloc(x, &x.vt2_lo, kv)))) ||
       (rc = dalloc(x, &x.rope, (size_t)x.cap_pad * (hd / 2))) ||
-      (rc = dalloc(x, &x.logits[0], (size_t)c.L * c.V)) || (rc = dalloc(x, &x.logits[1], (size_t)c.L * c.V)) ||
+      (rc = dalloc(x, &x.logits[0], (size_t)logit_rows(x) * c.V)) ||
+      (rc = dalloc(x, &x.logits[1], (size_t)logit_rows(x) * c.V)) ||
       (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * 64 * hd)) ||
-      (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 128)) || (rc = dalloc(x, &x.st, 1)) ||
-      (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)c.L * sjd::kRecInts)))
+      (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 128)) || (rc = dalloc(x, &x.st, x.B)) ||
+      (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)x.B * c.L * sjd::kRecInts)))
     return fail(rc);
   // split-K plan: aim for two to three workgroups per compute unit
   int ncu = 256;
@@ -335,9 +344,9 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     return fail(rc);
   // zero the caches (rows past the fill are read, masked, by the attention
   // tiles) and the activation pad rows
-  void* zero[] = {x.kc, x.kc_lo, x.vt, x.vt_lo, x.kc2, x.kc2_lo, x.vt2, x.vt2_lo};
-  bool ok = hipMemsetAsync(x.st, 0, sizeof(sjd::DevState), s) == hipSuccess;
-  for (void* p : zero) ok = ok && (!p || hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess);
+  void* zero[] = {x.kc, x.kc_lo, x.vt, x.vt_lo};
+  bool ok = hipMemsetAsync(x.st, 0, sizeof(sjd::DevState) * x.B, s) == hipSuccess;
+  for (void* p : zero) ok = ok && hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess;
   void* zero2[] = {x.xn, x.xn_lo};
   for (void* p : zero2) ok = ok && hipMemsetAsync(p, 0, xnsz * 2, s) == hipSuccess;
   void* zero3[] = {x.att, x.att_lo};
@@ -359,8 +368,12 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
         hipStreamSynchronize(s) != hipSuccess)
       return fail(SJD_EHIP);
   }
-  if (hipHostMalloc((void**)&x.h_n, sizeof(int32_t) * kRing, hipHostMallocDefault) != hipSuccess)
+  // pinned, device-visible: the step's last kernel writes the cached-row
+  // counts into it directly
+  if (hipHostMalloc((void**)&x.h_n, sizeof(int32_t) * kRing * x.B, hipHostMallocDefault) != hipSuccess)
     return fail(SJD_ENOMEM);
+  for (int i = 0; i < kRing * x.B; ++i) x.h_n[i] = 0;
+  if (hipHostGetDevicePointer((void**)&x.h_n_dev, x.h_n, 0) != hipSuccess) return fail(SJD_EHIP);
   for (int i = 0; i < kRing; ++i) {
     if (hipEventCreateWithFlags(&x.ev[i], hipEventDisableTiming) != hipSuccess) return fail(SJD_EHIP);
     x.n_events = i + 1;
@@ -372,48 +385,60 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
 
 namespace {
 
-// Caches the first n - 1 prompt tokens (windows of Mpad rows) into one
-// stream's caches.
-int prefill_stream(Ctx& x, const int32_t* d_prompt, int n, bool second, hipStream_t s) {
-  const sjd::Streams one{0, 0, 0};
+// Caches the first n - 1 prompt tokens (windows of Mpad rows) into the caches
+// of stream `cache`.
+int prefill_stream(Ctx& x, const int32_t* d_prompt, int n, int cache, hipStream_t s) {
+  const sjd::Streams one{sjd::kStreamsOne, 0, 0, nullptr};
   for (int start = 0; start < n - 1; start += x.Mpad) {
     const int M = (n - 1 - start) < x.Mpad ? (n - 1 - start) : x.Mpad;
     HIPTRY(sjd::launch_build_prefill(d_prompt, start, M, x.win, s));
-    TRY(forward(x, M, nullptr, start, nullptr, one, second, s));
+    TRY(forward(x, M, nullptr, start, nullptr, one, cache, s));
   }
   return SJD_OK;
 }
 
-int prefill(Ctx& x, const int32_t* d_prompt, int n, const int32_t* d_uncond, int n_u, uint64_t seed, hipStream_t s) {
-  x.prefilled = false;
-  TRY(prefill_stream(x, d_prompt, n, false, s));
-  if (d_uncond) TRY(prefill_stream(x, d_uncond, n_u, true, s));
-  HIPTRY(sjd::launch_state_init(x.st, d_prompt, n, d_uncond, n_u, x.c.L, x.c.V, x.c.vis_lo, x.c.eol_id,
+// image b (its caches: stream b) with prompt d_prompt; a guided context also
+// prefills the unconditional prompt into stream 1
+int prefill(Ctx& x, int b, const int32_t* d_prompt, int n, const int32_t* d_uncond, int n_u, uint64_t seed,
+            hipStream_t s) {
+  x.prefilled &= ~(1u << b);
+  TRY(prefill_stream(x, d_prompt, n, b, s));
+  if (d_uncond) TRY(prefill_stream(x, d_uncond, n_u, 1, s));
+  HIPTRY(sjd::launch_state_init(x.st + b, d_prompt, n, d_uncond, n_u, x.c.L, x.c.V, x.c.vis_lo, x.c.eol_id,
                                 x.c.row_len, seed, s));
-  x.delta = d_uncond ? n_u - n : 0;
-  x.prefilled = true;
-  x.steps = 0;
-  x.known_n = n - 1;
-  x.known_step = -1;
-  for (int i = 0; i < kRing; ++i) x.ev_step[i] = -2;
+  if (d_uncond) x.delta = n_u - n;
+  x.prefilled |= 1u << b;
+  // the image's cache-fill bound restarts; steps before this one say nothing about it
+  x.img_step0[b] = x.steps;
+  x.known_n[b] = n - 1;
+  x.known_step[b] = x.steps - 1;
   return SJD_OK;
 }
 
-sjd::Streams window_streams(const Ctx& x) {
-  return x.guided ? sjd::Streams{1, x.c.L, x.delta} : sjd::Streams{0, 0, 0};
+bool all_prefilled(const Ctx& x) { return x.prefilled == (1u << x.B) - 1u; }
+
+sjd::Streams window_streams(Ctx& x) {
+  if (x.guided) return sjd::Streams{sjd::kStreamsGuided, x.c.L, x.delta, nullptr};
+  if (x.B == 2) return sjd::Streams{sjd::kStreamsBatch, x.c.L, 0, &x.st[1].n};
+  return sjd::Streams{sjd::kStreamsOne, 0, 0, nullptr};
 }
 
 // window rows: one stream of L, or two streams in rows [0, L) and [32, 32 + L)
-int window_rows(const Ctx& x) { return x.guided ? 32 + x.c.L : x.c.L; }
+int window_rows(const Ctx& x) { return x.nstreams == 2 ? 32 + x.c.L : x.c.L; }
 
 }  // namespace
 
 extern "C" int sjd_prefill(sjd_ctx* h, const int32_t* d_prompt, int32_t n, uint64_t seed, void* stream) {
+  return sjd_prefill_image(h, 0, d_prompt, n, seed, stream);
+}
+
+extern "C" int sjd_prefill_image(sjd_ctx* h, int32_t image, const int32_t* d_prompt, int32_t n, uint64_t seed,
+                                 void* stream) {
   if (!h || !d_prompt || n < 1) return SJD_EINVAL;
   Ctx& x = h->x;
-  if (x.guided) return SJD_EINVAL;
+  if (x.guided || image < 0 || image >= x.B) return SJD_EINVAL;
   if (n + x.c.L > x.cap) return SJD_ESTATE;
-  return prefill(x, d_prompt, n, nullptr, 0, seed, (hipStream_t)stream);
+  return prefill(x, image, d_prompt, n, nullptr, 0, seed, (hipStream_t)stream);
 }
 
 extern "C" int sjd_prefill_cfg(sjd_ctx* h, const int32_t* d_prompt, int32_t n, const int32_t* d_uncond,
@@ -422,7 +447,7 @@ extern "C" int sjd_prefill_cfg(sjd_ctx* h, const int32_t* d_prompt, int32_t n, c
   Ctx& x = h->x;
   if (!x.guided) return SJD_EINVAL;
   if (n + x.c.L > x.cap || n_u + x.c.L > x.cap) return SJD_ESTATE;
-  return prefill(x, d_prompt, n, d_uncond, n_u, seed, (hipStream_t)stream);
+  return prefill(x, 0, d_prompt, n, d_uncond, n_u, seed, (hipStream_t)stream);
 }
 
 namespace sjd {
@@ -434,7 +459,7 @@ extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t s
   if (!h || !(temperature > 0.0f) || top_k < 0) return SJD_EINVAL;
   TRY(sjd::check_verify_limits(h->x.c.V, top_k));
   Ctx& x = h->x;
-  if (!x.prefilled) return SJD_ESTATE;
+  if (!all_prefilled(x)) return SJD_ESTATE;
   TRY(cache_check(x));
   hipStream_t s = (hipStream_t)stream;
   const sjd_config& c = x.c;
@@ -442,25 +467,25 @@ extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t s
   float* prev = x.logits[(x.steps + 1) & 1];
   const sjd::Streams sm = window_streams(x);
   HIPTRY(sjd::launch_build_window(x.st, x.win, c.L, c.K, c.vis_lo, sm, s));
-  TRY(forward(x, window_rows(x), &x.st->n, 0, cur, sm, false, s));
+  TRY(forward(x, window_rows(x), &x.st->n, 0, cur, sm, 0, s));
+  // image b: logits rows from 32 b (batch), decoder state x.st[b], Philox trial b
+  const int sstate = (int)(sizeof(sjd::DevState) / sizeof(int32_t));
+  const long long lstride = x.B == 2 ? 32LL * c.V : 0;
   sjd::VerifyArgs a{};
-  a.B = 1; a.L = c.L; a.V = c.V; a.K = c.K; a.D = c.D; a.top_k = top_k; a.T = temperature; a.flags = c.flags;
+  a.B = x.B; a.L = c.L; a.V = c.V; a.K = c.K; a.D = c.D; a.top_k = top_k; a.T = temperature; a.flags = c.flags;
   a.seed = seed; a.step = step; a.vis_lo = c.vis_lo; a.eol = c.eol_id; a.row_len = c.row_len;
-  a.cur = cur; a.draft = prev; a.draft_bstride = 0; a.q_off = &x.st->q_off; a.draft_tok = x.st->spine;
-  a.sib = x.st->sib; a.in_meta = &x.st->D_in; a.rec = x.rec;
+  a.cur = cur; a.cur_bstride = lstride; a.draft = prev; a.draft_bstride = lstride;
+  a.q_off = &x.st->q_off; a.draft_tok = x.st->spine; a.sib = x.st->sib; a.in_meta = &x.st->D_in;
+  a.state_stride = sstate; a.rec = x.rec;
   sjd::FinalizeOut o{};
-  o.out_meta = x.st->meta; o.meta_stride = 8; o.out_tok = x.st->tok; o.tok_stride = c.L;
-  o.out_next = x.st->spine; o.next_stride = c.L; o.out_sib = x.st->sib; o.sib_stride = c.D * (c.K - 1);
+  o.out_meta = x.st->meta; o.meta_stride = sstate; o.out_tok = x.st->tok; o.tok_stride = sstate;
+  o.out_next = x.st->spine; o.next_stride = sstate; o.out_sib = x.st->sib; o.sib_stride = sstate;
   HIPTRY(sjd::launch_verify(a, o, s));
-  sjd::KvPlanes all{nullptr, nullptr, x.kc, x.kc_lo, x.vt, x.vt_lo, nullptr, nullptr, nullptr, nullptr};
-  HIPTRY(sjd::launch_kv_move(x.st, all, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, 0, s));
-  if (x.guided) {
-    sjd::KvPlanes u{nullptr, nullptr, x.kc2, x.kc2_lo, x.vt2, x.vt2_lo, nullptr, nullptr, nullptr, nullptr};
-    HIPTRY(sjd::launch_kv_move(x.st, u, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, x.delta, s));
-  }
-  HIPTRY(sjd::launch_state_update(x.st, d_out_meta, d_out_tok, d_out_next, c.L, s));
+  const sjd::KvPlanes all{nullptr, nullptr, x.kc, x.kc_lo, x.vt, x.vt_lo, x.kv_elems};
+  HIPTRY(sjd::launch_kv_move(x.st, all, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, x.nstreams,
+                             x.B == 2 ? 1 : 0, x.guided ? x.delta : 0, s));
   const int slot = (int)(x.steps % kRing);
-  HIPTRY(hipMemcpyAsync(x.h_n + slot, &x.st->n, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HIPTRY(sjd::launch_state_update(x.st, d_out_meta, d_out_tok, d_out_next, c.L, x.B, x.h_n_dev + slot * x.B, s));
   HIPTRY(hipEventRecord(x.ev[slot], s));
   x.ev_step[slot] = x.steps;
   x.steps += 1;
@@ -470,12 +495,12 @@ extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t s
 extern "C" int sjd_forward_window(sjd_ctx* h, float* d_logits, void* stream) {
   if (!h || !d_logits) return SJD_EINVAL;
   Ctx& x = h->x;
-  if (!x.prefilled) return SJD_ESTATE;
+  if (!all_prefilled(x)) return SJD_ESTATE;
   TRY(cache_check(x));
   hipStream_t s = (hipStream_t)stream;
   const sjd::Streams sm = window_streams(x);
   HIPTRY(sjd::launch_build_window(x.st, x.win, x.c.L, x.c.K, x.c.vis_lo, sm, s));
-  return forward(x, window_rows(x), &x.st->n, 0, d_logits, sm, false, s);
+  return forward(x, window_rows(x), &x.st->n, 0, d_logits, sm, 0, s);
 }
 
 extern "C" void sjd_destroy(sjd_ctx* h) {

@@ -67,15 +67,27 @@ struct DevState {
   int32_t pad2[3];
 };
 
-// Guided (classifier-free guidance) windows run two streams in one forward:
-// rows [0, L) are the text-prompt stream, rows [32, 32 + L) the
-// unconditional stream (same tokens, positions shifted by delta, its own
-// cache); the other rows are padding. Off: rows [0, M) are one stream.
+// A window forward runs one stream (rows [0, M)) or two: rows [0, L) are
+// stream 0, rows [32, 32 + L) stream 1, the other rows padding (never
+// cached, never read). Each stream has its own key/value cache (stream 1's
+// at the stream-0 cache + sstride) and its own positions:
+//  - guided (classifier-free guidance): stream 1 is the unconditional
+//    stream: same window tokens (its own first pending token), positions
+//    shifted by delta;
+//  - batched: stream 1 is a second image with its own decoder state.
+enum { kStreamsOne = 0, kStreamsGuided = 1, kStreamsBatch = 2 };
 struct Streams {
-  int cfg;    // 1: two streams as above
-  int L;      // window rows per stream
-  int delta;  // unconditional stream position = text-stream position + delta
+  int mode;           // kStreams*
+  int L;              // window rows per stream (two-stream modes)
+  int delta;          // guided: stream-1 position = stream-0 position + delta
+  const int32_t* n2;  // batched: stream 1's cached rows (device scalar)
 };
+
+// cached rows before the window of the stream that row-half `second` is
+__device__ inline int stream_rows(const Streams& sm, int n0, bool second) {
+  if (!second) return n0;
+  return sm.mode == kStreamsBatch ? *sm.n2 : n0 + sm.delta;
+}
 
 // Key / value cache layout. Per layer and kv head, positions are grouped in
 // tiles of 32 (32 * hd elements each) stored in the register order of the
@@ -106,7 +118,7 @@ struct AttnArgs {
   const uint16_t* kc_lo;
   const uint16_t* vt;    // [Hkv][cap * hd] value cache of this layer (tiled)
   const uint16_t* vt_lo;
-  const uint16_t *kc2, *kc2_lo, *vt2, *vt2_lo;  // unconditional stream's caches (guided only)
+  size_t sstride;        // two-stream modes: stream 1's caches are these + sstride
   Streams st;
   const Window* win;
   const int32_t* n_dev;  // cached rows before the window (device scalar), or NULL -> n_host
@@ -135,7 +147,7 @@ hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, c
 // rotary embedding of q and k, key row and transposed value column into the caches
 struct KvPlanes {
   uint16_t *q, *q_lo, *kc, *kc_lo, *vt, *vt_lo;
-  uint16_t *kc2, *kc2_lo, *vt2, *vt2_lo;  // unconditional stream (guided only)
+  size_t sstride;  // two-stream modes: stream 1's caches are kc.. + sstride
 };
 // qkv: S fp32 partial planes [S][plane] summed in order
 hipError_t launch_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,

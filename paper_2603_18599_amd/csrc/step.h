@@ -13,10 +13,13 @@ hipError_t launch_build_prefill(const int32_t* prompt, int start, int M, Window*
 // that stream's first pending token), or NULL
 hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, const int32_t* uncond, int n_u, int L,
                              int V, int vis_lo, int eol, int row_len, uint64_t seed, hipStream_t s);
-// c.kc / c.vt hold the whole caches ([layers][Hkv][...]); q planes unused;
-// cache positions are shifted by off (the unconditional stream's delta)
-hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K, int off,
-                          hipStream_t s);
-hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L,
-                               hipStream_t s);
+// c.kc / c.vt hold the whole caches ([layers][Hkv][...]); q planes unused.
+// ncache caches (1 or 2): cache z at c + z * c.sstride, driven by state
+// st + z * st_step (0: one shared state), positions shifted by z ? off1 : 0
+hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K,
+                          int ncache, int st_step, int off1, hipStream_t s);
+// B images (states st[0..B), outputs [B][8], [B][L], [B][L]); host_n[B]:
+// pinned host memory that receives each image's cached rows (or NULL)
+hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L, int B,
+                               int32_t* host_n, hipStream_t s);
 }  // namespace sjd

@@ -17,32 +17,35 @@ namespace sjd {
 
 __global__ void k_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, Streams sm) {
   const int a = threadIdx.x;
-  const int loc = sm.cfg ? (a & 31) : a;  // window row within its stream
-  const bool second = sm.cfg && a >= 32;
-  if (loc >= L) {  // padding row of a guided window: never read, never cached
-    if (sm.cfg && a < 64) {
+  const bool two = sm.mode != kStreamsOne;
+  const int loc = two ? (a & 31) : a;  // window row within its stream
+  const bool second = two && a >= 32;
+  if (loc >= L) {  // padding row of a two-stream window: never read, never cached
+    if (two && a < 64) {
       w->tok[a] = vis_lo;
       w->pos[a] = st->n;
       w->anc[a] = 0ull;
     }
     return;
   }
-  const int n = st->n, n_s = st->n_s;
+  // batched: the second stream is the next image, with its own state
+  const DevState* d = second && sm.mode == kStreamsBatch ? st + 1 : st;
+  const int n = d->n, n_s = d->n_s;
   int tok, pos;
   uint64_t anc;
   if (loc < n_s) {
-    tok = loc == 0 ? (second ? st->pending_u : st->pending) : st->spine[loc - 1];
+    tok = loc == 0 ? (second && sm.mode == kStreamsGuided ? d->pending_u : d->pending) : d->spine[loc - 1];
     pos = n + loc;
     anc = loc == 63 ? ~0ull : ((1ull << (loc + 1)) - 1ull);
   } else {
-    const int t = loc - n_s, d = t / (K - 1), k = t % (K - 1);
-    const int y = st->sib[d * (K - 1) + k];
+    const int t = loc - n_s, dd = t / (K - 1), k = t % (K - 1);
+    const int y = d->sib[dd * (K - 1) + k];
     tok = y >= 0 ? y : vis_lo;
-    pos = n + 1 + d;
-    anc = ((1ull << (d + 1)) - 1ull) | (1ull << loc);
+    pos = n + 1 + dd;
+    anc = ((1ull << (dd + 1)) - 1ull) | (1ull << loc);
   }
   w->tok[a] = tok;
-  w->pos[a] = second ? pos + sm.delta : pos;
+  w->pos[a] = second && sm.mode == kStreamsGuided ? pos + sm.delta : pos;
   w->anc[a] = anc;
 }
 
@@ -92,8 +95,16 @@ __global__ void k_state_init(DevState* st, const int32_t* prompt, int n_p, const
 
 // Accepted sibling (meta[5] = k >= 2 at first rejected row r): its key and
 // value move from cache position n + n_s + r(K-1) + k-2 to n + r + 1.
-// grid (layers, Hkv), block hd
-__global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int cap, int K, int off) {
+// grid (layers, Hkv, caches), block hd: cache z is the one at c + z * sstride,
+// driven by state st + z * st_step, its positions shifted by z ? off1 : 0.
+__global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int cap, int K, int st_step, int off1) {
+  const int z = blockIdx.z;
+  st += z * st_step;
+  const int off = z ? off1 : 0;
+  c.kc += z * c.sstride;
+  c.kc_lo += z * c.sstride;
+  c.vt += z * c.sstride;
+  c.vt_lo += z * c.sstride;
   const int acc_k = st->meta[5];
   if (acc_k < 2) return;
   const int r = st->meta[1];
@@ -109,9 +120,16 @@ __global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int c
   c.vt_lo[vd] = c.vt_lo[vs];
 }
 
-__global__ void k_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L) {
+// grid B (one block per image of a batch); host_n[b] (pinned host memory)
+// receives the image's cached rows after the step
+__global__ void k_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L,
+                               int32_t* host_n) {
   __shared__ int32_t sm[8];
-  const int i = threadIdx.x;
+  const int i = threadIdx.x, b = blockIdx.x;
+  st += b;
+  if (out_meta) out_meta += 8 * b;
+  if (out_tok) out_tok += L * b;
+  if (out_next) out_next += L * b;
   if (i < 8) sm[i] = st->meta[i];
   __syncthreads();
   const int n_c = sm[0];
@@ -119,6 +137,7 @@ __global__ void k_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok
   if (out_tok && i < L) out_tok[i] = st->tok[i];
   if (out_next && i < L) out_next[i] = st->spine[i];
   if (out_meta && i < 8) out_meta[i] = i == 7 ? n_new : sm[i];
+  if (host_n && i == 0) host_n[b] = n_new;
   __syncthreads();
   if (i == 0 && n_c > 0) {
     st->pending = st->tok[n_c - 1];
@@ -148,14 +167,14 @@ hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, const
                      seed);
   return hipGetLastError();
 }
-hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K, int off,
-                          hipStream_t s) {
-  hipLaunchKernelGGL(k_kv_move, dim3(layers, Hkv), dim3(hd), 0, s, st, c, Hkv, hd, cap, K, off);
+hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K,
+                          int ncache, int st_step, int off1, hipStream_t s) {
+  hipLaunchKernelGGL(k_kv_move, dim3(layers, Hkv, ncache), dim3(hd), 0, s, st, c, Hkv, hd, cap, K, st_step, off1);
   return hipGetLastError();
 }
-hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L,
-                               hipStream_t s) {
-  hipLaunchKernelGGL(k_state_update, dim3(1), dim3(64), 0, s, st, out_meta, out_tok, out_next, L);
+hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L, int B,
+                               int32_t* host_n, hipStream_t s) {
+  hipLaunchKernelGGL(k_state_update, dim3(B), dim3(64), 0, s, st, out_meta, out_tok, out_next, L, host_n);
   return hipGetLastError();
 }
 

@@ -18,13 +18,18 @@ struct VerifyArgs {
   uint64_t seed;
   uint32_t step;
   int vis_lo, eol, row_len;
-  const float* cur;          // [B][L][V]
+  const float* cur;          // trial b, row j -> cur + b*cur_bstride + j*V (cur_bstride 0: L*V)
+  long long cur_bstride;
   const float* draft;        // draft rows: trial b, spine row j -> draft + b*draft_bstride + (q_off[b]+j)*V
   long long draft_bstride;
+  // per-trial inputs; with state_stride > 0 every one of them advances by
+  // state_stride int32 per trial (fields of an array of decoder states),
+  // otherwise by its packed size below
   const int32_t* q_off;      // [B] or NULL (= 0)
   const int32_t* draft_tok;  // [B][L]
   const int32_t* sib;        // [B][D][K-1] or NULL
   const int32_t* in_meta;    // [B][4]
+  int state_stride;
   int32_t* rec;              // [B][L][kRecInts] scratch
   int32_t* out_rows;         // [B][L][2] or NULL
   float* dbg_p;              // [B][L][V] or NULL

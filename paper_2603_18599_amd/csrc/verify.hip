@@ -34,6 +34,11 @@
 
 namespace sjd {
 
+// per-trial stride of a verify input whose packed per-trial size is `packed`
+SJD_DEV size_t trial_stride(const VerifyArgs& a, size_t packed) {
+  return a.state_stride > 0 ? (size_t)a.state_stride : packed;
+}
+
 constexpr uint64_t kNoKey = ~0ull;
 constexpr int kKcap = kVerifyMaxK;   // kept tokens per row held on chip
 constexpr int kCandCap = 256;        // threshold-bin entries ranked exactly
@@ -574,29 +579,29 @@ SJD_DEV RowLoad plan_load(const VerifyArgs& a, int row) {
   RowLoad r;
   const int b = row / a.L, j = row % a.L;
   const int Km1 = a.K - 1;
-  const int32_t* meta = a.in_meta + 4 * (size_t)b;
+  const int32_t* meta = a.in_meta + (size_t)b * trial_stride(a, 4);
   const int D_in = meta[0], n_q = meta[1];
   const long g0 = meta[2];
   const int n_s = a.L - Km1 * D_in;
   r.valid = !(D_in < 0 || D_in > a.D || a.K * D_in > a.L || n_q < 0 || n_q > n_s);
   r.need_p = false;
   r.need_q = false;
-  r.cur = a.cur + ((size_t)b * a.L + j) * a.V;
+  r.cur = a.cur + (size_t)b * (a.cur_bstride ? (size_t)a.cur_bstride : (size_t)a.L * a.V) + (size_t)j * a.V;
   r.draft = nullptr;
   if (!r.valid) return r;
   if (j < n_s) {
     const bool is_forced = forced_pos(a, g0 + j);
     r.need_p = !is_forced;
     if (!is_forced && j < n_q) {
-      const int x0 = a.draft_tok[(size_t)b * a.L + j] - a.vis_lo;
+      const int x0 = a.draft_tok[(size_t)b * trial_stride(a, a.L) + j] - a.vis_lo;
       if (x0 >= 0 && x0 < a.V) {
         r.need_q = true;
-        r.draft = a.draft + (size_t)b * a.draft_bstride + (size_t)((a.q_off ? a.q_off[b] : 0) + j) * a.V;
+        r.draft = a.draft + (size_t)b * a.draft_bstride + (size_t)((a.q_off ? a.q_off[(size_t)b * trial_stride(a, 1)] : 0) + j) * a.V;
       }
     }
   } else {
     const int sib_d = (j - n_s) / Km1, sib_k = (j - n_s) % Km1 + 2;
-    const int sib_tok = a.sib ? a.sib[((size_t)b * a.D + sib_d) * Km1 + (sib_k - 2)] : -1;
+    const int sib_tok = a.sib ? a.sib[(size_t)b * trial_stride(a, (size_t)a.D * Km1) + (size_t)sib_d * Km1 + (sib_k - 2)] : -1;
     r.need_p = !(sib_tok < 0 || forced_pos(a, g0 + sib_d) || forced_pos(a, g0 + sib_d + 1));
   }
   if (a.dbg_p) r.need_p = true;
@@ -615,7 +620,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   const int L = a.L, V = a.V, Km1 = a.K - 1;
   const int nchunk = V >> 2;
   if (!ld.valid) return;  // finalize flags the trial
-  const int32_t* meta = a.in_meta + 4 * (size_t)b;
+  const int32_t* meta = a.in_meta + (size_t)b * trial_stride(a, 4);
   const int D_in = meta[0];
   const long g0 = meta[2];
   const int n_s = L - Km1 * D_in;
@@ -659,7 +664,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   // ---- sibling rows: bonus draw from the sibling's own output row
   if (!spine) {
     const int sib_d = (j - n_s) / Km1, sib_k = (j - n_s) % Km1 + 2;
-    const int sib_tok = a.sib ? a.sib[((size_t)b * a.D + sib_d) * Km1 + (sib_k - 2)] : -1;
+    const int sib_tok = a.sib ? a.sib[(size_t)b * trial_stride(a, (size_t)a.D * Km1) + (size_t)sib_d * Km1 + (sib_k - 2)] : -1;
     int tok = -1, stage = 0;
     if (sib_tok < 0 || forced_pos(a, g0 + sib_d)) {
       tok = -1; stage = 0;
@@ -716,14 +721,14 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   for (int t = 0; t < 8; ++t) { stg.cand[t] = -1; stg.Nf[t] = 1.0f; stg.den[t] = 1.0f; }
   int ncand = 0;
   if (ld.need_q) {
-    stg.cand[0] = a.draft_tok[(size_t)b * L + j] - a.vis_lo;
+    stg.cand[0] = a.draft_tok[(size_t)b * trial_stride(a, L) + j] - a.vis_lo;
     ncand = 1;
     if (j < D_in && a.sib) {
       bool open = true;
 #pragma unroll
       for (int k = 0; k < 7; ++k) {
         if (open && k < Km1) {
-          int y = a.sib[((size_t)b * a.D + j) * Km1 + k];
+          int y = a.sib[(size_t)b * trial_stride(a, (size_t)a.D * Km1) + (size_t)j * Km1 + k];
           bool stop = y < 0;
           y -= a.vis_lo;
           stop |= (y < 0 || y >= V);
@@ -922,7 +927,7 @@ __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, Finaliz
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
   const int L = a.L, V = a.V, K = a.K, Km1 = a.K - 1, D = a.D;
-  const int32_t* meta = a.in_meta + 4 * (size_t)b;
+  const int32_t* meta = a.in_meta + (size_t)b * trial_stride(a, 4);
   const int D_in = meta[0];
   const long g0 = meta[2];
   const int n_s = L - Km1 * D_in;

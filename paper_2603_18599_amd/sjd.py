@@ -42,7 +42,8 @@ class Config(C.Structure):
                 ("vocab_size", C.c_int32), ("vis_lo", C.c_int32), ("V", C.c_int32), ("max_seq", C.c_int32),
                 ("L", C.c_int32), ("K", C.c_int32), ("D", C.c_int32), ("flags", C.c_uint32),
                 ("rms_eps", C.c_float), ("rope_theta", C.c_float), ("eol_id", C.c_int32),
-                ("row_len", C.c_int32), ("weights_f32", C.c_int32), ("cfg_w", C.c_float)]
+                ("row_len", C.c_int32), ("weights_f32", C.c_int32), ("cfg_w", C.c_float),
+                ("batch", C.c_int32)]
 
 
 class Weights(C.Structure):
@@ -50,8 +51,8 @@ class Weights(C.Structure):
                 ("d_lm_head", C.c_void_p)]
 
 
-EXPORTS = ["sjd_status_str", "sjd_verify", "sjd_init", "sjd_prefill", "sjd_prefill_cfg", "sjd_step",
-           "sjd_forward_window", "sjd_destroy"]
+EXPORTS = ["sjd_status_str", "sjd_verify", "sjd_init", "sjd_prefill", "sjd_prefill_image", "sjd_prefill_cfg",
+           "sjd_step", "sjd_forward_window", "sjd_destroy"]
 
 _lib = None
 
@@ -79,6 +80,8 @@ def load_library():
     lib.sjd_init.argtypes = [C.POINTER(Config), C.POINTER(Weights), C.c_void_p, C.POINTER(C.c_void_p)]
     lib.sjd_prefill.restype = C.c_int
     lib.sjd_prefill.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_uint64, C.c_void_p]
+    lib.sjd_prefill_image.restype = C.c_int
+    lib.sjd_prefill_image.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_uint64, C.c_void_p]
     lib.sjd_prefill_cfg.restype = C.c_int
     lib.sjd_prefill_cfg.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_uint64,
                                     C.c_void_p]
@@ -146,7 +149,7 @@ class Engine:
                    cfg["ffn_dim"], cfg["vocab_size"], cfg["vis_lo"], cfg["V"], cfg["max_seq"], cfg["L"], cfg["K"],
                    cfg["D"], cfg.get("flags", SJD_AC | SJD_PD), cfg.get("rms_eps", 1e-5),
                    cfg.get("rope_theta", 1e4), cfg.get("eol_id", -1), cfg.get("row_len", 0),
-                   1 if cfg.get("weights_f32", False) else 0, cfg.get("cfg_w", 0.0))
+                   1 if cfg.get("weights_f32", False) else 0, cfg.get("cfg_w", 0.0), cfg.get("batch", 1))
         names = ["attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd"]
         self._layer_ptrs = (C.c_void_p * (9 * cfg["n_layers"]))()
         for l in range(cfg["n_layers"]):
@@ -162,6 +165,11 @@ class Engine:
     def prefill(self, prompt, seed, stream=None):
         _check("sjd_prefill", load_library().sjd_prefill(self.h, _ptr(prompt), prompt.numel(), seed,
                                                           _stream(stream)))
+
+    def prefill_image(self, image, prompt, seed, stream=None):
+        """Batched contexts: (re)starts image `image` with `prompt`."""
+        _check("sjd_prefill_image", load_library().sjd_prefill_image(self.h, image, _ptr(prompt), prompt.numel(), seed,
+                                                                      _stream(stream)))
 
     def prefill_cfg(self, prompt, uncond, seed, stream=None):
         """Guided contexts (cfg_w != 0): text prompt and unconditional prompt."""

@@ -1,0 +1,154 @@
+"""Two images per step (batch = 2) on the GPU, through the C ABI: image b's
+window occupies rows [32 b, 32 b + L) of one forward (one pass over the
+weights), with its own cache, decoder state and prompt.
+- each image's window logits against the oracle's first window of that
+  image alone (prompts of different lengths);
+- greedy decoding of a batch gives each image the tokens of a one-image
+  context on the same prompt, also when one image is restarted mid-run
+  while the other continues;
+- each image's cache grows by its own committed counts;
+- mean committed tokens per step of batched GPU and oracle generations.
+"""
+import numpy as np
+import pytest
+import torch
+
+from model_util import make_engine, oracle_first_window, setup, weights_device, weights_numpy
+from synth_inputs import model_config, prompt_tokens
+
+pytestmark = pytest.mark.gpu
+
+TOL = 3e-2  # the window forward bound
+
+CASES = [
+    ("tiny", {"L": 16}, 9),
+    ("tiny", {"L": 32, "K": 2, "D": 2}, 40),
+    ("7b", {"n_layers": 2, "n_prompt": 40, "L": 32}, 70),
+]
+
+
+@pytest.mark.parametrize("name,over,n1", CASES, ids=[f"{n}-{i}" for i, (n, _, _) in enumerate(CASES)])
+def test_batched_window_forward_matches_oracle(orc, name, over, n1):
+    cfg = model_config(name, batch=2, **over)
+    cfg["max_seq"] = max(cfg["max_seq"], n1 + 2 * cfg["L"] + 8)
+    wt, p0 = setup(cfg, wseed=91, pseed=92, device="cuda")
+    p1 = prompt_tokens(dict(cfg, n_prompt=n1), 93)
+    print(f"case {name} {over} n1={n1}", flush=True)
+    eng = make_engine(cfg, weights_device(wt))
+    eng.prefill_image(0, p0.cuda(), 7)
+    eng.prefill_image(1, p1.cuda(), 8)
+    L, V = cfg["L"], cfg["V"]
+    got_t = torch.empty(32 + L, V, dtype=torch.float32, device="cuda")
+    eng.forward_window(got_t)
+    torch.cuda.synchronize()
+    got = got_t.cpu().numpy()
+    eng.close()
+    w_np = weights_numpy(wt)
+    for b, (p, seed) in enumerate(((p0, 7), (p1, 8))):
+        ref = oracle_first_window(orc, cfg, w_np, p.numpy().astype(np.int32), seed)
+        rows = got[32 * b:32 * b + L]
+        err = np.abs(rows - ref).max()
+        print(f"{name} {over} image {b}: max |logit error| = {err:.3e}", flush=True)
+        assert np.isfinite(rows).all()
+        assert err <= TOL, (b, err)
+
+
+def run_steps(eng, cfg, B, n_steps, *, seed, top_k, T=1.0):
+    """n_steps steps; per image the committed tokens, n_c and cached rows."""
+    meta = torch.zeros(B, 8, dtype=torch.int32, device="cuda")
+    tok = torch.zeros(B, cfg["L"], dtype=torch.int32, device="cuda")
+    toks = [[] for _ in range(B)]
+    ncs = [[] for _ in range(B)]
+    ns = [[] for _ in range(B)]
+    for _ in range(n_steps):
+        step = run_steps.counter
+        run_steps.counter += 1
+        eng.step(T, top_k, seed, step, out_meta=meta, out_tok=tok)
+        m = meta.cpu().numpy()
+        t = tok.cpu().numpy()
+        for b in range(B):
+            n_c = int(m[b, 0])
+            assert 1 <= n_c <= cfg["L"], m
+            toks[b].extend(t[b, :n_c].tolist())
+            ncs[b].append(n_c)
+            ns[b].append(int(m[b, 7]))
+    return toks, ncs, ns
+
+
+run_steps.counter = 0
+
+
+def single_greedy(cfg, wd, prompt, n_gen):
+    c1 = dict(cfg, batch=1)
+    eng = make_engine(c1, wd)
+    eng.prefill(prompt.cuda(), 1)
+    out = []
+    while len(out) < n_gen:
+        toks, _, _ = run_steps(eng, c1, 1, 1, seed=1, top_k=1)
+        out.extend(toks[0])
+    eng.close()
+    return out[:n_gen]
+
+
+@pytest.mark.parametrize("K,D,flags,L", [(4, 3, 3, 16), (2, 2, 1, 32), (1, 0, 0, 8)])
+def test_batched_greedy_equals_single_image(K, D, flags, L):
+    cfg = model_config("tiny", K=K, D=D, flags=flags, L=L, batch=2, n_gen=160)
+    cfg["max_seq"] = 1024  # 16 steps of up to L tokens
+    wt, p0 = setup(cfg, wseed=95, pseed=96)
+    p1 = prompt_tokens(dict(cfg, n_prompt=23), 97)
+    p2 = prompt_tokens(dict(cfg, n_prompt=5), 98)
+    wd = weights_device(wt)
+    eng = make_engine(cfg, wd)
+    eng.prefill_image(0, p0.cuda(), 1)
+    eng.prefill_image(1, p1.cuda(), 2)
+    t_a, nc_a, ns_a = run_steps(eng, cfg, 2, 6, seed=1, top_k=1)
+    # restart image 1 with a new prompt; image 0 continues
+    eng.prefill_image(1, p2.cuda(), 3)
+    t_b, nc_b, ns_b = run_steps(eng, cfg, 2, 10, seed=1, top_k=1)
+    eng.close()
+    # cache rows grow by each image's own committed counts
+    assert ns_a[0] == list(np.cumsum(nc_a[0]) + len(p0) - 1)
+    assert ns_a[1] == list(np.cumsum(nc_a[1]) + len(p1) - 1)
+    assert ns_b[1] == list(np.cumsum(nc_b[1]) + len(p2) - 1)
+    img0 = t_a[0] + t_b[0]
+    assert img0 == single_greedy(cfg, wd, p0, len(img0))
+    assert t_a[1] == single_greedy(cfg, wd, p1, len(t_a[1]))
+    assert t_b[1] == single_greedy(cfg, wd, p2, len(t_b[1]))
+    assert np.mean(nc_a[0] + nc_b[0]) > 1.0
+
+
+def test_batched_acceptance_statistics_match_oracle(orc):
+    cfg = model_config("tiny", n_gen=128, batch=2)
+    cfg["max_seq"] = 2048  # the faster image runs on while the slower one reaches 128 tokens
+    wt, p0 = setup(cfg, wseed=101, pseed=102)
+    p1 = prompt_tokens(dict(cfg, n_prompt=11), 103)
+    eng = make_engine(cfg, weights_device(wt))
+    gpu = [[], []]
+    for s in range(10):
+        eng.prefill_image(0, p0.cuda(), 500 + s)
+        eng.prefill_image(1, p1.cuda(), 600 + s)
+        ncs = [[], []]
+        while min(sum(c) for c in ncs) < 128:
+            _, nc1, _ = run_steps(eng, cfg, 2, 1, seed=700 + s, top_k=0)
+            for b in range(2):
+                ncs[b] += nc1[b]
+        for b in range(2):
+            # the image's steps until it had its 128 tokens
+            k = int(np.searchsorted(np.cumsum(ncs[b]), 128)) + 1
+            gpu[b] += ncs[b][:k]
+    eng.close()
+    m = orc.Model(cfg, weights_numpy(wt), max_seq=cfg["max_seq"])
+    ocfg = orc.ModelCfg(cfg["n_layers"], cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"],
+                        cfg["ffn_dim"], cfg["vocab_size"], cfg["vis_lo"], cfg["V"], cfg["max_seq"], 1e-5, 1e4)
+    for b, p in enumerate((p0, p1)):
+        orc_nc = []
+        for s in range(10):
+            g = orc.gen_cfg(L=cfg["L"], V=cfg["V"], K=cfg["K"], D=cfg["D"], top_k=0, seed=800 + 10 * b + s,
+                            n_prompt=len(p), n_gen=128, mcfg=ocfg, weights=m.w)
+            _, steps, hist = orc.generate(g, p.numpy().astype(np.int32))
+            orc_nc += sum(([i] * int(c) for i, c in enumerate(hist)), [])
+        a, o = np.array(gpu[b], float), np.array(orc_nc, float)
+        se = np.sqrt(a.var() / a.size + o.var() / o.size)
+        print(f"image {b}: mean n_c gpu {a.mean():.3f} ({a.size} steps) oracle {o.mean():.3f} ({o.size}) se {se:.3f}")
+        assert abs(a.mean() - o.mean()) < 4 * se + 0.02
+    m.close()
