@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--L", type=int, default=0, help="window slots (0 = the workload's)")
     ap.add_argument("--K", type=int, default=0, help="drafting candidates per tree row (0 = the workload's)")
     ap.add_argument("--D", type=int, default=-1, help="tree depth (-1 = the workload's)")
+    ap.add_argument("--batch", type=int, default=1, choices=[1, 2],
+                    help="images per step (2: both windows in one forward, one pass over the weights)")
+    ap.add_argument("--no-batch2", action="store_true", help="skip the two-images-per-step section")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -297,16 +300,18 @@ def cpu_baseline_verify(args, inp, K, D, top_k, T, seed, B, L):
             "kind": "oracle", "sample": f"{len(idx)} of {B} windows (one verification step), {dt:.1f} s"}
 
 
-def step_bytes(cfg, n_mean):
+def step_bytes(cfg, n_mean, B=1):
     """Algorithmic HBM bytes of one step: every weight streamed once (bf16),
     the LM head rows of the sampled range only, the cached keys and values
     read once (hi/lo bf16 planes, 4 bytes per element), the window's K/V
-    written, and the logits written and read back by the verification."""
+    written, and the logits written and read back by the verification; B
+    images share the weight stream, each has its own cache and logits
+    (n_mean: mean cached rows per image)."""
     d, H, Hkv, hd, F, V, L = (cfg[k] for k in ("d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim", "V", "L"))
     per_layer = (H * hd * d + 2 * Hkv * hd * d + d * H * hd + 3 * F * d) * 2
     weights = cfg["n_layers"] * per_layer + V * d * 2
-    kv = cfg["n_layers"] * 2 * Hkv * hd * 4 * (n_mean + L)
-    logits = 2 * L * V * 4 * 2  # written once, current + draft rows read once
+    kv = B * cfg["n_layers"] * 2 * Hkv * hd * 4 * (n_mean + L)
+    logits = B * 2 * L * V * 4 * 2  # written once, current + draft rows read once
     return weights + kv + logits, weights, kv
 
 
@@ -326,23 +331,33 @@ def bench_step(args):
         over["D"] = args.D
     if args.mode in ("sjd", "ac") and args.K <= 0:
         over["K"], over["D"] = 1, 0  # no drafting tree without PD
+    B = args.batch
+    over["batch"] = B
     cfg = model_config(args.workload, **over)
     seed = 11
     w = model_weights(cfg, 1, device="cuda")
-    prompt = prompt_tokens(cfg, 2)
-    if args.context == "mid":
-        prompt = torch.cat([prompt, image_history(cfg, cfg["n_gen"] // 2, 3)])
-    prompt = prompt.cuda()
+    prompts = []
+    for b in range(B):  # image b: its own prompt (and image so far)
+        p = prompt_tokens(cfg, 2 + 10 * b)
+        if args.context == "mid":
+            p = torch.cat([p, image_history(cfg, cfg["n_gen"] // 2, 3 + 10 * b)])
+        prompts.append(p.cuda())
+    prompt = prompts[0]
     eng = Engine(cfg, w)
     stream = torch.cuda.current_stream()
     K, W = args.steps, args.warmup
-    metas = torch.zeros(W + K, 8, dtype=torch.int32, device="cuda")
+    metas = torch.zeros(W + K, B, 8, dtype=torch.int32, device="cuda")
+
+    def prefill_all(sd):
+        for b in range(B):
+            eng.prefill_image(b, prompts[b], sd + 1000 * b, stream=stream)
+
     if not args.calibrate_copy:  # (counter runs: one prefill only, each dispatch is slow there)
-        eng.prefill(prompt, seed, stream=stream)
+        prefill_all(seed)
     torch.cuda.synchronize()
-    progress(f"model ready; prefill of {prompt.numel()} tokens")
+    progress(f"model ready; prefill of {B} x {prompt.numel()} tokens")
     t_pre = time.perf_counter()
-    eng.prefill(prompt, seed, stream=stream)
+    prefill_all(seed)
     torch.cuda.synchronize()
     prefill_ms = (time.perf_counter() - t_pre) * 1e3
     restarts = 0
@@ -354,8 +369,8 @@ def bench_step(args):
         except SjdError as e:
             if e.code != -4:
                 raise
-            restarts += 1  # image complete: the cache is full, start the next image
-            eng.prefill(prompt, seed + restarts, stream=stream)
+            restarts += 1  # an image is complete: its cache is full, start the next images
+            prefill_all(seed + restarts)
             eng.step(cfg["temperature"], cfg["top_k"], seed, t, out_meta=metas[t], stream=stream)
 
     progress("prefill done")
@@ -377,12 +392,12 @@ def bench_step(args):
     if args.calibrate_copy:
         profiler_region(False)
     m = metas.cpu().numpy()
-    ncs = m[W:, 0]
-    ns = m[W:, 7]
+    ncs = m[W:, :, 0]  # [step][image]
+    ns = m[W:, :, 7]
     step_ms = [a.elapsed_time(b) for a, b in evs]
     avg_ms = float(np.mean(step_ms))
     n_mean = float(np.mean(ns - ncs))
-    total, weights, kv = step_bytes(cfg, n_mean)
+    total, weights, kv = step_bytes(cfg, n_mean, B)
     achieved = total / (avg_ms * 1e-3) / 1e9
     res = dict(metric="image tokens/sec on 1 MI355X; mean accept length/step; verify HBM GB/s",
                value=float(ncs.sum()) / wall, unit="image tokens/s", n_gpus=1, steps=K, warmup=W,
@@ -392,10 +407,11 @@ def bench_step(args):
                                    f"{cfg['n_heads']}q/{cfg['n_kv_heads']}kv heads x {cfg['head_dim']}, "
                                    f"SwiGLU {cfg['ffn_dim']}, vocab {cfg['vocab_size']} (sampled {cfg['V']}), "
                                    f"L={cfg['L']} K={cfg['K']} D={cfg['D']}, mode {args.mode}, "
+                                   + (f"{B} images per step, " if B > 1 else "") +
                                    f"top-{cfg['top_k']}, T=1, "
                                    f"{cfg['n_prompt']}-token prompt, {cfg['n_gen']}-token image, "
                                    f"steps timed from KV length {prompt.numel() - 1}",
-                       "global_batch": 1, "seq_len": cfg["L"]},
+                       "global_batch": B, "seq_len": cfg["L"]},
                mean_accept_length=float(ncs.mean()), step_latency_ms=avg_ms,
                step_latency_p50_ms=float(np.percentile(step_ms, 50)),
                step_latency_p99_ms=float(np.percentile(step_ms, 99)),
@@ -405,7 +421,7 @@ def bench_step(args):
                          "kernel": "sjd_step (window forward + verification + KV commit)",
                          "bytes_per_launch": total, "weight_bytes": weights, "kv_bytes": kv,
                          "avg_launch_ms": avg_ms,
-                         "mfma_tflops": 2.0 * weights / 2 * cfg["L"] / (avg_ms * 1e-3) / 1e12})
+                         "mfma_tflops": 2.0 * weights / 2 * cfg["L"] * B / (avg_ms * 1e-3) / 1e12})
     eng.close()
     del w
     torch.cuda.empty_cache()
@@ -469,6 +485,12 @@ def main():
                                                 calibrate_copy=False))
             res["verify"] = {k: v[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length", "verify_GBps",
                                                "roofline", "config")}
+        if args.batch == 1 and not args.no_batch2 and not args.calibrate_copy:
+            # the same workload with two images per step (serving several requests)
+            b2 = bench_step(argparse.Namespace(**dict(vars(args), batch=2, no_cpu_baseline=True)))
+            res["batch2"] = {k: b2[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length",
+                                                "step_latency_ms", "config")}
+            res["batch2"]["roofline_frac"] = b2["roofline"]["frac"]
     print(json.dumps(res), flush=True)
 
 
