@@ -52,6 +52,7 @@ def parse():
     ap.add_argument("--batch", type=int, default=1, choices=[1, 2],
                     help="images per step (2: both windows in one forward, one pass over the weights)")
     ap.add_argument("--no-batch2", action="store_true", help="skip the two-images-per-step section")
+    ap.add_argument("--eager", action="store_true", help="enqueue every kernel directly (no captured graph)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -322,7 +323,7 @@ def bench_step(args):
     from paper_2603_18599_amd.sjd import Engine, SjdError
     from synth_inputs import image_history, model_config, model_weights, prompt_tokens
 
-    over = {"flags": {"sjd-pac": 3, "sjd": 0, "ac": 1, "pd": 2}[args.mode]}
+    over = {"flags": {"sjd-pac": 3, "sjd": 0, "ac": 1, "pd": 2}[args.mode] | (4 if args.eager else 0)}
     if args.L > 0:
         over["L"] = args.L
     if args.K > 0:
@@ -382,10 +383,13 @@ def bench_step(args):
         profiler_region(True)
         calibration_copy()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    host_s = 0.0  # host time spent enqueueing steps
     t0 = time.perf_counter()
     for i in range(K):
         evs[i][0].record(stream)
+        th = time.perf_counter()
         one(W + i)
+        host_s += time.perf_counter() - th
         evs[i][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -416,6 +420,7 @@ def bench_step(args):
                step_latency_p50_ms=float(np.percentile(step_ms, 50)),
                step_latency_p99_ms=float(np.percentile(step_ms, 99)),
                prefill_ms=prefill_ms, kv_rows_mean=n_mean, image_restarts=restarts,
+               host_enqueue_ms_per_step=host_s * 1e3 / K,
                roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic(args.workload),
                          "kernel": "sjd_step (window forward + verification + KV commit)",

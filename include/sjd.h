@@ -62,6 +62,10 @@ typedef enum {
 /* flags */
 #define SJD_AC 1u /* adaptive continuation: no break after the first rejection (Sec. 4.2) */
 #define SJD_PD 2u /* proactive drafting after a rejection (Sec. 4.1)                      */
+/* decoder contexts only: enqueue every kernel of a step directly instead of
+ * replaying the step's window forward from a captured HIP graph (the
+ * results are identical; for debugging and profiling) */
+#define SJD_EAGER 4u
 
 /* Returns a static string naming a status code. */
 SJD_API const char* sjd_status_str(int status);
@@ -154,7 +158,8 @@ typedef struct {
   int32_t vis_lo, V;     /* sampled range of the head: rows [vis_lo, vis_lo + V)       */
   int32_t max_seq;       /* KV capacity in tokens (prompt + generated + L)             */
   int32_t L, K, D;       /* window slots (1..64), candidates per depth (1..8), depth   */
-  uint32_t flags;        /* SJD_AC | SJD_PD (0 = vanilla SJD; Sec. 5.3's ablation)     */
+  uint32_t flags;        /* SJD_AC | SJD_PD (0 = vanilla SJD; Sec. 5.3's ablation),
+                            optionally | SJD_EAGER                                       */
   float rms_eps, rope_theta;
   int32_t eol_id, row_len;
   int32_t weights_f32;   /* 1: weights are fp32, 0: bf16                                */

@@ -241,6 +241,195 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   }
 }
 
+// Variant for 128-dim heads (four 32-dim output blocks, one per wave): the
+// waves exchange probabilities instead of outputs. Each wave scores its own
+// 32 keys as above, writes its P (hi / lo bf16, 4 KB) and softmax statistics
+// to LDS, and then forms the output of its own 32 dims over all 128 keys of
+// the chunk, loading those dims' value tiles of all four key blocks (the same
+// bytes as its own keys' full rows, still contiguous 1 KB loads). This
+// replaces a 64 KB fp32 output exchange and its reduction with a 16 KB
+// probability exchange; the partial then leaves in four independent 4 KB
+// slices.
+struct AttnPxSmem {
+  uint4 q[2][8][kWave];     // Q^T operand (hi, lo), 128 dims
+  uint4 p[4][2][2][kWave];  // [key block][16-key half][hi / lo][lane]: P^T operand
+  float m[4][32];
+  float l[4][32];
+};
+
+__global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
+  constexpr int HD = 128, NQ = HD / 16;
+  static_assert(kAttnChunk == 4 * 32, "one 32-key block per wave");
+  __shared__ AttnPxSmem sm;
+  const int h = blockIdx.x, sp = blockIdx.y;
+  const bool two = a.st.mode != kStreamsOne;
+  const bool second = two && blockIdx.z == 1;
+  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, second);
+  const int Ms = two ? a.st.L : a.M, nk = n + Ms;
+  const int kbeg = sp * kAttnChunk;
+  if (kbeg >= nk) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5;
+  const int kvh = h / (a.H / a.Hkv);
+  const int zs = blockIdx.z * 32;
+  const int slot = lane & 31;
+  const int gslot = zs + slot;
+  const bool slot_ok = two ? slot < Ms : gslot < Ms;
+  const size_t hbase = (size_t)kvh * a.cap * HD + (second ? a.sstride : 0);
+  const int kb = kbeg + wave * 32;  // this wave's key block
+  const bool has = kb < nk;
+
+  uint4 qs[2][2];
+  {
+    const size_t qo = (size_t)(slot_ok ? gslot : 0) * a.H * HD + (size_t)h * HD + half * (HD / 2);
+    const uint4* qp = (const uint4*)(a.q + qo);
+    const uint4* qpl = (const uint4*)(a.q_lo + qo);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int t = wave + 4 * i;
+      qs[0][i] = slot_ok ? qp[t] : make_uint4(0, 0, 0, 0);
+      qs[1][i] = slot_ok ? qpl[t] : make_uint4(0, 0, 0, 0);
+    }
+  }
+  // own keys (all dims), then this wave's 32 value dims of all four key blocks
+  uint4 kh[NQ], kl[NQ], vh[4][2], vl[4][2];
+  if (has) {
+    const uint4* kp = (const uint4*)(a.kc + hbase + (size_t)kb * HD + (size_t)lane * 8);
+    const uint4* kpl = (const uint4*)(a.kc_lo + hbase + (size_t)kb * HD + (size_t)lane * 8);
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+      kh[t] = kp[t * 64];
+      kl[t] = kpl[t * 64];
+    }
+  }
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const int kbw = kbeg + w * 32;
+    const uint4* vp = (const uint4*)(a.vt + hbase + (size_t)kbw * HD + (size_t)lane * 8);
+    const uint4* vpl = (const uint4*)(a.vt_lo + hbase + (size_t)kbw * HD + (size_t)lane * 8);
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {  // absent blocks: zeros (their P is zero; 0 * garbage could be NaN)
+      vh[w][jj] = kbw < nk ? vp[(wave * 2 + jj) * 64] : make_uint4(0, 0, 0, 0);
+      vl[w][jj] = kbw < nk ? vpl[(wave * 2 + jj) * 64] : make_uint4(0, 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    sm.q[0][wave + 4 * i][lane] = qs[0][i];
+    sm.q[1][wave + 4 * i][lane] = qs[1][i];
+  }
+  __syncthreads();
+
+  float m_w = -INFINITY, l_w = 0.0f;
+  uint4 pb[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)}, pbl[2] = {pb[0], pb[1]};
+  if (has) {
+    f32x16 s;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+      const bf16x8 khb = to_bf16x8(kh[t]), klb = to_bf16x8(kl[t]);
+      const bf16x8 qh = to_bf16x8(sm.q[0][t][lane]), ql = to_bf16x8(sm.q[1][t][lane]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, qh, s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, ql, s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(klb, qh, s, 0, 0, 0);
+    }
+    // mask (register r = 8jj + e holds key kb + 16jj + 8half + e)
+    if (kb + 32 <= n) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = slot_ok ? s[r] * a.scale : -INFINITY;
+    } else {
+      const uint64_t anc = slot_ok ? a.win->anc[gslot] : 0ull;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + 16 * (r >> 3) + 8 * half + (r & 7);
+        bool vis = slot_ok && key < nk;
+        if (vis && key >= n) vis = (anc >> (key - n)) & 1ull;
+        s[r] = vis ? s[r] * a.scale : -INFINITY;
+      }
+    }
+    float mloc = s[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[r]);
+    m_w = fmaxf(mloc, __shfl_xor(mloc, 32, kWave));
+    float lsum = 0.0f;
+    if (m_w != -INFINITY) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[r] = exp2f(s[r] - m_w);
+        lsum += s[r];
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+    }
+    l_w = lsum + __shfl_xor(lsum, 32, kWave);
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      uint32_t w[4], wl[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        uint16_t h0, l0, h1, l1;
+        split_bf16_finite(s[8 * jj + 2 * e], h0, l0);
+        split_bf16_finite(s[8 * jj + 2 * e + 1], h1, l1);
+        w[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        wl[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+      }
+      pb[jj] = make_uint4(w[0], w[1], w[2], w[3]);
+      pbl[jj] = make_uint4(wl[0], wl[1], wl[2], wl[3]);
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < 2; ++jj) {
+    sm.p[wave][jj][0][lane] = pb[jj];
+    sm.p[wave][jj][1][lane] = pbl[jj];
+  }
+  if (half == 0) {
+    sm.m[wave][slot] = m_w;
+    sm.l[wave][slot] = l_w;
+  }
+  __syncthreads();
+
+  // O^T (this wave's 32 dims x 32 slots) = sum over key blocks w of
+  // 2^(m_w - m) V_w^T . P_w^T
+  float mw[4], mx = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    mw[w] = sm.m[w][slot];
+    mx = fmaxf(mx, mw[w]);
+  }
+  f32x16 o;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) o[r] = 0.0f;
+  float ls = 0.0f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float f = mx == -INFINITY ? 0.0f : exp2f(mw[w] - mx);
+    ls += sm.l[w][slot] * f;
+    f32x16 t;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) t[r] = 0.0f;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      const bf16x8 vhb = to_bf16x8(vh[w][jj]), vlb = to_bf16x8(vl[w][jj]);
+      const bf16x8 ph = to_bf16x8(sm.p[w][jj][0][lane]), pl = to_bf16x8(sm.p[w][jj][1][lane]);
+      t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vhb, ph, t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vhb, pl, t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vlb, ph, t, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[r] += f * t[r];
+  }
+  // register r of lane (slot, half): dim 32 wave + 8(r/4) + 4 half + r%4
+  float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * 64 + zs + slot) * HD + wave * 32 + 4 * half;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) *(float4*)(wo + 8 * g) = make_float4(o[4 * g], o[4 * g + 1], o[4 * g + 2], o[4 * g + 3]);
+  if (wave == 0 && half == 0) {
+    float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 64 * 2 + (size_t)(zs + slot) * 2;
+    wml[0] = mx;
+    wml[1] = ls;
+  }
+}
+
 // out[slot][h*hd + dim] = sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m).
 // grid (H, HD / 32, slot halves), block 256: thread -> (slot, 4 consecutive dims); the
 // split loop is unrolled so that its loads are in flight together.
@@ -291,7 +480,7 @@ hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s) {
   const unsigned zh = (unsigned)(a.M + 31) / 32;  // 32-slot halves
   const dim3 g1(a.H, a.nsplit_max, zh), g2(a.H, hd / 32, zh);
   if (hd == 128) {
-    hipLaunchKernelGGL(k_attn_partial<128>, g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_attn_partial_px, g1, dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_attn_combine<128>, g2, dim3(256), 0, s, a);
   } else if (hd == 64) {
     hipLaunchKernelGGL(k_attn_partial<64>, g1, dim3(256), 0, s, a);

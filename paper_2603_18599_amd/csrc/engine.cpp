@@ -65,6 +65,12 @@ struct Ctx {
   int S_qkv = 1, S_o = 1, S_gu = 1, S_dn = 1, S_head = 1;
   long long steps = 0;
   unsigned prefilled = 0;  // bit b: image b prefilled
+  // the step's window forward (window build + ~10 kernels per layer + head),
+  // captured once per logits buffer on cap_stream and replayed on the
+  // caller's stream: its kernels and arguments never change for a context
+  bool use_graph = true;
+  hipStream_t cap_stream = nullptr;
+  hipGraphExec_t fwd_exec[2] = {nullptr, nullptr};
   // cache-fill bound, per image: cached rows after step ev_step[i] are
   // written by the step's last kernel into h_n[i * B + b] (pinned host ring)
   int32_t* h_n = nullptr;
@@ -102,7 +108,7 @@ int check_config(const sjd_config* c) {
   if (c->L < 1 || c->L > 64 || c->K < 1 || c->K > 8 || c->D < 0 || (long)c->K * c->D > c->L) return SJD_EINVAL;
   if (c->V > 65536) return SJD_ENOTSUP;
   if (c->max_seq < c->L + 2) return SJD_EINVAL;
-  if (c->flags & ~(SJD_AC | SJD_PD)) return SJD_EINVAL;
+  if (c->flags & ~(SJD_AC | SJD_PD | SJD_EAGER)) return SJD_EINVAL;
   if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
   if (!std::isfinite(c->cfg_w)) return SJD_EINVAL;
   if (c->batch < 0) return SJD_EINVAL;
@@ -232,6 +238,7 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   x.c = *cfg;
   const sjd_config& c = x.c;
   x.guided = c.cfg_w != 0.0f;
+  x.use_graph = !(c.flags & SJD_EAGER);
   x.B = c.batch == 2 ? 2 : 1;
   x.nstreams = x.guided || x.B == 2 ? 2 : 1;
   auto fail = [&](int rc) {
@@ -370,6 +377,8 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   }
   // pinned, device-visible: the step's last kernel writes the cached-row
   // counts into it directly
+  if (x.use_graph && hipStreamCreateWithFlags(&x.cap_stream, hipStreamNonBlocking) != hipSuccess)
+    return fail(SJD_EHIP);
   if (hipHostMalloc((void**)&x.h_n, sizeof(int32_t) * kRing * x.B, hipHostMallocDefault) != hipSuccess)
     return fail(SJD_ENOMEM);
   for (int i = 0; i < kRing * x.B; ++i) x.h_n[i] = 0;
@@ -406,7 +415,15 @@ int prefill(Ctx& x, int b, const int32_t* d_prompt, int n, const int32_t* d_unco
   if (d_uncond) TRY(prefill_stream(x, d_uncond, n_u, 1, s));
   HIPTRY(sjd::launch_state_init(x.st + b, d_prompt, n, d_uncond, n_u, x.c.L, x.c.V, x.c.vis_lo, x.c.eol_id,
                                 x.c.row_len, seed, s));
-  if (d_uncond) x.delta = n_u - n;
+  if (d_uncond && n_u - n != x.delta) {
+    // the captured forwards carry delta as an argument: capture again
+    for (hipGraphExec_t& e : x.fwd_exec)
+      if (e) {
+        (void)hipGraphExecDestroy(e);
+        e = nullptr;
+      }
+    x.delta = n_u - n;
+  }
   x.prefilled |= 1u << b;
   // the image's cache-fill bound restarts; steps before this one say nothing about it
   x.img_step0[b] = x.steps;
@@ -425,6 +442,36 @@ sjd::Streams window_streams(Ctx& x) {
 
 // window rows: one stream of L, or two streams in rows [0, L) and [32, 32 + L)
 int window_rows(const Ctx& x) { return x.nstreams == 2 ? 32 + x.c.L : x.c.L; }
+
+// A step's window build and forward into logits buffer `buf`: replayed from
+// a graph captured on the first step that uses the buffer (the kernels read
+// every per-step value, such as n and the window, from device state).
+int step_forward(Ctx& x, int buf, float* logits, hipStream_t s) {
+  const sjd::Streams sm = window_streams(x);
+  auto enqueue = [&](hipStream_t q) -> int {
+    HIPTRY(sjd::launch_build_window(x.st, x.win, x.c.L, x.c.K, x.c.vis_lo, sm, q));
+    return forward(x, window_rows(x), &x.st->n, 0, logits, sm, 0, q);
+  };
+  if (!x.use_graph) return enqueue(s);
+  if (!x.fwd_exec[buf]) {
+    hipGraph_t g = nullptr;
+    HIPTRY(hipStreamBeginCapture(x.cap_stream, hipStreamCaptureModeRelaxed));
+    const int rc = enqueue(x.cap_stream);
+    const hipError_t e = hipStreamEndCapture(x.cap_stream, &g);
+    if (rc != SJD_OK || e != hipSuccess) {
+      if (g) (void)hipGraphDestroy(g);
+      return rc != SJD_OK ? rc : SJD_EHIP;
+    }
+    const hipError_t ei = hipGraphInstantiate(&x.fwd_exec[buf], g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (ei != hipSuccess) {
+      x.fwd_exec[buf] = nullptr;
+      return SJD_EHIP;
+    }
+  }
+  HIPTRY(hipGraphLaunch(x.fwd_exec[buf], s));
+  return SJD_OK;
+}
 
 }  // namespace
 
@@ -465,14 +512,13 @@ extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t s
   const sjd_config& c = x.c;
   float* cur = x.logits[x.steps & 1];
   float* prev = x.logits[(x.steps + 1) & 1];
-  const sjd::Streams sm = window_streams(x);
-  HIPTRY(sjd::launch_build_window(x.st, x.win, c.L, c.K, c.vis_lo, sm, s));
-  TRY(forward(x, window_rows(x), &x.st->n, 0, cur, sm, 0, s));
+  TRY(step_forward(x, (int)(x.steps & 1), cur, s));
   // image b: logits rows from 32 b (batch), decoder state x.st[b], Philox trial b
   const int sstate = (int)(sizeof(sjd::DevState) / sizeof(int32_t));
   const long long lstride = x.B == 2 ? 32LL * c.V : 0;
   sjd::VerifyArgs a{};
-  a.B = x.B; a.L = c.L; a.V = c.V; a.K = c.K; a.D = c.D; a.top_k = top_k; a.T = temperature; a.flags = c.flags;
+  a.B = x.B; a.L = c.L; a.V = c.V; a.K = c.K; a.D = c.D; a.top_k = top_k; a.T = temperature;
+  a.flags = c.flags & (SJD_AC | SJD_PD);
   a.seed = seed; a.step = step; a.vis_lo = c.vis_lo; a.eol = c.eol_id; a.row_len = c.row_len;
   a.cur = cur; a.cur_bstride = lstride; a.draft = prev; a.draft_bstride = lstride;
   a.q_off = &x.st->q_off; a.draft_tok = x.st->spine; a.sib = x.st->sib; a.in_meta = &x.st->D_in;
@@ -507,6 +553,9 @@ extern "C" void sjd_destroy(sjd_ctx* h) {
   if (!h) return;
   Ctx& x = h->x;
   (void)hipDeviceSynchronize();
+  for (hipGraphExec_t& e : x.fwd_exec)
+    if (e) (void)hipGraphExecDestroy(e);
+  if (x.cap_stream) (void)hipStreamDestroy(x.cap_stream);
   for (void* p : x.owned) (void)hipFree(p);
   if (x.h_n) (void)hipHostFree(x.h_n);
   for (int i = 0; i < x.n_events; ++i) (void)hipEventDestroy(x.ev[i]);

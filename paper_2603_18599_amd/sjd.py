@@ -13,6 +13,7 @@ _LIB_NAME = "libsjd.so"
 
 SJD_AC = 1
 SJD_PD = 2
+SJD_EAGER = 4
 
 _STATUS = {0: "SJD_OK", -1: "SJD_EINVAL", -2: "SJD_ENOMEM", -3: "SJD_EHIP", -4: "SJD_ESTATE", -5: "SJD_ENOTSUP"}
 
