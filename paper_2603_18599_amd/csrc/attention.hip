@@ -431,8 +431,11 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
 }
 
 // out[slot][h*hd + dim] = sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m).
-// grid (H, HD / 32, slot halves), block 256: thread -> (slot, 4 consecutive dims); the
-// split loop is unrolled so that its loads are in flight together.
+// grid (H, HD / 32, slot halves), block 256: thread -> (slot, 4 consecutive dims).
+// The partials were written by workgroups on every XCD (far-memory round
+// trips), so the splits are taken in groups of kCombGroup whose loads are all
+// in flight at once; groups are merged with a running maximum.
+constexpr int kCombGroup = 16;
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   const int h = blockIdx.x, t = threadIdx.x;
@@ -450,21 +453,40 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   const int ns = (nk + kAttnChunk - 1) / kAttnChunk;
   const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * 128 + slot * 2;
   const float* wo = a.ws_o + ((size_t)h * a.nsplit_max * 64 + slot) * HD + dim0;
-  float mx = -INFINITY;
-#pragma unroll 8
-  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, wml[s * 128]);
+  float mx = -INFINITY, ls = 0.0f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  float ls = 0.0f;
-#pragma unroll 8
-  for (int s = 0; s < ns; ++s) {
-    const float2 ml = *(const float2*)(wml + s * 128);
-    const float4 v = *(const float4*)(wo + (size_t)s * 64 * HD);
-    const float f = ml.x == -INFINITY ? 0.0f : exp2f(ml.x - mx);
-    ls += ml.y * f;
-    acc.x += v.x * f;
-    acc.y += v.y * f;
-    acc.z += v.z * f;
-    acc.w += v.w * f;
+  for (int s0 = 0; s0 < ns; s0 += kCombGroup) {
+    float2 ml[kCombGroup];
+    float4 v[kCombGroup];
+#pragma unroll
+    for (int i = 0; i < kCombGroup; ++i) {
+      const int sx = s0 + i < ns ? s0 + i : ns - 1;
+      ml[i] = *(const float2*)(wml + (size_t)sx * 128);
+      v[i] = *(const float4*)(wo + (size_t)sx * 64 * HD);
+    }
+    float gm = mx;
+#pragma unroll
+    for (int i = 0; i < kCombGroup; ++i)
+      if (s0 + i < ns) gm = fmaxf(gm, ml[i].x);
+    if (gm != mx && mx != -INFINITY) {  // rescale what the earlier groups summed
+      const float r = exp2f(mx - gm);
+      ls *= r;
+      acc.x *= r;
+      acc.y *= r;
+      acc.z *= r;
+      acc.w *= r;
+    }
+    mx = gm;
+#pragma unroll
+    for (int i = 0; i < kCombGroup; ++i)
+      if (s0 + i < ns) {
+        const float f = ml[i].x == -INFINITY ? 0.0f : exp2f(ml[i].x - mx);
+        ls += ml[i].y * f;
+        acc.x += v[i].x * f;
+        acc.y += v[i].y * f;
+        acc.z += v[i].z * f;
+        acc.w += v[i].w * f;
+      }
   }
   ushort4 hi, lo;
   split_bf16(acc.x / ls, hi.x, lo.x);

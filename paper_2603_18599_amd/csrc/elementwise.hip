@@ -5,12 +5,20 @@
 
 namespace sjd {
 
-// x[m][:] = E[tok[m]][:] (fp32 residual stream)
+// x[m][:] = E[tok[m]][:] (fp32 residual stream); d is a multiple of 64, so
+// every 8-element chunk is whole
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, const Window* win, int d, float* x) {
   const int m = blockIdx.x;
   const int t = win->tok[m];
-  const uint16_t* row = E + (size_t)t * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)m * d + i] = bf16_to_f32(row[i]);
+  const uint4* row = (const uint4*)(E + (size_t)t * d);
+  float4* xr = (float4*)(x + (size_t)m * d);
+  for (int c = threadIdx.x; c < d / 8; c += blockDim.x) {
+    const uint4 u = row[c];
+    xr[2 * c] = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                            __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+    xr[2 * c + 1] = make_float4(__uint_as_float(u.z << 16), __uint_as_float(u.z & 0xFFFF0000u),
+                                __uint_as_float(u.w << 16), __uint_as_float(u.w & 0xFFFF0000u));
+  }
 }
 
 hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, float* x, hipStream_t s) {
@@ -21,6 +29,10 @@ hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, floa
 // x += sum_s part[s] (split-K partial planes of the projection that feeds
 // the residual, fixed order), y = x * g as hi / lo bf16 planes, ss[m][c] =
 // sum of x^2 over the 256 elements of chunk c. grid (chunks, M), one wave.
+// The planes were written moments ago by workgroups on every XCD, so each
+// load is a far-memory round trip: all SMAX loads are issued at once
+// (planes past S re-read the last plane and are not added).
+template <int SMAX>
 __global__ __launch_bounds__(64) void k_resid_norm(float* x, const float* part, int S, size_t plane,
                                                    const uint16_t* g, int d, uint16_t* y, uint16_t* y_lo, int ldy,
                                                    float* ss) {
@@ -30,14 +42,19 @@ __global__ __launch_bounds__(64) void k_resid_norm(float* x, const float* part, 
   if (i0 < d) {  // d is a multiple of 64, so a lane's 4 elements are all in range
     float* xr = x + (size_t)m * d + i0;
     float4 v = *(const float4*)xr;
-    const float* pr = part + (size_t)m * d + i0;
-#pragma unroll 4
-    for (int s = 0; s < S; ++s) {
-      const float4 p = *(const float4*)(pr + (size_t)s * plane);
-      v.x += p.x;
-      v.y += p.y;
-      v.z += p.z;
-      v.w += p.w;
+    if (S > 0) {
+      const float* pr = part + (size_t)m * d + i0;
+      float4 p[SMAX];
+#pragma unroll
+      for (int s = 0; s < SMAX; ++s) p[s] = *(const float4*)(pr + (size_t)(s < S ? s : S - 1) * plane);
+#pragma unroll
+      for (int s = 0; s < SMAX; ++s)
+        if (s < S) {
+          v.x += p[s].x;
+          v.y += p[s].y;
+          v.z += p[s].z;
+          v.w += p[s].w;
+        }
     }
     if (S > 0) *(float4*)xr = v;
     ssq = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
@@ -56,8 +73,18 @@ __global__ __launch_bounds__(64) void k_resid_norm(float* x, const float* part, 
 
 hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, const uint16_t* g, int M, int d,
                              uint16_t* y, uint16_t* y_lo, int ldy, float* ss, hipStream_t s) {
-  hipLaunchKernelGGL(k_resid_norm, dim3(norm_chunks(d), M), dim3(64), 0, s, x, part, S, plane, g, d, y, y_lo, ldy,
-                     ss);
+  const dim3 grid(norm_chunks(d), M);
+  if (S <= 4)
+    hipLaunchKernelGGL(k_resid_norm<4>, grid, dim3(64), 0, s, x, part, S, plane, g, d, y, y_lo, ldy, ss);
+  else if (S <= 8)
+    hipLaunchKernelGGL(k_resid_norm<8>, grid, dim3(64), 0, s, x, part, S, plane, g, d, y, y_lo, ldy, ss);
+  else if (S <= 16)
+    hipLaunchKernelGGL(k_resid_norm<16>, grid, dim3(64), 0, s, x, part, S, plane, g, d, y, y_lo, ldy, ss);
+  else if (S <= kGemmMaxSplits)
+    hipLaunchKernelGGL(k_resid_norm<kGemmMaxSplits>, grid, dim3(64), 0, s, x, part, S, plane, g, d, y, y_lo, ldy,
+                       ss);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
@@ -67,6 +94,7 @@ hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, c
 // windows: row m is slot m & 31 of stream m >> 5, cached at that stream's
 // own position in its own cache; padding rows get a zero q and no cache write.
 // grid (M, H + 2 * Hkv), block hd / 2
+template <int SMAX>
 __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,
                           int H, int Hkv, int hd, const float2* rope, KvPlanes o, int cap, Streams sm) {
   const int m = blockIdx.x, hh = blockIdx.y, i = threadIdx.x;
@@ -91,11 +119,21 @@ __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* w
   }
   const int ld = (H + 2 * Hkv) * hd;
   const float* src = qkv + (size_t)m * ld + (size_t)hh * hd;
-  float a = 0.0f, b = 0.0f;
-  for (int s = 0; s < S; ++s) {
-    a += src[(size_t)s * plane + i];
-    b += src[(size_t)s * plane + i + half];
+  // all plane loads in flight at once (see k_resid_norm)
+  float pa[SMAX], pb[SMAX];
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) {
+    const size_t so = (size_t)(s < S ? s : S - 1) * plane;
+    pa[s] = src[so + i];
+    pb[s] = src[so + i + half];
   }
+  float a = 0.0f, b = 0.0f;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < S) {
+      a += pa[s];
+      b += pb[s];
+    }
   if (hh < H + Hkv) {
     const float2 cs = rope[(size_t)win->pos[m] * half + i];
     const float o0 = a * cs.x - b * cs.y;
@@ -121,27 +159,47 @@ __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* w
 hipError_t launch_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,
                           int M, int H, int Hkv, int hd, const float2* rope, const KvPlanes& o, int cap,
                           const Streams& sm, hipStream_t s) {
-  hipLaunchKernelGGL(k_rope_kv, dim3(M, H + 2 * Hkv), dim3(hd / 2), 0, s, qkv, S, plane, win, n_dev, n_host, H, Hkv,
-                     hd, rope, o, cap, sm);
+  const dim3 grid(M, H + 2 * Hkv), block(hd / 2);
+  if (S < 1) return hipErrorInvalidValue;
+  if (S <= 4)
+    hipLaunchKernelGGL(k_rope_kv<4>, grid, block, 0, s, qkv, S, plane, win, n_dev, n_host, H, Hkv, hd, rope, o, cap, sm);
+  else if (S <= 8)
+    hipLaunchKernelGGL(k_rope_kv<8>, grid, block, 0, s, qkv, S, plane, win, n_dev, n_host, H, Hkv, hd, rope, o, cap, sm);
+  else if (S <= 16)
+    hipLaunchKernelGGL(k_rope_kv<16>, grid, block, 0, s, qkv, S, plane, win, n_dev, n_host, H, Hkv, hd, rope, o, cap,
+                       sm);
+  else if (S <= kGemmMaxSplits)
+    hipLaunchKernelGGL(k_rope_kv<kGemmMaxSplits>, grid, block, 0, s, qkv, S, plane, win, n_dev, n_host, H, Hkv, hd,
+                       rope, o, cap, sm);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
 // h[m][n] = silu(g) * u with g, u the plane sums of columns n and F + n.
 // grid (chunks of 256 columns, M), one wave, 4 columns per lane.
+// (all plane loads in flight at once, see k_resid_norm)
+template <int SMAX>
 __global__ __launch_bounds__(64) void k_swiglu(const float* P, int S, size_t plane, int F, uint16_t* h,
                                                uint16_t* h_lo, int ldh) {
   const int m = blockIdx.y;
   const int n0 = blockIdx.x * 256 + threadIdx.x * 4;
   if (n0 >= F) return;  // F is a multiple of 64: a lane's 4 columns are all in range
   const float* pg = P + (size_t)m * 2 * F + n0;
-  float4 gs = make_float4(0.f, 0.f, 0.f, 0.f), us = gs;
-#pragma unroll 4
-  for (int s = 0; s < S; ++s) {
-    const float4 a = *(const float4*)(pg + (size_t)s * plane);
-    const float4 b = *(const float4*)(pg + (size_t)s * plane + F);
-    gs.x += a.x; gs.y += a.y; gs.z += a.z; gs.w += a.w;
-    us.x += b.x; us.y += b.y; us.z += b.z; us.w += b.w;
+  float4 pa[SMAX], pb[SMAX];
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) {
+    const size_t so = (size_t)(s < S ? s : S - 1) * plane;
+    pa[s] = *(const float4*)(pg + so);
+    pb[s] = *(const float4*)(pg + so + F);
   }
+  float4 gs = make_float4(0.f, 0.f, 0.f, 0.f), us = gs;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < S) {
+      gs.x += pa[s].x; gs.y += pa[s].y; gs.z += pa[s].z; gs.w += pa[s].w;
+      us.x += pb[s].x; us.y += pb[s].y; us.z += pb[s].z; us.w += pb[s].w;
+    }
   ushort4 hi, lo;
   split_bf16(gs.x / (1.0f + expf(-gs.x)) * us.x, hi.x, lo.x);
   split_bf16(gs.y / (1.0f + expf(-gs.y)) * us.y, hi.y, lo.y);
@@ -153,7 +211,18 @@ __global__ __launch_bounds__(64) void k_swiglu(const float* P, int S, size_t pla
 
 hipError_t launch_swiglu(const float* P, int S, size_t plane, int M, int F, uint16_t* h, uint16_t* h_lo, int ldh,
                          hipStream_t s) {
-  hipLaunchKernelGGL(k_swiglu, dim3((F + 255) / 256, M), dim3(64), 0, s, P, S, plane, F, h, h_lo, ldh);
+  const dim3 grid((F + 255) / 256, M);
+  if (S < 1) return hipErrorInvalidValue;
+  if (S <= 4)
+    hipLaunchKernelGGL(k_swiglu<4>, grid, dim3(64), 0, s, P, S, plane, F, h, h_lo, ldh);
+  else if (S <= 8)
+    hipLaunchKernelGGL(k_swiglu<8>, grid, dim3(64), 0, s, P, S, plane, F, h, h_lo, ldh);
+  else if (S <= 16)
+    hipLaunchKernelGGL(k_swiglu<16>, grid, dim3(64), 0, s, P, S, plane, F, h, h_lo, ldh);
+  else if (S <= kGemmMaxSplits)
+    hipLaunchKernelGGL(k_swiglu<kGemmMaxSplits>, grid, dim3(64), 0, s, P, S, plane, F, h, h_lo, ldh);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
