@@ -62,9 +62,11 @@ typedef enum {
 /* flags */
 #define SJD_AC 1u /* adaptive continuation: no break after the first rejection (Sec. 4.2) */
 #define SJD_PD 2u /* proactive drafting after a rejection (Sec. 4.1)                      */
-/* decoder contexts only: enqueue every kernel of a step directly instead of
- * replaying the step's window forward from a captured HIP graph (the
- * results are identical; for debugging and profiling) */
+/* decoder contexts only, the reference mode: enqueue every kernel of a step
+ * directly instead of replaying the step's window forward from a captured
+ * HIP graph, and compute every draft row's distribution instead of reusing
+ * the statistics the previous step computed for that row (the results are
+ * bitwise identical; for debugging and profiling) */
 #define SJD_EAGER 4u
 
 /* Returns a static string naming a status code. */

@@ -53,6 +53,9 @@ struct Ctx {
   int delta = 0;
   float2* rope = nullptr;
   float* logits[2] = {nullptr, nullptr};
+  // target-row statistics of the step that wrote logits[i] ([B][L]); the
+  // next step's draft rows reuse them instead of selecting again
+  sjd::RowStatsCache* stats[2] = {nullptr, nullptr};
   float* attn_o = nullptr;
   float* attn_ml = nullptr;
   int nsplit_max = 0;
@@ -325,6 +328,7 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       (rc = dalloc(x, &x.rope, (size_t)x.cap_pad * (hd / 2))) ||
       (rc = dalloc(x, &x.logits[0], (size_t)logit_rows(x) * c.V)) ||
       (rc = dalloc(x, &x.logits[1], (size_t)logit_rows(x) * c.V)) ||
+      (rc = dalloc(x, &x.stats[0], (size_t)x.B * c.L)) || (rc = dalloc(x, &x.stats[1], (size_t)x.B * c.L)) ||
       (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * 64 * hd)) ||
       (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 128)) || (rc = dalloc(x, &x.st, x.B)) ||
       (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)x.B * c.L * sjd::kRecInts)))
@@ -351,8 +355,10 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     return fail(rc);
   // zero the caches (rows past the fill are read, masked, by the attention
   // tiles) and the activation pad rows
+  bool ok0 = true;
+  for (auto* st : x.stats) ok0 = ok0 && hipMemsetAsync(st, 0, sizeof(sjd::RowStatsCache) * x.B * c.L, s) == hipSuccess;
   void* zero[] = {x.kc, x.kc_lo, x.vt, x.vt_lo};
-  bool ok = hipMemsetAsync(x.st, 0, sizeof(sjd::DevState) * x.B, s) == hipSuccess;
+  bool ok = ok0 && hipMemsetAsync(x.st, 0, sizeof(sjd::DevState) * x.B, s) == hipSuccess;
   for (void* p : zero) ok = ok && hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess;
   void* zero2[] = {x.xn, x.xn_lo};
   for (void* p : zero2) ok = ok && hipMemsetAsync(p, 0, xnsz * 2, s) == hipSuccess;
@@ -523,6 +529,11 @@ extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t s
   a.cur = cur; a.cur_bstride = lstride; a.draft = prev; a.draft_bstride = lstride;
   a.q_off = &x.st->q_off; a.draft_tok = x.st->spine; a.sib = x.st->sib; a.in_meta = &x.st->D_in;
   a.state_stride = sstate; a.rec = x.rec;
+  if (x.use_graph) {  // (SJD_EAGER, the reference mode, recomputes every draft distribution)
+    a.stats_out = x.stats[x.steps & 1];
+    a.stats_in = x.stats[(x.steps + 1) & 1];
+    a.stats_tag = (uint32_t)(x.steps + 2);  // zeroed entries (tag 0) never match
+  }
   sjd::FinalizeOut o{};
   o.out_meta = x.st->meta; o.meta_stride = sstate; o.out_tok = x.st->tok; o.tok_stride = sstate;
   o.out_next = x.st->spine; o.next_stride = sstate; o.out_sib = x.st->sib; o.sib_stride = sstate;

@@ -11,6 +11,17 @@ constexpr int kRecInts = 16;  // per-row record: tok, stage, 7 drafting candidat
 constexpr int kVerifyMaxV = 65536;  // logits per row held on chip
 constexpr int kVerifyMaxK = 2048;   // kept (top-k) tokens per row when V > kVerifyMaxK
 
+// Target-distribution statistics of one logits row (top-k / temperature
+// softmax): its largest logit, the kept-set threshold (value, index), and
+// the normaliser, tagged with the step that computed them.
+struct RowStatsCache {
+  float m, T, tau_v;
+  int32_t tau_x, all, top_k;
+  uint32_t tag;
+  int32_t pad;
+  double invZ;
+};
+
 struct VerifyArgs {
   int B, L, V, K, D, top_k;
   float T;
@@ -31,6 +42,14 @@ struct VerifyArgs {
   const int32_t* in_meta;    // [B][4]
   int state_stride;
   int32_t* rec;              // [B][L][kRecInts] scratch
+  // A draft row is the previous step's target row of the same logits, so
+  // its distribution was computed there: stats_out[b][j] receives every
+  // target row's statistics tagged stats_tag, and a draft row (b, q_off + j)
+  // whose stats_in entry carries stats_tag - 1 with the same temperature and
+  // top_k skips its own selection (both NULL: always computed)
+  RowStatsCache* stats_out;  // [B][L] or NULL
+  const RowStatsCache* stats_in;
+  uint32_t stats_tag;
   int32_t* out_rows;         // [B][L][2] or NULL
   float* dbg_p;              // [B][L][V] or NULL
 };

@@ -569,6 +569,7 @@ struct RowLoad {
   bool need_q;  // its draft row is read (a spine row with a valid draft token)
   const float* cur;
   const float* draft;
+  const RowStatsCache* q_cached;  // the draft row's statistics from the previous step, or NULL
 };
 
 SJD_DEV bool forced_pos(const VerifyArgs& a, long g) {
@@ -588,6 +589,7 @@ SJD_DEV RowLoad plan_load(const VerifyArgs& a, int row) {
   r.need_q = false;
   r.cur = a.cur + (size_t)b * (a.cur_bstride ? (size_t)a.cur_bstride : (size_t)a.L * a.V) + (size_t)j * a.V;
   r.draft = nullptr;
+  r.q_cached = nullptr;
   if (!r.valid) return r;
   if (j < n_s) {
     const bool is_forced = forced_pos(a, g0 + j);
@@ -596,7 +598,12 @@ SJD_DEV RowLoad plan_load(const VerifyArgs& a, int row) {
       const int x0 = a.draft_tok[(size_t)b * trial_stride(a, a.L) + j] - a.vis_lo;
       if (x0 >= 0 && x0 < a.V) {
         r.need_q = true;
-        r.draft = a.draft + (size_t)b * a.draft_bstride + (size_t)((a.q_off ? a.q_off[(size_t)b * trial_stride(a, 1)] : 0) + j) * a.V;
+        const int qrow = (a.q_off ? a.q_off[(size_t)b * trial_stride(a, 1)] : 0) + j;
+        r.draft = a.draft + (size_t)b * a.draft_bstride + (size_t)qrow * a.V;
+        if (a.stats_in) {
+          const RowStatsCache* c = a.stats_in + (size_t)b * a.L + qrow;
+          if (c->tag == a.stats_tag - 1u && c->T == a.T && c->top_k == a.top_k) r.q_cached = c;
+        }
       }
     }
   } else {
@@ -642,6 +649,12 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
     __syncthreads();
     ps.invZ = softmax_weights<BLOCK, NC>(sh.sp_p, nk, ps.m, a.T, sh);
     for (int i = tid; i < nk; i += BLOCK) sh.sp_p[i] = (float)((double)sh.sp_p[i] * ps.invZ);
+    if (a.stats_out && tid == 0) {
+      RowStatsCache c;
+      c.m = ps.m; c.T = ps.T; c.tau_v = ps.tau_v; c.tau_x = ps.tau_x; c.all = ps.all ? 1 : 0;
+      c.top_k = a.top_k; c.tag = a.stats_tag; c.pad = 0; c.invZ = ps.invZ;
+      a.stats_out[(size_t)b * L + j] = c;
+    }
     if (a.dbg_p) {
       float4* dst = (float4*)(a.dbg_p + ((size_t)b * L + j) * V);
 #pragma unroll
@@ -743,10 +756,22 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
 
   int out_tok = -1, out_stage = 0;
   if (ncand > 0) {
-    // draft row: selection, then its logits at the kept entries
     const float* draft_row = ld.draft;
-    if (!PF) load_row<BLOCK, NC>(vq, draft_row, V);
     RowStats qs{};
+    if (ld.q_cached) {
+      // the previous step computed this row's distribution: its statistics,
+      // and the draft logits at the target's kept entries (gathered)
+      const RowStatsCache c = *ld.q_cached;
+      qs.m = c.m; qs.T = c.T; qs.tau_v = c.tau_v; qs.tau_x = c.tau_x; qs.all = c.all != 0; qs.invZ = c.invZ;
+      for (int i = tid; i < nk; i += BLOCK) {
+        const int x = (int)sh.sp_x[i];
+        const float l = draft_row[x];
+        sh.sp_q[i] = qs.in_set(l, x) ? (float)((double)expf((l - qs.m) / a.T) * qs.invZ) : 0.0f;
+      }
+      __syncthreads();
+    } else {
+    // draft row: selection, then its logits at the kept entries
+    if (!PF) load_row<BLOCK, NC>(vq, draft_row, V);
     float qmx, qmn;
     row_maxmin<BLOCK, NC>(vq, sh, qmx, qmn);
     qs.m = qmx;
@@ -781,6 +806,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       sh.sp_q[i] = in_q ? (float)((double)expf((sh.sp_q[i] - qs.m) / a.T) * qs.invZ) : 0.0f;
     }
     __syncthreads();
+    }
     auto qrow_c = [&](int ent) -> float { return sh.sp_q[ent]; };
 
     float Qsum = 0.0f;
@@ -914,7 +940,7 @@ __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
   float4 v[NC];
   if constexpr (PF) {
     float4 vq[NC];
-    if (ld.need_q) load_row<BLOCK, NC>(vq, ld.draft, a.V);
+    if (ld.need_q && !ld.q_cached) load_row<BLOCK, NC>(vq, ld.draft, a.V);
     if (ld.need_p) load_row<BLOCK, NC>(v, ld.cur, a.V);
     verify_row<BLOCK, NC, true>(a, sh, row, ld, v, vq);
   } else {

@@ -115,12 +115,15 @@ def test_acceptance_statistics_match_oracle(orc, mode, flags, K, D, L):
     assert abs(a.mean() - b.mean()) < 4 * se + 0.02
 
 
-@pytest.mark.parametrize("kind", ["single", "guided", "batch"])
-def test_graph_replay_equals_eager(kind):
-    """The step's window forward is replayed from a captured HIP graph; with
-    SJD_EAGER every kernel is enqueued directly. Sampled generations (same
-    seeds) must agree bit for bit: tokens, committed counts and cache rows,
-    over many replays of both captured graphs with eager work in between."""
+@pytest.mark.parametrize("kind,top_k", [("single", 0), ("single", 37), ("guided", 0), ("batch", 37)])
+def test_graph_replay_equals_eager(kind, top_k):
+    """By default the step's window forward is replayed from a captured HIP
+    graph and each draft row reuses the target-row statistics the previous
+    step computed for it; SJD_EAGER (the reference mode) enqueues every
+    kernel directly and recomputes every draft distribution. Sampled
+    generations (same seeds) must agree bit for bit: tokens, committed counts
+    and cache rows, over many replays of both captured graphs with eager work
+    in between."""
     from paper_2603_18599_amd.sjd import SJD_EAGER
     from synth_inputs import prompt_tokens
     over = {"guided": {"cfg_w": 3.0}, "batch": {"batch": 2}}.get(kind, {})
@@ -142,7 +145,7 @@ def test_graph_replay_equals_eager(kind):
             eng.prefill(prompt.cuda(), 5)
         rec = []
         for t in range(24):
-            eng.step(1.0, 0, 9, t, out_meta=meta, out_tok=tok)
+            eng.step(1.0, top_k, 9, t, out_meta=meta, out_tok=tok)
             rec.append((meta.cpu().numpy().copy(), tok.cpu().numpy().copy()))
         eng.close()
         runs.append(rec)
