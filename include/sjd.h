@@ -68,6 +68,10 @@ typedef enum {
  * the statistics the previous step computed for that row (the results are
  * bitwise identical; for debugging and profiling) */
 #define SJD_EAGER 4u
+/* decoder contexts only: use the closed-form split-K plan instead of the
+ * process-wide plan timed by the first context that meets each projection
+ * shape (sjd_init then times a few GEMM + consumer pairs on layer 0) */
+#define SJD_NO_TUNE 8u
 
 /* Returns a static string naming a status code. */
 SJD_API const char* sjd_status_str(int status);
@@ -161,7 +165,7 @@ typedef struct {
   int32_t max_seq;       /* KV capacity in tokens (prompt + generated + L)             */
   int32_t L, K, D;       /* window slots (1..64), candidates per depth (1..8), depth   */
   uint32_t flags;        /* SJD_AC | SJD_PD (0 = vanilla SJD; Sec. 5.3's ablation),
-                            optionally | SJD_EAGER                                       */
+                            optionally | SJD_EAGER | SJD_NO_TUNE                         */
   float rms_eps, rope_theta;
   int32_t eol_id, row_len;
   int32_t weights_f32;   /* 1: weights are fp32, 0: bf16                                */

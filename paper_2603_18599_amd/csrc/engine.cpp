@@ -7,7 +7,12 @@
 
 #include <array>
 #include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <map>
+#include <mutex>
+#include <tuple>
 #include <utility>
 #include <vector>
 
@@ -111,7 +116,7 @@ int check_config(const sjd_config* c) {
   if (c->L < 1 || c->L > 64 || c->K < 1 || c->K > 8 || c->D < 0 || (long)c->K * c->D > c->L) return SJD_EINVAL;
   if (c->V > 65536) return SJD_ENOTSUP;
   if (c->max_seq < c->L + 2) return SJD_EINVAL;
-  if (c->flags & ~(SJD_AC | SJD_PD | SJD_EAGER)) return SJD_EINVAL;
+  if (c->flags & ~(SJD_AC | SJD_PD | SJD_EAGER | SJD_NO_TUNE)) return SJD_EINVAL;
   if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
   if (!std::isfinite(c->cfg_w)) return SJD_EINVAL;
   if (c->batch < 0) return SJD_EINVAL;
@@ -194,6 +199,114 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
     HIPTRY(sjd::launch_gemm(g, s));
   }
   return SJD_OK;
+}
+
+// ---- split-K plan
+// How many workgroups share a projection's K range decides both the GEMM's
+// time and how many partial planes its consumer (RoPE, residual + RMSNorm,
+// SwiGLU) sums; the interaction is not smooth (measured on the 7B shape, the
+// step is 3% faster with 5 / 8 / 4 / 16 splits than with the closed-form
+// plan). So the first context of a process that meets a projection shape
+// times every candidate pair (GEMM + consumer) on its own weights at 32
+// rows and keeps the fastest for the process: every context of the process
+// uses the same plan, so their arithmetic agrees.
+enum { kProjQkv = 0, kProjO = 1, kProjGu = 2, kProjDown = 3 };
+std::mutex g_plan_mu;
+std::map<std::tuple<int, int, int>, int> g_plan;  // (projection, N, K) -> splits
+
+// candidate split counts: one to three workgroups per compute unit, at
+// least two k-steps per workgroup, plus the closed-form choice
+std::vector<int> split_candidates(int N, int K, int ncu, int fallback) {
+  const int groups = (N / 32 + 3) / 4, T = K / 64;
+  std::vector<int> out;
+  for (int S = 1; S <= sjd::kGemmMaxSplits; ++S) {
+    if (S > 1 && T / S < 2) break;
+    const long wg = (long)groups * S;
+    if (wg >= ncu && wg <= 3L * ncu) out.push_back(S);
+  }
+  bool has = false;
+  for (int S : out) has |= S == fallback;
+  if (!has) out.push_back(fallback);
+  return out;
+}
+
+// Times GEMM + consumer per candidate (layer 0's weights, 32 rows, current
+// buffer contents) and returns the fastest; within 1% the smaller split wins.
+int tune_projection(Ctx& x, int proj, const std::vector<int>& cand, hipStream_t s) {
+  const sjd_config& c = x.c;
+  const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
+  const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv, M = 32;
+  const auto& w = x.lw[0];
+  const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d, guplane = (size_t)x.Mpad * 2 * F;
+  const sjd::Streams one{sjd::kStreamsOne, 0, 0, nullptr};
+  auto pair = [&](int S) -> hipError_t {
+    sjd::GemmArgs g{};
+    g.M = M; g.S = S;
+    if (proj == kProjQkv || proj == kProjGu) {
+      g.ss = x.ss; g.ss_n = sjd::norm_chunks(d); g.inv_d = 1.0f / (float)d; g.eps = c.rms_eps;
+      g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.K = d;
+    }
+    hipError_t e;
+    switch (proj) {
+      case kProjQkv: {
+        g.W = w[1]; g.N = Nqkv; g.out = x.qkv; g.plane = qplane; g.ldo = Nqkv;
+        if ((e = sjd::launch_gemm(g, s)) != hipSuccess) return e;
+        const sjd::KvPlanes kv{x.q, x.q_lo, x.kc, x.kc_lo, x.vt, x.vt_lo, x.kv_elems};
+        return sjd::launch_rope_kv(x.qkv, S, qplane, x.win, nullptr, 0, M, H, Hkv, hd, x.rope, kv, x.cap_pad, one, s);
+      }
+      case kProjO:
+        g.A = x.att; g.A_lo = x.att_lo; g.lda = x.ld_q; g.W = w[4]; g.N = d; g.K = Nq;
+        g.out = x.rpart; g.plane = rplane; g.ldo = d;
+        if ((e = sjd::launch_gemm(g, s)) != hipSuccess) return e;
+        return sjd::launch_resid_norm(x.x, x.rpart, S, rplane, w[5], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s);
+      case kProjGu:
+        g.W = w[6]; g.N = 2 * F; g.out = x.gup; g.plane = guplane; g.ldo = 2 * F;
+        if ((e = sjd::launch_gemm(g, s)) != hipSuccess) return e;
+        return sjd::launch_swiglu(x.gup, S, guplane, M, F, x.hbuf, x.hbuf_lo, x.ld_f, s);
+      default:
+        g.A = x.hbuf; g.A_lo = x.hbuf_lo; g.lda = x.ld_f; g.W = w[8]; g.N = d; g.K = F;
+        g.out = x.rpart; g.plane = rplane; g.ldo = d;
+        if ((e = sjd::launch_gemm(g, s)) != hipSuccess) return e;
+        return sjd::launch_resid_norm(x.x, x.rpart, S, rplane, w[0], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s);
+    }
+  };
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    if (e0) (void)hipEventDestroy(e0);
+    return -1;
+  }
+  // two interleaved rounds over the candidates; each keeps its faster round
+  constexpr int kReps = 10, kRounds = 2;
+  std::vector<float> t(cand.size(), 0.0f);
+  bool ok = true;
+  for (int round = 0; round < kRounds && ok; ++round)
+    for (size_t i = 0; i < cand.size() && ok; ++i) {
+      const int S = cand[i];
+      for (int r = 0; r < 2 && ok; ++r) ok = pair(S) == hipSuccess;
+      ok = ok && hipEventRecord(e0, s) == hipSuccess;
+      for (int r = 0; r < kReps && ok; ++r) ok = pair(S) == hipSuccess;
+      ok = ok && hipEventRecord(e1, s) == hipSuccess && hipEventSynchronize(e1) == hipSuccess;
+      float ms = 0.0f;
+      ok = ok && hipEventElapsedTime(&ms, e0, e1) == hipSuccess;
+      const float us = ms * 1e3f / kReps;
+      if (round == 0 || us < t[i]) t[i] = us;
+    }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (!ok) return -1;
+  // fastest; within 1% of it, the candidate with more workgroups (more
+  // parallelism to absorb what the neighbouring kernels leave behind)
+  size_t fast = 0;
+  for (size_t i = 1; i < t.size(); ++i)
+    if (t[i] < t[fast]) fast = i;
+  int best = cand[fast];
+  for (size_t i = 0; i < t.size(); ++i)
+    if (t[i] <= t[fast] * 1.01f && cand[i] > best) best = cand[i];
+  if (std::getenv("SJD_LOG_PLAN"))
+    for (size_t i = 0; i < t.size(); ++i)
+      std::fprintf(stderr, "[sjd] plan: projection %d splits %d: %.2f us%s\n", proj, cand[i], t[i],
+                   cand[i] == best ? " <- chosen" : "");
+  return best;
 }
 
 // Refreshes the cache-fill bound of every image from completed steps;
@@ -333,7 +446,9 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 128)) || (rc = dalloc(x, &x.st, x.B)) ||
       (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)x.B * c.L * sjd::kRecInts)))
     return fail(rc);
-  // split-K plan: aim for two to three workgroups per compute unit
+  // split-K plan: the closed form aims for two to three workgroups per
+  // compute unit; unless SJD_NO_TUNE, the process-wide tuned plan replaces it
+  // (tuned below, by the first context that meets a shape)
   int ncu = 256;
   {
     int dev = 0;
@@ -342,23 +457,47 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       ncu = prop.multiProcessorCount;
   }
   const int target = 5 * ncu / 2;
-  x.S_qkv = sjd::gemm_splits(Nq + 2 * Nkv, d, target);
-  x.S_o = sjd::gemm_splits(d, Nq, target);
-  x.S_gu = sjd::gemm_splits(2 * F, d, target);
-  x.S_dn = sjd::gemm_splits(d, F, target);
+  const int Nqkv = Nq + 2 * Nkv;
+  struct Proj { int kind, N, K; int* S; int closed; std::vector<int> cand; bool tune; };
+  Proj projs[4] = {{kProjQkv, Nqkv, d, &x.S_qkv, sjd::gemm_splits(Nqkv, d, target), {}, false},
+                   {kProjO, d, Nq, &x.S_o, sjd::gemm_splits(d, Nq, target), {}, false},
+                   {kProjGu, 2 * F, d, &x.S_gu, sjd::gemm_splits(2 * F, d, target), {}, false},
+                   {kProjDown, d, F, &x.S_dn, sjd::gemm_splits(d, F, target), {}, false}};
+  const bool tune = !(c.flags & SJD_NO_TUNE);
+  int smax[4];
+  {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    for (int i = 0; i < 4; ++i) {
+      Proj& p = projs[i];
+      *p.S = p.closed;
+      if (tune) {
+        auto it = g_plan.find(std::make_tuple(p.kind, p.N, p.K));
+        if (it != g_plan.end()) {
+          *p.S = it->second;
+        } else {
+          p.cand = split_candidates(p.N, p.K, ncu, p.closed);
+          p.tune = true;
+        }
+      }
+      smax[i] = *p.S;
+      for (int S : p.cand) smax[i] = S > smax[i] ? S : smax[i];
+    }
+  }
   x.S_head = 1;
-  const int sr = x.S_o > x.S_dn ? x.S_o : x.S_dn;
-  if ((rc = dalloc(x, &x.qkv, (size_t)x.S_qkv * Mp * (Nq + 2 * Nkv))) ||
+  const int sr = smax[1] > smax[3] ? smax[1] : smax[3];
+  if ((rc = dalloc(x, &x.qkv, (size_t)smax[0] * Mp * Nqkv)) ||
       (rc = dalloc(x, &x.rpart, (size_t)sr * Mp * d)) ||
-      (rc = dalloc(x, &x.gup, (size_t)x.S_gu * Mp * 2 * F)) ||
+      (rc = dalloc(x, &x.gup, (size_t)smax[2] * Mp * 2 * F)) ||
       (rc = dalloc(x, &x.ss, (size_t)Mp * sjd::norm_chunks(d))))
     return fail(rc);
   // zero the caches (rows past the fill are read, masked, by the attention
-  // tiles) and the activation pad rows
+  // tiles), the window and the activation planes (pad rows stay finite)
   bool ok0 = true;
   for (auto* st : x.stats) ok0 = ok0 && hipMemsetAsync(st, 0, sizeof(sjd::RowStatsCache) * x.B * c.L, s) == hipSuccess;
   void* zero[] = {x.kc, x.kc_lo, x.vt, x.vt_lo};
   bool ok = ok0 && hipMemsetAsync(x.st, 0, sizeof(sjd::DevState) * x.B, s) == hipSuccess;
+  ok = ok && hipMemsetAsync(x.win, 0, sizeof(sjd::Window), s) == hipSuccess;
+  ok = ok && hipMemsetAsync(x.x, 0, (size_t)Mp * d * sizeof(float), s) == hipSuccess;
   for (void* p : zero) ok = ok && hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess;
   void* zero2[] = {x.xn, x.xn_lo};
   for (void* p : zero2) ok = ok && hipMemsetAsync(p, 0, xnsz * 2, s) == hipSuccess;
@@ -381,10 +520,33 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
         hipStreamSynchronize(s) != hipSuccess)
       return fail(SJD_EHIP);
   }
-  // pinned, device-visible: the step's last kernel writes the cached-row
-  // counts into it directly
+  // tune the projections this process has not met yet (their consumers
+  // write layer 0's cache rows 0..31 and the work planes: cleared after)
+  bool tuned = false;
+  for (Proj& p : projs) {
+    if (!p.tune) continue;
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    auto it = g_plan.find(std::make_tuple(p.kind, p.N, p.K));
+    if (it == g_plan.end()) {
+      const int S = p.cand.size() > 1 ? tune_projection(x, p.kind, p.cand, s) : p.cand[0];
+      if (S < 1) return fail(SJD_EHIP);
+      it = g_plan.emplace(std::make_tuple(p.kind, p.N, p.K), S).first;
+      tuned = true;
+    }
+    *p.S = it->second;
+  }
+  if (tuned) {
+    bool okz = hipMemsetAsync(x.x, 0, (size_t)Mp * d * sizeof(float), s) == hipSuccess;
+    for (void* p : zero) okz = okz && hipMemsetAsync(p, 0, kv * 2, s) == hipSuccess;
+    for (void* p : zero2) okz = okz && hipMemsetAsync(p, 0, xnsz * 2, s) == hipSuccess;
+    for (void* p : zero5) okz = okz && hipMemsetAsync(p, 0, (size_t)Mp * Nq * 2, s) == hipSuccess;
+    for (void* p : zero4) okz = okz && hipMemsetAsync(p, 0, (size_t)Mp * x.ld_f * 2, s) == hipSuccess;
+    if (!okz || hipStreamSynchronize(s) != hipSuccess) return fail(SJD_EHIP);
+  }
   if (x.use_graph && hipStreamCreateWithFlags(&x.cap_stream, hipStreamNonBlocking) != hipSuccess)
     return fail(SJD_EHIP);
+  // pinned, device-visible: the step's last kernel writes the cached-row
+  // counts into it directly
   if (hipHostMalloc((void**)&x.h_n, sizeof(int32_t) * kRing * x.B, hipHostMallocDefault) != hipSuccess)
     return fail(SJD_ENOMEM);
   for (int i = 0; i < kRing * x.B; ++i) x.h_n[i] = 0;

@@ -14,6 +14,7 @@ _LIB_NAME = "libsjd.so"
 SJD_AC = 1
 SJD_PD = 2
 SJD_EAGER = 4
+SJD_NO_TUNE = 8
 
 _STATUS = {0: "SJD_OK", -1: "SJD_EINVAL", -2: "SJD_ENOMEM", -3: "SJD_EHIP", -4: "SJD_ESTATE", -5: "SJD_ENOTSUP"}
 
@@ -59,7 +60,9 @@ _lib = None
 
 
 def lib_path():
-    return os.path.join(HERE, _LIB_NAME)
+    """The in-tree library, or the one SJD_LIBRARY names (another build of
+    the same sources, e.g. to compare two builds in one process tree)."""
+    return os.environ.get("SJD_LIBRARY") or os.path.join(HERE, _LIB_NAME)
 
 
 def load_library():
