@@ -249,7 +249,9 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
 // bytes as its own keys' full rows, still contiguous 1 KB loads). This
 // replaces a 64 KB fp32 output exchange and its reduction with a 16 KB
 // probability exchange; the partial then leaves in four independent 4 KB
-// slices.
+// slices. A workgroup serves every query head of its key / value head
+// (grouped-query attention) from the same registers: the tiles are read
+// once per group instead of once per query head.
 struct AttnPxSmem {
   uint4 q[2][8][kWave];     // Q^T operand (hi, lo), 128 dims
   uint4 p[4][2][2][kWave];  // [key block][16-key half][hi / lo][lane]: P^T operand
@@ -261,7 +263,8 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
   constexpr int HD = 128, NQ = HD / 16;
   static_assert(kAttnChunk == 4 * 32, "one 32-key block per wave");
   __shared__ AttnPxSmem sm;
-  const int h = blockIdx.x, sp = blockIdx.y;
+  const int kvh = blockIdx.x, sp = blockIdx.y;
+  const int G = a.H / a.Hkv;  // query heads sharing this key/value head
   const bool two = a.st.mode != kStreamsOne;
   const bool second = two && blockIdx.z == 1;
   const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, second);
@@ -269,7 +272,6 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
   const int kbeg = sp * kAttnChunk;
   if (kbeg >= nk) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5;
-  const int kvh = h / (a.H / a.Hkv);
   const int zs = blockIdx.z * 32;
   const int slot = lane & 31;
   const int gslot = zs + slot;
@@ -278,19 +280,23 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
   const int kb = kbeg + wave * 32;  // this wave's key block
   const bool has = kb < nk;
 
-  uint4 qs[2][2];
-  {
+  // the first query head's q chunks go first (small, cache-resident; vector
+  // loads return in order, so a q load issued after the tiles would wait for
+  // all of them), then the key / value tiles, which stay in registers for
+  // every query head of the group
+  auto load_q = [&](int h, uint4 (&qr)[2][2]) {
     const size_t qo = (size_t)(slot_ok ? gslot : 0) * a.H * HD + (size_t)h * HD + half * (HD / 2);
     const uint4* qp = (const uint4*)(a.q + qo);
     const uint4* qpl = (const uint4*)(a.q_lo + qo);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int t = wave + 4 * i;
-      qs[0][i] = slot_ok ? qp[t] : make_uint4(0, 0, 0, 0);
-      qs[1][i] = slot_ok ? qpl[t] : make_uint4(0, 0, 0, 0);
+      qr[0][i] = slot_ok ? qp[t] : make_uint4(0, 0, 0, 0);
+      qr[1][i] = slot_ok ? qpl[t] : make_uint4(0, 0, 0, 0);
     }
-  }
-  // own keys (all dims), then this wave's 32 value dims of all four key blocks
+  };
+  uint4 qs[2][2];
+  load_q(kvh * G, qs);
   uint4 kh[NQ], kl[NQ], vh[4][2], vl[4][2];
   if (has) {
     const uint4* kp = (const uint4*)(a.kc + hbase + (size_t)kb * HD + (size_t)lane * 8);
@@ -312,121 +318,128 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
       vl[w][jj] = kbw < nk ? vpl[(wave * 2 + jj) * 64] : make_uint4(0, 0, 0, 0);
     }
   }
+  // mask of this wave's keys for this lane's slot (the same for every head)
+  uint32_t vis = 0;
+  if (has && slot_ok) {
+    const uint64_t anc = kb + 32 <= n ? 0ull : a.win->anc[gslot];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    sm.q[0][wave + 4 * i][lane] = qs[0][i];
-    sm.q[1][wave + 4 * i][lane] = qs[1][i];
+    for (int r = 0; r < 16; ++r) {
+      const int key = kb + 16 * (r >> 3) + 8 * half + (r & 7);
+      bool v = key < nk;
+      if (v && key >= n) v = (anc >> (key - n)) & 1ull;
+      vis |= (v ? 1u : 0u) << r;
+    }
   }
-  __syncthreads();
 
-  float m_w = -INFINITY, l_w = 0.0f;
-  uint4 pb[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)}, pbl[2] = {pb[0], pb[1]};
-  if (has) {
-    f32x16 s;
+  for (int g = 0; g < G; ++g) {
+    const int h = kvh * G + g;
+    if (g > 0) load_q(h, qs);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s[r] = 0.0f;
-#pragma unroll
-    for (int t = 0; t < NQ; ++t) {
-      const bf16x8 khb = to_bf16x8(kh[t]), klb = to_bf16x8(kl[t]);
-      const bf16x8 qh = to_bf16x8(sm.q[0][t][lane]), ql = to_bf16x8(sm.q[1][t][lane]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, qh, s, 0, 0, 0);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, ql, s, 0, 0, 0);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(klb, qh, s, 0, 0, 0);
+    for (int i = 0; i < 2; ++i) {
+      sm.q[0][wave + 4 * i][lane] = qs[0][i];
+      sm.q[1][wave + 4 * i][lane] = qs[1][i];
     }
-    // mask (register r = 8jj + e holds key kb + 16jj + 8half + e)
-    if (kb + 32 <= n) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = slot_ok ? s[r] * a.scale : -INFINITY;
-    } else {
-      const uint64_t anc = slot_ok ? a.win->anc[gslot] : 0ull;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb + 16 * (r >> 3) + 8 * half + (r & 7);
-        bool vis = slot_ok && key < nk;
-        if (vis && key >= n) vis = (anc >> (key - n)) & 1ull;
-        s[r] = vis ? s[r] * a.scale : -INFINITY;
-      }
-    }
-    float mloc = s[0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[r]);
-    m_w = fmaxf(mloc, __shfl_xor(mloc, 32, kWave));
-    float lsum = 0.0f;
-    if (m_w != -INFINITY) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = exp2f(s[r] - m_w);
-        lsum += s[r];
-      }
-    } else {
+    __syncthreads();  // (also: every wave is done with the previous head's P)
+
+    float m_w = -INFINITY, l_w = 0.0f;
+    uint4 pb[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)}, pbl[2] = {pb[0], pb[1]};
+    if (has) {
+      f32x16 s;
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = 0.0f;
-    }
-    l_w = lsum + __shfl_xor(lsum, 32, kWave);
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      uint32_t w[4], wl[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        uint16_t h0, l0, h1, l1;
-        split_bf16_finite(s[8 * jj + 2 * e], h0, l0);
-        split_bf16_finite(s[8 * jj + 2 * e + 1], h1, l1);
-        w[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        wl[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+      for (int t = 0; t < NQ; ++t) {
+        const bf16x8 khb = to_bf16x8(kh[t]), klb = to_bf16x8(kl[t]);
+        const bf16x8 qh = to_bf16x8(sm.q[0][t][lane]), ql = to_bf16x8(sm.q[1][t][lane]);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, qh, s, 0, 0, 0);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(khb, ql, s, 0, 0, 0);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(klb, qh, s, 0, 0, 0);
       }
-      pb[jj] = make_uint4(w[0], w[1], w[2], w[3]);
-      pbl[jj] = make_uint4(wl[0], wl[1], wl[2], wl[3]);
+      // mask (register r = 8jj + e holds key kb + 16jj + 8half + e)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = (vis >> r) & 1u ? s[r] * a.scale : -INFINITY;
+      float mloc = s[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[r]);
+      m_w = fmaxf(mloc, __shfl_xor(mloc, 32, kWave));
+      float lsum = 0.0f;
+      if (m_w != -INFINITY) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[r] = exp2f(s[r] - m_w);
+          lsum += s[r];
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+      }
+      l_w = lsum + __shfl_xor(lsum, 32, kWave);
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        uint32_t w[4], wl[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint16_t h0, l0, h1, l1;
+          split_bf16_finite(s[8 * jj + 2 * e], h0, l0);
+          split_bf16_finite(s[8 * jj + 2 * e + 1], h1, l1);
+          w[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+          wl[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        }
+        pb[jj] = make_uint4(w[0], w[1], w[2], w[3]);
+        pbl[jj] = make_uint4(wl[0], wl[1], wl[2], wl[3]);
+      }
     }
-  }
-#pragma unroll
-  for (int jj = 0; jj < 2; ++jj) {
-    sm.p[wave][jj][0][lane] = pb[jj];
-    sm.p[wave][jj][1][lane] = pbl[jj];
-  }
-  if (half == 0) {
-    sm.m[wave][slot] = m_w;
-    sm.l[wave][slot] = l_w;
-  }
-  __syncthreads();
-
-  // O^T (this wave's 32 dims x 32 slots) = sum over key blocks w of
-  // 2^(m_w - m) V_w^T . P_w^T
-  float mw[4], mx = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    mw[w] = sm.m[w][slot];
-    mx = fmaxf(mx, mw[w]);
-  }
-  f32x16 o;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) o[r] = 0.0f;
-  float ls = 0.0f;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const float f = mx == -INFINITY ? 0.0f : exp2f(mw[w] - mx);
-    ls += sm.l[w][slot] * f;
-    f32x16 t;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) t[r] = 0.0f;
 #pragma unroll
     for (int jj = 0; jj < 2; ++jj) {
-      const bf16x8 vhb = to_bf16x8(vh[w][jj]), vlb = to_bf16x8(vl[w][jj]);
-      const bf16x8 ph = to_bf16x8(sm.p[w][jj][0][lane]), pl = to_bf16x8(sm.p[w][jj][1][lane]);
-      t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vhb, ph, t, 0, 0, 0);
-      t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vhb, pl, t, 0, 0, 0);
-      t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vlb, ph, t, 0, 0, 0);
+      sm.p[wave][jj][0][lane] = pb[jj];
+      sm.p[wave][jj][1][lane] = pbl[jj];
     }
+    if (half == 0) {
+      sm.m[wave][slot] = m_w;
+      sm.l[wave][slot] = l_w;
+    }
+    __syncthreads();
+
+    // O^T (this wave's 32 dims x 32 slots) = sum over key blocks w of
+    // 2^(m_w - m) V_w^T . P_w^T
+    float mw[4], mx = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) o[r] += f * t[r];
-  }
-  // register r of lane (slot, half): dim 32 wave + 8(r/4) + 4 half + r%4
-  float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * 64 + zs + slot) * HD + wave * 32 + 4 * half;
+    for (int w = 0; w < 4; ++w) {
+      mw[w] = sm.m[w][slot];
+      mx = fmaxf(mx, mw[w]);
+    }
+    f32x16 o;
 #pragma unroll
-  for (int g = 0; g < 4; ++g) *(float4*)(wo + 8 * g) = make_float4(o[4 * g], o[4 * g + 1], o[4 * g + 2], o[4 * g + 3]);
-  if (wave == 0 && half == 0) {
-    float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 64 * 2 + (size_t)(zs + slot) * 2;
-    wml[0] = mx;
-    wml[1] = ls;
+    for (int r = 0; r < 16; ++r) o[r] = 0.0f;
+    float ls = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = mx == -INFINITY ? 0.0f : exp2f(mw[w] - mx);
+      ls += sm.l[w][slot] * f;
+      f32x16 t;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) t[r] = 0.0f;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const bf16x8 vhb = to_bf16x8(vh[w][jj]), vlb = to_bf16x8(vl[w][jj]);
+        const bf16x8 ph = to_bf16x8(sm.p[w][jj][0][lane]), pl = to_bf16x8(sm.p[w][jj][1][lane]);
+        t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vhb, ph, t, 0, 0, 0);
+        t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vhb, pl, t, 0, 0, 0);
+        t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vlb, ph, t, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[r] += f * t[r];
+    }
+    // register r of lane (slot, half): dim 32 wave + 8(r/4) + 4 half + r%4
+    float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * 64 + zs + slot) * HD + wave * 32 + 4 * half;
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4)
+      *(float4*)(wo + 8 * q4) = make_float4(o[4 * q4], o[4 * q4 + 1], o[4 * q4 + 2], o[4 * q4 + 3]);
+    if (wave == 0 && half == 0) {
+      float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 64 * 2 + (size_t)(zs + slot) * 2;
+      wml[0] = mx;
+      wml[1] = ls;
+    }
   }
 }
 
@@ -502,7 +515,9 @@ hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s) {
   const unsigned zh = (unsigned)(a.M + 31) / 32;  // 32-slot halves
   const dim3 g1(a.H, a.nsplit_max, zh), g2(a.H, hd / 32, zh);
   if (hd == 128) {
-    hipLaunchKernelGGL(k_attn_partial_px, g1, dim3(256), 0, s, a);
+    // one workgroup per key / value head: its tiles are read once for the
+    // whole group of query heads that share them
+    hipLaunchKernelGGL(k_attn_partial_px, dim3(a.Hkv, a.nsplit_max, zh), dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_attn_combine<128>, g2, dim3(256), 0, s, a);
   } else if (hd == 64) {
     hipLaunchKernelGGL(k_attn_partial<64>, g1, dim3(256), 0, s, a);
