@@ -136,6 +136,7 @@ def read_counter(dirname, counter):
     files = glob.glob(os.path.join(dirname, "**", "*counter_collection.csv"), recursive=True)
     if not files:
         raise SystemExit(f"no counter_collection.csv under {dirname}")
+    files = [max(files, key=os.path.getmtime)]  # the newest run only (dispatch ids restart per run)
     out = {}
     for f in files:
         with open(f) as fh:
@@ -420,7 +421,7 @@ def bench_step(args):
                step_latency_p50_ms=float(np.percentile(step_ms, 50)),
                step_latency_p99_ms=float(np.percentile(step_ms, 99)),
                prefill_ms=prefill_ms, kv_rows_mean=n_mean, image_restarts=restarts,
-               host_enqueue_ms_per_step=host_s * 1e3 / K,
+               host_enqueue_ms_per_step=host_s * 1e3 / K, split_plan=eng.plan(),
                roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic(args.workload),
                          "kernel": "sjd_step (window forward + verification + KV commit)",

@@ -239,6 +239,14 @@ SJD_API int sjd_step(sjd_ctx* ctx, float temperature, int32_t top_k, uint64_t se
  * d_logits[32 + L][V], image b's rows from row 32 b). For parity tests. */
 SJD_API int sjd_forward_window(sjd_ctx* ctx, float* d_logits, void* stream);
 
+/* The context's split-K plan: how many workgroups share the K range of the
+ * QKV, O, gate|up, down and LM-head projections (splits[0..min(n,5))).
+ * Chosen at sjd_init: the closed form, the process-wide timed plan (the
+ * first context of a process that meets a projection shape times
+ * GEMM + consumer pairs; SJD_NO_TUNE skips this), or the environment
+ * variable SJD_SPLITS="qkv,o,gu,down" when set. */
+SJD_API int sjd_get_plan(const sjd_ctx* ctx, int32_t* splits, int32_t n);
+
 SJD_API void sjd_destroy(sjd_ctx* ctx);
 
 #ifdef __cplusplus

@@ -231,8 +231,8 @@ std::vector<int> split_candidates(int N, int K, int ncu, int fallback) {
 }
 
 // Times GEMM + consumer per candidate (layer 0's weights, 32 rows, current
-// buffer contents) and returns the fastest; within 1% the smaller split wins.
-int tune_projection(Ctx& x, int proj, const std::vector<int>& cand, hipStream_t s) {
+// buffer contents) and returns the chosen split (see below).
+int tune_projection(Ctx& x, int proj, const std::vector<int>& cand, int closed, hipStream_t s) {
   const sjd_config& c = x.c;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv, M = 32;
@@ -294,14 +294,16 @@ int tune_projection(Ctx& x, int proj, const std::vector<int>& cand, hipStream_t 
   (void)hipEventDestroy(e0);
   (void)hipEventDestroy(e1);
   if (!ok) return -1;
-  // fastest; within 1% of it, the candidate with more workgroups (more
-  // parallelism to absorb what the neighbouring kernels leave behind)
-  size_t fast = 0;
-  for (size_t i = 1; i < t.size(); ++i)
-    if (t[i] < t[fast]) fast = i;
-  int best = cand[fast];
+  // the closed-form choice unless a candidate beats it by more than 3%
+  // (then the fastest): near-ties keep the same plan however noisy the
+  // timing (another process, a profiler attached)
+  size_t ref = 0;
   for (size_t i = 0; i < t.size(); ++i)
-    if (t[i] <= t[fast] * 1.01f && cand[i] > best) best = cand[i];
+    if (cand[i] == closed) ref = i;
+  size_t pick = ref;
+  for (size_t i = 0; i < t.size(); ++i)
+    if (t[i] < t[ref] * 0.97f && t[i] < t[pick]) pick = i;
+  const int best = cand[pick];
   if (std::getenv("SJD_LOG_PLAN"))
     for (size_t i = 0; i < t.size(); ++i)
       std::fprintf(stderr, "[sjd] plan: projection %d splits %d: %.2f us%s\n", proj, cand[i], t[i],
@@ -463,13 +465,21 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
                    {kProjO, d, Nq, &x.S_o, sjd::gemm_splits(d, Nq, target), {}, false},
                    {kProjGu, 2 * F, d, &x.S_gu, sjd::gemm_splits(2 * F, d, target), {}, false},
                    {kProjDown, d, F, &x.S_dn, sjd::gemm_splits(d, F, target), {}, false}};
-  const bool tune = !(c.flags & SJD_NO_TUNE);
+  // SJD_SPLITS="qkv,o,gu,down" pins the plan (e.g. to profile the plan a
+  // run without the profiler chose)
+  int pinned[4] = {0, 0, 0, 0};
+  if (const char* env = std::getenv("SJD_SPLITS")) {
+    if (std::sscanf(env, "%d,%d,%d,%d", &pinned[0], &pinned[1], &pinned[2], &pinned[3]) != 4) return fail(SJD_EINVAL);
+    for (int v : pinned)
+      if (v < 1 || v > sjd::kGemmMaxSplits) return fail(SJD_EINVAL);
+  }
+  const bool tune = !(c.flags & SJD_NO_TUNE) && pinned[0] == 0;
   int smax[4];
   {
     std::lock_guard<std::mutex> lk(g_plan_mu);
     for (int i = 0; i < 4; ++i) {
       Proj& p = projs[i];
-      *p.S = p.closed;
+      *p.S = pinned[0] ? pinned[i] : p.closed;
       if (tune) {
         auto it = g_plan.find(std::make_tuple(p.kind, p.N, p.K));
         if (it != g_plan.end()) {
@@ -528,7 +538,7 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     std::lock_guard<std::mutex> lk(g_plan_mu);
     auto it = g_plan.find(std::make_tuple(p.kind, p.N, p.K));
     if (it == g_plan.end()) {
-      const int S = p.cand.size() > 1 ? tune_projection(x, p.kind, p.cand, s) : p.cand[0];
+      const int S = p.cand.size() > 1 ? tune_projection(x, p.kind, p.cand, p.closed, s) : p.cand[0];
       if (S < 1) return fail(SJD_EHIP);
       it = g_plan.emplace(std::make_tuple(p.kind, p.N, p.K), S).first;
       tuned = true;
@@ -720,6 +730,14 @@ extern "C" int sjd_forward_window(sjd_ctx* h, float* d_logits, void* stream) {
   const sjd::Streams sm = window_streams(x);
   HIPTRY(sjd::launch_build_window(x.st, x.win, x.c.L, x.c.K, x.c.vis_lo, sm, s));
   return forward(x, window_rows(x), &x.st->n, 0, d_logits, sm, 0, s);
+}
+
+extern "C" int sjd_get_plan(const sjd_ctx* h, int32_t* splits, int32_t n) {
+  if (!h || !splits || n < 1) return SJD_EINVAL;
+  const Ctx& x = h->x;
+  const int32_t v[5] = {x.S_qkv, x.S_o, x.S_gu, x.S_dn, x.S_head};
+  for (int i = 0; i < n && i < 5; ++i) splits[i] = v[i];
+  return SJD_OK;
 }
 
 extern "C" void sjd_destroy(sjd_ctx* h) {

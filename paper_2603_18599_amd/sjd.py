@@ -54,7 +54,7 @@ class Weights(C.Structure):
 
 
 EXPORTS = ["sjd_status_str", "sjd_verify", "sjd_init", "sjd_prefill", "sjd_prefill_image", "sjd_prefill_cfg",
-           "sjd_step", "sjd_forward_window", "sjd_destroy"]
+           "sjd_step", "sjd_forward_window", "sjd_get_plan", "sjd_destroy"]
 
 _lib = None
 
@@ -84,6 +84,8 @@ def load_library():
     lib.sjd_init.argtypes = [C.POINTER(Config), C.POINTER(Weights), C.c_void_p, C.POINTER(C.c_void_p)]
     lib.sjd_prefill.restype = C.c_int
     lib.sjd_prefill.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_uint64, C.c_void_p]
+    lib.sjd_get_plan.restype = C.c_int
+    lib.sjd_get_plan.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.c_int32]
     lib.sjd_prefill_image.restype = C.c_int
     lib.sjd_prefill_image.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_uint64, C.c_void_p]
     lib.sjd_prefill_cfg.restype = C.c_int
@@ -169,6 +171,12 @@ class Engine:
     def prefill(self, prompt, seed, stream=None):
         _check("sjd_prefill", load_library().sjd_prefill(self.h, _ptr(prompt), prompt.numel(), seed,
                                                           _stream(stream)))
+
+    def plan(self):
+        """Split-K plan [qkv, o, gate|up, down, head] chosen at init."""
+        out = (C.c_int32 * 5)()
+        _check("sjd_get_plan", load_library().sjd_get_plan(self.h, out, 5))
+        return list(out)
 
     def prefill_image(self, image, prompt, seed, stream=None):
         """Batched contexts: (re)starts image `image` with `prompt`."""
