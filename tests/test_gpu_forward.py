@@ -48,3 +48,26 @@ def test_window_forward_matches_oracle(orc, name, over):
     print(f"{name} {over}: max |logit error| = {err:.3e}, logit std = {ref.std():.3f}", flush=True)
     assert np.isfinite(got).all()
     assert err <= TOL, err
+
+
+@pytest.mark.parametrize("plan", ["1,1,1,1", "7,3,5,11", "32,32,2,32"])
+def test_window_forward_under_pinned_split_plans(orc, monkeypatch, plan):
+    """The split-K plan is chosen at init (timed, or pinned by SJD_SPLITS);
+    the forward must match the oracle under any plan, including uneven
+    splits of the K range and the extremes (no split, 32 partial planes)."""
+    cfg = model_config("mid", n_layers=2)
+    w, prompt = setup(cfg, wseed=13, pseed=14, device="cuda")
+    monkeypatch.setenv("SJD_SPLITS", plan)
+    eng = make_engine(cfg, weights_device(w))
+    assert eng.plan()[:4] == [int(v) for v in plan.split(",")]
+    eng.prefill(prompt.cuda(), 5)
+    logits = torch.empty(cfg["L"], cfg["V"], dtype=torch.float32, device="cuda")
+    eng.forward_window(logits)
+    torch.cuda.synchronize()
+    got = logits.cpu().numpy()
+    eng.close()
+    ref = oracle_first_window(orc, cfg, weights_numpy(w), prompt.numpy().astype(np.int32), 5)
+    err = np.abs(got - ref).max()
+    print(f"plan {plan}: max |logit error| = {err:.3e}", flush=True)
+    assert np.isfinite(got).all()
+    assert err <= TOL, err
