@@ -122,4 +122,79 @@ SJD_DEV int wave_incl_scan(int v) {
   return v;
 }
 
+
+// --------------------------------------------- DPP reductions (all lanes on)
+// Cross-lane steps through DPP instead of the LDS permute network: within
+// each 16-lane row by quad permutations and mirrors, across the four rows by
+// reading lanes 0, 16, 32 and 48 (the results are wave-uniform). Every lane
+// of the wave must be active: a lane outside the exec mask would feed stale
+// data into its neighbours.
+namespace dpp {
+enum : int { kXor1 = 0xB1, kXor2 = 0x4E, kHalfMirror = 0x141, kMirror = 0x140, kShr1 = 0x111, kShr2 = 0x112,
+             kShr4 = 0x114, kShr8 = 0x118, kBcast15 = 0x142, kBcast31 = 0x143 };
+template <int CTRL, int ROWS = 0xF>
+SJD_DEV uint32_t mov(uint32_t v) { return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xF, false); }
+SJD_DEV uint32_t lane(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
+}  // namespace dpp
+
+// op over each 16-lane row, the result in every lane of the row
+template <class T, class Op>
+SJD_DEV T row_reduce32(T v, Op op) {
+  static_assert(sizeof(T) == 4, "32-bit payload");
+  auto step = [&](uint32_t u) { return __builtin_bit_cast(T, u); };
+  v = op(v, step(dpp::mov<dpp::kXor1>(__builtin_bit_cast(uint32_t, v))));
+  v = op(v, step(dpp::mov<dpp::kXor2>(__builtin_bit_cast(uint32_t, v))));
+  v = op(v, step(dpp::mov<dpp::kHalfMirror>(__builtin_bit_cast(uint32_t, v))));
+  v = op(v, step(dpp::mov<dpp::kMirror>(__builtin_bit_cast(uint32_t, v))));
+  return v;
+}
+template <class T, class Op>
+SJD_DEV T wave_reduce32(T v, Op op) {
+  v = row_reduce32(v, op);
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const T a = __builtin_bit_cast(T, dpp::lane(u, 0)), b = __builtin_bit_cast(T, dpp::lane(u, 16));
+  const T c = __builtin_bit_cast(T, dpp::lane(u, 32)), d = __builtin_bit_cast(T, dpp::lane(u, 48));
+  return op(op(a, b), op(c, d));
+}
+// 64-bit payloads move as two 32-bit halves
+template <int CTRL>
+SJD_DEV uint64_t mov64(uint64_t v) {
+  return ((uint64_t)dpp::mov<CTRL>((uint32_t)(v >> 32)) << 32) | dpp::mov<CTRL>((uint32_t)v);
+}
+template <class T, class Op>
+SJD_DEV T wave_reduce64(T v, Op op) {
+  static_assert(sizeof(T) == 8, "64-bit payload");
+  auto as = [](uint64_t u) { return __builtin_bit_cast(T, u); };
+  auto bits = [](T x) { return __builtin_bit_cast(uint64_t, x); };
+  v = op(v, as(mov64<dpp::kXor1>(bits(v))));
+  v = op(v, as(mov64<dpp::kXor2>(bits(v))));
+  v = op(v, as(mov64<dpp::kHalfMirror>(bits(v))));
+  v = op(v, as(mov64<dpp::kMirror>(bits(v))));
+  const uint64_t u = bits(v);
+  auto at = [&](int l) { return as(((uint64_t)dpp::lane((uint32_t)(u >> 32), l) << 32) | dpp::lane((uint32_t)u, l)); };
+  return op(op(at(0), at(16)), op(at(32), at(48)));
+}
+SJD_DEV float wave_max_dpp(float v) { return wave_reduce32(v, [](float a, float b) { return fmaxf(a, b); }); }
+SJD_DEV double wave_sum_d_dpp(double v) { return wave_reduce64(v, [](double a, double b) { return a + b; }); }
+SJD_DEV uint64_t wave_min_u64_dpp(uint64_t v) {
+  return wave_reduce64(v, [](uint64_t a, uint64_t b) { return a < b ? a : b; });
+}
+// inclusive prefix sum over the wave (lane order)
+SJD_DEV int wave_incl_scan_dpp(int v) {
+  v += (int)dpp::mov<dpp::kShr1>((uint32_t)v);
+  v += (int)dpp::mov<dpp::kShr2>((uint32_t)v);
+  v += (int)dpp::mov<dpp::kShr4>((uint32_t)v);
+  v += (int)dpp::mov<dpp::kShr8>((uint32_t)v);
+  v += (int)dpp::mov<dpp::kBcast15, 0xA>((uint32_t)v);
+  v += (int)dpp::mov<dpp::kBcast31, 0xC>((uint32_t)v);
+  return v;
+}
+// OR over each aligned group of 8 lanes, the result in every lane of the group
+SJD_DEV uint32_t or8_dpp(uint32_t v) {
+  v |= dpp::mov<dpp::kXor1>(v);
+  v |= dpp::mov<dpp::kXor2>(v);
+  v |= dpp::mov<dpp::kHalfMirror>(v);
+  return v;
+}
+
 }  // namespace sjd

@@ -48,6 +48,7 @@ template <int BLOCK, int NC>
 struct VSh {
   static constexpr int W = BLOCK / kWave;
   static constexpr int NW = BLOCK * NC / 8;  // bitmap words (32 entries each)
+  static_assert(W <= 16, "the drafting merge holds 8 keys of each wave in two registers per lane");
   uint32_t bm[NW];    // kept set of the target row
   int32_t pre[NW];    // its per-word prefix popcounts
   uint32_t bmq[NW];   // kept set of the draft row
@@ -59,8 +60,10 @@ struct VSh {
     uint32_t hist[kBins];
     float qc[kKcap];  // draft row's kept weights (its normaliser)
   };
-  float cand_v[kCandCap];
-  int cand_x[kCandCap];
+  float cand_v[kCandCap + 8];  // threshold-bin entries, then sentinels that
+  int cand_x[kCandCap + 8];    // outrank nothing (-inf, INT_MAX)
+  uint64_t pd_w[W * 8];  // per-wave drafting keys
+  int pd_o[8];            // the drafting draws
   double red_d[W];
   uint64_t red_u[W];
   float red_f[2 * W];
@@ -73,10 +76,8 @@ static_assert(kBins == kKcap, "the draft weights reuse the histogram");
 // ------------------------------------------------------------ block helpers
 template <int W>
 SJD_DEV void block_maxmin(float& mx, float& mn, float* red) {
-  mx = wave_max(mx);
-  float t = -mn;
-  t = wave_max(t);
-  mn = -t;
+  mx = wave_max_dpp(mx);
+  mn = -wave_max_dpp(-mn);
   const int w = threadIdx.x / kWave;
   __syncthreads();
   if ((threadIdx.x & (kWave - 1)) == 0) {
@@ -95,7 +96,7 @@ SJD_DEV void block_maxmin(float& mx, float& mn, float* red) {
 }
 template <int W>
 SJD_DEV double block_sum_d(double v, double* red) {
-  v = wave_sum_d(v);
+  v = wave_sum_d_dpp(v);
   const int w = threadIdx.x / kWave;
   if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
   __syncthreads();
@@ -107,7 +108,7 @@ SJD_DEV double block_sum_d(double v, double* red) {
 }
 template <int W>
 SJD_DEV uint64_t block_min_u64(uint64_t v, uint64_t* red) {
-  v = wave_min_u64(v);
+  v = wave_min_u64_dpp(v);
   const int w = threadIdx.x / kWave;
   if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
   __syncthreads();
@@ -120,7 +121,7 @@ SJD_DEV uint64_t block_min_u64(uint64_t v, uint64_t* red) {
 // exclusive prefix sum over the block (thread order)
 template <int W>
 SJD_DEV int block_excl_scan(int v, int* red) {
-  const int incl = wave_incl_scan(v);
+  const int incl = wave_incl_scan_dpp(v);
   const int w = threadIdx.x / kWave;
   if ((threadIdx.x & (kWave - 1)) == kWave - 1) red[w] = incl;
   __syncthreads();
@@ -129,6 +130,10 @@ SJD_DEV int block_excl_scan(int v, int* red) {
   __syncthreads();
   return base + incl - v;
 }
+
+// d / T with the division skipped at T = 1, where IEEE division returns d
+// exactly
+SJD_DEV float over_T(float d, float T) { return T == 1.0f ? d : d / T; }
 
 SJD_DEV float comp(const float4& v, int e) { return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w; }
 SJD_DEV uint32_t compu(const uint4& v, int e) { return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w; }
@@ -147,7 +152,7 @@ struct RowStats {
   SJD_DEV bool in_set(float l, int x) const { return all || l > tau_v || (l == tau_v && x <= tau_x); }
   SJD_DEV float prob(float l, int x) const {
     if (!in_set(l, x)) return 0.0f;
-    const float w = expf((l - m) / T);
+    const float w = expf(over_T(l - m, T));
     return (float)((double)w * invZ);
   }
 };
@@ -316,9 +321,7 @@ SJD_DEV void bitmap_from_tau(const float4 (&v)[NC], int V, const RowStats& st, u
       for (int e = 0; e < 4; ++e) bits |= (st.in_set(comp(v[i], e), 4 * c + e) ? 1u : 0u) << e;
     }
     bits <<= 4 * (tid & 7);
-    bits |= __shfl_xor(bits, 1, kWave);
-    bits |= __shfl_xor(bits, 2, kWave);
-    bits |= __shfl_xor(bits, 4, kWave);
+    bits = or8_dpp(bits);
     if ((tid & 7) == 0) bm[(tid >> 3) + i * (BLOCK / 8)] = bits;
   }
 }
@@ -345,6 +348,10 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
     fast = fast && (scale < INFINITY) && (scale > 0.0f);
     if (fast) {
       for (int b = tid; b < kBins; b += BLOCK) sh.hist[b] = 0;
+      for (int b = tid; b < kCandCap + 8; b += BLOCK) {
+        sh.cand_v[b] = -INFINITY;
+        sh.cand_x[b] = 0x7FFFFFFF;
+      }
       if (tid == 0) sh.ncand = 0;
       __syncthreads();
       // bin of a value: (l - mn) * scale rounded once (fma), truncated,
@@ -404,20 +411,24 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
             }
           }
           bits <<= 4 * (tid & 7);
-          bits |= __shfl_xor(bits, 1, kWave);
-          bits |= __shfl_xor(bits, 2, kWave);
-          bits |= __shfl_xor(bits, 4, kWave);
+          bits = or8_dpp(bits);
           if ((tid & 7) == 0) bm[(tid >> 3) + i * (BLOCK / 8)] = bits;
         }
         __syncthreads();
         // exact rank inside the threshold bin; the first rem join the set
+        // (entries past c are sentinels, so the inner loop runs in blocks
+        // of eight whose loads issue together)
+        const int cpad = (c + 7) & ~7;
         for (int i = tid; i < c; i += BLOCK) {
           const float vi = sh.cand_v[i];
           const int xi = sh.cand_x[i];
           int r = 0;
-          for (int j = 0; j < c; ++j) {
-            const float vj = sh.cand_v[j];
-            r += (vj > vi) || (vj == vi && sh.cand_x[j] < xi);
+          for (int j0 = 0; j0 < cpad; j0 += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const float vj = sh.cand_v[j0 + u];
+              r += (vj > vi) || (vj == vi && sh.cand_x[j0 + u] < xi);
+            }
           }
           if (r < rem) atomicOr(&bm[xi >> 5], 1u << (xi & 31));
           if (r == rem - 1) {
@@ -498,7 +509,7 @@ SJD_DEV double softmax_weights(float* w, int n, float m, float T, VSh<BLOCK, NC>
   constexpr int W = BLOCK / kWave;
   double z = 0.0;
   for (int i = threadIdx.x; i < n; i += BLOCK) {
-    const float e = expf((w[i] - m) / T);
+    const float e = expf(over_T(w[i] - m, T));
     w[i] = e;
     z += (double)e;
   }
@@ -572,6 +583,12 @@ struct RowLoad {
   const RowStatsCache* q_cached;  // the draft row's statistics from the previous step, or NULL
 };
 
+// the logits row of (trial, window row)
+SJD_DEV const float* row_logits(const VerifyArgs& a, int row) {
+  const int b = row / a.L, j = row % a.L;
+  return a.cur + (size_t)b * (a.cur_bstride ? (size_t)a.cur_bstride : (size_t)a.L * a.V) + (size_t)j * a.V;
+}
+
 SJD_DEV bool forced_pos(const VerifyArgs& a, long g) {
   return a.row_len > 0 && g >= 0 && (g % (a.row_len + 1)) == a.row_len;
 }
@@ -580,14 +597,18 @@ SJD_DEV RowLoad plan_load(const VerifyArgs& a, int row) {
   RowLoad r;
   const int b = row / a.L, j = row % a.L;
   const int Km1 = a.K - 1;
+  // every word the plan may need that lies in bounds whatever the window
+  // says, loaded before any of them is used
   const int32_t* meta = a.in_meta + (size_t)b * trial_stride(a, 4);
   const int D_in = meta[0], n_q = meta[1];
   const long g0 = meta[2];
+  const int dtok = a.draft_tok[(size_t)b * trial_stride(a, a.L) + j];
+  const int qoff = a.q_off ? a.q_off[(size_t)b * trial_stride(a, 1)] : 0;
   const int n_s = a.L - Km1 * D_in;
   r.valid = !(D_in < 0 || D_in > a.D || a.K * D_in > a.L || n_q < 0 || n_q > n_s);
   r.need_p = false;
   r.need_q = false;
-  r.cur = a.cur + (size_t)b * (a.cur_bstride ? (size_t)a.cur_bstride : (size_t)a.L * a.V) + (size_t)j * a.V;
+  r.cur = row_logits(a, row);
   r.draft = nullptr;
   r.q_cached = nullptr;
   if (!r.valid) return r;
@@ -595,10 +616,10 @@ SJD_DEV RowLoad plan_load(const VerifyArgs& a, int row) {
     const bool is_forced = forced_pos(a, g0 + j);
     r.need_p = !is_forced;
     if (!is_forced && j < n_q) {
-      const int x0 = a.draft_tok[(size_t)b * trial_stride(a, a.L) + j] - a.vis_lo;
+      const int x0 = dtok - a.vis_lo;
       if (x0 >= 0 && x0 < a.V) {
         r.need_q = true;
-        const int qrow = (a.q_off ? a.q_off[(size_t)b * trial_stride(a, 1)] : 0) + j;
+        const int qrow = qoff + j;
         r.draft = a.draft + (size_t)b * a.draft_bstride + (size_t)qrow * a.V;
         if (a.stats_in) {
           const RowStatsCache* c = a.stats_in + (size_t)b * a.L + qrow;
@@ -635,6 +656,40 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   const bool ac = (a.flags & kFlagAC) != 0;
   const bool pd = (a.flags & kFlagPD) != 0 && Km1 > 0;
   const bool spine = j < n_s;
+
+  // candidates: the spine draft, then (tree rows) its siblings; an
+  // out-of-range or repeated candidate ends the list
+  Stages stg;
+  stg.n = 0;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) { stg.cand[t] = -1; stg.Nf[t] = 1.0f; stg.den[t] = 1.0f; }
+  int ncand = 0;
+  if (spine && ld.need_q) {
+    stg.cand[0] = a.draft_tok[(size_t)b * trial_stride(a, L) + j] - a.vis_lo;
+    ncand = 1;
+    if (j < D_in && a.sib) {
+      bool open = true;
+#pragma unroll
+      for (int k = 0; k < 7; ++k) {
+        if (open && k < Km1) {
+          int y = a.sib[(size_t)b * trial_stride(a, (size_t)a.D * Km1) + (size_t)j * Km1 + k];
+          bool stop = y < 0;
+          y -= a.vis_lo;
+          stop |= (y < 0 || y >= V);
+#pragma unroll
+          for (int t = 0; t < 8; ++t) stop |= (t <= k) && (stg.cand[t] == y);
+          if (stop) open = false;
+          else { stg.cand[k + 1] = y; ncand = k + 2; }
+        }
+      }
+    }
+  }
+
+  // draft logits at the candidates, loaded now so that the accept loop
+  // does not wait for them
+  float qcl[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) qcl[t] = t < ncand ? ld.draft[stg.cand[t]] : 0.0f;
 
   RowStats ps{};
   int nk = 0;
@@ -726,34 +781,6 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
     return;
   }
 
-  // candidates: the spine draft, then (tree rows) its siblings; an
-  // out-of-range or repeated candidate ends the list
-  Stages stg;
-  stg.n = 0;
-#pragma unroll
-  for (int t = 0; t < 8; ++t) { stg.cand[t] = -1; stg.Nf[t] = 1.0f; stg.den[t] = 1.0f; }
-  int ncand = 0;
-  if (ld.need_q) {
-    stg.cand[0] = a.draft_tok[(size_t)b * trial_stride(a, L) + j] - a.vis_lo;
-    ncand = 1;
-    if (j < D_in && a.sib) {
-      bool open = true;
-#pragma unroll
-      for (int k = 0; k < 7; ++k) {
-        if (open && k < Km1) {
-          int y = a.sib[(size_t)b * trial_stride(a, (size_t)a.D * Km1) + (size_t)j * Km1 + k];
-          bool stop = y < 0;
-          y -= a.vis_lo;
-          stop |= (y < 0 || y >= V);
-#pragma unroll
-          for (int t = 0; t < 8; ++t) stop |= (t <= k) && (stg.cand[t] == y);
-          if (stop) open = false;
-          else { stg.cand[k + 1] = y; ncand = k + 2; }
-        }
-      }
-    }
-  }
-
   int out_tok = -1, out_stage = 0;
   if (ncand > 0) {
     const float* draft_row = ld.draft;
@@ -766,7 +793,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       for (int i = tid; i < nk; i += BLOCK) {
         const int x = (int)sh.sp_x[i];
         const float l = draft_row[x];
-        sh.sp_q[i] = qs.in_set(l, x) ? (float)((double)expf((l - qs.m) / a.T) * qs.invZ) : 0.0f;
+        sh.sp_q[i] = qs.in_set(l, x) ? (float)((double)expf(over_T(l - qs.m, a.T)) * qs.invZ) : 0.0f;
       }
       __syncthreads();
     } else {
@@ -803,7 +830,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
     for (int i = tid; i < nk; i += BLOCK) {
       const int x = (int)sh.sp_x[i];
       const bool in_q = (sh.bmq[x >> 5] >> (x & 31)) & 1u;
-      sh.sp_q[i] = in_q ? (float)((double)expf((sh.sp_q[i] - qs.m) / a.T) * qs.invZ) : 0.0f;
+      sh.sp_q[i] = in_q ? (float)((double)expf(over_T(sh.sp_q[i] - qs.m, a.T)) * qs.invZ) : 0.0f;
     }
     __syncthreads();
     }
@@ -813,11 +840,15 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
     float Nf = 1.0f;
     for (int k = 1; k <= ncand; ++k) {
       int x = stg.cand[0];
+      float lq = qcl[0];
 #pragma unroll
-      for (int t = 1; t < 8; ++t) x = (t == k - 1) ? stg.cand[t] : x;
+      for (int t = 1; t < 8; ++t) {
+        x = (t == k - 1) ? stg.cand[t] : x;
+        lq = (t == k - 1) ? qcl[t] : lq;
+      }
       const float den = 1.0f - Qsum;
       const float px = kept(sh, x) ? sh.sp_p[rank_of(sh, x)] : 0.0f;
-      const float qx = qs.prob(draft_row[x], x);
+      const float qx = qs.prob(lq, x);
       const float pk = stg.rho(px, qx, x) / Nf;
       const float qk = den > 0.0f ? qx / den : 0.0f;
       const Stream us(a.seed, kTagAcc, (uint32_t)(k - 1), (uint32_t)j, (uint32_t)b, a.step);
@@ -899,20 +930,44 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
         }
       }
     }
+    // each wave's Km1 smallest keys in order (keys are distinct: they carry
+    // the token), then the Km1 smallest of those W lists
+    const int lane = tid & (kWave - 1), w = tid / kWave;
+    uint64_t mine = kNoKey;
 #pragma unroll
     for (int t = 0; t < 7; ++t) {
       if (t < Km1) {
-        const uint64_t best = block_min_u64<W>(loc[0], sh.red_u);
-        if (best != kNoKey) {
-          pds[t] = (int)(uint32_t)best;
-          if (loc[0] == best) {
+        const uint64_t m = wave_min_u64_dpp(loc[0]);
+        if (m != kNoKey && loc[0] == m) {
 #pragma unroll
-            for (int u = 0; u < 6; ++u) loc[u] = loc[u + 1];
-            loc[6] = kNoKey;
+          for (int u = 0; u < 6; ++u) loc[u] = loc[u + 1];
+          loc[6] = kNoKey;
+        }
+        if (lane == t) mine = m;
+      }
+    }
+    if (lane < 8) sh.pd_w[w * 8 + lane] = mine;
+    __syncthreads();
+    if (w == 0) {
+      uint64_t c0 = kNoKey, c1 = kNoKey;
+      if (lane < W * 8) c0 = sh.pd_w[lane];
+      if (lane + kWave < W * 8) c1 = sh.pd_w[lane + kWave];
+#pragma unroll
+      for (int t = 0; t < 7; ++t) {
+        if (t < Km1) {
+          const uint64_t m = wave_min_u64_dpp(c0 < c1 ? c0 : c1);
+          if (m != kNoKey) {
+            if (c0 == m) c0 = kNoKey;
+            if (c1 == m) c1 = kNoKey;
           }
+          if (lane == 0) sh.pd_o[t] = m == kNoKey ? -1 : (int)(uint32_t)m;
         }
       }
     }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < 7; ++t)
+      if (t < Km1) pds[t] = sh.pd_o[t];
   }
 
   if (tid == 0) {
@@ -936,14 +991,18 @@ template <int BLOCK, int NC, bool PF>
 __global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
   __shared__ VSh<BLOCK, NC> sh;
   const int row = blockIdx.x;
-  const RowLoad ld = plan_load(a, row);
   float4 v[NC];
   if constexpr (PF) {
+    // the row's own logits are read before the plan is known (the row lies
+    // in the logits buffer whatever the window says; a row that turns out to
+    // be unused costs one read)
+    load_row<BLOCK, NC>(v, row_logits(a, row), a.V);
+    const RowLoad ld = plan_load(a, row);
     float4 vq[NC];
     if (ld.need_q && !ld.q_cached) load_row<BLOCK, NC>(vq, ld.draft, a.V);
-    if (ld.need_p) load_row<BLOCK, NC>(v, ld.cur, a.V);
     verify_row<BLOCK, NC, true>(a, sh, row, ld, v, vq);
   } else {
+    const RowLoad ld = plan_load(a, row);
     verify_row<BLOCK, NC, false>(a, sh, row, ld, v, v);
   }
 }
