@@ -60,16 +60,19 @@ struct VSh {
     uint32_t hist[kBins];
     float qc[kKcap];  // draft row's kept weights (its normaliser)
   };
-  float cand_v[kCandCap + 8];  // threshold-bin entries, then sentinels that
-  int cand_x[kCandCap + 8];    // outrank nothing (-inf, INT_MAX)
+  uint32_t hist_q[kBins];  // the draft row's histogram when both rows are selected together
+  // per selected row (target, draft): threshold-bin entries, then sentinels
+  // that outrank nothing (-inf, INT_MAX)
+  float cand_v[2][kCandCap + 8];
+  int cand_x[2][kCandCap + 8];
   uint64_t pd_w[W * 8];  // per-wave drafting keys
   int pd_o[8];            // the drafting draws
-  double red_d[W];
+  double red_d[2 * W];
   uint64_t red_u[W];
-  float red_f[2 * W];
-  int red_i[W];
-  float tau_v;
-  int tau_x, bin, above, ncand;
+  float red_f[4 * W];
+  int red_i[2 * W];
+  float tau_v[2];
+  int tau_x[2], bin[2], above[2], ncand[2];
 };
 static_assert(kBins == kKcap, "the draft weights reuse the histogram");
 
@@ -130,6 +133,13 @@ SJD_DEV int block_excl_scan(int v, int* red) {
   __syncthreads();
   return base + incl - v;
 }
+
+// Max / min that propagate NaN (IEEE 754-2019 maximum / minimum): one
+// v_maximum3 / v_minimum3 per pair, with no quieting copy of each operand
+// (fmaxf / fminf make one, which doubles the live registers of a pass over
+// a row held in registers). Logits are finite or -inf here.
+SJD_DEV float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+SJD_DEV float vmin(float a, float b) { return __builtin_elementwise_minimum(a, b); }
 
 // d / T with the division skipped at T = 1, where IEEE division returns d
 // exactly
@@ -209,16 +219,16 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       if (i < per && run < rem && run + cnts[i] >= rem) {
-        sh.bin = nb - 1 - (tid * per + i);
-        sh.above = run;
+        sh.bin[0] = nb - 1 - (tid * per + i);
+        sh.above[0] = run;
       }
       run += cnts[i];
     }
     __syncthreads();
-    last_bin = sh.bin;
+    last_bin = sh.bin[0];
     prefix |= (uint32_t)last_bin << shift;
     pmask |= (uint32_t)(nb - 1) << shift;
-    rem -= sh.above;
+    rem -= sh.above[0];
     __syncthreads();
   }
   const int eq = (int)sh.hist[last_bin];
@@ -262,15 +272,15 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       if (i < per && run < rem && run + cnts[i] >= rem) {
-        sh.bin = tid * per + i;
-        sh.above = run;
+        sh.bin[0] = tid * per + i;
+        sh.above[0] = run;
       }
       run += cnts[i];
     }
     __syncthreads();
-    ipre |= (uint32_t)sh.bin << shift;
+    ipre |= (uint32_t)sh.bin[0] << shift;
     imask |= 2047u << shift;
-    rem -= sh.above;
+    rem -= sh.above[0];
     __syncthreads();
   }
   tau_x = (int)ipre;
@@ -285,8 +295,8 @@ SJD_DEV void row_maxmin(const float4 (&v)[NC], VSh<BLOCK, NC>& sh, float& mx, fl
   mn = INFINITY;
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
-    mx = fmaxf(mx, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
-    mn = fminf(mn, fminf(fminf(v[i].x, v[i].y), fminf(v[i].z, v[i].w)));
+    mx = vmax(mx, vmax(vmax(v[i].x, v[i].y), vmax(v[i].z, v[i].w)));
+    mn = vmin(mn, vmin(vmin(v[i].x, v[i].y), vmin(v[i].z, v[i].w)));
   }
   block_maxmin<W>(mx, mn, sh.red_f);
   if (mn == -INFINITY) {
@@ -298,7 +308,7 @@ SJD_DEV void row_maxmin(const float4 (&v)[NC], VSh<BLOCK, NC>& sh, float& mx, fl
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float l = comp(v[i], e);
-        if (l > -INFINITY) mn = fminf(mn, l);
+        if (l > -INFINITY) mn = vmin(mn, l);
       }
     }
     block_maxmin<W>(t, mn, sh.red_f);
@@ -349,18 +359,18 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
     if (fast) {
       for (int b = tid; b < kBins; b += BLOCK) sh.hist[b] = 0;
       for (int b = tid; b < kCandCap + 8; b += BLOCK) {
-        sh.cand_v[b] = -INFINITY;
-        sh.cand_x[b] = 0x7FFFFFFF;
+        sh.cand_v[0][b] = -INFINITY;
+        sh.cand_x[0][b] = 0x7FFFFFFF;
       }
-      if (tid == 0) sh.ncand = 0;
+      if (tid == 0) sh.ncand[0] = 0;
       __syncthreads();
-      // bin of a value: (l - mn) * scale rounded once (fma), truncated,
-      // clamped; monotone in l, so every entry of a higher bin outranks
-      // every entry of a lower one (-inf converts to INT_MIN, clamped to 0)
+      // bin of a value: (l - mn) * scale rounded once (fma), clamped to
+      // [0, kBins - 1] (one med3), truncated; monotone in l, so every entry
+      // of a higher bin outranks every entry of a lower one (-inf lands in
+      // bin 0, +inf in the last)
       const float off = -mn * scale;
       auto binof = [&](float l) -> int {
-        const int b = __float2int_rz(__builtin_fmaf(l, scale, off));
-        return min(max(b, 0), kBins - 1);
+        return (int)__builtin_amdgcn_fmed3f(__builtin_fmaf(l, scale, off), 0.0f, (float)(kBins - 1));
       };
 #pragma unroll
       for (int i = 0; i < NC; ++i) {
@@ -384,29 +394,34 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
 #pragma unroll
       for (int i = 0; i < per; ++i) {
         if (run < k && run + cnts[i] >= k) {
-          sh.bin = kBins - 1 - (tid * per + i);
-          sh.above = run;
+          sh.bin[0] = kBins - 1 - (tid * per + i);
+          sh.above[0] = run;
         }
         run += cnts[i];
       }
       __syncthreads();
-      const int bstar = sh.bin, rem = k - sh.above, c = (int)sh.hist[bstar];
+      const int bstar = sh.bin[0], rem = k - sh.above[0], c = (int)sh.hist[bstar];
       if (c <= kCandCap) {
         // entries of higher bins are kept; the threshold bin's are collected
 #pragma unroll
         for (int i = 0; i < NC; ++i) {
           const int ch = tid + i * BLOCK;
-          uint32_t bits = 0;
+          uint32_t bits = 0, hit = 0;
           if (ch < nchunk) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const float l = comp(v[i], e);
-              const int b = binof(l);
+              const int b = binof(comp(v[i], e));
               bits |= (b > bstar ? 1u : 0u) << e;
-              if (b == bstar) {
-                const int p = atomicAdd(&sh.ncand, 1);
-                sh.cand_v[p] = l;
-                sh.cand_x[p] = 4 * ch + e;
+              hit |= (b == bstar ? 1u : 0u) << e;
+            }
+          }
+          if (hit) {  // rare: one branch per chunk, not per entry
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if ((hit >> e) & 1u) {
+                const int p = atomicAdd(&sh.ncand[0], 1);
+                sh.cand_v[0][p] = comp(v[i], e);
+                sh.cand_x[0][p] = 4 * ch + e;
               }
             }
           }
@@ -420,25 +435,25 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
         // of eight whose loads issue together)
         const int cpad = (c + 7) & ~7;
         for (int i = tid; i < c; i += BLOCK) {
-          const float vi = sh.cand_v[i];
-          const int xi = sh.cand_x[i];
+          const float vi = sh.cand_v[0][i];
+          const int xi = sh.cand_x[0][i];
           int r = 0;
           for (int j0 = 0; j0 < cpad; j0 += 8) {
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-              const float vj = sh.cand_v[j0 + u];
-              r += (vj > vi) || (vj == vi && sh.cand_x[j0 + u] < xi);
+              const float vj = sh.cand_v[0][j0 + u];
+              r += (vj > vi) || (vj == vi && sh.cand_x[0][j0 + u] < xi);
             }
           }
           if (r < rem) atomicOr(&bm[xi >> 5], 1u << (xi & 31));
           if (r == rem - 1) {
-            sh.tau_v = vi;
-            sh.tau_x = xi;
+            sh.tau_v[0] = vi;
+            sh.tau_x[0] = xi;
           }
         }
         __syncthreads();
-        st.tau_v = sh.tau_v;
-        st.tau_x = sh.tau_x;
+        st.tau_v = sh.tau_v[0];
+        st.tau_x = sh.tau_x[0];
         have_bitmap = true;
       } else {
         fast = false;
@@ -467,9 +482,9 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
     if (wi < NW) pre[wi] = run;
     run += cnt[i];
   }
-  if (tid == BLOCK - 1) sh.ncand = run;
+  if (tid == BLOCK - 1) sh.ncand[0] = run;
   __syncthreads();
-  const int total = sh.ncand;
+  const int total = sh.ncand[0];
   __syncthreads();
   return total;
 }
@@ -500,6 +515,302 @@ SJD_DEV void compact_row(const float4 (&v)[NC], int V, const uint32_t* bm, const
       }
     }
   }
+}
+
+// ------------------------------------------------------ two rows at once
+// A spine row whose draft distribution is not cached selects its target row
+// (registers v) and its draft row (registers u) together: the same passes
+// with one set of barriers and two independent instruction streams. The
+// kept sets, ranks, thresholds and normalisers are those the one-row
+// functions give (same per-thread orders, same reduction trees).
+
+template <int W>
+SJD_DEV void block_maxmin2(float (&mx)[2], float (&mn)[2], float* red) {
+  float a0 = wave_max_dpp(mx[0]), a1 = wave_max_dpp(mx[1]);
+  float b0 = wave_max_dpp(-mn[0]), b1 = wave_max_dpp(-mn[1]);
+  const int w = threadIdx.x / kWave;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    red[w] = a0;
+    red[W + w] = a1;
+    red[2 * W + w] = b0;
+    red[3 * W + w] = b1;
+  }
+  __syncthreads();
+  a0 = red[0];
+  a1 = red[W];
+  b0 = red[2 * W];
+  b1 = red[3 * W];
+#pragma unroll
+  for (int i = 1; i < W; ++i) {
+    a0 = fmaxf(a0, red[i]);
+    a1 = fmaxf(a1, red[W + i]);
+    b0 = fmaxf(b0, red[2 * W + i]);
+    b1 = fmaxf(b1, red[3 * W + i]);
+  }
+  mx[0] = a0;
+  mx[1] = a1;
+  mn[0] = -b0;
+  mn[1] = -b1;
+  __syncthreads();
+}
+
+template <int W>
+SJD_DEV void block_excl_scan2(int& a, int& b, int* red) {
+  const int ia = wave_incl_scan_dpp(a), ib = wave_incl_scan_dpp(b);
+  const int w = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == kWave - 1) {
+    red[w] = ia;
+    red[W + w] = ib;
+  }
+  __syncthreads();
+  int ba = 0, bb = 0;
+  for (int i = 0; i < w; ++i) {
+    ba += red[i];
+    bb += red[W + i];
+  }
+  __syncthreads();
+  a = ba + ia - a;
+  b = bb + ib - b;
+}
+
+template <int W>
+SJD_DEV void block_sum_d2(double& a, double& b, double* red) {
+  a = wave_sum_d_dpp(a);
+  b = wave_sum_d_dpp(b);
+  const int w = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    red[w] = a;
+    red[W + w] = b;
+  }
+  __syncthreads();
+  double ra = 0.0, rb = 0.0;
+#pragma unroll
+  for (int i = 0; i < W; ++i) {
+    ra += red[i];
+    rb += red[W + i];
+  }
+  __syncthreads();
+  a = ra;
+  b = rb;
+}
+
+// Largest value and smallest value above -inf of both rows.
+template <int BLOCK, int NC>
+SJD_DEV void row_maxmin2(const float4 (&v)[NC], const float4 (&u)[NC], VSh<BLOCK, NC>& sh, float (&mx)[2],
+                         float (&mn)[2]) {
+  constexpr int W = BLOCK / kWave;
+  mx[0] = mx[1] = -INFINITY;
+  mn[0] = mn[1] = INFINITY;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    mx[0] = vmax(mx[0], vmax(vmax(v[i].x, v[i].y), vmax(v[i].z, v[i].w)));
+    mn[0] = vmin(mn[0], vmin(vmin(v[i].x, v[i].y), vmin(v[i].z, v[i].w)));
+    mx[1] = vmax(mx[1], vmax(vmax(u[i].x, u[i].y), vmax(u[i].z, u[i].w)));
+    mn[1] = vmin(mn[1], vmin(vmin(u[i].x, u[i].y), vmin(u[i].z, u[i].w)));
+  }
+  block_maxmin2<W>(mx, mn, sh.red_f);
+  if (mn[0] == -INFINITY || mn[1] == -INFINITY) {
+    float t[2] = {-INFINITY, -INFINITY}, m2[2] = {INFINITY, INFINITY};
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float a = comp(v[i], e), b = comp(u[i], e);
+        if (a > -INFINITY) m2[0] = vmin(m2[0], a);
+        if (b > -INFINITY) m2[1] = vmin(m2[1], b);
+      }
+    }
+    block_maxmin2<W>(t, m2, sh.red_f);
+    if (mn[0] == -INFINITY) mn[0] = m2[0];
+    if (mn[1] == -INFINITY) mn[1] = m2[1];
+  }
+}
+
+// Top-k selection of both rows by the histogram path. Returns false, with
+// nothing decided, when either row needs the one-row path (every entry kept,
+// a degenerate value range, or more than kCandCap entries in a threshold
+// bin); the decision is uniform over the workgroup.
+template <int BLOCK, int NC>
+SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, int top_k, const float (&mx)[2],
+                          const float (&mn)[2], VSh<BLOCK, NC>& sh, RowStats& ps, RowStats& qs, int& nk,
+                          int& nq) {
+  constexpr int W = BLOCK / kWave;
+  constexpr int NW = VSh<BLOCK, NC>::NW;
+  const int tid = threadIdx.x;
+  const int nchunk = V >> 2;
+  const int k = (top_k <= 0 || top_k >= V) ? V : top_k;
+  if (k >= V) return false;
+  float scale[2], off[2];
+  bool fast = true;
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    bool f = (mx[r] < INFINITY) && (mn[r] < INFINITY) && (mx[r] > mn[r]);
+    scale[r] = f ? (float)kBins / (mx[r] - mn[r]) : 0.0f;
+    f = f && (scale[r] < INFINITY) && (scale[r] > 0.0f);
+    fast = fast && f;
+    off[r] = -mn[r] * scale[r];
+  }
+  if (!fast) return false;
+  for (int b = tid; b < kBins; b += BLOCK) {
+    sh.hist[b] = 0;
+    sh.hist_q[b] = 0;
+  }
+  for (int b = tid; b < kCandCap + 8; b += BLOCK) {
+    sh.cand_v[0][b] = -INFINITY;
+    sh.cand_x[0][b] = 0x7FFFFFFF;
+    sh.cand_v[1][b] = -INFINITY;
+    sh.cand_x[1][b] = 0x7FFFFFFF;
+  }
+  if (tid == 0) {
+    sh.ncand[0] = 0;
+    sh.ncand[1] = 0;
+  }
+  __syncthreads();
+  auto binof = [&](float l, int r) -> int {
+    return (int)__builtin_amdgcn_fmed3f(__builtin_fmaf(l, scale[r], off[r]), 0.0f, (float)(kBins - 1));
+  };
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int c = tid + i * BLOCK;
+    if (c < nchunk) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        atomicAdd(&sh.hist[binof(comp(v[i], e), 0)], 1u);
+        atomicAdd(&sh.hist_q[binof(comp(u[i], e), 1)], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  constexpr int per = kBins / BLOCK;
+  int cp[per], cq[per];
+  int sp = 0, sq = 0;
+#pragma unroll
+  for (int i = 0; i < per; ++i) {
+    cp[i] = (int)sh.hist[kBins - 1 - (tid * per + i)];
+    cq[i] = (int)sh.hist_q[kBins - 1 - (tid * per + i)];
+    sp += cp[i];
+    sq += cq[i];
+  }
+  block_excl_scan2<W>(sp, sq, sh.red_i);
+#pragma unroll
+  for (int i = 0; i < per; ++i) {
+    if (sp < k && sp + cp[i] >= k) {
+      sh.bin[0] = kBins - 1 - (tid * per + i);
+      sh.above[0] = sp;
+    }
+    if (sq < k && sq + cq[i] >= k) {
+      sh.bin[1] = kBins - 1 - (tid * per + i);
+      sh.above[1] = sq;
+    }
+    sp += cp[i];
+    sq += cq[i];
+  }
+  __syncthreads();
+  const int bs0 = sh.bin[0], bs1 = sh.bin[1];
+  const int rem0 = k - sh.above[0], rem1 = k - sh.above[1];
+  const int c0 = (int)sh.hist[bs0], c1 = (int)sh.hist_q[bs1];
+  if (c0 > kCandCap || c1 > kCandCap) return false;
+  // entries of higher bins are kept; the threshold bins' are collected
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int ch = tid + i * BLOCK;
+    uint32_t bp = 0, bq = 0, hp = 0, hq = 0;
+    if (ch < nchunk) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int b0 = binof(comp(v[i], e), 0), b1 = binof(comp(u[i], e), 1);
+        bp |= (b0 > bs0 ? 1u : 0u) << e;
+        hp |= (b0 == bs0 ? 1u : 0u) << e;
+        bq |= (b1 > bs1 ? 1u : 0u) << e;
+        hq |= (b1 == bs1 ? 1u : 0u) << e;
+      }
+    }
+    if (hp | hq) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if ((hp >> e) & 1u) {
+          const int p = atomicAdd(&sh.ncand[0], 1);
+          sh.cand_v[0][p] = comp(v[i], e);
+          sh.cand_x[0][p] = 4 * ch + e;
+        }
+        if ((hq >> e) & 1u) {
+          const int p = atomicAdd(&sh.ncand[1], 1);
+          sh.cand_v[1][p] = comp(u[i], e);
+          sh.cand_x[1][p] = 4 * ch + e;
+        }
+      }
+    }
+    bp <<= 4 * (tid & 7);
+    bq <<= 4 * (tid & 7);
+    bp = or8_dpp(bp);
+    bq = or8_dpp(bq);
+    if ((tid & 7) == 0) {
+      sh.bm[(tid >> 3) + i * (BLOCK / 8)] = bp;
+      sh.bmq[(tid >> 3) + i * (BLOCK / 8)] = bq;
+    }
+  }
+  __syncthreads();
+  // exact rank inside each threshold bin; the first rem join the set
+  for (int t = tid; t < c0 + c1; t += BLOCK) {
+    const int r = t < c0 ? 0 : 1;
+    const int i = t - (r ? c0 : 0);
+    const int c = r ? c1 : c0;
+    const float vi = sh.cand_v[r][i];
+    const int xi = sh.cand_x[r][i];
+    int rank = 0;
+    for (int j0 = 0; j0 < c; j0 += 8) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float vj = sh.cand_v[r][j0 + q];
+        rank += (vj > vi) || (vj == vi && sh.cand_x[r][j0 + q] < xi);
+      }
+    }
+    const int rem = r ? rem1 : rem0;
+    if (rank < rem) atomicOr(r ? &sh.bmq[xi >> 5] : &sh.bm[xi >> 5], 1u << (xi & 31));
+    if (rank == rem - 1) {
+      sh.tau_v[r] = vi;
+      sh.tau_x[r] = xi;
+    }
+  }
+  __syncthreads();
+  ps.all = qs.all = false;
+  ps.tau_v = sh.tau_v[0];
+  ps.tau_x = sh.tau_x[0];
+  qs.tau_v = sh.tau_v[1];
+  qs.tau_x = sh.tau_x[1];
+  // per-word prefix popcounts of both bitmaps
+  constexpr int WPT = NW / BLOCK > 0 ? NW / BLOCK : 1;
+  int np[WPT], nqw[WPT];
+  int rp = 0, rq = 0;
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int wi = tid * WPT + i;
+    np[i] = wi < NW ? __popc(sh.bm[wi]) : 0;
+    nqw[i] = wi < NW ? __popc(sh.bmq[wi]) : 0;
+    rp += np[i];
+    rq += nqw[i];
+  }
+  block_excl_scan2<W>(rp, rq, sh.red_i);
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int wi = tid * WPT + i;
+    if (wi < NW) {
+      sh.pre[wi] = rp;
+      sh.preq[wi] = rq;
+    }
+    rp += np[i];
+    rq += nqw[i];
+  }
+  if (tid == BLOCK - 1) {
+    sh.ncand[0] = rp;
+    sh.ncand[1] = rq;
+  }
+  __syncthreads();
+  nk = sh.ncand[0];
+  nq = sh.ncand[1];
+  __syncthreads();
+  return true;
 }
 
 // Softmax weights over a compact list of logits: w[i] = expf((w[i] - m) / T)
@@ -691,19 +1002,81 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
 #pragma unroll
   for (int t = 0; t < 8; ++t) qcl[t] = t < ncand ? ld.draft[stg.cand[t]] : 0.0f;
 
-  RowStats ps{};
+  RowStats ps{}, qs{};
   int nk = 0;
+  bool q_ready = false;  // the draft distribution at the target's kept entries is in sp_q
   if (ld.need_p) {
     if (!PF) load_row<BLOCK, NC>(v, ld.cur, V);
-    float mx, mn;
-    row_maxmin<BLOCK, NC>(v, sh, mx, mn);
-    ps.m = mx;
-    ps.T = a.T;
-    nk = select_kept<BLOCK, NC>(v, V, a.top_k, mx, mn, sh, sh.bm, sh.pre, ps);
-    compact_row<BLOCK, NC>(v, V, sh.bm, sh.pre, sh.sp_x, sh.sp_p);
-    __syncthreads();
-    ps.invZ = softmax_weights<BLOCK, NC>(sh.sp_p, nk, ps.m, a.T, sh);
-    for (int i = tid; i < nk; i += BLOCK) sh.sp_p[i] = (float)((double)sh.sp_p[i] * ps.invZ);
+    if constexpr (PF) {
+      if (ld.need_q && !ld.q_cached) {
+        // target and draft rows together
+        float mx2[2], mn2[2];
+        row_maxmin2<BLOCK, NC>(v, vq, sh, mx2, mn2);
+        ps.m = mx2[0];
+        qs.m = mx2[1];
+        ps.T = qs.T = a.T;
+        int nq = 0;
+        if (select_kept2<BLOCK, NC>(v, vq, V, a.top_k, mx2, mn2, sh, ps, qs, nk, nq)) {
+          // target compaction; the draft logits at the target's kept entries
+          // (by target rank) and at its own (by draft rank, its normaliser)
+#pragma unroll
+          for (int i = 0; i < NC; ++i) {
+            const int c = tid + i * BLOCK;
+            if (c < nchunk) {
+              const int sh4 = 4 * (c & 7);
+              const uint32_t wp = sh.bm[c >> 3], wq = sh.bmq[c >> 3];
+              const uint32_t np = (wp >> sh4) & 15u, nqb = (wq >> sh4) & 15u;
+              if (np | nqb) {
+                int rp = sh.pre[c >> 3] + __popc(wp & ((1u << sh4) - 1u));
+                int rq = sh.preq[c >> 3] + __popc(wq & ((1u << sh4) - 1u));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  if ((np >> e) & 1u) {
+                    sh.sp_x[rp] = (uint16_t)(4 * c + e);
+                    sh.sp_p[rp] = comp(v[i], e);
+                    sh.sp_q[rp] = comp(vq[i], e);
+                    ++rp;
+                  }
+                  if ((nqb >> e) & 1u) sh.qc[rq++] = comp(vq[i], e);
+                }
+              }
+            }
+          }
+          __syncthreads();
+          double zp = 0.0, zq = 0.0;
+          const int nmax = nk > nq ? nk : nq;
+          for (int i = tid; i < nmax; i += BLOCK) {
+            if (i < nk) {
+              const float e = expf(over_T(sh.sp_p[i] - ps.m, a.T));
+              sh.sp_p[i] = e;
+              zp += (double)e;
+            }
+            if (i < nq) zq += (double)expf(over_T(sh.qc[i] - qs.m, a.T));
+          }
+          block_sum_d2<W>(zp, zq, sh.red_d);
+          ps.invZ = 1.0 / zp;
+          qs.invZ = 1.0 / zq;
+          for (int i = tid; i < nk; i += BLOCK) {
+            sh.sp_p[i] = (float)((double)sh.sp_p[i] * ps.invZ);
+            const int x = (int)sh.sp_x[i];
+            const bool in_q = (sh.bmq[x >> 5] >> (x & 31)) & 1u;
+            sh.sp_q[i] = in_q ? (float)((double)expf(over_T(sh.sp_q[i] - qs.m, a.T)) * qs.invZ) : 0.0f;
+          }
+          q_ready = true;
+        }
+      }
+    }
+    if (!q_ready) {
+      float mx, mn;
+      row_maxmin<BLOCK, NC>(v, sh, mx, mn);
+      ps.m = mx;
+      ps.T = a.T;
+      nk = select_kept<BLOCK, NC>(v, V, a.top_k, mx, mn, sh, sh.bm, sh.pre, ps);
+      compact_row<BLOCK, NC>(v, V, sh.bm, sh.pre, sh.sp_x, sh.sp_p);
+      __syncthreads();
+      ps.invZ = softmax_weights<BLOCK, NC>(sh.sp_p, nk, ps.m, a.T, sh);
+      for (int i = tid; i < nk; i += BLOCK) sh.sp_p[i] = (float)((double)sh.sp_p[i] * ps.invZ);
+    }
     if (a.stats_out && tid == 0) {
       RowStatsCache c;
       c.m = ps.m; c.T = ps.T; c.tau_v = ps.tau_v; c.tau_x = ps.tau_x; c.all = ps.all ? 1 : 0;
@@ -784,8 +1157,9 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   int out_tok = -1, out_stage = 0;
   if (ncand > 0) {
     const float* draft_row = ld.draft;
-    RowStats qs{};
-    if (ld.q_cached) {
+    if (q_ready) {
+      // computed together with the target row
+    } else if (ld.q_cached) {
       // the previous step computed this row's distribution: its statistics,
       // and the draft logits at the target's kept entries (gathered)
       const RowStatsCache c = *ld.q_cached;
@@ -988,7 +1362,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
 // previous one finishes.
 // One workgroup per row (row = trial * L + window row).
 template <int BLOCK, int NC, bool PF>
-__global__ __launch_bounds__(BLOCK) void k_verify_rows(VerifyArgs a) {
+__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 512 ? 4 : 1))) void k_verify_rows(VerifyArgs a) {
   __shared__ VSh<BLOCK, NC> sh;
   const int row = blockIdx.x;
   float4 v[NC];
