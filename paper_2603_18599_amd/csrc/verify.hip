@@ -1279,43 +1279,42 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   if (pd) {
     const int excl = ac ? out_tok : fresh;
     const Stream rs(a.seed, kTagPd, 0, (uint32_t)j, (uint32_t)b, a.step);
-    uint64_t loc[7];
+    // this thread's keys: Philox blocks tid, tid + BLOCK, ... of the compact
+    // list (keys carry the token, so they are distinct)
+    constexpr int KB = (kKcap / 4 + BLOCK - 1) / BLOCK;
+    uint64_t key[4 * KB];
 #pragma unroll
-    for (int t = 0; t < 7; ++t) loc[t] = kNoKey;
-    for (int jj = tid; 4 * jj < nk; jj += BLOCK) {
-      const uint4 wd = rs.block((uint32_t)jj);
+    for (int q = 0; q < KB; ++q) {
+      const int jj = tid + q * BLOCK;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int ent = 4 * jj + e;
-        if (ent < nk) {
-          const int x = (int)sh.sp_x[ent];
-          const float pw = sh.sp_p[ent];
-          if (pw > 0.0f && x != excl) {
-            uint64_t pk = pack_key(exp1(compu(wd, e)) / pw, x);
+      for (int e = 0; e < 4; ++e) key[4 * q + e] = kNoKey;
+      if (4 * jj < nk) {
+        const uint4 wd = rs.block((uint32_t)jj);
 #pragma unroll
-            for (int t = 0; t < 7; ++t) {
-              if (t < Km1 && pk < loc[t]) {
-                const uint64_t tmp = loc[t];
-                loc[t] = pk;
-                pk = tmp;
-              }
-            }
+        for (int e = 0; e < 4; ++e) {
+          const int ent = 4 * jj + e;
+          if (ent < nk) {
+            const int x = (int)sh.sp_x[ent];
+            const float pw = sh.sp_p[ent];
+            if (pw > 0.0f && x != excl) key[4 * q + e] = pack_key(exp1(compu(wd, e)) / pw, x);
           }
         }
       }
     }
-    // each wave's Km1 smallest keys in order (keys are distinct: they carry
-    // the token), then the Km1 smallest of those W lists
+    // each wave's Km1 smallest keys in order, then the Km1 smallest of
+    // those W lists
     const int lane = tid & (kWave - 1), w = tid / kWave;
     uint64_t mine = kNoKey;
 #pragma unroll
     for (int t = 0; t < 7; ++t) {
       if (t < Km1) {
-        const uint64_t m = wave_min_u64_dpp(loc[0]);
-        if (m != kNoKey && loc[0] == m) {
+        uint64_t lm = key[0];
 #pragma unroll
-          for (int u = 0; u < 6; ++u) loc[u] = loc[u + 1];
-          loc[6] = kNoKey;
+        for (int q = 1; q < 4 * KB; ++q) lm = key[q] < lm ? key[q] : lm;
+        const uint64_t m = wave_min_u64_dpp(lm);
+        if (m != kNoKey) {
+#pragma unroll
+          for (int q = 0; q < 4 * KB; ++q) key[q] = key[q] == m ? kNoKey : key[q];
         }
         if (lane == t) mine = m;
       }
