@@ -1356,10 +1356,9 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   }
 }
 
-// Persistent over rows: workgroup w takes rows w, w + grid, ... With PF the
-// first row's data is loaded before the loop and each later row's while the
-// previous one finishes.
-// One workgroup per row (row = trial * L + window row).
+// One workgroup per row (row = trial * L + window row); for 512 threads or
+// more the register budget is capped so that two workgroups share a compute
+// unit.
 template <int BLOCK, int NC, bool PF>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 512 ? 4 : 1))) void k_verify_rows(VerifyArgs a) {
   __shared__ VSh<BLOCK, NC> sh;
