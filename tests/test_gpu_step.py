@@ -115,8 +115,9 @@ def test_acceptance_statistics_match_oracle(orc, mode, flags, K, D, L):
     assert abs(a.mean() - b.mean()) < 4 * se + 0.02
 
 
-@pytest.mark.parametrize("kind,top_k", [("single", 0), ("single", 37), ("guided", 0), ("batch", 37)])
-def test_graph_replay_equals_eager(kind, top_k):
+@pytest.mark.parametrize("kind,top_k,T", [("single", 0, 1.0), ("single", 37, 1.0), ("single", 37, 0.6),
+                                          ("guided", 0, 1.0), ("batch", 37, 1.0), ("batch", 0, 1.7)])
+def test_graph_replay_equals_eager(kind, top_k, T):
     """By default the step's window forward is replayed from a captured HIP
     graph and each draft row reuses the target-row statistics the previous
     step computed for it; SJD_EAGER (the reference mode) enqueues every
@@ -145,7 +146,7 @@ def test_graph_replay_equals_eager(kind, top_k):
             eng.prefill(prompt.cuda(), 5)
         rec = []
         for t in range(24):
-            eng.step(1.0, top_k, 9, t, out_meta=meta, out_tok=tok)
+            eng.step(T, top_k, 9, t, out_meta=meta, out_tok=tok)
             rec.append((meta.cpu().numpy().copy(), tok.cpu().numpy().copy()))
         eng.close()
         runs.append(rec)

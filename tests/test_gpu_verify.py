@@ -72,6 +72,17 @@ def test_verify_chain_matches_oracle(orc, V, top_k):
     assert (gpu["meta"][:, 0] >= 1).all()
 
 
+@pytest.mark.parametrize("V,top_k,T", [(4096, 200, 0.7), (16384, 2000, 1.9), (16384, 1500, 0.25), (2048, 0, 3.0), (65536, 2000, 0.6)])
+def test_verify_temperature_matches_oracle(orc, V, top_k, T):
+    # T != 1 divides every logit difference by T (T = 1 skips the division,
+    # which returns its operand exactly); the tree rows exercise Theorem 2's
+    # stages at the tempered distributions
+    B, L, K, D = 4, 32, 4, 3
+    inp = verify_inputs(B, L, V, top_k=top_k, seed=V + 17, K=K, D=D, D_in=2, draft_noise=1.0, temperature=T)
+    gpu, ref = run_both(orc, inp, K=K, D=D, top_k=top_k, T=T, seed=13, step=2)
+    check(gpu, ref, K, D)
+
+
 def test_verify_tree_rows_with_siblings(orc):
     B, L, V, K, D = 8, 32, 4096, 4, 3
     inp = verify_inputs(B, L, V, top_k=300, seed=11, K=K, D=D, D_in=3, draft_noise=1.5)
