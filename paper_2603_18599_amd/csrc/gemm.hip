@@ -58,15 +58,33 @@ struct GemmSmem {
 // is padded to a multiple of the ring: padded steps reload the last real
 // tile and stage a zero activation tile, so they add nothing.
 // MT = 32-row tiles of A (M <= 32 MT).
+// Workgroups are dealt to the XCDs round-robin by launch index (index i runs
+// on XCD i % kXcds). The grid is one-dimensional, and (column group, K
+// split) is chosen so that each XCD runs a contiguous run of the
+// split-major order: its workgroups share few K splits, so each XCD pulls
+// few activation tiles into its own L2 (with the plain 2D order, every XCD
+// ran every split and fetched the whole activation).
+constexpr int kXcds = 8;
+SJD_DEV void gemm_tile_of(int id, int groups, int splits, int& group, int& split) {
+  const int total = groups * splits;
+  const int q = total / kXcds, r = total % kXcds;
+  const int xcd = id % kXcds, j = id / kXcds;
+  const int lin = xcd < r ? xcd * (q + 1) + j : r * (q + 1) + (xcd - r) * q + j;
+  split = lin / groups;
+  group = lin % groups;
+}
+
 template <int kRing, int MT>
 __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   __shared__ GemmSmem<MT> sm;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
   const int r32 = lane & 31, half = lane >> 5;
   const int T = g.K / 64, nblk = g.N / 32;
-  const int nb = blockIdx.x * kGWaves + wave;  // this wave's 32-column block
+  const int groups = (nblk + kGWaves - 1) / kGWaves;
+  int group, sp;
+  gemm_tile_of((int)blockIdx.x, groups, g.S, group, sp);
+  const int nb = group * kGWaves + wave;  // this wave's 32-column block
   const bool active = nb < nblk;
-  const int sp = blockIdx.y;
   const int st0 = (int)((long)T * sp / g.S), st1 = (int)((long)T * (sp + 1) / g.S);
   const int n = st1 - st0;
   const int npad = (n + kRing - 1) / kRing * kRing;
@@ -208,7 +226,7 @@ int gemm_splits(int N, int K, int target_wgs) {
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M < 1 || g.M > 64 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
   if (g.cfg_rows < 0 || g.cfg_rows > 32 || (g.cfg_rows > 0 && g.M < 32 + g.cfg_rows)) return hipErrorInvalidValue;
-  const dim3 grid((g.N / 32 + kGWaves - 1) / kGWaves, g.S);
+  const dim3 grid((unsigned)(((g.N / 32 + kGWaves - 1) / kGWaves) * g.S));
   if (g.M <= 32) hipLaunchKernelGGL((k_gemm<kRingDepth, 1>), grid, dim3(kGB), 0, s, g);
   else hipLaunchKernelGGL((k_gemm<kRingDepth, 2>), grid, dim3(kGB), 0, s, g);
   return hipGetLastError();
