@@ -39,6 +39,7 @@ constexpr int kGWaves = kGB / kWave;
 // k-steps held per wave (the current one plus one in flight): deeper rings
 // help a lone workgroup but lose once every compute unit holds several
 constexpr int kRingDepth = 2;
+constexpr int kRingDeep = 4;
 // RMSNorm chunk sums held in registers (d <= 4096; larger d reads the rest late)
 constexpr int kSsRegs = 16;
 
@@ -227,8 +228,15 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M < 1 || g.M > 64 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
   if (g.cfg_rows < 0 || g.cfg_rows > 32 || (g.cfg_rows > 0 && g.M < 32 + g.cfg_rows)) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(((g.N / 32 + kGWaves - 1) / kGWaves) * g.S));
-  if (g.M <= 32) hipLaunchKernelGGL((k_gemm<kRingDepth, 1>), grid, dim3(kGB), 0, s, g);
-  else hipLaunchKernelGGL((k_gemm<kRingDepth, 2>), grid, dim3(kGB), 0, s, g);
+  // at one workgroup per compute unit or fewer nothing else hides a
+  // workgroup's load latency: keep more weight tiles in flight
+  const bool lone = grid.x <= 256;
+  if (g.M <= 32) {
+    if (lone) hipLaunchKernelGGL((k_gemm<kRingDeep, 1>), grid, dim3(kGB), 0, s, g);
+    else hipLaunchKernelGGL((k_gemm<kRingDepth, 1>), grid, dim3(kGB), 0, s, g);
+  } else {
+    hipLaunchKernelGGL((k_gemm<kRingDepth, 2>), grid, dim3(kGB), 0, s, g);
+  }
   return hipGetLastError();
 }
 
