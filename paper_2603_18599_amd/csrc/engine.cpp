@@ -466,9 +466,10 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
                    {kProjGu, 2 * F, d, &x.S_gu, sjd::gemm_splits(2 * F, d, target), {}, false},
                    {kProjDown, d, F, &x.S_dn, sjd::gemm_splits(d, F, target), {}, false}};
   // SJD_SPLITS="qkv,o,gu,down" pins the plan (e.g. to profile the plan a
-  // run without the profiler chose)
+  // run without the profiler chose); unset or empty: no pin
   int pinned[4] = {0, 0, 0, 0};
-  if (const char* env = std::getenv("SJD_SPLITS")) {
+  const char* env = std::getenv("SJD_SPLITS");
+  if (env && *env) {
     if (std::sscanf(env, "%d,%d,%d,%d", &pinned[0], &pinned[1], &pinned[2], &pinned[3]) != 4) return fail(SJD_EINVAL);
     for (int v : pinned)
       if (v < 1 || v > sjd::kGemmMaxSplits) return fail(SJD_EINVAL);
