@@ -234,6 +234,24 @@ SJD_API int sjd_prefill_cfg(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, co
 SJD_API int sjd_step(sjd_ctx* ctx, float temperature, int32_t top_k, uint64_t seed, uint32_t step,
              int32_t* d_out_meta, int32_t* d_out_tok, int32_t* d_out_next, void* stream);
 
+/* Replaces the drafts of image `image`'s next step with the caller's (the
+ * problem statement's step takes the previous iteration's drafts X^{t-1}
+ * and their distributions P^{t-1} as inputs; Alg. 1): d_draft_tok[L] are
+ * vocabulary ids, row j's draft (the next window holds the pending token
+ * and d_draft_tok[0 .. L-2]; row L-1's draft is verified but not fed), and
+ * d_draft_logits[L][V] (may be NULL) row j's draft distribution as logits
+ * over [vis_lo, vis_lo + V), taken through the step's temperature / top-k
+ * softmax like the context's own. The next window is a plain chain (no
+ * drafting siblings); with NULL logits no row has a draft distribution and
+ * every row draws from its own (like appended placeholders). The following
+ * sjd_step then verifies these drafts; its outputs, adaptive continuation,
+ * drafting and KV commit are as usual, and the steps after it use the
+ * context's own drafts again. Device pointers, read on `stream` (copied,
+ * so the caller may reuse them once the stream passes this call).
+ * SJD_ESTATE before the image is prefilled. */
+SJD_API int sjd_set_drafts(sjd_ctx* ctx, int32_t image, const int32_t* d_draft_tok, const float* d_draft_logits,
+                           void* stream);
+
 /* Window forward only (no verification): logits of the current window into
  * d_logits[L][V] (a guided context: the guided logits; a batched context:
  * d_logits[32 + L][V], image b's rows from row 32 b). For parity tests. */

@@ -722,6 +722,26 @@ extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t s
   return SJD_OK;
 }
 
+extern "C" int sjd_set_drafts(sjd_ctx* h, int32_t image, const int32_t* d_draft_tok, const float* d_draft_logits,
+                              void* stream) {
+  if (!h || !d_draft_tok) return SJD_EINVAL;
+  Ctx& x = h->x;
+  if (image < 0 || image >= x.B) return SJD_EINVAL;
+  if (!(x.prefilled & (1u << image))) return SJD_ESTATE;
+  hipStream_t s = (hipStream_t)stream;
+  const sjd_config& c = x.c;
+  HIPTRY(sjd::launch_set_drafts(x.st + image, d_draft_tok, c.L, d_draft_logits != nullptr, s));
+  if (d_draft_logits) {
+    // the next step reads its draft rows from the buffer the step before it
+    // wrote, at q_off = 0; the statistics cached with those rows no longer
+    // describe them
+    float* prev = x.logits[(x.steps + 1) & 1] + (size_t)image * 32 * c.V;
+    HIPTRY(hipMemcpyAsync(prev, d_draft_logits, (size_t)c.L * c.V * sizeof(float), hipMemcpyDeviceToDevice, s));
+    HIPTRY(hipMemsetAsync(x.stats[(x.steps + 1) & 1], 0, sizeof(sjd::RowStatsCache) * (size_t)x.B * c.L, s));
+  }
+  return SJD_OK;
+}
+
 extern "C" int sjd_forward_window(sjd_ctx* h, float* d_logits, void* stream) {
   if (!h || !d_logits) return SJD_EINVAL;
   Ctx& x = h->x;

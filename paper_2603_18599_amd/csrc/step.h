@@ -9,6 +9,9 @@ namespace sjd {
 hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, const Streams& sm,
                                hipStream_t s);
 hipError_t launch_build_prefill(const int32_t* prompt, int start, int M, Window* w, hipStream_t s);
+// next window from caller drafts: chain of tok[0..L) (row j's draft), row j's
+// draft distribution from row j of the draft logits when has_q
+hipError_t launch_set_drafts(DevState* st, const int32_t* tok, int L, bool has_q, hipStream_t s);
 // uncond: the unconditional prompt of a guided context (its last token is
 // that stream's first pending token), or NULL
 hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, const int32_t* uncond, int n_u, int L,

@@ -152,6 +152,27 @@ __global__ void k_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok
   }
 }
 
+// Caller-supplied drafts of the next step: a plain chain (no drafting
+// siblings) whose row j carries tok[j]; with has_q, row j's draft
+// distribution is row j of the draft logits (q_off 0), otherwise no row has
+// one and every row draws from its own distribution.
+__global__ void k_set_drafts(DevState* st, const int32_t* tok, int L, int has_q) {
+  const int j = threadIdx.x;
+  if (j < L) st->spine[j] = tok[j];
+  if (j == 0) {
+    st->n_s = L;
+    st->D_in = 0;
+    st->n_q = has_q ? L : 0;
+    st->q_off = 0;
+  }
+}
+
+hipError_t launch_set_drafts(DevState* st, const int32_t* tok, int L, bool has_q, hipStream_t s) {
+  if (L < 1 || L > 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_set_drafts, dim3(1), dim3(64), 0, s, st, tok, L, has_q ? 1 : 0);
+  return hipGetLastError();
+}
+
 hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, const Streams& sm,
                                hipStream_t s) {
   hipLaunchKernelGGL(k_build_window, dim3(1), dim3(64), 0, s, st, w, L, K, vis_lo, sm);

@@ -54,7 +54,7 @@ class Weights(C.Structure):
 
 
 EXPORTS = ["sjd_status_str", "sjd_verify", "sjd_init", "sjd_prefill", "sjd_prefill_image", "sjd_prefill_cfg",
-           "sjd_step", "sjd_forward_window", "sjd_get_plan", "sjd_destroy"]
+           "sjd_set_drafts", "sjd_step", "sjd_forward_window", "sjd_get_plan", "sjd_destroy"]
 
 _lib = None
 
@@ -94,6 +94,8 @@ def load_library():
     lib.sjd_step.restype = C.c_int
     lib.sjd_step.argtypes = [C.c_void_p, C.c_float, C.c_int32, C.c_uint64, C.c_uint32, C.c_void_p, C.c_void_p,
                              C.c_void_p, C.c_void_p]
+    lib.sjd_set_drafts.restype = C.c_int
+    lib.sjd_set_drafts.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.sjd_forward_window.restype = C.c_int
     lib.sjd_forward_window.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
     lib.sjd_destroy.restype = None
@@ -187,6 +189,12 @@ class Engine:
         """Guided contexts (cfg_w != 0): text prompt and unconditional prompt."""
         _check("sjd_prefill_cfg", load_library().sjd_prefill_cfg(self.h, _ptr(prompt), prompt.numel(), _ptr(uncond),
                                                                   uncond.numel(), seed, _stream(stream)))
+
+    def set_drafts(self, draft_tok, draft_logits=None, image=0, stream=None):
+        """The next step verifies draft_tok (int32 [L], vocabulary ids) against
+        draft_logits (float32 [L][V] logits over the sampled range, or None)."""
+        _check("sjd_set_drafts", load_library().sjd_set_drafts(self.h, image, _ptr(draft_tok), _ptr(draft_logits),
+                                                                _stream(stream)))
 
     def step(self, temperature, top_k, seed, step, out_meta=None, out_tok=None, out_next=None, stream=None):
         _check("sjd_step", load_library().sjd_step(self.h, temperature, top_k, seed, step, _ptr(out_meta),
