@@ -52,6 +52,10 @@ def parse():
     ap.add_argument("--batch", type=int, default=1, choices=[1, 2],
                     help="images per step (2: both windows in one forward, one pass over the weights)")
     ap.add_argument("--no-batch2", action="store_true", help="skip the two-images-per-step section")
+    ap.add_argument("--cfg-w", type=float, default=0.0,
+                    help="classifier-free guidance weight (Sec. 5.1 samples with 3): a text-prompt and an "
+                         "unconditional stream in one window forward; 0 = unguided")
+    ap.add_argument("--no-guided", action="store_true", help="skip the guided (CFG weight 3) section")
     ap.add_argument("--eager", action="store_true", help="enqueue every kernel directly (no captured graph)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
@@ -302,17 +306,18 @@ def cpu_baseline_verify(args, inp, K, D, top_k, T, seed, B, L):
             "kind": "oracle", "sample": f"{len(idx)} of {B} windows (one verification step), {dt:.1f} s"}
 
 
-def step_bytes(cfg, n_mean, B=1):
+def step_bytes(cfg, n_mean, B=1, streams=None):
     """Algorithmic HBM bytes of one step: every weight streamed once (bf16),
     the LM head rows of the sampled range only, the cached keys and values
     read once (hi/lo bf16 planes, 4 bytes per element), the window's K/V
     written, and the logits written and read back by the verification; B
     images share the weight stream, each has its own cache and logits
-    (n_mean: mean cached rows per image)."""
+    (n_mean: mean cached rows per image); a guided step has two streams
+    (two caches) and one image's logits."""
     d, H, Hkv, hd, F, V, L = (cfg[k] for k in ("d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim", "V", "L"))
     per_layer = (H * hd * d + 2 * Hkv * hd * d + d * H * hd + 3 * F * d) * 2
     weights = cfg["n_layers"] * per_layer + V * d * 2
-    kv = B * cfg["n_layers"] * 2 * Hkv * hd * 4 * (n_mean + L)
+    kv = (streams or B) * cfg["n_layers"] * 2 * Hkv * hd * 4 * (n_mean + L)
     logits = B * 2 * L * V * 4 * 2  # written once, current + draft rows read once
     return weights + kv + logits, weights, kv
 
@@ -335,6 +340,11 @@ def bench_step(args):
         over["K"], over["D"] = 1, 0  # no drafting tree without PD
     B = args.batch
     over["batch"] = B
+    guided = args.cfg_w != 0.0
+    if guided:
+        if B != 1:
+            raise SystemExit("guidance runs one image per step (--batch 1)")
+        over["cfg_w"] = args.cfg_w
     cfg = model_config(args.workload, **over)
     seed = 11
     w = model_weights(cfg, 1, device="cuda")
@@ -345,12 +355,21 @@ def bench_step(args):
             p = torch.cat([p, image_history(cfg, cfg["n_gen"] // 2, 3 + 10 * b)])
         prompts.append(p.cuda())
     prompt = prompts[0]
+    uncond = None
+    if guided:  # the unconditional stream: its own prompt ids, the same image so far
+        u = prompt_tokens(cfg, 77)
+        if args.context == "mid":
+            u = torch.cat([u, image_history(cfg, cfg["n_gen"] // 2, 3)])
+        uncond = u.cuda()
     eng = Engine(cfg, w)
     stream = torch.cuda.current_stream()
     K, W = args.steps, args.warmup
     metas = torch.zeros(W + K, B, 8, dtype=torch.int32, device="cuda")
 
     def prefill_all(sd):
+        if guided:
+            eng.prefill_cfg(prompts[0], uncond, sd, stream=stream)
+            return
         for b in range(B):
             eng.prefill_image(b, prompts[b], sd + 1000 * b, stream=stream)
 
@@ -402,7 +421,7 @@ def bench_step(args):
     step_ms = [a.elapsed_time(b) for a, b in evs]
     avg_ms = float(np.mean(step_ms))
     n_mean = float(np.mean(ns - ncs))
-    total, weights, kv = step_bytes(cfg, n_mean, B)
+    total, weights, kv = step_bytes(cfg, n_mean, B, streams=2 if guided else None)
     achieved = total / (avg_ms * 1e-3) / 1e9
     res = dict(metric="image tokens/sec on 1 MI355X; mean accept length/step; verify HBM GB/s",
                value=float(ncs.sum()) / wall, unit="image tokens/s", n_gpus=1, steps=K, warmup=W,
@@ -413,6 +432,7 @@ def bench_step(args):
                                    f"SwiGLU {cfg['ffn_dim']}, vocab {cfg['vocab_size']} (sampled {cfg['V']}), "
                                    f"L={cfg['L']} K={cfg['K']} D={cfg['D']}, mode {args.mode}, "
                                    + (f"{B} images per step, " if B > 1 else "") +
+                                   (f"CFG weight {args.cfg_w:g} (text + unconditional stream), " if guided else "") +
                                    f"top-{cfg['top_k']}, T=1, "
                                    f"{cfg['n_prompt']}-token prompt, {cfg['n_gen']}-token image, "
                                    f"steps timed from KV length {prompt.numel() - 1}",
@@ -497,6 +517,12 @@ def main():
             res["batch2"] = {k: b2[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length",
                                                 "step_latency_ms", "config")}
             res["batch2"]["roofline_frac"] = b2["roofline"]["frac"]
+        if args.batch == 1 and args.cfg_w == 0.0 and not args.no_guided and not args.calibrate_copy:
+            # the paper's sampling setting: guidance weight 3 (Sec. 5.1), both streams in one forward
+            gd = bench_step(argparse.Namespace(**dict(vars(args), cfg_w=3.0, no_cpu_baseline=True)))
+            res["guided"] = {k: gd[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length",
+                                                "step_latency_ms", "config")}
+            res["guided"]["roofline_frac"] = gd["roofline"]["frac"]
     print(json.dumps(res), flush=True)
 
 
