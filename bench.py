@@ -270,7 +270,6 @@ def bench_verify(args):
     ms_per_step = wall * 1e3 / args.steps
     value = total_nc / wall
 
-    # closed form of E[n_c] for these inputs (positions independent given the logits)
     res = dict(metric="image tokens/sec on 1 MI355X; mean accept length/step; verify HBM GB/s",
                value=value, unit="image tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
                ms_per_step=ms_per_step, higher_is_better=True, scaling="weak", vs_baseline=None, dtype="f32",
@@ -283,9 +282,46 @@ def bench_verify(args):
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic("verify"),
                          "kernel": "k_verify_rows + k_verify_finalize", "bytes_per_launch": bytes_per_launch,
                          "avg_launch_ms": avg_ms})
+    res["expected_accept_length"], res["expected_accept_length_over_drafts"] = chain_expected_nc(
+        inp["cur"], inp["draft"], inp["draft_tok"], top_k, c["temperature"])
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline_verify(args, inp, K, D, top_k, c["temperature"], seed, B, L)
     return res
+
+
+def chain_expected_nc(cur, draft, draft_tok, top_k, T, chunk=128):
+    """Closed-form mean committed length of these chain windows, reported
+    beside the measured mean. A step commits the accepted prefix plus one
+    token, at most L, and given the logits the rows are independent:
+    E[n_c] = 1 + sum_{i=1}^{L-1} prod_{j<i} a_j, averaged over the windows.
+    Returns (a_j given the drafted tokens x_j: min(1, p_j(x_j) / q_j(x_j)),
+    the exact expectation of the timed steps, whose accept draws are fresh
+    each step while the drafts are fixed; a_j over draft draws from q_j:
+    sum_x min(p_j, q_j), one minus the total-variation distance, Sec. 3).
+    p and q are the top-k softmaxes of the current and draft logits at
+    temperature T (plain torch ops: a statistic of the inputs, not part of
+    the measured path)."""
+    import torch
+
+    B, L, V = cur.shape
+    k = V if top_k <= 0 or top_k >= V else top_k
+
+    def topk_softmax(x):
+        vals, idx = torch.topk(x / T, k, dim=1)
+        return torch.zeros_like(x).scatter_(1, idx, torch.softmax(vals.double(), dim=1).float())
+
+    def expect(a):
+        return (1.0 + torch.cumprod(a[:, :L - 1], dim=1).sum(1)).sum().item()
+
+    given, over = 0.0, 0.0
+    for w0 in range(0, B, chunk):
+        p = topk_softmax(cur[w0:w0 + chunk].reshape(-1, V).float())
+        q = topk_softmax(draft[w0:w0 + chunk].reshape(-1, V).float())
+        x = draft_tok[w0:w0 + chunk].reshape(-1, 1).long()
+        px, qx = p.gather(1, x).double(), q.gather(1, x).double()
+        given += expect(torch.clamp(px / qx, max=1.0).view(-1, L))
+        over += expect(torch.minimum(p, q).double().sum(1).view(-1, L))
+    return given / B, over / B
 
 
 def cpu_baseline_verify(args, inp, K, D, top_k, T, seed, B, L):

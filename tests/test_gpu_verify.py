@@ -151,6 +151,54 @@ def test_verify_full_size_sampled(orc):
     compare_verify(gpu, ref, K=c["K"], D=c["D"])
 
 
+def test_verify_full_size_accept_length_closed_form():
+    """At the benchmark's full size (4096 chain windows x 32 rows x 16384,
+    top-2000), the mean committed length over the windows and four step
+    indices matches its closed form. A step commits the accepted prefix plus
+    one token (at most L) and, given the logits, the rows are independent:
+    E[n_c] = 1 + sum_{i=1}^{L-1} prod_{j<i} a_j per window. With the drafted
+    tokens x_j fixed (every step reuses them, only the accept draws are
+    fresh), a_j = min(1, p_j(x_j) / q_j(x_j)); averaged over drafts drawn
+    from q_j, a_j = sum_x min(p_j, q_j) (one minus the total variation
+    distance). The first is checked against the kernel's outcomes, the second
+    against the first (the inputs' drafts follow q)."""
+    import paper_2603_18599_amd as sjd
+    from paper_2603_18599_amd.sjd import verify_outputs
+    c = CONFIGS["verify"]
+    B, L, V, k = c["B"], c["L"], c["V"], c["top_k"]
+    inp = verify_inputs(B, L, V, top_k=k, seed=4321, device="cuda")
+
+    def topk_softmax(x):
+        vals, idx = torch.topk(x, k, dim=1)
+        return torch.zeros_like(x).scatter_(1, idx, torch.softmax(vals.double(), dim=1).float())
+
+    def expect(a):
+        return 1.0 + torch.cumprod(a[:, :L - 1], dim=1).sum(1)
+    given, over = [], []
+    for w0 in range(0, B, 128):
+        p = topk_softmax(inp["cur"][w0:w0 + 128].reshape(-1, V))
+        q = topk_softmax(inp["draft"][w0:w0 + 128].reshape(-1, V))
+        x = inp["draft_tok"][w0:w0 + 128].reshape(-1, 1).long()
+        given.append(expect(torch.clamp(p.gather(1, x).double() / q.gather(1, x).double(), max=1.0).view(-1, L)))
+        over.append(expect(torch.minimum(p, q).double().sum(1).view(-1, L)))
+    given, over = torch.cat(given).cpu().numpy(), torch.cat(over).cpu().numpy()
+    ncs = []
+    for step in range(4):
+        out = verify_outputs(B, L, c["K"], c["D"])
+        sjd.sjd_verify(inp["cur"], inp["draft"], inp["draft_tok"], inp["meta"], out, K=c["K"], D=c["D"], top_k=k,
+                       seed=17, step=step)
+        torch.cuda.synchronize()
+        ncs.append(out["meta"][:, 0].cpu().numpy().astype(float))
+    nc = np.stack(ncs)  # [step][window]
+    se = nc.std() / np.sqrt(nc.size)
+    d = given - over
+    se_d = d.std() / np.sqrt(d.size)
+    print(f"mean n_c {nc.mean():.4f}; closed form given the drafts {given.mean():.4f} (se {se:.4f}), "
+          f"over draft draws {over.mean():.4f} (se {se_d:.4f})")
+    assert abs(nc.mean() - given.mean()) < 5 * se
+    assert abs(d.mean()) < 5 * se_d
+
+
 def test_verify_is_deterministic(orc):
     import paper_2603_18599_amd as sjd
     from paper_2603_18599_amd.sjd import verify_outputs
