@@ -545,8 +545,9 @@ def main():
         if not args.no_verify:
             v = bench_verify(argparse.Namespace(steps=10, warmup=2, no_cpu_baseline=True, cpu_sample=0,
                                                 calibrate_copy=False))
-            res["verify"] = {k: v[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length", "verify_GBps",
-                                               "roofline", "config")}
+            res["verify"] = {k: v[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length",
+                                               "expected_accept_length", "expected_accept_length_over_drafts",
+                                               "verify_GBps", "roofline", "config")}
         if args.batch == 1 and not args.no_batch2 and not args.calibrate_copy:
             # the same workload with two images per step (serving several requests)
             b2 = bench_step(argparse.Namespace(**dict(vars(args), batch=2, no_cpu_baseline=True)))
