@@ -2,7 +2,9 @@
 oracle's fp64-accumulated forward on the same weights, prompt and window:
 logits within 3e-2 max-abs. Shapes: the tiny and mid models, slices (few
 layers) of the 7B-shaped and 8B GQA large-vocabulary models at their full
-widths, and the full 32-layer 7B-shaped model (the benchmark's model)."""
+widths, the full 32-layer 7B-shaped model (the benchmark's model), and
+narrow models with 128-dim heads over caches of 700-2100 rows (the
+split-KV attention with many chunks)."""
 import numpy as np
 import pytest
 import torch
@@ -27,6 +29,16 @@ CASES = [
     ("tiny", {"L": 64, "n_prompt": 100}),
     ("7b", {"n_layers": 2, "L": 64, "n_prompt": 70}),
     ("8b", {"n_layers": 2, "L": 48, "n_prompt": 40}),
+    # 128-dim heads over long caches: the split-KV attention with many
+    # 128-key chunks and their combine (the 7B benchmark step takes 10 chunks
+    # per head at 1239 cached rows; prefill windows of 64 rows take two slot
+    # halves), on narrow bf16 models so that the oracle's prefill stays quick
+    ("tiny", {"n_layers": 1, "d_model": 512, "n_heads": 4, "n_kv_heads": 4, "head_dim": 128, "ffn_dim": 1024,
+              "n_prompt": 1271, "L": 32, "weights_f32": False}),
+    ("tiny", {"n_layers": 2, "d_model": 512, "n_heads": 4, "n_kv_heads": 2, "head_dim": 128, "ffn_dim": 1024,
+              "n_prompt": 700, "weights_f32": False}),
+    ("tiny", {"n_layers": 1, "d_model": 256, "n_heads": 2, "n_kv_heads": 2, "head_dim": 128, "ffn_dim": 512,
+              "n_prompt": 2100, "L": 64, "weights_f32": False}),
 ]
 
 
