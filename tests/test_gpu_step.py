@@ -82,6 +82,33 @@ def test_greedy_window_equals_autoregressive(K, D, flags, L):
     assert np.mean(ncs) > 1.0  # the window actually ran ahead
 
 
+HD128 = [dict(d_model=512, n_heads=4, n_kv_heads=4, head_dim=128, ffn_dim=1024),
+         dict(d_model=512, n_heads=4, n_kv_heads=2, head_dim=128, ffn_dim=1024)]
+
+
+@pytest.mark.parametrize("shape", HD128, ids=["mha", "gqa"])
+def test_greedy_window_equals_autoregressive_128_dim_heads(shape):
+    """As above with 128-dim heads (the large models' head size) over caches
+    of several hundred rows: the 128-dim tiled key/value layout, the KV
+    commit of accepted rows and the attention over many key chunks, all
+    inside the decoding loop."""
+    over = dict(shape, n_layers=2, n_prompt=300, L=32, K=4, D=3, flags=3, weights_f32=False)
+    base = model_config("tiny", **over)
+    w, prompt = setup(base, wseed=23, pseed=24)
+    wd = weights_device(w)
+    eng = make_engine(base, wd)
+    win, ncs, ns = generate(eng, base, prompt, seed=1, n_gen=160, top_k=1)
+    eng.close()
+    ar_cfg = model_config("tiny", **dict(over, L=1, K=1, D=0))
+    eng = make_engine(ar_cfg, wd)
+    ar, ar_ncs, _ = generate(eng, ar_cfg, prompt, seed=1, n_gen=160, top_k=1)
+    eng.close()
+    assert ns == list(np.cumsum(ncs) + base["n_prompt"] - 1)
+    assert set(ar_ncs) == {1}
+    assert win == ar
+    assert np.mean(ncs) > 1.0
+
+
 @pytest.mark.parametrize("mode,flags,K,D,L", [("sjd-pac", 3, 4, 3, 16), ("ac", 1, 1, 0, 16), ("pd", 2, 4, 3, 16),
                                               ("sjd", 0, 1, 0, 16), ("sjd-pac", 3, 4, 3, 64)])
 def test_acceptance_statistics_match_oracle(orc, mode, flags, K, D, L):
