@@ -24,6 +24,9 @@ CASES = [
     ("tiny", {"L": 16}, 9),
     ("tiny", {"L": 32, "K": 2, "D": 2}, 40),
     ("7b", {"n_layers": 2, "n_prompt": 40, "L": 32}, 70),
+    # 128-dim heads over long caches (many key chunks for both images)
+    ("tiny", {"n_layers": 1, "d_model": 512, "n_heads": 4, "n_kv_heads": 4, "head_dim": 128, "ffn_dim": 1024,
+              "n_prompt": 1200, "L": 32, "weights_f32": False}, 650),
 ]
 
 

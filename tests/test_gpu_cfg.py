@@ -56,6 +56,9 @@ FWD_CASES = [
     ("tiny", {"L": 16}, 9),    # unconditional prompt longer than the text prompt
     ("tiny", {"L": 32}, 5),    # shorter; a full 32-row stream
     ("7b", {"n_layers": 2, "n_prompt": 40, "L": 32}, 70),  # more than one prefill window
+    # 128-dim heads over long caches (many key chunks in both streams)
+    ("tiny", {"n_layers": 1, "d_model": 512, "n_heads": 4, "n_kv_heads": 2, "head_dim": 128, "ffn_dim": 1024,
+              "n_prompt": 700, "L": 32, "weights_f32": False}, 1100),
 ]
 
 
