@@ -109,6 +109,30 @@ def test_greedy_window_equals_autoregressive_128_dim_heads(shape):
     assert np.mean(ncs) > 1.0
 
 
+def test_greedy_window_equals_autoregressive_full_7b(monkeypatch):
+    """The benchmark's model, cache length and launch configuration (7B
+    shape, 32 layers, vocab 65536, 1240 cached rows so the attention takes
+    10 key chunks per head, the split plan 5 / 8 / 4 / 8 the benchmark
+    profiles): greedy window decoding equals one-slot decoding token for
+    token, a property that holds at any size."""
+    monkeypatch.setenv("SJD_SPLITS", "5,8,4,8")
+    over = dict(n_prompt=1240, n_gen=48)
+    base = model_config("7b", **over)
+    w, prompt = setup(base, wseed=31, pseed=32, device="cuda")
+    wd = weights_device(w)
+    eng = make_engine(base, wd)
+    win, ncs, ns = generate(eng, base, prompt, seed=1, n_gen=40, top_k=1)
+    eng.close()
+    ar_cfg = model_config("7b", **dict(over, L=1, K=1, D=0))
+    eng = make_engine(ar_cfg, wd)
+    ar, ar_ncs, _ = generate(eng, ar_cfg, prompt, seed=1, n_gen=40, top_k=1)
+    eng.close()
+    print(f"committed per step {ncs}")
+    assert ns == list(np.cumsum(ncs) + base["n_prompt"] - 1)
+    assert set(ar_ncs) == {1}
+    assert win == ar
+
+
 @pytest.mark.parametrize("mode,flags,K,D,L", [("sjd-pac", 3, 4, 3, 16), ("ac", 1, 1, 0, 16), ("pd", 2, 4, 3, 16),
                                               ("sjd", 0, 1, 0, 16), ("sjd-pac", 3, 4, 3, 64)])
 def test_acceptance_statistics_match_oracle(orc, mode, flags, K, D, L):
