@@ -109,21 +109,25 @@ def test_greedy_window_equals_autoregressive_128_dim_heads(shape):
     assert np.mean(ncs) > 1.0
 
 
-def test_greedy_window_equals_autoregressive_full_7b(monkeypatch):
-    """The benchmark's model, cache length and launch configuration (7B
-    shape, 32 layers, vocab 65536, 1240 cached rows so the attention takes
-    10 key chunks per head, the split plan 5 / 8 / 4 / 8 the benchmark
-    profiles): greedy window decoding equals one-slot decoding token for
-    token, a property that holds at any size."""
+@pytest.mark.parametrize("name,n_prompt", [("7b", 1240), ("8b", 4159)])
+def test_greedy_window_equals_autoregressive_full_size(monkeypatch, name, n_prompt):
+    """The benchmark's models at their benchmark cache lengths and launch
+    configuration (7B shape: 32 layers, vocab 65536, 1239 cached rows, 10
+    key chunks per head, the split plan 5 / 8 / 4 / 8 the benchmark
+    profiles; 8B GQA shape: 32 layers, 32768 sampled visual rows of a
+    184622-token vocabulary, 4158 cached rows): greedy window decoding
+    equals one-slot decoding token for token, a property that holds at any
+    size. Both engines run one pinned split plan, so their GEMMs sum in the
+    same order."""
     monkeypatch.setenv("SJD_SPLITS", "5,8,4,8")
-    over = dict(n_prompt=1240, n_gen=48)
-    base = model_config("7b", **over)
+    over = dict(n_prompt=n_prompt, n_gen=48)
+    base = model_config(name, **over)
     w, prompt = setup(base, wseed=31, pseed=32, device="cuda")
     wd = weights_device(w)
     eng = make_engine(base, wd)
     win, ncs, ns = generate(eng, base, prompt, seed=1, n_gen=40, top_k=1)
     eng.close()
-    ar_cfg = model_config("7b", **dict(over, L=1, K=1, D=0))
+    ar_cfg = model_config(name, **dict(over, L=1, K=1, D=0))
     eng = make_engine(ar_cfg, wd)
     ar, ar_ncs, _ = generate(eng, ar_cfg, prompt, seed=1, n_gen=40, top_k=1)
     eng.close()
