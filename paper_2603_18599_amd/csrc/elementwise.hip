@@ -93,11 +93,16 @@ hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, c
 // position n + m (tiled layout), all as hi / lo bf16 planes. Two-stream
 // windows: row m is slot m & 31 of stream m >> 5, cached at that stream's
 // own position in its own cache; padding rows get a zero q and no cache write.
-// grid (M, H + 2 * Hkv), block hd / 2
+// grid (H + 2 * Hkv, M), block hd / 2. Head-major: workgroups are dealt to
+// the XCDs round-robin by launch index, so (with H + 2 Hkv a multiple of 8)
+// every row of one head runs on one XCD. A cache tile interleaves the rows
+// of 8 positions in each 16-byte chunk, and its lines then fill in one L2
+// instead of leaving as partial lines from eight (the row-major grid wrote
+// 5.8 MB per launch for about 1.5 MB of data, and the step took 60 us longer).
 template <int SMAX>
 __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,
                           int H, int Hkv, int hd, const float2* rope, KvPlanes o, int cap, Streams sm) {
-  const int m = blockIdx.x, hh = blockIdx.y, i = threadIdx.x;
+  const int m = blockIdx.y, hh = blockIdx.x, i = threadIdx.x;
   const int half = hd / 2;
   const bool two = sm.mode != kStreamsOne;
   const bool second = two && m >= 32;
@@ -159,7 +164,7 @@ __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* w
 hipError_t launch_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,
                           int M, int H, int Hkv, int hd, const float2* rope, const KvPlanes& o, int cap,
                           const Streams& sm, hipStream_t s) {
-  const dim3 grid(M, H + 2 * Hkv), block(hd / 2);
+  const dim3 grid(H + 2 * Hkv, M), block(hd / 2);
   if (S < 1) return hipErrorInvalidValue;
   if (S <= 4)
     hipLaunchKernelGGL(k_rope_kv<4>, grid, block, 0, s, qkv, S, plane, win, n_dev, n_host, H, Hkv, hd, rope, o, cap, sm);
