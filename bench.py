@@ -477,7 +477,7 @@ def bench_step(args):
                step_latency_p50_ms=float(np.percentile(step_ms, 50)),
                step_latency_p99_ms=float(np.percentile(step_ms, 99)),
                prefill_ms=prefill_ms, kv_rows_mean=n_mean, image_restarts=restarts,
-               host_enqueue_ms_per_step=host_s * 1e3 / K, split_plan=eng.plan(),
+               host_enqueue_ms_per_step=host_s * 1e3 / K, split_plan=eng.plan(), split_pin=eng.plan_pin(),
                roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic(args.workload),
                          "kernel": "sjd_step (window forward + verification + KV commit)",

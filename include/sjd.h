@@ -257,12 +257,16 @@ SJD_API int sjd_set_drafts(sjd_ctx* ctx, int32_t image, const int32_t* d_draft_t
  * d_logits[32 + L][V], image b's rows from row 32 b). For parity tests. */
 SJD_API int sjd_forward_window(sjd_ctx* ctx, float* d_logits, void* stream);
 
-/* The context's split-K plan: how many workgroups share the K range of the
- * QKV, O, gate|up, down and LM-head projections (splits[0..min(n,5))).
- * Chosen at sjd_init: the closed form, the process-wide timed plan (the
- * first context of a process that meets a projection shape times
- * GEMM + consumer pairs; SJD_NO_TUNE skips this), or the environment
- * variable SJD_SPLITS="qkv,o,gu,down" when set. */
+/* The context's GEMM plan, written to splits[0 .. min(n, 20)): for windows
+ * of up to 32 rows, [0..5) how many workgroups share the K range of the
+ * QKV, O, gate|up, down and LM-head projections and [5..10) how many 32-column
+ * blocks each workgroup takes (4 or 8); [10..20) the same for windows of
+ * more rows (two streams, L > 32, prefill). Chosen at sjd_init: the closed
+ * form, the process-wide timed plan (the first context of a process that
+ * meets a projection shape and row class times GEMM + consumer pairs;
+ * SJD_NO_TUNE skips this), or the environment variable
+ * SJD_SPLITS="qkv,o,gu,down" (each entry S or S:blocks) for windows of up
+ * to 32 rows when set. */
 SJD_API int sjd_get_plan(const sjd_ctx* ctx, int32_t* splits, int32_t n);
 
 SJD_API void sjd_destroy(sjd_ctx* ctx);

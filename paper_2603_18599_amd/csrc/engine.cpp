@@ -70,7 +70,13 @@ struct Ctx {
   sjd::DevState* st = nullptr;
   sjd::Window* win = nullptr;
   int32_t* rec = nullptr;
-  int S_qkv = 1, S_o = 1, S_gu = 1, S_dn = 1, S_head = 1;
+  // GEMM plan per projection (QKV, O, gate|up, down): split count and column
+  // blocks per workgroup, for windows of <= 32 rows [0] and of more [1]
+  // (two streams, L > 32, prefill windows); the LM head runs wide, unsplit
+  struct Plan {
+    int S = 1, wide = 0;
+  };
+  Plan plan[2][4];
   long long steps = 0;
   unsigned prefilled = 0;  // bit b: image b prefilled
   // the step's window forward (window build + ~10 kernels per layer + head),
@@ -137,6 +143,8 @@ int check_config(const sjd_config* c) {
     if ((e) != hipSuccess) return SJD_EHIP;      \
   } while (0)
 
+enum { kProjQkv = 0, kProjO = 1, kProjGu = 2, kProjDown = 3 };
+
 // Window forward of M rows: two streams (sm.mode != kStreamsOne, see
 // Streams), or one stream on the caches of stream `cache` (a prefill).
 int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, const sjd::Streams& sm, int cache,
@@ -147,6 +155,7 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
   HIPTRY(sjd::launch_embed(x.embed, x.win, M, d, x.x, s));
   const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d, guplane = (size_t)x.Mpad * 2 * F;
   int pend = 0;  // partial planes of the last residual projection not yet added into x
+  const Ctx::Plan* P = x.plan[M > 32 ? 1 : 0];
   sjd::GemmArgs normed{};  // GEMM arguments that apply the RMSNorm row scale
   normed.ss = x.ss;
   normed.ss_n = sjd::norm_chunks(d);
@@ -158,10 +167,10 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
     sjd::KvPlanes kv{x.q, x.q_lo, x.kc + lofs, x.kc_lo + lofs, x.vt + lofs, x.vt_lo + lofs, x.kv_elems};
     HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, pend, rplane, w[0], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
     sjd::GemmArgs g = normed;
-    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = w[1]; g.N = Nqkv; g.K = d; g.S = x.S_qkv;
-    g.out = x.qkv; g.plane = qplane; g.ldo = Nqkv;
+    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = w[1]; g.N = Nqkv; g.K = d; g.S = P[kProjQkv].S;
+    g.wide = P[kProjQkv].wide; g.out = x.qkv; g.plane = qplane; g.ldo = Nqkv;
     HIPTRY(sjd::launch_gemm(g, s));
-    HIPTRY(sjd::launch_rope_kv(x.qkv, x.S_qkv, qplane, x.win, n_dev, n_host, M, H, Hkv, hd, x.rope, kv, x.cap_pad,
+    HIPTRY(sjd::launch_rope_kv(x.qkv, P[kProjQkv].S, qplane, x.win, n_dev, n_host, M, H, Hkv, hd, x.rope, kv, x.cap_pad,
                                sm, s));
     sjd::AttnArgs a{};
     a.q = x.q; a.q_lo = x.q_lo; a.kc = kv.kc; a.kc_lo = kv.kc_lo; a.vt = kv.vt; a.vt_lo = kv.vt_lo; a.win = x.win;
@@ -172,25 +181,26 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
     a.ldo = x.ld_q;
     HIPTRY(sjd::launch_attention(a, hd, s));
     g = sjd::GemmArgs{};
-    g.A = x.att; g.A_lo = x.att_lo; g.lda = x.ld_q; g.M = M; g.W = w[4]; g.N = d; g.K = Nq; g.S = x.S_o;
-    g.out = x.rpart; g.plane = rplane; g.ldo = d;
+    g.A = x.att; g.A_lo = x.att_lo; g.lda = x.ld_q; g.M = M; g.W = w[4]; g.N = d; g.K = Nq; g.S = P[kProjO].S;
+    g.wide = P[kProjO].wide; g.out = x.rpart; g.plane = rplane; g.ldo = d;
     HIPTRY(sjd::launch_gemm(g, s));
-    HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, x.S_o, rplane, w[5], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
+    HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, P[kProjO].S, rplane, w[5], M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
     g = normed;
-    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = w[6]; g.N = 2 * F; g.K = d; g.S = x.S_gu;
-    g.out = x.gup; g.plane = guplane; g.ldo = 2 * F;
+    g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = w[6]; g.N = 2 * F; g.K = d; g.S = P[kProjGu].S;
+    g.wide = P[kProjGu].wide; g.out = x.gup; g.plane = guplane; g.ldo = 2 * F;
     HIPTRY(sjd::launch_gemm(g, s));
-    HIPTRY(sjd::launch_swiglu(x.gup, x.S_gu, guplane, M, F, x.hbuf, x.hbuf_lo, x.ld_f, s));
+    HIPTRY(sjd::launch_swiglu(x.gup, P[kProjGu].S, guplane, M, F, x.hbuf, x.hbuf_lo, x.ld_f, s));
     g = sjd::GemmArgs{};
-    g.A = x.hbuf; g.A_lo = x.hbuf_lo; g.lda = x.ld_f; g.M = M; g.W = w[8]; g.N = d; g.K = F; g.S = x.S_dn;
-    g.out = x.rpart; g.plane = rplane; g.ldo = d;
+    g.A = x.hbuf; g.A_lo = x.hbuf_lo; g.lda = x.ld_f; g.M = M; g.W = w[8]; g.N = d; g.K = F; g.S = P[kProjDown].S;
+    g.wide = P[kProjDown].wide; g.out = x.rpart; g.plane = rplane; g.ldo = d;
     HIPTRY(sjd::launch_gemm(g, s));
-    pend = x.S_dn;
+    pend = P[kProjDown].S;
   }
   if (logits) {
     HIPTRY(sjd::launch_resid_norm(x.x, x.rpart, pend, rplane, x.fnorm, M, d, x.xn, x.xn_lo, x.ld_d, x.ss, s));
     sjd::GemmArgs g = normed;
     g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = x.head; g.N = c.V; g.K = d; g.S = 1;
+    g.wide = 1;  // measured faster at 32 and 64 rows
     g.out = logits; g.plane = 0; g.ldo = c.V;
     if (sm.mode == sjd::kStreamsGuided) {  // rows [0, L) of the output: guided logits
       g.cfg_rows = sm.L;
@@ -210,38 +220,49 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
 // times every candidate pair (GEMM + consumer) on its own weights at 32
 // rows and keeps the fastest for the process: every context of the process
 // uses the same plan, so their arithmetic agrees.
-enum { kProjQkv = 0, kProjO = 1, kProjGu = 2, kProjDown = 3 };
 std::mutex g_plan_mu;
-std::map<std::tuple<int, int, int>, int> g_plan;  // (projection, N, K) -> splits
+// (projection, N, K, row class) -> plan
+std::map<std::tuple<int, int, int, int>, Ctx::Plan> g_plan;
 
-// candidate split counts: one to three workgroups per compute unit, at
-// least two k-steps per workgroup, plus the closed-form choice
-std::vector<int> split_candidates(int N, int K, int ncu, int fallback) {
-  const int groups = (N / 32 + 3) / 4, T = K / 64;
-  std::vector<int> out;
-  for (int S = 1; S <= sjd::kGemmMaxSplits; ++S) {
-    if (S > 1 && T / S < 2) break;
-    const long wg = (long)groups * S;
-    if (wg >= ncu && wg <= 3L * ncu) out.push_back(S);
+// candidate plans: 4 and 8 column blocks per workgroup, one to three
+// workgroups per compute unit, at least two k-steps per workgroup, plus
+// the closed-form choice
+std::vector<Ctx::Plan> plan_candidates(int N, int K, int ncu, Ctx::Plan fallback) {
+  const int T = K / 64;
+  std::vector<Ctx::Plan> out;
+  for (int wide = 0; wide < 2; ++wide) {
+    const int nw = wide ? 8 : 4;
+    const int groups = (N / 32 + nw - 1) / nw;
+    for (int S = 1; S <= sjd::kGemmMaxSplits; ++S) {
+      if (S > 1 && T / S < 2) break;
+      const long wg = (long)groups * S;
+      if (wg >= ncu && wg <= 3L * ncu) out.push_back(Ctx::Plan{S, wide});
+    }
   }
   bool has = false;
-  for (int S : out) has |= S == fallback;
+  for (const Ctx::Plan& p : out) has |= p.S == fallback.S && p.wide == fallback.wide;
   if (!has) out.push_back(fallback);
   return out;
 }
 
-// Times GEMM + consumer per candidate (layer 0's weights, 32 rows, current
-// buffer contents) and returns the chosen split (see below).
-int tune_projection(Ctx& x, int proj, const std::vector<int>& cand, int closed, hipStream_t s) {
+// Times GEMM + consumer per candidate (M rows, current buffer contents) and
+// returns the chosen plan (see below; S < 1: error). Repetition r runs layer
+// r's weights (mod the layer count): the projections of the large models
+// fit in the 256 MB last-level cache one layer at a time, and a plan timed
+// on cache-resident weights is not the one that streams fastest from HBM.
+Ctx::Plan tune_projection(Ctx& x, int proj, const std::vector<Ctx::Plan>& cand, Ctx::Plan closed, int M,
+                          hipStream_t s) {
   const sjd_config& c = x.c;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
-  const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv, M = 32;
-  const auto& w = x.lw[0];
+  const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv;
+  const Ctx::Plan fail{0, 0};
   const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d, guplane = (size_t)x.Mpad * 2 * F;
   const sjd::Streams one{sjd::kStreamsOne, 0, 0, nullptr};
-  auto pair = [&](int S) -> hipError_t {
+  auto pair = [&](const Ctx::Plan& pl, int rep) -> hipError_t {
+    const auto& w = x.lw[rep % c.n_layers];
+    const int S = pl.S;
     sjd::GemmArgs g{};
-    g.M = M; g.S = S;
+    g.M = M; g.S = S; g.wide = pl.wide;
     if (proj == kProjQkv || proj == kProjGu) {
       g.ss = x.ss; g.ss_n = sjd::norm_chunks(d); g.inv_d = 1.0f / (float)d; g.eps = c.rms_eps;
       g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.K = d;
@@ -273,7 +294,7 @@ int tune_projection(Ctx& x, int proj, const std::vector<int>& cand, int closed, 
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
     if (e0) (void)hipEventDestroy(e0);
-    return -1;
+    return fail;
   }
   // two interleaved rounds over the candidates; each keeps its faster round
   constexpr int kReps = 10, kRounds = 2;
@@ -281,10 +302,10 @@ int tune_projection(Ctx& x, int proj, const std::vector<int>& cand, int closed, 
   bool ok = true;
   for (int round = 0; round < kRounds && ok; ++round)
     for (size_t i = 0; i < cand.size() && ok; ++i) {
-      const int S = cand[i];
-      for (int r = 0; r < 2 && ok; ++r) ok = pair(S) == hipSuccess;
+      const Ctx::Plan pl = cand[i];
+      for (int r = 0; r < 2 && ok; ++r) ok = pair(pl, kReps + r) == hipSuccess;
       ok = ok && hipEventRecord(e0, s) == hipSuccess;
-      for (int r = 0; r < kReps && ok; ++r) ok = pair(S) == hipSuccess;
+      for (int r = 0; r < kReps && ok; ++r) ok = pair(pl, r) == hipSuccess;
       ok = ok && hipEventRecord(e1, s) == hipSuccess && hipEventSynchronize(e1) == hipSuccess;
       float ms = 0.0f;
       ok = ok && hipEventElapsedTime(&ms, e0, e1) == hipSuccess;
@@ -293,22 +314,21 @@ int tune_projection(Ctx& x, int proj, const std::vector<int>& cand, int closed, 
     }
   (void)hipEventDestroy(e0);
   (void)hipEventDestroy(e1);
-  if (!ok) return -1;
+  if (!ok) return fail;
   // the closed-form choice unless a candidate beats it by more than 3%
   // (then the fastest): near-ties keep the same plan however noisy the
   // timing (another process, a profiler attached)
   size_t ref = 0;
   for (size_t i = 0; i < t.size(); ++i)
-    if (cand[i] == closed) ref = i;
+    if (cand[i].S == closed.S && cand[i].wide == closed.wide) ref = i;
   size_t pick = ref;
   for (size_t i = 0; i < t.size(); ++i)
     if (t[i] < t[ref] * 0.97f && t[i] < t[pick]) pick = i;
-  const int best = cand[pick];
   if (std::getenv("SJD_LOG_PLAN"))
     for (size_t i = 0; i < t.size(); ++i)
-      std::fprintf(stderr, "[sjd] plan: projection %d splits %d: %.2f us%s\n", proj, cand[i], t[i],
-                   cand[i] == best ? " <- chosen" : "");
-  return best;
+      std::fprintf(stderr, "[sjd] plan: projection %d, %d rows: %d splits x %d blocks: %.2f us%s\n", proj, M,
+                   cand[i].S, cand[i].wide ? 8 : 4, t[i], i == pick ? " <- chosen" : "");
+  return cand[pick];
 }
 
 // Refreshes the cache-fill bound of every image from completed steps;
@@ -460,41 +480,64 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   }
   const int target = 5 * ncu / 2;
   const int Nqkv = Nq + 2 * Nkv;
-  struct Proj { int kind, N, K; int* S; int closed; std::vector<int> cand; bool tune; };
-  Proj projs[4] = {{kProjQkv, Nqkv, d, &x.S_qkv, sjd::gemm_splits(Nqkv, d, target), {}, false},
-                   {kProjO, d, Nq, &x.S_o, sjd::gemm_splits(d, Nq, target), {}, false},
-                   {kProjGu, 2 * F, d, &x.S_gu, sjd::gemm_splits(2 * F, d, target), {}, false},
-                   {kProjDown, d, F, &x.S_dn, sjd::gemm_splits(d, F, target), {}, false}};
-  // SJD_SPLITS="qkv,o,gu,down" pins the plan (e.g. to profile the plan a
-  // run without the profiler chose); unset or empty: no pin
-  int pinned[4] = {0, 0, 0, 0};
+  // one plan per projection and row class (windows of <= 32 rows; of more:
+  // timed only for contexts whose steps run them, else the closed form, which
+  // serves their 64-row prefill windows)
+  const int kind_N[4] = {Nqkv, d, 2 * F, d}, kind_K[4] = {d, Nq, d, F};
+  const bool step64 = x.nstreams == 2 || c.L > 32;
+  struct Proj { int kind, N, K, cls; Ctx::Plan closed; std::vector<Ctx::Plan> cand; bool tune; };
+  std::vector<Proj> projs;
+  for (int cls = 0; cls < 2; ++cls)
+    for (int k = 0; k < 4; ++k) {
+      Proj p{k, kind_N[k], kind_K[k], cls, Ctx::Plan{}, {}, false};
+      p.closed = Ctx::Plan{sjd::gemm_splits(p.N, p.K, target, cls == 1), cls};
+      projs.push_back(p);
+    }
+  // SJD_SPLITS="qkv,o,gu,down" pins the plan of windows of <= 32 rows (e.g.
+  // to profile the plan a run without the profiler chose); an entry "S:8"
+  // runs 8 column blocks per workgroup, "S" or "S:4" four; unset or empty:
+  // no pin
+  Ctx::Plan pin[4];
+  bool pinned = false;
   const char* env = std::getenv("SJD_SPLITS");
   if (env && *env) {
-    if (std::sscanf(env, "%d,%d,%d,%d", &pinned[0], &pinned[1], &pinned[2], &pinned[3]) != 4) return fail(SJD_EINVAL);
-    for (int v : pinned)
-      if (v < 1 || v > sjd::kGemmMaxSplits) return fail(SJD_EINVAL);
+    const char* q = env;
+    for (int i = 0; i < 4; ++i) {
+      char* end = nullptr;
+      const long v = std::strtol(q, &end, 10);
+      if (end == q || v < 1 || v > sjd::kGemmMaxSplits) return fail(SJD_EINVAL);
+      long wv = 4;
+      if (*end == ':') {
+        q = end + 1;
+        wv = std::strtol(q, &end, 10);
+        if (end == q || (wv != 4 && wv != 8)) return fail(SJD_EINVAL);
+      }
+      if (*end != (i < 3 ? ',' : '\0')) return fail(SJD_EINVAL);
+      pin[i] = Ctx::Plan{(int)v, wv == 8 ? 1 : 0};
+      q = end + 1;
+    }
+    pinned = true;
   }
-  const bool tune = !(c.flags & SJD_NO_TUNE) && pinned[0] == 0;
-  int smax[4];
+  const bool tune = !(c.flags & SJD_NO_TUNE) && !pinned;
+  int smax[4] = {1, 1, 1, 1};
   {
     std::lock_guard<std::mutex> lk(g_plan_mu);
-    for (int i = 0; i < 4; ++i) {
-      Proj& p = projs[i];
-      *p.S = pinned[0] ? pinned[i] : p.closed;
-      if (tune) {
-        auto it = g_plan.find(std::make_tuple(p.kind, p.N, p.K));
+    for (Proj& p : projs) {
+      Ctx::Plan& dst = x.plan[p.cls][p.kind];
+      dst = pinned && p.cls == 0 ? pin[p.kind] : p.closed;
+      if (tune && (p.cls == 0 || step64)) {
+        auto it = g_plan.find(std::make_tuple(p.kind, p.N, p.K, p.cls));
         if (it != g_plan.end()) {
-          *p.S = it->second;
+          dst = it->second;
         } else {
-          p.cand = split_candidates(p.N, p.K, ncu, p.closed);
+          p.cand = plan_candidates(p.N, p.K, ncu, p.closed);
           p.tune = true;
         }
       }
-      smax[i] = *p.S;
-      for (int S : p.cand) smax[i] = S > smax[i] ? S : smax[i];
+      smax[p.kind] = dst.S > smax[p.kind] ? dst.S : smax[p.kind];
+      for (const Ctx::Plan& q : p.cand) smax[p.kind] = q.S > smax[p.kind] ? q.S : smax[p.kind];
     }
   }
-  x.S_head = 1;
   const int sr = smax[1] > smax[3] ? smax[1] : smax[3];
   if ((rc = dalloc(x, &x.qkv, (size_t)smax[0] * Mp * Nqkv)) ||
       (rc = dalloc(x, &x.rpart, (size_t)sr * Mp * d)) ||
@@ -537,14 +580,16 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   for (Proj& p : projs) {
     if (!p.tune) continue;
     std::lock_guard<std::mutex> lk(g_plan_mu);
-    auto it = g_plan.find(std::make_tuple(p.kind, p.N, p.K));
+    const auto key = std::make_tuple(p.kind, p.N, p.K, p.cls);
+    auto it = g_plan.find(key);
     if (it == g_plan.end()) {
-      const int S = p.cand.size() > 1 ? tune_projection(x, p.kind, p.cand, p.closed, s) : p.cand[0];
-      if (S < 1) return fail(SJD_EHIP);
-      it = g_plan.emplace(std::make_tuple(p.kind, p.N, p.K), S).first;
+      const Ctx::Plan best =
+          p.cand.size() > 1 ? tune_projection(x, p.kind, p.cand, p.closed, p.cls ? 64 : 32, s) : p.cand[0];
+      if (best.S < 1) return fail(SJD_EHIP);
+      it = g_plan.emplace(key, best).first;
       tuned = true;
     }
-    *p.S = it->second;
+    x.plan[p.cls][p.kind] = it->second;
   }
   if (tuned) {
     bool okz = hipMemsetAsync(x.x, 0, (size_t)Mp * d * sizeof(float), s) == hipSuccess;
@@ -756,8 +801,16 @@ extern "C" int sjd_forward_window(sjd_ctx* h, float* d_logits, void* stream) {
 extern "C" int sjd_get_plan(const sjd_ctx* h, int32_t* splits, int32_t n) {
   if (!h || !splits || n < 1) return SJD_EINVAL;
   const Ctx& x = h->x;
-  const int32_t v[5] = {x.S_qkv, x.S_o, x.S_gu, x.S_dn, x.S_head};
-  for (int i = 0; i < n && i < 5; ++i) splits[i] = v[i];
+  int32_t v[20];
+  for (int cls = 0; cls < 2; ++cls) {
+    for (int k = 0; k < 4; ++k) {
+      v[10 * cls + k] = x.plan[cls][k].S;
+      v[10 * cls + 5 + k] = x.plan[cls][k].wide ? 8 : 4;
+    }
+    v[10 * cls + 4] = 1;  // LM head: unsplit, 8 column blocks per workgroup
+    v[10 * cls + 9] = 8;
+  }
+  for (int i = 0; i < n && i < 20; ++i) splits[i] = v[i];
   return SJD_OK;
 }
 

@@ -36,9 +36,13 @@ struct GemmArgs {
   // u + cfg_w (c - u) with c = product row m, u = product row 32 + m
   int cfg_rows;
   float cfg_w;
+  // 8 column blocks per workgroup (else 4): half the activation loads per
+  // weight byte; the grid is N / 256 column groups x S
+  int wide;
 };
 
-int gemm_splits(int N, int K, int target_wgs);
+// splits for about target_wgs workgroups of 4 (or, wide, 8) column blocks
+int gemm_splits(int N, int K, int target_wgs, bool wide);
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 
 // Repacks rows [row0, row0 + N) of a row-major [*][K] bf16 (or fp32, then

@@ -7,11 +7,14 @@
 //  - weights are pre-tiled (see forward.h): a wave reads one 32-row x 64-k
 //    tile per k-step as four contiguous 1 KB loads, the next k-step in flight,
 //    and the column blocks' tiles of a k-step form one contiguous stripe;
-//  - the activation tile of a k-step (32 rows x 64 k, hi and lo planes, 8 KB)
-//    is staged once per workgroup into LDS (double buffered) and shared by
-//    the four waves, each of which owns a different 32-column block. Loading
-//    A per wave from L2 instead costs twice the weight bytes again and halves
-//    the achieved weight bandwidth;
+//  - the activation tile of a k-step (32 rows x 64 k, hi and lo planes, 8 KB
+//    per 32 rows) is staged once per workgroup into LDS (double buffered) and
+//    shared by its NW waves (4 or 8), each of which owns a different
+//    32-column block. Loading A per wave from L2 instead costs twice the
+//    weight bytes again and halves the achieved weight bandwidth; eight
+//    column blocks per workgroup halve the activation loads per weight byte
+//    again, which 64-row windows need most (their QKV, gate/up and LM-head
+//    GEMMs ran 17-27% faster);
 //  - the contraction index is permuted identically in A and W (any
 //    permutation of k leaves the sum unchanged), so both operands load as
 //    16-byte chunks straight into the MFMA register layout;
@@ -34,8 +37,9 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGB = 256;
-constexpr int kGWaves = kGB / kWave;
+// column blocks (= waves) per workgroup: 4, or 8 when GemmArgs::wide
+constexpr int kGWaves = 4;
+constexpr int kGWavesWide = 8;
 // k-steps held per wave (the current one plus one in flight): deeper rings
 // help a lone workgroup but lose once every compute unit holds several
 constexpr int kRingDepth = 2;
@@ -75,16 +79,16 @@ SJD_DEV void gemm_tile_of(int id, int groups, int splits, int& group, int& split
   group = lin % groups;
 }
 
-template <int kRing, int MT>
-__global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
+template <int kRing, int MT, int NW>
+__global__ __launch_bounds__(NW * kWave) void k_gemm(GemmArgs g) {
   __shared__ GemmSmem<MT> sm;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
   const int r32 = lane & 31, half = lane >> 5;
   const int T = g.K / 64, nblk = g.N / 32;
-  const int groups = (nblk + kGWaves - 1) / kGWaves;
+  const int groups = (nblk + NW - 1) / NW;
   int group, sp;
   gemm_tile_of((int)blockIdx.x, groups, g.S, group, sp);
-  const int nb = group * kGWaves + wave;  // this wave's 32-column block
+  const int nb = group * NW + wave;  // this wave's 32-column block
   const bool active = nb < nblk;
   const int st0 = (int)((long)T * sp / g.S), st1 = (int)((long)T * (sp + 1) / g.S);
   const int n = st1 - st0;
@@ -101,20 +105,30 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
     for (int c = 0; c < kSsRegs; ++c) ssv[c] = ssr[c < g.ss_n ? c : 0];
 
   // element (row mt*32 + r32, k = kb*64 + half*32 + i*8 + e) of a tile sits
-  // in chunk i of lane r32 + 32*half of row tile mt; wave w stages chunk w
+  // in chunk i of lane r32 + 32*half of row tile mt. The 8 MT staged chunks
+  // of a k-step (plane, row tile, chunk) are numbered q = (plane MT + mt) 4
+  // + chunk, and wave w stages q = w, w + NW, ...
+  constexpr int NS = 8 * MT / NW;  // chunks staged per wave
+  static_assert(NS >= 1 && NS * NW == 8 * MT, "staging split");
   const uint16_t* wp = g.W + (size_t)(active ? nb : 0) * 2048 + (size_t)lane * 8;
   const size_t wstep = (size_t)nblk * 2048;  // next k-step of the same column block
-  const size_t aofs = (size_t)r32 * g.lda + half * 32 + wave * 8;
-  const size_t tstride = (size_t)32 * g.lda;  // next row tile
-  const uint16_t* sap = g.A + aofs;
-  const uint16_t* salp = g.A_lo + aofs;
+  const uint16_t* sap[NS];
+  int s_pl[NS], s_mt[NS], s_ch[NS];
+#pragma unroll
+  for (int j = 0; j < NS; ++j) {
+    const int q = wave + NW * j;
+    s_ch[j] = q & 3;
+    s_mt[j] = (q >> 2) % MT;
+    s_pl[j] = (q >> 2) / MT;
+    sap[j] = (s_pl[j] ? g.A_lo : g.A) + (size_t)(s_mt[j] * 32 + r32) * g.lda + half * 32 + s_ch[j] * 8;
+  }
 
   f32x16 acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
-  u32x4 w[kRing][4], ra[kRing][MT], ral[kRing][MT];
+  u32x4 w[kRing][4], ra[kRing][NS];
   // step t of this workgroup's range, clamped to the last real step
   auto kstep = [&](int t) { return st0 + (t < n ? t : n - 1); };
   // steps past the range read 4 KB of the (cache-resident, finite) A plane
@@ -123,10 +137,7 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   auto issue = [&](int t, int slot) {
     const int st = kstep(t);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      ra[slot][mt] = *(const u32x4*)(sap + mt * tstride + st * 64);
-      ral[slot][mt] = *(const u32x4*)(salp + mt * tstride + st * 64);
-    }
+    for (int j = 0; j < NS; ++j) ra[slot][j] = *(const u32x4*)(sap[j] + st * 64);
     const uint16_t* src = t < n ? wp + (size_t)st * wstep : wpad;
 #pragma unroll
     for (int i = 0; i < 4; ++i) w[slot][i] = __builtin_nontemporal_load((const u32x4*)(src + i * 512));
@@ -134,10 +145,7 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
   auto stage = [&](int t, int slot, int buf) {
     const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      sm.a[buf][0][mt][wave][lane] = t < n ? ra[slot][mt] : z;
-      sm.a[buf][1][mt][wave][lane] = t < n ? ral[slot][mt] : z;
-    }
+    for (int j = 0; j < NS; ++j) sm.a[buf][s_pl[j]][s_mt[j]][s_ch[j]][lane] = t < n ? ra[slot][j] : z;
   };
 
   if (n > 0) {
@@ -199,8 +207,9 @@ __global__ __launch_bounds__(kGB) void k_gemm(GemmArgs g) {
 // (an uneven split leaves a tail of workgroups one step longer); among them
 // the one whose workgroup count is nearest the target (by ratio), if within
 // a factor of two, else ceil(0.8 target / groups).
-int gemm_splits(int N, int K, int target_wgs) {
-  const int groups = (N / 32 + kGWaves - 1) / kGWaves;
+int gemm_splits(int N, int K, int target_wgs, bool wide) {
+  const int nw = wide ? kGWavesWide : kGWaves;
+  const int groups = (N / 32 + nw - 1) / nw;
   const int T = K / 64;
   int smax = T / 2 > 0 ? T / 2 : 1;  // at least two k-steps per workgroup
   if (smax > kGemmMaxSplits) smax = kGemmMaxSplits;
@@ -227,15 +236,19 @@ int gemm_splits(int N, int K, int target_wgs) {
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M < 1 || g.M > 64 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
   if (g.cfg_rows < 0 || g.cfg_rows > 32 || (g.cfg_rows > 0 && g.M < 32 + g.cfg_rows)) return hipErrorInvalidValue;
-  const dim3 grid((unsigned)(((g.N / 32 + kGWaves - 1) / kGWaves) * g.S));
+  const int nw = g.wide ? kGWavesWide : kGWaves;
+  const dim3 grid((unsigned)(((g.N / 32 + nw - 1) / nw) * g.S)), block((unsigned)(nw * kWave));
   // at one workgroup per compute unit or fewer nothing else hides a
   // workgroup's load latency: keep more weight tiles in flight
   const bool lone = grid.x <= 256;
-  if (g.M <= 32) {
-    if (lone) hipLaunchKernelGGL((k_gemm<kRingDeep, 1>), grid, dim3(kGB), 0, s, g);
-    else hipLaunchKernelGGL((k_gemm<kRingDepth, 1>), grid, dim3(kGB), 0, s, g);
+  if (g.wide) {
+    if (g.M <= 32) hipLaunchKernelGGL((k_gemm<kRingDepth, 1, kGWavesWide>), grid, block, 0, s, g);
+    else hipLaunchKernelGGL((k_gemm<kRingDepth, 2, kGWavesWide>), grid, block, 0, s, g);
+  } else if (g.M <= 32) {
+    if (lone) hipLaunchKernelGGL((k_gemm<kRingDeep, 1, kGWaves>), grid, block, 0, s, g);
+    else hipLaunchKernelGGL((k_gemm<kRingDepth, 1, kGWaves>), grid, block, 0, s, g);
   } else {
-    hipLaunchKernelGGL((k_gemm<kRingDepth, 2>), grid, dim3(kGB), 0, s, g);
+    hipLaunchKernelGGL((k_gemm<kRingDepth, 2, kGWaves>), grid, block, 0, s, g);
   }
   return hipGetLastError();
 }

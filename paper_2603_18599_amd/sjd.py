@@ -174,11 +174,18 @@ class Engine:
         _check("sjd_prefill", load_library().sjd_prefill(self.h, _ptr(prompt), prompt.numel(), seed,
                                                           _stream(stream)))
 
-    def plan(self):
-        """Split-K plan [qkv, o, gate|up, down, head] chosen at init."""
-        out = (C.c_int32 * 5)()
-        _check("sjd_get_plan", load_library().sjd_get_plan(self.h, out, 5))
-        return list(out)
+    def plan(self, rows64=False):
+        """GEMM plan chosen at init for windows of up to 32 rows (or, rows64,
+        of more): splits [qkv, o, gate|up, down, head] followed by the column
+        blocks per workgroup of each."""
+        out = (C.c_int32 * 20)()
+        _check("sjd_get_plan", load_library().sjd_get_plan(self.h, out, 20))
+        return list(out)[10:] if rows64 else list(out)[:10]
+
+    def plan_pin(self):
+        """The plan for windows of up to 32 rows as an SJD_SPLITS value."""
+        p = self.plan()
+        return ",".join(f"{p[i]}:{p[5 + i]}" for i in range(4))
 
     def prefill_image(self, image, prompt, seed, stream=None):
         """Batched contexts: (re)starts image `image` with `prompt`."""

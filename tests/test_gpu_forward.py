@@ -62,16 +62,42 @@ def test_window_forward_matches_oracle(orc, name, over):
     assert err <= TOL, err
 
 
-@pytest.mark.parametrize("plan", ["1,1,1,1", "7,3,5,11", "32,32,2,32"])
+@pytest.mark.parametrize("plan", ["1,1,1,1", "7,3,5,11", "32,32,2,32", "7:8,3,5:8,11:8", "1:8,32:8,2:8,32:8"])
 def test_window_forward_under_pinned_split_plans(orc, monkeypatch, plan):
-    """The split-K plan is chosen at init (timed, or pinned by SJD_SPLITS);
+    """The GEMM plan is chosen at init (timed, or pinned by SJD_SPLITS);
     the forward must match the oracle under any plan, including uneven
-    splits of the K range and the extremes (no split, 32 partial planes)."""
+    splits of the K range, the extremes (no split, more splits than k-steps)
+    and 8 column blocks per workgroup (":8")."""
     cfg = model_config("mid", n_layers=2)
     w, prompt = setup(cfg, wseed=13, pseed=14, device="cuda")
     monkeypatch.setenv("SJD_SPLITS", plan)
     eng = make_engine(cfg, weights_device(w))
-    assert eng.plan()[:4] == [int(v) for v in plan.split(",")]
+    entries = [e.split(":") for e in plan.split(",")]
+    assert eng.plan()[:4] == [int(e[0]) for e in entries]
+    assert eng.plan()[5:9] == [int(e[1]) if len(e) > 1 else 4 for e in entries]
+    eng.prefill(prompt.cuda(), 5)
+    logits = torch.empty(cfg["L"], cfg["V"], dtype=torch.float32, device="cuda")
+    eng.forward_window(logits)
+    torch.cuda.synchronize()
+    got = logits.cpu().numpy()
+    eng.close()
+    ref = oracle_first_window(orc, cfg, weights_numpy(w), prompt.numpy().astype(np.int32), 5)
+    err = np.abs(got - ref).max()
+    print(f"plan {plan}: max |logit error| = {err:.3e}", flush=True)
+    assert np.isfinite(got).all()
+    assert err <= TOL, err
+
+
+@pytest.mark.parametrize("plan", ["3:8,2:8,2:8,3:8", "1:8,1,3:8,1:8"])
+def test_window_forward_wide_groups_with_idle_waves(orc, monkeypatch, plan):
+    """8 column blocks per workgroup on a model whose projections are not
+    whole groups of 8 blocks (QKV 18 blocks, O and down 6, gate|up 24):
+    the waves past the last block stage their share of the activation
+    tile, take part in every barrier and store nothing."""
+    cfg = model_config("tiny", d_model=192, n_heads=3, n_kv_heads=3, head_dim=64, ffn_dim=384)
+    w, prompt = setup(cfg, wseed=15, pseed=16, device="cuda")
+    monkeypatch.setenv("SJD_SPLITS", plan)
+    eng = make_engine(cfg, weights_device(w))
     eng.prefill(prompt.cuda(), 5)
     logits = torch.empty(cfg["L"], cfg["V"], dtype=torch.float32, device="cuda")
     eng.forward_window(logits)
