@@ -224,9 +224,11 @@ std::mutex g_plan_mu;
 // (projection, N, K, row class) -> plan
 std::map<std::tuple<int, int, int, int>, Ctx::Plan> g_plan;
 
-// candidate plans: 4 and 8 column blocks per workgroup, one to three
-// workgroups per compute unit, at least two k-steps per workgroup, plus
-// the closed-form choice
+// candidate plans: 4 and 8 column blocks per workgroup, three quarters to
+// three workgroups per compute unit (a grid just short of one per unit
+// leaves a few idle but none doubled up: the 7B QKV projection ran fastest
+// at 5 splits of 48 eight-block groups, 240 workgroups), at least two
+// k-steps per workgroup, plus the closed-form choice
 std::vector<Ctx::Plan> plan_candidates(int N, int K, int ncu, Ctx::Plan fallback) {
   const int T = K / 64;
   std::vector<Ctx::Plan> out;
@@ -236,7 +238,7 @@ std::vector<Ctx::Plan> plan_candidates(int N, int K, int ncu, Ctx::Plan fallback
     for (int S = 1; S <= sjd::kGemmMaxSplits; ++S) {
       if (S > 1 && T / S < 2) break;
       const long wg = (long)groups * S;
-      if (wg >= ncu && wg <= 3L * ncu) out.push_back(Ctx::Plan{S, wide});
+      if (4 * wg >= 3L * ncu && wg <= 3L * ncu) out.push_back(Ctx::Plan{S, wide});
     }
   }
   bool has = false;
