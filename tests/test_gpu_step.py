@@ -113,13 +113,12 @@ def test_greedy_window_equals_autoregressive_128_dim_heads(shape):
 def test_greedy_window_equals_autoregressive_full_size(monkeypatch, name, n_prompt):
     """The benchmark's models at their benchmark cache lengths and launch
     configuration (7B shape: 32 layers, vocab 65536, 1239 cached rows, 10
-    key chunks per head, the split plan 5 / 8 / 4 / 8 the benchmark
-    profiles; 8B GQA shape: 32 layers, 32768 sampled visual rows of a
-    184622-token vocabulary, 4158 cached rows): greedy window decoding
-    equals one-slot decoding token for token, a property that holds at any
-    size. Both engines run one pinned split plan, so their GEMMs sum in the
-    same order."""
-    monkeypatch.setenv("SJD_SPLITS", "5,8,4,8")
+    key chunks per head, the GEMM plan the benchmark profiles; 8B GQA shape:
+    32 layers, 32768 sampled visual rows of a 184622-token vocabulary, 4158
+    cached rows): greedy window decoding equals one-slot decoding token for
+    token, a property that holds at any size. Both engines run one pinned
+    plan, so their GEMMs sum in the same order."""
+    monkeypatch.setenv("SJD_SPLITS", "5:8,8,5:8,8")
     over = dict(n_prompt=n_prompt, n_gen=48)
     base = model_config(name, **over)
     w, prompt = setup(base, wseed=31, pseed=32, device="cuda")
