@@ -109,3 +109,16 @@ def test_window_forward_wide_groups_with_idle_waves(orc, monkeypatch, plan):
     print(f"plan {plan}: max |logit error| = {err:.3e}", flush=True)
     assert np.isfinite(got).all()
     assert err <= TOL, err
+
+
+@pytest.mark.parametrize("plan", ["5:6,8,4,8", "5,8,4", "0,8,4,8", "33,8,4,8", "5,8,4,8,", "5:,8,4,8", "a,8,4,8"])
+def test_malformed_plan_pins_are_rejected(monkeypatch, plan):
+    """SJD_SPLITS takes four entries S or S:blocks (1 <= S <= 32, blocks 4
+    or 8); anything else fails sjd_init with SJD_EINVAL before any launch."""
+    from paper_2603_18599_amd.sjd import SjdError
+    cfg = model_config("tiny", n_layers=1)
+    w, _ = setup(cfg, wseed=17, pseed=18)
+    monkeypatch.setenv("SJD_SPLITS", plan)
+    with pytest.raises(SjdError) as e:
+        make_engine(cfg, weights_device(w))
+    assert e.value.code == -1
