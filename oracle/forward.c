@@ -61,6 +61,14 @@ void orc_kv_move(orc_kv* kv, int src, int dst) {
   }
 }
 
+void orc_kv_row(const orc_kv* kv, int layer, int row, double* k, double* v) {
+  const orc_model_cfg* c = &kv->cfg;
+  size_t n = (size_t)c->n_kv_heads * c->head_dim;
+  size_t off = ((size_t)layer * c->max_seq + (size_t)row) * n;
+  memcpy(k, kv->k + off, n * sizeof(double));
+  memcpy(v, kv->v + off, n * sizeof(double));
+}
+
 static inline float bf16_to_f32(uint16_t h) {
   uint32_t u = (uint32_t)h << 16;
   float f;

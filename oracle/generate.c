@@ -65,8 +65,8 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
   uint64_t anc[64];
   int32_t* sib = (int32_t*)malloc(sizeof(int32_t) * (size_t)(D * Km1 + 1));
   int32_t* osib = (int32_t*)malloc(sizeof(int32_t) * (size_t)(D * Km1 + 1));
-  orc_kv* kv = cfg->mcfg ? orc_kv_new(cfg->mcfg) : NULL;
-  orc_kv* kvu = cfg_on ? orc_kv_new(cfg->mcfg) : NULL;          /* unconditional stream */
+  orc_kv* kv = cfg->mcfg ? (cfg->kv ? cfg->kv : orc_kv_new(cfg->mcfg)) : NULL;
+  orc_kv* kvu = cfg_on ? (cfg->kv_u ? cfg->kv_u : orc_kv_new(cfg->mcfg)) : NULL; /* unconditional stream */
   float* curu = cfg_on ? (float*)malloc(sizeof(float) * (size_t)L * V) : NULL;
   int32_t upos[64];
   int ret = -1;
@@ -157,6 +157,7 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
     io.cur = cur; io.draft = dr; io.draft_tok = spine; io.sib = sib; io.in_meta = meta;
     io.out_meta = ometa; io.out_tok = otok; io.out_next = onext; io.out_sib = osib;
     if (orc_verify(&c1, &io) != 0) goto done;
+    if (cfg->step_meta) memcpy(cfg->step_meta + (size_t)step * 8, ometa, sizeof(ometa));
     const int n_c = ometa[0], r = ometa[1], acc_k = ometa[5];
     if (kv && acc_k >= 2) orc_kv_move(kv, n + n_s + r * Km1 + (acc_k - 2), n + r + 1);
     if (cfg_on && acc_k >= 2) orc_kv_move(kvu, nu_c + n_s + r * Km1 + (acc_k - 2), nu_c + r + 1);
@@ -180,8 +181,8 @@ int orc_generate(const orc_gen_cfg* cfg, const int32_t* prompt, int32_t* out_tok
   ret = gen;
 done:
   free(hist); free(cur); free(prev); free(dr); free(ctx); free(sib); free(osib); free(curu);
-  orc_kv_free(kv);
-  orc_kv_free(kvu);
+  if (kv != cfg->kv) orc_kv_free(kv);
+  if (kvu != cfg->kv_u) orc_kv_free(kvu);
   return ret;
 }
 

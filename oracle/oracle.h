@@ -90,6 +90,10 @@ int orc_race_topn_ranked(const float* w, const int* rank, int V, int n, int excl
  * else the n smallest keys of each, out[trials][n]. */
 void orc_race_many(const float* w, int V, int n, uint64_t seed, uint32_t tag, uint32_t stage,
                    uint32_t row, uint32_t step, int trials, int* out);
+/* the same with the exponential of token x taken from element rank[x] (the
+ * ranked races above; rank may be NULL) */
+void orc_race_many_ranked(const float* w, const int* rank, int V, int n, uint64_t seed, uint32_t tag,
+                          uint32_t stage, uint32_t row, uint32_t step, int trials, int* out);
 
 /* ---------- one verification step over a batch of independent trials ------ */
 
@@ -159,6 +163,9 @@ orc_kv* orc_kv_new(const orc_model_cfg* cfg);
 void orc_kv_free(orc_kv* kv);
 /* Copy cache row src to row dst in every layer. */
 void orc_kv_move(orc_kv* kv, int src, int dst);
+/* Key and value row `row` of layer `layer` (Hkv*hd doubles each, rotary
+ * already applied to the key), for inspection by the tests. */
+void orc_kv_row(const orc_kv* kv, int layer, int row, double* k, double* v);
 
 /* M slots; slot a holds token tok[a] at position pos[a]; it attends to cache
  * rows [0, n) and to window slot b iff bit b of anc[a] is set (anc[a] must
@@ -199,6 +206,14 @@ typedef struct {
   float cfg_w;
   const int32_t* uncond;
   int32_t n_uncond;
+  /* optional, for inspection (NULL: unused): step_meta[max_steps][8]
+   * receives every step's verification out-meta; kv (and kv_u, the
+   * unconditional stream's) is a cache made by orc_kv_new that the driver
+   * uses instead of allocating its own, so that it holds the final cache
+   * when the generation returns */
+  int32_t* step_meta;
+  orc_kv* kv;
+  orc_kv* kv_u;
 } orc_gen_cfg;
 
 /* Generates up to n_gen tokens after prompt[0..n_prompt). out_tok receives

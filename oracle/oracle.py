@@ -45,7 +45,8 @@ class GenCfg(C.Structure):
     _fields_ = [("v", VerifyCfg), ("n_prompt", C.c_int32), ("n_gen", C.c_int32),
                 ("max_steps", C.c_int32), ("mcfg", C.c_void_p), ("w", C.c_void_p),
                 ("toy_V", C.c_int32), ("toy_salt", C.c_uint64),
-                ("cfg_w", C.c_float), ("uncond", C.c_void_p), ("n_uncond", C.c_int32)]
+                ("cfg_w", C.c_float), ("uncond", C.c_void_p), ("n_uncond", C.c_int32),
+                ("step_meta", C.c_void_p), ("kv", C.c_void_p), ("kv_u", C.c_void_p)]
 
 
 _lib = None
@@ -70,6 +71,13 @@ def lib():
             [C.c_uint32] * 5 + [C.c_void_p, C.c_void_p]
         _lib.orc_race_many.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_uint64] + [C.c_uint32] * 4 + \
             [C.c_int, C.c_void_p]
+        _lib.orc_race_many_ranked.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_uint64] + \
+            [C.c_uint32] * 4 + [C.c_int, C.c_void_p]
+        _lib.orc_race_ranked.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_uint64] + [C.c_uint32] * 5 + \
+            [C.c_void_p]
+        _lib.orc_race_topn_ranked.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_uint64] + \
+            [C.c_uint32] * 5 + [C.c_void_p, C.c_void_p]
+        _lib.orc_kv_row.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
         _lib.orc_verify.argtypes = [C.POINTER(VerifyCfg), C.POINTER(VerifyIO)]
         _lib.orc_kv_new.restype = C.c_void_p
         _lib.orc_kv_new.argtypes = [C.POINTER(ModelCfg)]
@@ -135,6 +143,35 @@ def race_many(w, n, trials, seed=0, tag=TAG_RES, stage=0, row=0, step=0):
     out = np.zeros((trials, max(n, 1)), np.int32)
     lib().orc_race_many(_p(w), w.size, n, seed, tag, stage, row, step, trials, _p(out))
     return out[:, 0] if n <= 1 else out
+
+
+def race_many_ranked(w, rank, n, trials, seed=0, tag=TAG_RES, stage=0, row=0, step=0):
+    """race_many with the exponential of token x taken from stream element
+    rank[x] (rank int32 [V], -1 for tokens that take no part)."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    rank = np.ascontiguousarray(rank, dtype=np.int32)
+    assert rank.size == w.size
+    out = np.zeros((trials, max(n, 1)), np.int32)
+    lib().orc_race_many_ranked(_p(w), _p(rank), w.size, n, seed, tag, stage, row, step, trials, _p(out))
+    return out[:, 0] if n <= 1 else out
+
+
+def race_ranked(w, rank, seed, tag, stage, row, trial, step):
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    rank = np.ascontiguousarray(rank, dtype=np.int32)
+    gap = np.zeros(1, np.float32)
+    x = lib().orc_race_ranked(_p(w), _p(rank), w.size, seed, tag, stage, row, trial, step, _p(gap))
+    return int(x), float(gap[0])
+
+
+def race_topn_ranked(w, rank, n, excl, seed, tag, stage, row, trial, step):
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    rank = np.ascontiguousarray(rank, dtype=np.int32)
+    out = np.zeros(max(n, 1), np.int32)
+    gap = np.zeros(1, np.float32)
+    lib().orc_race_topn_ranked(_p(w), _p(rank), w.size, n, excl, seed, tag, stage, row, trial, step, _p(out),
+                               _p(gap))
+    return out[:n], float(gap[0])
 
 
 def verify(cur, draft, draft_tok, in_meta, *, K, D, top_k, T=1.0, flags=AC | PD, seed=0, step=0,
@@ -213,14 +250,29 @@ def generate_many(cfg, prompt, runs, seed0):
     return out, steps, hist
 
 
-def generate(cfg, prompt):
+def generate(cfg, prompt, step_meta=False, model=None, model_u=None):
+    """One generation. With step_meta, also returns every step's out-meta
+    [steps, 8]; with model (and model_u for the unconditional stream of a
+    guided generation), the generation runs on that Model's cache, which then
+    holds the final cache."""
     prompt = np.ascontiguousarray(prompt, dtype=np.int32)
     out = np.zeros(cfg.n_gen + 2 * cfg.v.L + 2, np.int32)
     steps = np.zeros(1, np.int32)
     hist = np.zeros(cfg.v.L + 2, np.int64)
-    g = lib().orc_generate(C.byref(cfg), _p(prompt), _p(out), _p(steps), _p(hist))
+    sm = np.zeros((cfg.max_steps, 8), np.int32) if step_meta else None
+    cfg.step_meta = _p(sm)
+    cfg.kv = model.kv if model is not None else None
+    cfg.kv_u = model_u.kv if model_u is not None else None
+    try:
+        g = lib().orc_generate(C.byref(cfg), _p(prompt), _p(out), _p(steps), _p(hist))
+    finally:
+        cfg.step_meta = None
+        cfg.kv = None
+        cfg.kv_u = None
     if g < 0:
         raise RuntimeError("orc_generate failed")
+    if step_meta:
+        return out[:g], int(steps[0]), hist, sm[:int(steps[0])]
     return out[:g], int(steps[0]), hist
 
 
@@ -267,6 +319,14 @@ class Model:
 
     def kv_move(self, src, dst):
         lib().orc_kv_move(self.kv, src, dst)
+
+    def kv_row(self, layer, row):
+        """(key, value) of cache row `row` in layer `layer`, float64 [Hkv*hd] each."""
+        n = self.cfg.n_kv_heads * self.cfg.head_dim
+        k = np.zeros(n, np.float64)
+        v = np.zeros(n, np.float64)
+        lib().orc_kv_row(self.kv, layer, row, _p(k), _p(v))
+        return k, v
 
     def close(self):
         if self.kv:

@@ -136,9 +136,15 @@ int orc_race_topn_ranked(const float* w, const int* rank, int V, int n, int excl
 
 void orc_race_many(const float* w, int V, int n, uint64_t seed, uint32_t tag, uint32_t stage,
                    uint32_t row, uint32_t step, int trials, int* out) {
+  orc_race_many_ranked(w, NULL, V, n, seed, tag, stage, row, step, trials, out);
+}
+
+void orc_race_many_ranked(const float* w, const int* rank, int V, int n, uint64_t seed, uint32_t tag,
+                          uint32_t stage, uint32_t row, uint32_t step, int trials, int* out) {
 #pragma omp parallel for schedule(static)
   for (int b = 0; b < trials; ++b) {
-    if (n <= 1) out[b] = orc_race(w, V, seed, tag, stage, row, (uint32_t)b, step, NULL);
-    else orc_race_topn(w, V, n, -1, seed, tag, stage, row, (uint32_t)b, step, out + (size_t)b * n, NULL);
+    if (n <= 1) out[b] = orc_race_ranked(w, rank, V, seed, tag, stage, row, (uint32_t)b, step, NULL);
+    else orc_race_topn_ranked(w, rank, V, n, -1, seed, tag, stage, row, (uint32_t)b, step,
+                              out + (size_t)b * n, NULL);
   }
 }

@@ -18,3 +18,18 @@ def orc():
     from oracle import oracle as o
     o.lib()
     return o
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    """Reports the near-tie decisions of every GPU-vs-oracle verify comparison
+    (the parity bar excludes decisions within 1e-6 of a tie; they are
+    counted and printed here)."""
+    try:
+        import parity
+    except ImportError:
+        return
+    lines = parity.summary()
+    if lines:
+        terminalreporter.section("verify parity: near-tie report")
+        for l in lines:
+            terminalreporter.write_line(l)

@@ -2,21 +2,31 @@
 classes of the parity bar:
   (i)   accept near-tie   |u - ratio| < 1e-6,
   (ii)  race near-tie     relative gap of the two smallest keys < 1e-6,
-  (iii) ill-conditioned residual  r(x) / max(p, q) < 1e-6 at the winner.
+  (iii) ill-conditioned residual  r(x) / max(p, q) < 1e-6 at the winner,
+  (iv)  drafting near-tie relative gap of consecutive drafting keys < 1e-6.
 Any other difference in a sampled decision is a failure. Trials whose rows
 all agree must agree bit for bit in every output (meta, committed tokens,
-next window)."""
+next window).
+
+Every comparison is reported: how many decisions the oracle took within the
+tie band of each class, and how many of the differing rows each class
+explains. The records accumulate in RECORDS (printed at the end of the
+pytest session by conftest.py)."""
 import numpy as np
 
 TIE = 1e-6
+CLASSES = ("accept", "race", "drafting", "residual")  # oracle margin columns 0..3
+RECORDS = []
 
 
-def compare_verify(gpu, ref, *, K, D, report=None):
+def compare_verify(gpu, ref, *, K, D, report=None, label=""):
     """gpu/ref: dicts of numpy arrays with keys meta, tok, next, sib, rows;
-    ref also has margin. Returns (n_rows_mismatch, n_explained)."""
+    ref also has margin. Returns (n_rows_mismatch, n_explained); appends a
+    record with the per-class counts to RECORDS (and to report, if given)."""
     B, L = ref["tok"].shape
     row_bad = np.zeros((B, L), bool)
     explained = 0
+    expl_by = {c: 0 for c in CLASSES}
     unexplained = []
     gr, rr, mg = gpu["rows"], ref["rows"], ref["margin"]
     diff = (gr != rr).any(-1)
@@ -25,6 +35,7 @@ def compare_verify(gpu, ref, *, K, D, report=None):
         if m[0] < TIE or m[1] < TIE or m[3] < TIE:
             explained += 1
             row_bad[b, j] = True
+            expl_by[CLASSES[int(np.argmin([m[0], m[1], np.inf, m[3]]))]] += 1
         else:
             unexplained.append((int(b), int(j), gr[b, j].tolist(), rr[b, j].tolist(), m.tolist()))
     assert not unexplained, f"unexplained row mismatches (b, j, gpu, oracle, margins): {unexplained[:10]}"
@@ -43,6 +54,32 @@ def compare_verify(gpu, ref, *, K, D, report=None):
             gaps = [mg[b, n_c + d, 2] for d in range(Dn)]
             assert min(gaps) < TIE, f"sibling draw differs on trial {b} without a near-tie"
             explained += 1
+            expl_by["drafting"] += 1
+    near = {c: int((mg[..., i] < TIE).sum()) for i, c in enumerate(CLASSES)}
+    rec = dict(label=label, trials=int(B), rows=int(B * L), rows_mismatch=int(diff.sum()), explained=explained,
+               near_ties=near, explained_by=expl_by)
+    RECORDS.append(rec)
     if report is not None:
-        report.append(dict(rows_mismatch=int(diff.sum()), explained=explained, trials=B))
+        report.append(rec)
     return int(diff.sum()), explained
+
+
+def summary():
+    """One line per comparison plus the totals."""
+    if not RECORDS:
+        return []
+    lines = []
+    tot = {c: 0 for c in CLASSES}
+    tex = {c: 0 for c in CLASSES}
+    rows = mism = 0
+    for r in RECORDS:
+        rows += r["rows"]
+        mism += r["rows_mismatch"]
+        for c in CLASSES:
+            tot[c] += r["near_ties"][c]
+            tex[c] += r["explained_by"][c]
+        lines.append(f"{r['label'] or 'verify'}: {r['rows']} rows, {r['rows_mismatch']} differ "
+                     f"(explained: {r['explained_by']}); decisions within 1e-6 of a tie: {r['near_ties']}")
+    lines.append(f"total: {len(RECORDS)} comparisons, {rows} rows, {mism} rows differ, all explained "
+                 f"(by class {tex}); near-tie decisions by class {tot}")
+    return lines

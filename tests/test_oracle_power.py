@@ -14,6 +14,7 @@ import numpy as np
 import pytest
 
 import test_oracle_forward as tf
+import test_oracle_kv as tk
 import test_oracle_sequence as ts
 import test_oracle_verify as tv
 
@@ -88,6 +89,22 @@ PLANTS = {
                           "int vis = t < n || (t - n <= a);", forward_torch),
     # rotary sign slip
     "rope_sign": ("forward.c", "v[i] = a * cs - b * sn;", "v[i] = a * cs + b * sn;", forward_torch),
+    # accepted sibling's key/value row moved one row short (onto the last kept spine row)
+    "kv_move_dest_off_by_one": ("generate.c", "orc_kv_move(kv, n + n_s + r * Km1 + (acc_k - 2), n + r + 1);",
+                                "orc_kv_move(kv, n + n_s + r * Km1 + (acc_k - 2), n + r);",
+                                lambda o: tk.test_cache_equals_recompute_after_sibling_commits(o, 0, 1.0, 8, 3, 2)),
+    # the row of the neighbouring sibling moved instead of the accepted one
+    "kv_move_wrong_sibling": ("generate.c", "orc_kv_move(kv, n + n_s + r * Km1 + (acc_k - 2), n + r + 1);",
+                              "orc_kv_move(kv, n + n_s + r * Km1 + (acc_k - 2) + (acc_k == 2), n + r + 1);",
+                              lambda o: tk.test_cache_equals_recompute_after_sibling_commits(o, 0, 1.0, 8, 3, 2)),
+    # the unconditional stream's cache not backtracked
+    "kv_move_guided_missing": ("generate.c", "if (cfg_on && acc_k >= 2) orc_kv_move(",
+                               "if (0 && cfg_on && acc_k >= 2) orc_kv_move(",
+                               lambda o: tk.test_guided_caches_equal_recompute_after_sibling_commits(o)),
+    # a ranked race reads stream element x instead of the token's rank
+    "race_ignores_rank": ("rng.c", "const uint32_t e_idx = rank ? (uint32_t)rank[x] : (uint32_t)x;\n    float e = orc_exp1",
+                          "const uint32_t e_idx = (uint32_t)x;\n    float e = orc_exp1",
+                          lambda o: __import__("test_oracle_rng").test_ranked_race_is_the_race_over_the_compact_list(o)),
     # tie order of the top-k set reversed
     "topk_tie_order": ("verify.c", "return (x->idx > y->idx) - (x->idx < y->idx);",
                        "return (x->idx < y->idx) - (x->idx > y->idx);", lambda o: tv.test_topk_tie_order(o)),

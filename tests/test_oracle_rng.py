@@ -109,7 +109,7 @@ def _chi2_p(counts, probs):
                                [5e-3, 7.0, 0.25, 3.0, 1e-1], [0.0, 0.0, 2.0, 0.0, 0.0]])
 def test_race_winner_law(orc, w):
     w = np.array(w, np.float32)
-    n = 400_000
+    n = 1_000_000
     win = orc.race_many(w, 1, n, seed=77, tag=orc.TAG_RES, stage=1, row=3, step=5)
     counts = np.bincount(win, minlength=w.size).astype(float)
     p = w.astype(np.float64) / w.sum()
@@ -120,7 +120,7 @@ def test_race_topn_tuple_law(orc):
     """Ordered draws of 3 from 5 without replacement: P(c1,c2,c3) =
     w1/S * w2/(S-w1) * w3/(S-w1-w2) (successive sampling), 60 tuples."""
     w = np.array([0.05, 0.4, 0.15, 0.3, 0.1], np.float32)
-    n = 600_000
+    n = 1_000_000
     draws = orc.race_many(w, 3, n, seed=9, tag=orc.TAG_PD, stage=0, row=1, step=2)
     tuples = list(itertools.permutations(range(5), 3))
     index = {t: i for i, t in enumerate(tuples)}
@@ -136,6 +136,70 @@ def test_race_topn_tuple_law(orc):
     probs = np.array([wd[a] / S * wd[b] / (S - wd[a]) * wd[c] / (S - wd[a] - wd[b]) for a, b, c in tuples])
     assert abs(probs.sum() - 1) < 1e-12
     assert _chi2_p(counts, probs) > 1e-4
+
+
+# Ranked races: the verification step draws one stream element per kept
+# (top-k) token, element rank[x] for token x, its position among the kept
+# tokens in index order. The ranks are a bijection from the kept tokens onto
+# elements 0 .. k-1, all independent uniforms, so the laws must be the
+# unranked ones; pinned here with a non-identity rank (a kept subset of a
+# larger vocabulary).
+KEPT = np.array([2, 3, 7, 8, 11, 15])
+
+
+def _ranked(weights, V=16):
+    w = np.zeros(V, np.float32)
+    w[KEPT[:len(weights)]] = weights
+    rank = np.full(V, -1, np.int32)
+    rank[KEPT[:len(weights)]] = np.arange(len(weights))
+    return w, rank
+
+
+def test_ranked_race_winner_law(orc):
+    w, rank = _ranked([0.3, 1.2, 0.05, 2.0, 0.7, 0.4])
+    n = 1_000_000
+    win = orc.race_many_ranked(w, rank, 1, n, seed=31, tag=orc.TAG_RES, stage=2, row=5, step=9)
+    counts = np.bincount(win, minlength=w.size).astype(float)
+    assert _chi2_p(counts, w.astype(np.float64) / w.sum()) > 1e-4
+
+
+def test_ranked_race_topn_tuple_law(orc):
+    """Ordered draws of 3 from the 5 kept tokens without replacement
+    (successive sampling), 60 tuples."""
+    w, rank = _ranked([0.05, 0.4, 0.15, 0.3, 0.1])
+    kept = KEPT[:5]
+    n = 1_000_000
+    draws = orc.race_many_ranked(w, rank, 3, n, seed=12, tag=orc.TAG_PD, stage=0, row=4, step=3)
+    pos = np.full(w.size, -1)
+    pos[kept] = np.arange(5)
+    d = pos[draws]
+    assert (d >= 0).all()
+    tuples = list(itertools.permutations(range(5), 3))
+    lut = np.full(125, -1)
+    for i, t in enumerate(tuples):
+        lut[t[0] * 25 + t[1] * 5 + t[2]] = i
+    ids = lut[d[:, 0] * 25 + d[:, 1] * 5 + d[:, 2]]
+    assert (ids >= 0).all()
+    counts = np.bincount(ids, minlength=len(tuples)).astype(float)
+    wd = w[kept].astype(np.float64)
+    S = wd.sum()
+    probs = np.array([wd[a] / S * wd[b] / (S - wd[a]) * wd[c] / (S - wd[a] - wd[b]) for a, b, c in tuples])
+    assert _chi2_p(counts, probs) > 1e-4
+
+
+def test_ranked_race_is_the_race_over_the_compact_list(orc):
+    """Element rank[x] of the stream for token x: the ranked race over the
+    vocabulary picks the token the plain race over the compacted kept list
+    picks (same keys), and the ranked draws without replacement exclude a
+    token by vocabulary id."""
+    w, rank = _ranked([0.3, 1.2, 0.05, 2.0, 0.7, 0.4])
+    wc = w[KEPT]
+    for trial in range(200):
+        x, g1 = orc.race_ranked(w, rank, 5, orc.TAG_BONUS, 1, 2, trial, 7)
+        y, g2 = orc.race(wc, 5, orc.TAG_BONUS, 1, 2, trial, 7)
+        assert x == KEPT[y] and g1 == g2
+        top, _ = orc.race_topn_ranked(w, rank, 3, int(KEPT[1]), 5, orc.TAG_PD, 0, 2, trial, 7)
+        assert KEPT[1] not in top.tolist() and len(set(top.tolist())) == 3
 
 
 def test_race_topn_exclusion_and_padding(orc):

@@ -69,20 +69,20 @@ MODES = {"sjd": 0, "ac": 1, "pd": 2, "ac+pd": 3}
 @pytest.mark.parametrize("mode", sorted(MODES))
 @pytest.mark.parametrize("L,K,D", [(1, 1, 0), (2, 2, 1), (3, 2, 1), (4, 2, 2), (4, 3, 1), (5, 2, 2), (6, 3, 2)])
 def test_sequence_law_equals_autoregressive(orc, mode, L, K, D):
-    pval, steps, hist = check_law(orc, L=L, K=K, D=D, flags=MODES[mode], runs=200_000)
+    pval, steps, hist = check_law(orc, L=L, K=K, D=D, flags=MODES[mode], runs=1_000_000)
     assert pval > 1e-4, pval
     if L == 1:
         assert (steps == 5).all()
 
 
 def test_sequence_law_larger_vocab_topk_temperature(orc):
-    pval, _, _ = check_law(orc, L=4, K=3, D=1, flags=3, runs=400_000, N=4, V=4, salt=11, top_k=3, T=0.8)
+    pval, _, _ = check_law(orc, L=4, K=3, D=1, flags=3, runs=1_000_000, N=4, V=4, salt=11, top_k=3, T=0.8)
     assert pval > 1e-4, pval
 
 
 def test_sequence_law_with_forced_row_ends(orc):
     # rows of 2 image tokens followed by the row-end token 2 (inside the vocab)
-    pval, _, _ = check_law(orc, L=4, K=2, D=2, flags=3, runs=300_000, N=6, V=3, salt=5, row_len=2, eol=2)
+    pval, _, _ = check_law(orc, L=4, K=2, D=2, flags=3, runs=1_000_000, N=6, V=3, salt=5, row_len=2, eol=2)
     assert pval > 1e-4, pval
 
 

@@ -126,7 +126,7 @@ CASES = {
 @pytest.mark.parametrize("case", sorted(CASES))
 def test_single_draft_lossless_and_acceptance(orc, case):
     lp, lq = (a.astype(np.float32) for a in CASES[case])
-    n = 400_000
+    n = 1_000_000
     p, q, tok, acc, drafts = _single_row_case(orc, lp, lq, n, seed=sum(map(ord, case)))
     counts = np.bincount(tok, minlength=p.size)
     assert chi2_p(counts, p) > 1e-4
@@ -145,7 +145,7 @@ def test_single_draft_with_topk_and_temperature(orc):
     rng = np.random.default_rng(5)
     lp = (rng.standard_normal(8) * 2).astype(np.float32)
     lq = (lp + rng.standard_normal(8)).astype(np.float32)
-    n = 300_000
+    n = 1_000_000
     V = 8
     for top_k, T in [(4, 1.0), (5, 0.6)]:
         p = softmax_topk_np(lp, top_k, T)
@@ -166,7 +166,7 @@ def test_k_candidates_without_replacement_lossless(orc, K):
     lp = np.array([0.3, -1.0, 2.0, 0.1, 0.5, -0.2], np.float32)
     lq = np.array([1.0, 0.2, -0.5, 0.0, 1.5, -2.0], np.float32)
     p, q = softmax_topk_np(lp, 0), softmax_topk_np(lq, 0)
-    n = 400_000
+    n = 1_000_000
     cand = draw_without_replacement(rng, q, K, n)
     L = K  # one tree row (depth 0) plus K - 1 sibling rows
     cur = np.zeros((n, L, V), np.float32)
@@ -246,7 +246,7 @@ def test_single_slot_window_is_plain_ar(orc):
     """L = 1: one slot, no draft distribution, one committed token per step,
     drawn from p by the stage-0 race of that row."""
     rng = np.random.default_rng(8)
-    n, V = 200_000, 7
+    n, V = 1_000_000, 7
     lp = (rng.standard_normal(V) * 1.5).astype(np.float32)
     meta = np.tile(np.array([0, 0, 0, 0], np.int32), (n, 1))
     dummy = np.zeros((n, 1), np.int32)
@@ -255,7 +255,7 @@ def test_single_slot_window_is_plain_ar(orc):
     assert (out["meta"][:, 0] == 1).all()
     p = softmax_topk_np(lp, 0)
     assert chi2_p(np.bincount(out["tok"][:, 0], minlength=V), p) > 1e-4
-    for b in range(0, n, 20000):
+    for b in range(0, n, 50000):
         x, _ = orc.race(orc.topk_softmax(lp, 0), 21, orc.TAG_RES, 0, 0, b, 4)
         assert out["tok"][b, 0] == x
 
@@ -328,7 +328,7 @@ def test_vanilla_sjd_tail_is_fresh(orc):
     """AC off (Sec. 3.3): rows after the first rejection are redrawn from their
     target rows, independently of the old drafts."""
     rng = np.random.default_rng(14)
-    n, L, V = 200_000, 4, 5
+    n, L, V = 1_000_000, 4, 5
     lp = (rng.standard_normal((L, V)) * 1.5).astype(np.float32)
     lq = (lp + rng.standard_normal((L, V)) * 2.0).astype(np.float32)
     p = np.stack([softmax_topk_np(r, 0) for r in lp])
