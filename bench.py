@@ -57,6 +57,8 @@ def parse():
                          "unconditional stream in one window forward; 0 = unguided")
     ap.add_argument("--no-guided", action="store_true", help="skip the guided (CFG weight 3) section")
     ap.add_argument("--eager", action="store_true", help="enqueue every kernel directly (no captured graph)")
+    ap.add_argument("--tune", action="store_true",
+                    help="time candidate GEMM plans at init (SJD_TUNE) instead of the recorded / closed-form plan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -365,7 +367,8 @@ def bench_step(args):
     from paper_2603_18599_amd.sjd import Engine, SjdError
     from synth_inputs import image_history, model_config, model_weights, prompt_tokens
 
-    over = {"flags": {"sjd-pac": 3, "sjd": 0, "ac": 1, "pd": 2}[args.mode] | (4 if args.eager else 0)}
+    over = {"flags": {"sjd-pac": 3, "sjd": 0, "ac": 1, "pd": 2}[args.mode] | (4 if args.eager else 0)
+            | (16 if getattr(args, "tune", False) else 0)}
     if args.L > 0:
         over["L"] = args.L
     if args.K > 0:

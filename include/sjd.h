@@ -56,7 +56,9 @@ typedef enum {
   SJD_ENOMEM = -2,  /* device allocation failed                                 */
   SJD_EHIP = -3,    /* HIP runtime error                                        */
   SJD_ESTATE = -4,  /* call not valid in the context's state (e.g. cache full)  */
-  SJD_ENOTSUP = -5  /* valid request this build does not support                */
+  SJD_ENOTSUP = -5, /* valid request this build does not support                */
+  SJD_ENONFINITE = -6 /* SJD_CHECK_FINITE only: a logit is NaN or +inf; the
+                         verification was not enqueued                          */
 } sjd_status;
 
 /* flags */
@@ -68,10 +70,25 @@ typedef enum {
  * the statistics the previous step computed for that row (the results are
  * bitwise identical; for debugging and profiling) */
 #define SJD_EAGER 4u
-/* decoder contexts only: use the closed-form split-K plan instead of the
- * process-wide plan timed by the first context that meets each projection
- * shape (sjd_init then times a few GEMM + consumer pairs on layer 0) */
+/* decoder contexts only: the GEMM plan (how many workgroups share each
+ * projection's K range) sets the summation order and therefore the rounding
+ * of the logits. By default it is fixed: the plan recorded for the shape
+ * (the timed choice on MI355X for the shapes this library ships plans for),
+ * else a closed form, so that a seed gives the same tokens in every process.
+ * SJD_TUNE times candidate plans at sjd_init instead (the first context of a
+ * process that meets a projection shape times GEMM + consumer pairs; every
+ * later context of the process reuses its choice): possibly faster on other
+ * shapes, but the choice depends on timing, so two processes may round
+ * differently. SJD_NO_TUNE forces the closed form. */
 #define SJD_NO_TUNE 8u
+#define SJD_TUNE 16u
+/* debug: check every logits row a verification reads for NaN and +inf first
+ * (-inf marks an excluded token and is allowed). The call then synchronises
+ * its stream and returns SJD_ENONFINITE, with nothing verified and no state
+ * changed, if one is found. sjd_verify: in sjd_verify_params.flags;
+ * decoder contexts: in sjd_config.flags. */
+#define SJD_CHECK_FINITE 32u
+
 
 /* Returns a static string naming a status code. */
 SJD_API const char* sjd_status_str(int status);
@@ -112,7 +129,7 @@ typedef struct {
   int32_t top_k;      /* >= 0; the kept set (top_k, or V when top_k is 0 or >= V)
                          may hold at most 2048 tokens (SJD_ENOTSUP otherwise)    */
   float temperature;  /* > 0                                                      */
-  uint32_t flags;     /* SJD_AC | SJD_PD                                          */
+  uint32_t flags;     /* SJD_AC | SJD_PD, optionally | SJD_CHECK_FINITE             */
   uint64_t seed;
   uint32_t step;      /* counter word 3 of every random stream                   */
   int32_t vis_lo;     /* token id of logits entry 0                               */
@@ -140,8 +157,10 @@ typedef struct {
 } sjd_verify_io;
 
 /* Ownership: all buffers belong to the caller and must not overlap. The
- * library keeps a grow-only per-device scratch buffer for per-row records
- * (B * L * 48 bytes), allocated on first use. Errors: SJD_EINVAL for
+ * library keeps a grow-only scratch buffer for per-row records (B * L * 64
+ * bytes) per device and stream, allocated on first use: calls on different
+ * streams never share it, and growing it waits for the work its stream has
+ * queued. Errors: SJD_EINVAL for
  * out-of-range parameters, NULL required pointers or misaligned logits
  * (16-byte alignment), SJD_ENOMEM, SJD_EHIP. Drafts outside the support end
  * that row's candidate list (an invalid spine draft makes the row a plain
@@ -165,7 +184,8 @@ typedef struct {
   int32_t max_seq;       /* KV capacity in tokens (prompt + generated + L)             */
   int32_t L, K, D;       /* window slots (1..64), candidates per depth (1..8), depth   */
   uint32_t flags;        /* SJD_AC | SJD_PD (0 = vanilla SJD; Sec. 5.3's ablation),
-                            optionally | SJD_EAGER | SJD_NO_TUNE                         */
+                            optionally | SJD_EAGER | SJD_NO_TUNE | SJD_TUNE |
+                            SJD_CHECK_FINITE                                              */
   float rms_eps, rope_theta;
   int32_t eol_id, row_len;
   int32_t weights_f32;   /* 1: weights are fp32, 0: bf16                                */
@@ -203,10 +223,14 @@ typedef struct sjd_ctx sjd_ctx;
  * head_dim other than 64 or 128, or V > 65536. */
 SJD_API int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* stream, sjd_ctx** out);
 
-/* Starts a generation: writes the keys/values of d_prompt[0 .. n-2], makes
- * d_prompt[n-1] the pending token and fills the window with placeholders
- * (stream tag 6, step word 0xFFFFFFFF). n >= 1, n + L <= max_seq.
- * sjd_prefill is sjd_prefill_image for image 0. */
+/* Starts a generation (Sec. 3.3: the positions of the first window are
+ * initialised and appended before the first parallel forward): writes the
+ * keys/values of d_prompt[0 .. n-2], makes d_prompt[n-1] the pending token
+ * and fills the window with placeholders, uniform over the sampled range
+ * (stream tag 6, step word 0xFFFFFFFF) and carrying no draft distribution.
+ * n >= 1, n + L <= max_seq. Prompt ids should lie in [0, vocab_size); an id
+ * outside it is fed to the model as token vis_lo (nothing is read outside
+ * the embedding table). sjd_prefill is sjd_prefill_image for image 0. */
 SJD_API int sjd_prefill(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, uint64_t seed, void* stream);
 
 /* sjd_prefill for image `image` (0 .. batch-1) of a batched context; the
@@ -225,14 +249,34 @@ SJD_API int sjd_prefill_image(sjd_ctx* ctx, int32_t image, const int32_t* d_prom
 SJD_API int sjd_prefill_cfg(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, const int32_t* d_uncond,
                             int32_t n_u, uint64_t seed, void* stream);
 
-/* One SJD-PAC iteration (Alg. 1): window forward, verification, drafting,
- * KV commit. Outputs (device, may be NULL): d_out_meta[8] as in sjd_verify
- * plus word 7 = cached rows after the step; d_out_tok[L] committed tokens;
- * d_out_next[L] next spine drafts; a batched context writes one such block
- * per image ([batch][8], [batch][L], [batch][L]). SJD_ESTATE if a cache
- * cannot take another window (checked against a host-side upper bound). */
-SJD_API int sjd_step(sjd_ctx* ctx, float temperature, int32_t top_k, uint64_t seed, uint32_t step,
-             int32_t* d_out_meta, int32_t* d_out_tok, int32_t* d_out_next, void* stream);
+/* One SJD-PAC iteration (Alg. 1): takes the drafts X^{t-1} and their draft
+ * distributions P^{t-1}, runs the window forward, verification, drafting and
+ * KV commit, and returns the committed tokens and the next drafts X^t (whose
+ * distributions P^t the context keeps for the next step).
+ *  d_draft_tok: NULL = the context's own drafts (what the previous step or
+ *    the prefill left); otherwise [batch][L] vocabulary ids, row j's draft
+ *    (the window feeds the pending token and drafts 0 .. L-2; draft L-1 is
+ *    verified, not fed), as a plain chain without drafting siblings: the
+ *    same as sjd_set_drafts for every image followed by this step.
+ *  d_draft_logits: with caller drafts, NULL or [batch][L][V] logits over
+ *    [vis_lo, vis_lo + V), row j's draft distribution through this step's
+ *    temperature / top-k softmax; NULL gives the rows no draft distribution
+ *    (each row draws from its own target row, lossless whatever the drafts'
+ *    origin; the context's previous rows describe its own drafts, not the
+ *    caller's). Must be NULL when d_draft_tok is NULL.
+ *  L, V: the context's window slots and sampled range (0 = the context's;
+ *    any other value is SJD_EINVAL).
+ * Outputs (device, may be NULL): d_out_meta[8] as in sjd_verify plus word
+ * 7 = cached rows after the step; d_out_tok[L] committed tokens;
+ * d_out_next[L] next spine drafts (-1 past n_s'); a batched context writes
+ * one such block per image ([batch][8], [batch][L], [batch][L]).
+ * SJD_ESTATE if a cache cannot take another window (checked against a
+ * host-side upper bound). With SJD_CHECK_FINITE the call synchronises after
+ * the forward and returns SJD_ENONFINITE (state unchanged) if a logit of
+ * the window or of the draft rows is NaN or +inf. */
+SJD_API int sjd_step(sjd_ctx* ctx, const int32_t* d_draft_tok, const float* d_draft_logits, int32_t L, int32_t V,
+                     float temperature, int32_t top_k, uint64_t seed, uint32_t step, int32_t* d_out_meta,
+                     int32_t* d_out_tok, int32_t* d_out_next, void* stream);
 
 /* Replaces the drafts of image `image`'s next step with the caller's (the
  * problem statement's step takes the previous iteration's drafts X^{t-1}
@@ -247,7 +291,10 @@ SJD_API int sjd_step(sjd_ctx* ctx, float temperature, int32_t top_k, uint64_t se
  * sjd_step then verifies these drafts; its outputs, adaptive continuation,
  * drafting and KV commit are as usual, and the steps after it use the
  * context's own drafts again. Device pointers, read on `stream` (copied,
- * so the caller may reuse them once the stream passes this call).
+ * so the caller may reuse them once the stream passes this call). A draft
+ * outside [vis_lo, vis_lo + V) is verified as no draft (its row draws from
+ * p and counts as rejected); one outside [0, vocab_size) (e.g. the -1 that
+ * pads d_out_next) is fed to the model as token vis_lo.
  * SJD_ESTATE before the image is prefilled. */
 SJD_API int sjd_set_drafts(sjd_ctx* ctx, int32_t image, const int32_t* d_draft_tok, const float* d_draft_logits,
                            void* stream);

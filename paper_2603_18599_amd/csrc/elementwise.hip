@@ -6,10 +6,14 @@
 namespace sjd {
 
 // x[m][:] = E[tok[m]][:] (fp32 residual stream); d is a multiple of 64, so
-// every 8-element chunk is whole
-__global__ __launch_bounds__(256) void k_embed(const uint16_t* E, const Window* win, int d, float* x) {
+// every 8-element chunk is whole. Token ids come from callers (prompts,
+// drafts); an id outside [0, vocab) is read as token `fallback`, so no read
+// leaves the embedding table.
+__global__ __launch_bounds__(256) void k_embed(const uint16_t* E, const Window* win, int d, int vocab, int fallback,
+                                               float* x) {
   const int m = blockIdx.x;
-  const int t = win->tok[m];
+  int t = win->tok[m];
+  t = (t >= 0 && t < vocab) ? t : fallback;
   const uint4* row = (const uint4*)(E + (size_t)t * d);
   float4* xr = (float4*)(x + (size_t)m * d);
   for (int c = threadIdx.x; c < d / 8; c += blockDim.x) {
@@ -21,8 +25,10 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, const Window* 
   }
 }
 
-hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, float* x, hipStream_t s) {
-  hipLaunchKernelGGL(k_embed, dim3(M), dim3(256), 0, s, E, win, d, x);
+hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, int vocab, int fallback, float* x,
+                        hipStream_t s) {
+  if (fallback < 0 || fallback >= vocab) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_embed, dim3(M), dim3(256), 0, s, E, win, d, vocab, fallback, x);
   return hipGetLastError();
 }
 

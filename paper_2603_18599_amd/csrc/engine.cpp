@@ -70,6 +70,7 @@ struct Ctx {
   sjd::DevState* st = nullptr;
   sjd::Window* win = nullptr;
   int32_t* rec = nullptr;
+  int32_t* nonfinite = nullptr;  // SJD_CHECK_FINITE: count of NaN / +inf logits found
   // GEMM plan per projection (QKV, O, gate|up, down): split count and column
   // blocks per workgroup, for windows of <= 32 rows [0] and of more [1]
   // (two streams, L > 32, prefill windows); the LM head runs wide, unsplit
@@ -122,7 +123,7 @@ int check_config(const sjd_config* c) {
   if (c->L < 1 || c->L > 64 || c->K < 1 || c->K > 8 || c->D < 0 || (long)c->K * c->D > c->L) return SJD_EINVAL;
   if (c->V > 65536) return SJD_ENOTSUP;
   if (c->max_seq < c->L + 2) return SJD_EINVAL;
-  if (c->flags & ~(SJD_AC | SJD_PD | SJD_EAGER | SJD_NO_TUNE)) return SJD_EINVAL;
+  if (c->flags & ~(SJD_AC | SJD_PD | SJD_EAGER | SJD_NO_TUNE | SJD_TUNE | SJD_CHECK_FINITE)) return SJD_EINVAL;
   if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
   if (!std::isfinite(c->cfg_w)) return SJD_EINVAL;
   if (c->batch < 0) return SJD_EINVAL;
@@ -152,7 +153,7 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
   const sjd_config& c = x.c;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv;
-  HIPTRY(sjd::launch_embed(x.embed, x.win, M, d, x.x, s));
+  HIPTRY(sjd::launch_embed(x.embed, x.win, M, d, c.vocab_size, c.vis_lo, x.x, s));
   const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d, guplane = (size_t)x.Mpad * 2 * F;
   int pend = 0;  // partial planes of the last residual projection not yet added into x
   const Ctx::Plan* P = x.plan[M > 32 ? 1 : 0];
@@ -215,11 +216,40 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
 // How many workgroups share a projection's K range decides both the GEMM's
 // time and how many partial planes its consumer (RoPE, residual + RMSNorm,
 // SwiGLU) sums; the interaction is not smooth (measured on the 7B shape, the
-// step is 3% faster with 5 / 8 / 4 / 16 splits than with the closed-form
-// plan). So the first context of a process that meets a projection shape
-// times every candidate pair (GEMM + consumer) on its own weights at 32
-// rows and keeps the fastest for the process: every context of the process
-// uses the same plan, so their arithmetic agrees.
+// step is 3% faster with the timed plan than with the closed form). The
+// split count also sets the summation order, so the plan must not depend on
+// timing by default: a context takes the plan recorded for its shape (the
+// choice of the timed search below on MI355X, for the shapes listed), else
+// the closed form. With SJD_TUNE the first context of a process that meets a
+// projection shape times every candidate pair (GEMM + consumer) on its own
+// weights and keeps the fastest for the process: every context of the
+// process uses the same plan, so their arithmetic agrees.
+struct RecordedPlan {
+  int kind, N, K, cls, S, wide;
+};
+const RecordedPlan kRecordedPlans[] = {
+    // {projection (0 QKV, 1 O, 2 gate|up, 3 down), N, K, row class (0: windows
+    //  of <= 32 rows, 1: more), splits, 8 column blocks per workgroup}
+    // 7B shape (d 4096, 32 x 128 heads, FFN 11008)
+    {0, 12288, 4096, 0, 5, 1}, {1, 4096, 4096, 0, 8, 0}, {2, 22016, 4096, 0, 5, 1}, {3, 4096, 11008, 0, 8, 0},
+    {0, 12288, 4096, 1, 5, 1}, {1, 4096, 4096, 1, 8, 0}, {2, 22016, 4096, 1, 5, 1}, {3, 4096, 11008, 1, 15, 1},
+    // 8B GQA shape (d 4096, 32 / 8 x 128 heads, FFN 14336); its O projection is the 7B one
+    {0, 6144, 4096, 0, 5, 0}, {2, 28672, 4096, 0, 2, 1}, {3, 4096, 14336, 0, 8, 0},
+    {0, 6144, 4096, 1, 5, 0}, {2, 28672, 4096, 1, 2, 1}, {3, 4096, 14336, 1, 16, 1},
+    // mid shape (d 1024, 16 x 64 heads, FFN 2816)
+    {0, 3072, 1024, 0, 8, 0}, {1, 1024, 1024, 0, 8, 0}, {2, 5632, 1024, 0, 5, 0}, {3, 1024, 2816, 0, 22, 0},
+    {0, 3072, 1024, 1, 8, 0}, {2, 5632, 1024, 1, 5, 0},
+};
+
+bool recorded_plan(int kind, int N, int K, int cls, Ctx::Plan* out) {
+  for (const RecordedPlan& r : kRecordedPlans)
+    if (r.kind == kind && r.N == N && r.K == K && r.cls == cls) {
+      *out = Ctx::Plan{r.S, r.wide};
+      return true;
+    }
+  return false;
+}
+
 std::mutex g_plan_mu;
 // (projection, N, K, row class) -> plan
 std::map<std::tuple<int, int, int, int>, Ctx::Plan> g_plan;
@@ -468,7 +498,8 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       (rc = dalloc(x, &x.stats[0], (size_t)x.B * c.L)) || (rc = dalloc(x, &x.stats[1], (size_t)x.B * c.L)) ||
       (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * 64 * hd)) ||
       (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 128)) || (rc = dalloc(x, &x.st, x.B)) ||
-      (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)x.B * c.L * sjd::kRecInts)))
+      (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)x.B * c.L * sjd::kRecInts)) ||
+      (rc = dalloc(x, &x.nonfinite, 16)))
     return fail(rc);
   // split-K plan: the closed form aims for two to three workgroups per
   // compute unit; unless SJD_NO_TUNE, the process-wide tuned plan replaces it
@@ -520,13 +551,15 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
     }
     pinned = true;
   }
-  const bool tune = !(c.flags & SJD_NO_TUNE) && !pinned;
+  const bool tune = (c.flags & SJD_TUNE) && !(c.flags & SJD_NO_TUNE) && !pinned;
+  const bool recorded = !(c.flags & (SJD_TUNE | SJD_NO_TUNE));
   int smax[4] = {1, 1, 1, 1};
   {
     std::lock_guard<std::mutex> lk(g_plan_mu);
     for (Proj& p : projs) {
       Ctx::Plan& dst = x.plan[p.cls][p.kind];
       dst = pinned && p.cls == 0 ? pin[p.kind] : p.closed;
+      if (recorded && !(pinned && p.cls == 0)) recorded_plan(p.kind, p.N, p.K, p.cls, &dst);
       if (tune && (p.cls == 0 || step64)) {
         auto it = g_plan.find(std::make_tuple(p.kind, p.N, p.K, p.cls));
         if (it != g_plan.end()) {
@@ -727,18 +760,67 @@ namespace sjd {
 int check_verify_limits(int V, int top_k);
 }
 
-extern "C" int sjd_step(sjd_ctx* h, float temperature, int32_t top_k, uint64_t seed, uint32_t step,
-                        int32_t* d_out_meta, int32_t* d_out_tok, int32_t* d_out_next, void* stream) {
+namespace {
+
+// The caller's drafts for image `image`'s next step (sjd_set_drafts).
+int set_drafts(Ctx& x, int image, const int32_t* d_draft_tok, const float* d_draft_logits, hipStream_t s) {
+  const sjd_config& c = x.c;
+  HIPTRY(sjd::launch_set_drafts(x.st + image, d_draft_tok, c.L, d_draft_logits != nullptr, s));
+  if (d_draft_logits) {
+    // the next step reads its draft rows from the buffer the step before it
+    // wrote, at q_off = 0; the statistics cached with those rows no longer
+    // describe them
+    float* prev = x.logits[(x.steps + 1) & 1] + (size_t)image * 32 * c.V;
+    HIPTRY(hipMemcpyAsync(prev, d_draft_logits, (size_t)c.L * c.V * sizeof(float), hipMemcpyDeviceToDevice, s));
+    HIPTRY(hipMemsetAsync(x.stats[(x.steps + 1) & 1], 0, sizeof(sjd::RowStatsCache) * (size_t)x.B * c.L, s));
+  }
+  return SJD_OK;
+}
+
+// SJD_CHECK_FINITE: counts NaN / +inf among n floats at p (synchronises s);
+// *bad receives whether any was found.
+int check_finite(Ctx& x, const float* p, size_t n, bool* bad, hipStream_t s) {
+  HIPTRY(sjd::launch_count_nonfinite(p, n, x.nonfinite, true, s));
+  int32_t h = 0;
+  HIPTRY(hipMemcpyAsync(&h, x.nonfinite, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HIPTRY(hipStreamSynchronize(s));
+  *bad = h != 0;
+  return SJD_OK;
+}
+
+}  // namespace
+
+extern "C" int sjd_step(sjd_ctx* h, const int32_t* d_draft_tok, const float* d_draft_logits, int32_t L, int32_t V,
+                        float temperature, int32_t top_k, uint64_t seed, uint32_t step, int32_t* d_out_meta,
+                        int32_t* d_out_tok, int32_t* d_out_next, void* stream) {
   if (!h || !(temperature > 0.0f) || top_k < 0) return SJD_EINVAL;
+  if ((L != 0 && L != h->x.c.L) || (V != 0 && V != h->x.c.V)) return SJD_EINVAL;
+  if (!d_draft_tok && d_draft_logits) return SJD_EINVAL;
   TRY(sjd::check_verify_limits(h->x.c.V, top_k));
   Ctx& x = h->x;
   if (!all_prefilled(x)) return SJD_ESTATE;
   TRY(cache_check(x));
   hipStream_t s = (hipStream_t)stream;
   const sjd_config& c = x.c;
+  const bool check = (c.flags & SJD_CHECK_FINITE) != 0;
+  if (d_draft_tok) {
+    if (check && d_draft_logits) {
+      bool bad = false;
+      TRY(check_finite(x, d_draft_logits, (size_t)x.B * c.L * c.V, &bad, s));
+      if (bad) return SJD_ENONFINITE;
+    }
+    for (int b = 0; b < x.B; ++b)
+      TRY(set_drafts(x, b, d_draft_tok + (size_t)b * c.L,
+                     d_draft_logits ? d_draft_logits + (size_t)b * c.L * c.V : nullptr, s));
+  }
   float* cur = x.logits[x.steps & 1];
   float* prev = x.logits[(x.steps + 1) & 1];
   TRY(step_forward(x, (int)(x.steps & 1), cur, s));
+  if (check) {
+    bool bad = false;
+    TRY(check_finite(x, cur, (size_t)logit_rows(x) * c.V, &bad, s));
+    if (bad) return SJD_ENONFINITE;
+  }
   // image b: logits rows from 32 b (batch), decoder state x.st[b], Philox trial b
   const int sstate = (int)(sizeof(sjd::DevState) / sizeof(int32_t));
   const long long lstride = x.B == 2 ? 32LL * c.V : 0;
@@ -775,18 +857,7 @@ extern "C" int sjd_set_drafts(sjd_ctx* h, int32_t image, const int32_t* d_draft_
   Ctx& x = h->x;
   if (image < 0 || image >= x.B) return SJD_EINVAL;
   if (!(x.prefilled & (1u << image))) return SJD_ESTATE;
-  hipStream_t s = (hipStream_t)stream;
-  const sjd_config& c = x.c;
-  HIPTRY(sjd::launch_set_drafts(x.st + image, d_draft_tok, c.L, d_draft_logits != nullptr, s));
-  if (d_draft_logits) {
-    // the next step reads its draft rows from the buffer the step before it
-    // wrote, at q_off = 0; the statistics cached with those rows no longer
-    // describe them
-    float* prev = x.logits[(x.steps + 1) & 1] + (size_t)image * 32 * c.V;
-    HIPTRY(hipMemcpyAsync(prev, d_draft_logits, (size_t)c.L * c.V * sizeof(float), hipMemcpyDeviceToDevice, s));
-    HIPTRY(hipMemsetAsync(x.stats[(x.steps + 1) & 1], 0, sizeof(sjd::RowStatsCache) * (size_t)x.B * c.L, s));
-  }
-  return SJD_OK;
+  return set_drafts(x, image, d_draft_tok, d_draft_logits, (hipStream_t)stream);
 }
 
 extern "C" int sjd_forward_window(sjd_ctx* h, float* d_logits, void* stream) {

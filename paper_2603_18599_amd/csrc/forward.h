@@ -140,7 +140,9 @@ constexpr int kAttnChunk = 128;  // keys per workgroup (4 waves x 32)
 hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s);
 
 // elementwise kernels
-hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, float* x, hipStream_t s);
+// ids outside [0, vocab) are read as token fallback (in [0, vocab))
+hipError_t launch_embed(const uint16_t* E, const Window* win, int M, int d, int vocab, int fallback, float* x,
+                        hipStream_t s);
 // RMSNorm split in two: x += sum of S fp32 partial planes (fixed order; S
 // may be 0), y = x * g as hi / lo bf16 planes (row stride ldy) and the
 // sums of squares of x over 256-element chunks, ss[m][c] (c < norm_chunks(d));

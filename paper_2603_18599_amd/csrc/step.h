@@ -11,6 +11,8 @@ hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int 
 hipError_t launch_build_prefill(const int32_t* prompt, int start, int M, Window* w, hipStream_t s);
 // next window from caller drafts: chain of tok[0..L) (row j's draft), row j's
 // draft distribution from row j of the draft logits when has_q
+// adds the count of NaN / +inf entries of p[0 .. n) to *cnt (zeroed first when reset)
+hipError_t launch_count_nonfinite(const float* p, size_t n, int32_t* cnt, bool reset, hipStream_t s);
 hipError_t launch_set_drafts(DevState* st, const int32_t* tok, int L, bool has_q, hipStream_t s);
 // uncond: the unconditional prompt of a guided context (its last token is
 // that stream's first pending token), or NULL

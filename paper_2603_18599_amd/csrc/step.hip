@@ -167,6 +167,29 @@ __global__ void k_set_drafts(DevState* st, const int32_t* tok, int L, int has_q)
   }
 }
 
+// SJD_CHECK_FINITE: counts the NaN and +inf entries of p[0 .. n) into *cnt
+// (-inf marks an excluded token and is allowed).
+__global__ void k_zero1(int32_t* cnt) { *cnt = 0; }
+__global__ __launch_bounds__(256) void k_count_nonfinite(const float* p, size_t n, int32_t* cnt) {
+  int bad = 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const float v = p[i];
+    bad += (v != v) || (v == INFINITY);
+  }
+  const int tot = wave_sum_i(bad);
+  if ((threadIdx.x & (kWave - 1)) == 0 && tot) atomicAdd(cnt, tot);
+}
+
+hipError_t launch_count_nonfinite(const float* p, size_t n, int32_t* cnt, bool reset, hipStream_t s) {
+  if (reset) hipLaunchKernelGGL(k_zero1, dim3(1), dim3(1), 0, s, cnt);
+  if (n > 0) {
+    size_t blocks = (n + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(k_count_nonfinite, dim3((unsigned)blocks), dim3(256), 0, s, p, n, cnt);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_set_drafts(DevState* st, const int32_t* tok, int L, bool has_q, hipStream_t s) {
   if (L < 1 || L > 64) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_set_drafts, dim3(1), dim3(64), 0, s, st, tok, L, has_q ? 1 : 0);

@@ -15,8 +15,11 @@ SJD_AC = 1
 SJD_PD = 2
 SJD_EAGER = 4
 SJD_NO_TUNE = 8
+SJD_TUNE = 16
+SJD_CHECK_FINITE = 32
 
-_STATUS = {0: "SJD_OK", -1: "SJD_EINVAL", -2: "SJD_ENOMEM", -3: "SJD_EHIP", -4: "SJD_ESTATE", -5: "SJD_ENOTSUP"}
+_STATUS = {0: "SJD_OK", -1: "SJD_EINVAL", -2: "SJD_ENOMEM", -3: "SJD_EHIP", -4: "SJD_ESTATE", -5: "SJD_ENOTSUP",
+           -6: "SJD_ENONFINITE"}
 
 
 class SjdError(RuntimeError):
@@ -92,8 +95,8 @@ def load_library():
     lib.sjd_prefill_cfg.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_uint64,
                                     C.c_void_p]
     lib.sjd_step.restype = C.c_int
-    lib.sjd_step.argtypes = [C.c_void_p, C.c_float, C.c_int32, C.c_uint64, C.c_uint32, C.c_void_p, C.c_void_p,
-                             C.c_void_p, C.c_void_p]
+    lib.sjd_step.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_float, C.c_int32,
+                             C.c_uint64, C.c_uint32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.sjd_set_drafts.restype = C.c_int
     lib.sjd_set_drafts.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.sjd_forward_window.restype = C.c_int
@@ -203,9 +206,14 @@ class Engine:
         _check("sjd_set_drafts", load_library().sjd_set_drafts(self.h, image, _ptr(draft_tok), _ptr(draft_logits),
                                                                 _stream(stream)))
 
-    def step(self, temperature, top_k, seed, step, out_meta=None, out_tok=None, out_next=None, stream=None):
-        _check("sjd_step", load_library().sjd_step(self.h, temperature, top_k, seed, step, _ptr(out_meta),
-                                                    _ptr(out_tok), _ptr(out_next), _stream(stream)))
+    def step(self, temperature, top_k, seed, step, out_meta=None, out_tok=None, out_next=None, stream=None,
+             draft_tok=None, draft_logits=None):
+        """One iteration. draft_tok (int32 [batch, L] vocabulary ids) and
+        draft_logits (float32 [batch, L, V] or None) replace the context's
+        own drafts for this step (None: the context's)."""
+        _check("sjd_step", load_library().sjd_step(self.h, _ptr(draft_tok), _ptr(draft_logits), 0, 0, temperature,
+                                                    top_k, seed, step, _ptr(out_meta), _ptr(out_tok),
+                                                    _ptr(out_next), _stream(stream)))
 
     def forward_window(self, logits, stream=None):
         _check("sjd_forward_window", load_library().sjd_forward_window(self.h, _ptr(logits), _stream(stream)))

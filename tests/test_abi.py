@@ -42,7 +42,7 @@ def test_verify_rejects_bad_params_on_host():
     good = dict(B=1, L=4, V=16, K=2, D=1, top_k=0, temperature=1.0, flags=3, seed=0, step=0, vis_lo=0,
                 eol_id=-1, row_len=0)
     bad = [dict(B=0), dict(L=0), dict(L=65), dict(V=6), dict(K=0), dict(K=9), dict(D=3), dict(top_k=-1),
-           dict(temperature=0.0), dict(temperature=float("nan")), dict(flags=8)]
+           dict(temperature=0.0), dict(temperature=float("nan")), dict(flags=8), dict(flags=16)]
     io = sjd.VerifyIO()  # NULL pointers
     for b in bad:
         p = dict(good)

@@ -120,3 +120,115 @@ def test_set_drafts_rejects_bad_calls():
     with pytest.raises(sjd.SjdError):  # no such image
         eng.set_drafts(tok, image=1)
     eng.close()
+
+
+def test_step_draft_arguments_equal_set_drafts():
+    """sjd_step's draft arguments (the problem statement's X^{t-1}, P^{t-1})
+    do what sjd_set_drafts followed by sjd_step does, bit for bit, and the
+    step after them uses the context's own drafts again."""
+    cfg = model_config("tiny")
+    w, prompt = setup(cfg, wseed=81, pseed=82)
+    wd = weights_device(w)
+    L, V = cfg["L"], cfg["V"]
+    tok, q = drafts(cfg, 9, 1.0)
+    outs = []
+    for use_args in (False, True):
+        eng = make_engine(cfg, wd)
+        eng.prefill(prompt.cuda(), 6)
+        res = []
+        for t in range(3):
+            meta = torch.zeros(8, dtype=torch.int32, device="cuda")
+            tk = torch.zeros(L, dtype=torch.int32, device="cuda")
+            nx = torch.zeros(L, dtype=torch.int32, device="cuda")
+            if t == 1 and use_args:
+                eng.step(1.0, 0, 3, t, out_meta=meta, out_tok=tk, out_next=nx, draft_tok=tok.cuda(),
+                         draft_logits=q.cuda())
+            else:
+                if t == 1:
+                    eng.set_drafts(tok.cuda(), q.cuda())
+                eng.step(1.0, 0, 3, t, out_meta=meta, out_tok=tk, out_next=nx)
+            res.append((meta.cpu().numpy(), tk.cpu().numpy(), nx.cpu().numpy()))
+        eng.close()
+        outs.append(res)
+    for a, b in zip(*outs):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
+def test_out_of_range_drafts_are_fed_safely():
+    """Drafts outside the vocabulary (the -1 that pads a step's next-draft
+    output, or any id past the table) are fed to the model as token vis_lo
+    and verified as no draft: the step runs, and the committed prefix ends at
+    the first such row. A draft outside the sampled range but inside the
+    vocabulary is verified the same way."""
+    cfg = model_config("8b", n_layers=1, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn_dim=512,
+                       n_prompt=8, n_gen=400, row_len=0)
+    w, prompt = setup(cfg, wseed=91, pseed=92)
+    eng = make_engine(cfg, weights_device(w))
+    eng.prefill(prompt.cuda(), 1)
+    L, V, lo = cfg["L"], cfg["V"], cfg["vis_lo"]
+    meta = torch.zeros(8, dtype=torch.int32, device="cuda")
+    tk = torch.zeros(L, dtype=torch.int32, device="cuda")
+    nx = torch.zeros(L, dtype=torch.int32, device="cuda")
+    eng.step(1.0, 50, 1, 0, out_meta=meta, out_tok=tk, out_next=nx)
+    for t, bad in enumerate([-1, cfg["vocab_size"] + 5, 7, 2**31 - 1]):
+        d = nx.clone()
+        j = 3 + t
+        d[j] = bad
+        eng.step(1.0, 50, 1, 1 + t, out_meta=meta, out_tok=tk, out_next=nx, draft_tok=d,
+                 draft_logits=torch.randn(L, V, device="cuda"))
+        torch.cuda.synchronize()
+        m = meta.cpu().numpy()
+        n_c = int(m[0])
+        assert 1 <= n_c <= j + 1, (bad, m)
+        got = tk.cpu().numpy()[:n_c]
+        assert ((got >= lo) & (got < lo + V)).all()
+    # feeding a step's own padded next-draft output straight back
+    nx[L - 4:] = -1
+    eng.step(1.0, 50, 1, 9, out_meta=meta, out_tok=tk, out_next=nx, draft_tok=nx.clone())
+    torch.cuda.synchronize()
+    assert int(meta[0]) == 1  # without draft distributions only row 0 commits
+    eng.close()
+
+
+def test_check_finite_flag():
+    """SJD_CHECK_FINITE: a NaN or +inf logit makes the call return
+    SJD_ENONFINITE with nothing verified; clean inputs give the same results
+    as without the flag (-inf entries are allowed)."""
+    from synth_inputs import verify_inputs
+    B, L, V, K, D = 3, 16, 4096, 4, 3
+    inp = verify_inputs(B, L, V, top_k=100, seed=5, device="cuda")
+    inp["cur"][1, 2, 7] = -float("inf")
+    outs = []
+    for flags in (3, 3 | sjd.sjd.SJD_CHECK_FINITE):
+        out = verify_outputs(B, L, K, D)
+        sjd.sjd_verify(inp["cur"], inp["draft"], inp["draft_tok"], inp["meta"], out, K=K, D=D, top_k=100,
+                       flags=flags, seed=1, sib=inp["sib"])
+        torch.cuda.synchronize()
+        outs.append({k: v.cpu() for k, v in out.items()})
+    for k in outs[0]:
+        assert torch.equal(outs[0][k], outs[1][k])
+    for bad in (float("nan"), float("inf")):
+        cur = inp["cur"].clone()
+        cur[2, 5, 11] = bad
+        out = verify_outputs(B, L, K, D)
+        with pytest.raises(sjd.SjdError) as e:
+            sjd.sjd_verify(cur, inp["draft"], inp["draft_tok"], inp["meta"], out, K=K, D=D, top_k=100,
+                           flags=3 | sjd.sjd.SJD_CHECK_FINITE, seed=1, sib=inp["sib"])
+        assert e.value.code == -6
+    cfg = model_config("tiny", flags=3 | sjd.sjd.SJD_CHECK_FINITE)
+    w, prompt = setup(cfg, wseed=31, pseed=32)
+    eng = make_engine(cfg, weights_device(w))
+    eng.prefill(prompt.cuda(), 2)
+    meta = torch.zeros(8, dtype=torch.int32, device="cuda")
+    eng.step(1.0, 0, 2, 0, out_meta=meta)
+    n0 = int(meta[7])
+    q = torch.zeros(cfg["L"], cfg["V"], device="cuda")
+    q[4, 9] = float("nan")
+    with pytest.raises(sjd.SjdError) as e:
+        eng.step(1.0, 0, 2, 1, draft_tok=torch.zeros(cfg["L"], dtype=torch.int32, device="cuda"), draft_logits=q)
+    assert e.value.code == -6
+    eng.step(1.0, 0, 2, 1, out_meta=meta)
+    torch.cuda.synchronize()
+    assert int(meta[7]) == n0 + int(meta[0])
+    eng.close()

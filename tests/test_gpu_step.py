@@ -209,3 +209,67 @@ def test_graph_replay_equals_eager(kind, top_k, T):
         for b in range(m0.shape[0]):
             n_c = int(m0[b, 0])
             assert np.array_equal(t0[b, :n_c], t1[b, :n_c])
+
+
+def _oracle_spine_logits(orc, cfg, w_np, tokens, n, pending, spine):
+    """The oracle's logits of a window's spine rows over a cache recomputed
+    from tokens[0 .. n): slot 0 = pending at position n, slot i = spine[i-1]."""
+    from model_util import causal, oracle_model
+    m = oracle_model(orc, cfg, w_np)
+    try:
+        for s0 in range(0, n, 64):
+            M = min(64, n - s0)
+            m.forward(s0, tokens[s0:s0 + M], list(range(s0, s0 + M)), causal(M), logits=False)
+        toks = [int(pending)] + [int(t) for t in spine[:-1]]
+        return m.forward(n, toks, [n + i for i in range(len(toks))], causal(len(toks)))
+    finally:
+        m.close()
+
+
+def test_sibling_commit_moves_the_right_cache_row(orc):
+    """A step that accepts a drafted sibling commits it from its sibling slot
+    (Sec. 4.1) and moves that slot's key/value row to the committed prefix
+    ("KV cache update & backtracking", Tab. 4). Decode the tiny model with
+    sampling until steps accept siblings; after each such step the next
+    window's spine logits must equal the oracle's over a cache recomputed
+    from the prompt and the committed tokens (cache = recompute), within the
+    forward's 3e-2 bar. A wrong source or destination row leaves a stale
+    row in the cache that this comparison sees."""
+    cfg = model_config("tiny")
+    w, prompt = setup(cfg, wseed=11, pseed=12)
+    w_np = weights_numpy(w)
+    eng = make_engine(cfg, weights_device(w))
+    L, V = cfg["L"], cfg["V"]
+    meta = torch.zeros(8, dtype=torch.int32, device="cuda")
+    tok = torch.zeros(L, dtype=torch.int32, device="cuda")
+    nxt = torch.zeros(L, dtype=torch.int32, device="cuda")
+    logits = torch.empty(L, V, dtype=torch.float32, device="cuda")
+    seed = 5
+    eng.prefill(prompt.cuda(), seed)
+    hist = prompt.numpy().astype(np.int32).tolist()
+    checked, worst = 0, 0.0
+    try:
+        for step in range(400):
+            eng.step(1.0, 0, seed, step, out_meta=meta, out_tok=tok, out_next=nxt)
+            m, t, nx = meta.cpu().numpy(), tok.cpu().numpy(), nxt.cpu().numpy()
+            n_c = int(m[0])
+            hist.extend(t[:n_c].tolist())
+            if m[5] < 2:
+                continue
+            print(f"step {step}: sibling {int(m[5])} accepted at row {int(m[1])}, n_c {n_c}", flush=True)
+            n = int(m[7])
+            assert n == len(hist) - 1
+            eng.forward_window(logits)
+            torch.cuda.synchronize()
+            n_s = int(m[3])
+            ref = _oracle_spine_logits(orc, cfg, w_np, np.array(hist, np.int32), n, hist[-1], nx[:n_s])
+            err = float(np.abs(logits.cpu().numpy()[:n_s] - ref).max())
+            worst = max(worst, err)
+            assert err <= 3e-2, f"step {step}: window logits differ from a recomputed cache by {err}"
+            checked += 1
+            if checked == 4:
+                break
+    finally:
+        eng.close()
+    assert checked >= 1, "no step accepted a drafted sibling"
+    print(f"sibling commits checked: {checked}, max logit error {worst:.2e}")

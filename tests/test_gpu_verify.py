@@ -57,10 +57,11 @@ def orc_verify_trials(orc, sub, trial_ids, **kw):
     return {k: np.concatenate([o[k] for o in outs]) for k in outs[0]}
 
 
-def check(gpu, ref, K, D, want_p=True):
+def check(gpu, ref, K, D, want_p=True, label=None):
+    import os
     if want_p:
         assert np.abs(gpu["p"] - ref["p"]).max() <= 1e-5
-    return compare_verify(gpu, ref, K=K, D=D)
+    return compare_verify(gpu, ref, K=K, D=D, label=label or os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0])
 
 
 @pytest.mark.parametrize("V,top_k", [(1024, 0), (4096, 200), (16384, 2000), (65536, 2000)])
@@ -148,7 +149,7 @@ def test_verify_full_size_sampled(orc):
     sample = [0, 1, 77, 500, 1023, 1024, 2047, 2048, 3000, 4000, 4094, 4095]
     gpu, ref = run_both(orc, inp, K=c["K"], D=c["D"], top_k=c["top_k"], seed=99, step=5, want_p=False,
                         oracle_trials=sample)
-    compare_verify(gpu, ref, K=c["K"], D=c["D"])
+    compare_verify(gpu, ref, K=c["K"], D=c["D"], label="full-size 4096x32x16384, 12 sampled trials")
 
 
 def test_verify_full_size_accept_length_closed_form():
