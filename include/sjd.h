@@ -89,6 +89,9 @@ typedef enum {
  * decoder contexts: in sjd_config.flags. */
 #define SJD_CHECK_FINITE 32u
 
+/* Rows (B * L) sjd_verify_noalloc can take: its record scratch is a static
+ * device array of this many 64-byte records (8 MiB per device). */
+#define SJD_VERIFY_NOALLOC_MAX_ROWS 131072
 
 /* Returns a static string naming a status code. */
 SJD_API const char* sjd_status_str(int status);
@@ -170,6 +173,18 @@ typedef struct {
  * are left untouched (the meta lives in device memory, so this cannot be
  * reported as a status). */
 SJD_API int sjd_verify(const sjd_verify_params* params, const sjd_verify_io* io, void* stream);
+
+/* sjd_verify for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, kernels and results, but no allocation of any kind. The
+ * per-row records live in a static device array of
+ * SJD_VERIFY_NOALLOC_MAX_ROWS records, one per device for the life of the
+ * process; B * L above that limit returns SJD_EINVAL with nothing enqueued.
+ * Every call on a device shares that device's array, so calls that overlap
+ * on one device (other streams, other threads) race and must be ordered by
+ * the caller; a call leaves its records behind, and none of the next call's
+ * results depend on them. */
+SJD_API int sjd_verify_noalloc(const sjd_verify_params* params, const sjd_verify_io* io, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Decoder context: weights, KV cache and window state of one generation.

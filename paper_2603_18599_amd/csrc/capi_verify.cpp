@@ -141,3 +141,17 @@ extern "C" int sjd_verify(const sjd_verify_params* p, const sjd_verify_io* io, v
   }
   return enqueue_verify(p, io, (int32_t*)rec, (hipStream_t)stream);
 }
+
+extern "C" int sjd_verify_noalloc(const sjd_verify_params* p, const sjd_verify_io* io, void* stream) {
+  int st = check_verify_call(p, io);
+  if (st != SJD_OK) return st;
+  if ((long)p->B * p->L > SJD_VERIFY_NOALLOC_MAX_ROWS) return SJD_EINVAL;
+  int32_t* rec = nullptr;
+  if (sjd::noalloc_scratch(&rec) != hipSuccess) return SJD_EHIP;
+  if (p->flags & SJD_CHECK_FINITE) {
+    // the count word follows the largest record block
+    st = check_finite(p, io, rec + (size_t)SJD_VERIFY_NOALLOC_MAX_ROWS * sjd::kRecInts, (hipStream_t)stream);
+    if (st != SJD_OK) return st;
+  }
+  return enqueue_verify(p, io, rec, (hipStream_t)stream);
+}

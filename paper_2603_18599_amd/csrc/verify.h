@@ -63,4 +63,9 @@ struct FinalizeOut {
 
 hipError_t launch_verify(const VerifyArgs& a, const FinalizeOut& o, hipStream_t s);
 
+// Device address, on the current device, of the static record scratch of
+// sjd_verify_noalloc (SJD_VERIFY_NOALLOC_MAX_ROWS rows of kRecInts words);
+// looked up once per device.
+hipError_t noalloc_scratch(int32_t** out);
+
 }  // namespace sjd

@@ -27,7 +27,11 @@
 // Every decision is taken in fp32 with fp64 sums (the paper fixes no
 // precision); contraction into FMA is off in this file so each operation
 // rounds as IEEE specifies.
+#include <mutex>
+#include <vector>
+
 #include "device.h"
+#include "sjd.h"
 #include "verify.h"
 
 #pragma clang fp contract(off)
@@ -1476,6 +1480,32 @@ __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, Finaliz
     om[0] = n_c; om[1] = r; om[2] = Dn; om[3] = n_s2; om[4] = n_q2; om[5] = acc_k;
     om[6] = (int32_t)(g0 + n_c); om[7] = 0;
   }
+}
+
+// ------------------------------------------------------------ no-alloc scratch
+// The per-row records of sjd_verify_noalloc live in a static device array
+// (every device the library runs on holds its own copy until the process
+// ends). Host code never passes the array's name to a kernel: its device
+// address is looked up per device with hipGetSymbolAddress and kept.
+// (plus 64 words: the SJD_CHECK_FINITE count word follows the records)
+static __device__ __align__(256) int32_t scratch[(size_t)SJD_VERIFY_NOALLOC_MAX_ROWS * kRecInts + 64];
+
+hipError_t noalloc_scratch(int32_t** out) {
+  static std::mutex mu;
+  static std::vector<int32_t*> addr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  if ((int)addr.size() <= dev) addr.resize(dev + 1, nullptr);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = (int32_t*)p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 // ------------------------------------------------------------ launch

@@ -17,6 +17,7 @@ SJD_EAGER = 4
 SJD_NO_TUNE = 8
 SJD_TUNE = 16
 SJD_CHECK_FINITE = 32
+SJD_VERIFY_NOALLOC_MAX_ROWS = 131072
 
 _STATUS = {0: "SJD_OK", -1: "SJD_EINVAL", -2: "SJD_ENOMEM", -3: "SJD_EHIP", -4: "SJD_ESTATE", -5: "SJD_ENOTSUP",
            -6: "SJD_ENONFINITE"}
@@ -56,7 +57,7 @@ class Weights(C.Structure):
                 ("d_lm_head", C.c_void_p)]
 
 
-EXPORTS = ["sjd_status_str", "sjd_verify", "sjd_init", "sjd_prefill", "sjd_prefill_image", "sjd_prefill_cfg",
+EXPORTS = ["sjd_status_str", "sjd_verify", "sjd_verify_noalloc", "sjd_init", "sjd_prefill", "sjd_prefill_image", "sjd_prefill_cfg",
            "sjd_set_drafts", "sjd_step", "sjd_forward_window", "sjd_get_plan", "sjd_destroy"]
 
 _lib = None
@@ -83,6 +84,8 @@ def load_library():
     lib.sjd_status_str.argtypes = [C.c_int]
     lib.sjd_verify.restype = C.c_int
     lib.sjd_verify.argtypes = [C.POINTER(VerifyParams), C.POINTER(VerifyIO), C.c_void_p]
+    lib.sjd_verify_noalloc.restype = C.c_int
+    lib.sjd_verify_noalloc.argtypes = [C.POINTER(VerifyParams), C.POINTER(VerifyIO), C.c_void_p]
     lib.sjd_init.restype = C.c_int
     lib.sjd_init.argtypes = [C.POINTER(Config), C.POINTER(Weights), C.c_void_p, C.POINTER(C.c_void_p)]
     lib.sjd_prefill.restype = C.c_int
@@ -130,16 +133,19 @@ def _check(fn, rc):
 
 
 def sjd_verify(cur, draft, draft_tok, in_meta, out, *, K, D, top_k, temperature=1.0, flags=SJD_AC | SJD_PD,
-               seed=0, step=0, sib=None, vis_lo=0, eol_id=-1, row_len=0, out_rows=None, dbg_p=None, stream=None):
-    """Standalone verification (sjd_verify in include/sjd.h). cur/draft:
-    float32 [B,L,V] device tensors; draft_tok int32 [B,L]; in_meta int32
-    [B,4]; out: dict of int32 device tensors meta [B,8], tok [B,L], next
-    [B,L], sib [B,D,K-1]."""
+               seed=0, step=0, sib=None, vis_lo=0, eol_id=-1, row_len=0, out_rows=None, dbg_p=None, stream=None,
+               noalloc=False):
+    """Standalone verification (sjd_verify in include/sjd.h; noalloc:
+    sjd_verify_noalloc). cur/draft: float32 [B,L,V] device tensors; draft_tok
+    int32 [B,L]; in_meta int32 [B,4]; out: dict of int32 device tensors meta
+    [B,8], tok [B,L], next [B,L], sib [B,D,K-1]."""
     B, L, V = cur.shape
     p = VerifyParams(B, L, V, K, D, top_k, temperature, flags, seed, step, vis_lo, eol_id, row_len)
     io = VerifyIO(_ptr(cur), _ptr(draft), _ptr(draft_tok), _ptr(sib), _ptr(in_meta), _ptr(out["meta"]),
                   _ptr(out["tok"]), _ptr(out["next"]), _ptr(out["sib"]), _ptr(out_rows), _ptr(dbg_p))
-    _check("sjd_verify", load_library().sjd_verify(C.byref(p), C.byref(io), _stream(stream)))
+    lib = load_library()
+    fn = "sjd_verify_noalloc" if noalloc else "sjd_verify"
+    _check(fn, getattr(lib, fn)(C.byref(p), C.byref(io), _stream(stream)))
 
 
 def verify_outputs(B, L, K, D, device="cuda"):

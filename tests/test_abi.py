@@ -55,6 +55,23 @@ def test_verify_rejects_bad_params_on_host():
     assert lib.sjd_verify(None, None, None) == -1
 
 
+def test_noalloc_verify_rejects_rows_beyond_its_scratch_on_host():
+    """sjd_verify_noalloc takes at most SJD_VERIFY_NOALLOC_MAX_ROWS rows;
+    beyond that it returns SJD_EINVAL before any HIP call (the pointers
+    below are never dereferenced)."""
+    from paper_2603_18599_amd import sjd
+    lib = sjd.load_library()
+    hdr = open(os.path.join(ROOT, "include", "sjd.h")).read()
+    cap = int(re.search(r"#define SJD_VERIFY_NOALLOC_MAX_ROWS (\d+)", hdr).group(1))
+    assert cap == sjd.SJD_VERIFY_NOALLOC_MAX_ROWS
+    fake = 1 << 20  # 16-byte aligned, never read
+    io = sjd.VerifyIO(fake, fake, fake, None, fake, fake, fake, fake, fake, None, None)
+    L = 32
+    prm = sjd.VerifyParams(cap // L + 1, L, 16, 2, 1, 0, 1.0, 3, 0, 0, 0, -1, 0)
+    assert lib.sjd_verify_noalloc(C.byref(prm), C.byref(io), None) == -1
+    assert lib.sjd_verify_noalloc(None, None, None) == -1
+
+
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     from paper_2603_18599_amd import sjd
     monkeypatch.setattr(sjd, "_lib", None)
