@@ -9,8 +9,13 @@ Prints ONE JSON line. Workloads (synthetic, seeded; see synth_inputs.py):
            65536, bf16 random-init weights), generating a 48x48 image with
            row-end tokens after a 64-token random prompt; top-2000, T = 1,
            K = 4, D = 3. value = committed image tokens per second. The same
-           line carries the verify workload's numbers under "verify".
+           line carries the other workloads under "verify", "tiny", "mid" and
+           "8b" (each with its roofline fraction and oracle baseline), and
+           the 7B step with two images per step ("batch2") and with guidance
+           weight 3 ("guided").
   8b, mid, tiny: the other decoder shapes.
+  --sweep: ablation modes and the K/D/L grid on a small model (one JSON line
+           per configuration).
   verify : sjd_verify over 4096 independent windows of 32 rows x 16384 logits
            (current logits N(0, 2^2), draft = current + N(0, 0.5^2), drafts
            drawn from top-2000 softmax of the draft logits), one launch per
@@ -60,7 +65,11 @@ def parse():
     ap.add_argument("--tune", action="store_true",
                     help="time candidate GEMM plans at init (SJD_TUNE) instead of the recorded / closed-form plan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (trials); 0 = default")
+    ap.add_argument("--no-configs", action="store_true", help="skip the tiny, mid and 8b sections of the 7b line")
+    ap.add_argument("--sweep", action="store_true",
+                    help="ablation modes and K in 2..5 x D in 2..4 x L in {32, 64} on --workload (tiny or mid)")
+    ap.add_argument("--sweep-images", type=int, default=4, help="whole images generated per sweep configuration")
+    ap.add_argument("--cpu-sample", type=int, default=0, help="oracle sample size (verify windows); 0 = 1024")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 256 MiB device-to-device copy before the timed region (the reference kernel "
                          "of known size for HBM counter runs) and mark copy + timed region as the profiler's "
@@ -224,8 +233,56 @@ def cpu_cores():
         return os.cpu_count() or 1
 
 
-def bench_verify(args):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for l in fh:
+                if l.startswith("model name"):
+                    return l.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+class omp_threads:
+    """Sets the OpenMP thread count of the oracle's parallel regions (called
+    from this thread) for the duration of a with-block."""
+
+    def __init__(self, n):
+        import ctypes
+        self.n = n
+        self.gomp = None
+        for name in ("libgomp.so.1", "libgomp.so"):
+            try:
+                self.gomp = ctypes.CDLL(name)
+                break
+            except OSError:
+                continue
+
+    def __enter__(self):
+        if self.gomp is not None:
+            self.prev = self.gomp.omp_get_max_threads()
+            self.gomp.omp_set_num_threads(self.n)
+        return self
+
+    def __exit__(self, *a):
+        if self.gomp is not None:
+            self.gomp.omp_set_num_threads(self.prev)
+
+
+def all_threads():
+    return int(os.environ.get("OMP_NUM_THREADS", cpu_cores()))
+
+
+def nc_histogram(ncs, L):
+    """counts of the committed lengths 1 .. L (index 0 = n_c of 1)"""
     import numpy as np
+    h = np.bincount(np.asarray(ncs, dtype=np.int64).ravel(), minlength=L + 1)[1:L + 1]
+    return [int(v) for v in h]
+
+
+# ---------------------------------------------------------------------------- verify workload
+def bench_verify(args, cpu=True):
     import torch
 
     import paper_2603_18599_amd as sjd
@@ -241,9 +298,10 @@ def bench_verify(args):
     stream = torch.cuda.current_stream()
     seed = 7
 
-    def step(t):
+    def step(t, rows=None):
         sjd.sjd_verify(inp["cur"], inp["draft"], inp["draft_tok"], inp["meta"], out, K=K, D=D, top_k=top_k,
-                       temperature=c["temperature"], seed=seed, step=t, sib=inp["sib"], stream=stream)
+                       temperature=c["temperature"], seed=seed, step=t, sib=inp["sib"], stream=stream,
+                       out_rows=rows)
 
     for t in range(args.warmup):
         step(t)
@@ -252,42 +310,47 @@ def bench_verify(args):
         profiler_region(True)
         calibration_copy()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    nc_sum = torch.zeros((), dtype=torch.int64, device="cuda")
+    ncs = torch.zeros(args.steps, B, dtype=torch.int32, device="cuda")
     t0 = time.perf_counter()
     for t in range(args.steps):
         evs[t][0].record(stream)
         step(1000 + t)
         evs[t][1].record(stream)
-        nc_sum += out["meta"][:, 0].sum()
+        ncs[t].copy_(out["meta"][:, 0])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     if getattr(args, "calibrate_copy", False):
         profiler_region(False)
     kern_ms = [a.elapsed_time(b) for a, b in evs]
     avg_ms = sum(kern_ms) / len(kern_ms)
-    total_nc = int(nc_sum.item())
-    mean_nc = total_nc / (args.steps * B)
-    bytes_per_launch = 2.0 * B * L * V * 4  # current + draft logits, read once
+    nc = ncs.cpu().numpy()
+    total_nc = int(nc.sum())
+    bytes_per_launch = 2.0 * B * L * V * 4  # current + draft logits, each read once
     achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
-    ms_per_step = wall * 1e3 / args.steps
-    value = total_nc / wall
-
     res = dict(metric="image tokens/sec on 1 MI355X; mean accept length/step; verify HBM GB/s",
-               value=value, unit="image tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
-               ms_per_step=ms_per_step, higher_is_better=True, scaling="weak", vs_baseline=None, dtype="f32",
-               data="synthetic",
+               value=total_nc / wall, unit="image tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+               ms_per_step=wall * 1e3 / args.steps, higher_is_better=True, scaling="weak", vs_baseline=None,
+               dtype="f32", data="synthetic",
                config={"workload": f"verify: {B} windows x {L} rows x {V} logits, top-{top_k}, T=1, "
                                    f"chain drafts, K={K} D={D} drafting",
                        "global_batch": B, "seq_len": L},
-               mean_accept_length=mean_nc, verify_GBps=achieved,
+               mean_accept_length=total_nc / nc.size, nc_hist=nc_histogram(nc, L), verify_GBps=achieved,
                roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic("verify"),
                          "kernel": "k_verify_rows + k_verify_finalize", "bytes_per_launch": bytes_per_launch,
                          "avg_launch_ms": avg_ms})
     res["expected_accept_length"], res["expected_accept_length_over_drafts"] = chain_expected_nc(
         inp["cur"], inp["draft"], inp["draft_tok"], top_k, c["temperature"])
-    if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline_verify(args, inp, K, D, top_k, c["temperature"], seed, B, L)
+    if cpu and not args.no_cpu_baseline:
+        # the GPU's decisions of step 1000 on the sampled windows, for the
+        # parity report beside the oracle's timing
+        rows = torch.zeros(B, L, 2, dtype=torch.int32, device="cuda")
+        step(1000, rows)
+        torch.cuda.synchronize()
+        gpu = {k: v.cpu().numpy() for k, v in out.items()}
+        gpu["rows"] = rows.cpu().numpy()
+        res["cpu_baseline"], res["parity_sample"] = cpu_baseline_verify(args, inp, gpu, K, D, top_k,
+                                                                        c["temperature"], seed, B, L, V)
     return res
 
 
@@ -326,47 +389,86 @@ def chain_expected_nc(cur, draft, draft_tok, top_k, T, chunk=128):
     return given / B, over / B
 
 
-def cpu_baseline_verify(args, inp, K, D, top_k, T, seed, B, L):
-    """The oracle (plain C, OpenMP over trials) on a bounded sample of the same
-    windows, scaled to committed tokens per second."""
+def cpu_baseline_verify(args, inp, gpu, K, D, top_k, T, seed, B, L, V):
+    """The oracle (plain C, OpenMP over windows) on a bounded sample of the
+    same windows and step, on all host cores and on one core, scaled to
+    committed tokens per second; its decisions on the sample are compared
+    with the GPU's (near-tie report)."""
     import numpy as np
 
     from oracle import oracle as orc
-    n = args.cpu_sample or 2048
-    idx = np.arange(n)
+    from oracle.parity import compare_verify
+    n = args.cpu_sample or 1024
+    n1 = max(8, n // 16)
     cpu = {k: (v[:n].cpu().numpy() if v is not None else None) for k, v in inp.items()}
-    t0 = time.perf_counter()
-    r = orc.verify(cpu["cur"], cpu["draft"], cpu["draft_tok"], cpu["meta"], K=K, D=D, top_k=top_k, T=T, seed=seed,
-                   step=1000, sib=cpu["sib"])
-    dt = time.perf_counter() - t0
-    toks = int(r["meta"][:, 0].sum())
-    return {"value": toks / dt, "unit": "image tokens/s", "cores": int(os.environ.get("OMP_NUM_THREADS", cpu_cores())),
-            "kind": "oracle", "sample": f"{len(idx)} of {B} windows (one verification step), {dt:.1f} s"}
+
+    def run(m):
+        sub = {k: (v[:m] if v is not None else None) for k, v in cpu.items()}
+        t0 = time.perf_counter()
+        r = orc.verify(sub["cur"], sub["draft"], sub["draft_tok"], sub["meta"], K=K, D=D, top_k=top_k, T=T,
+                       seed=seed, step=1000, sib=sub["sib"])
+        return r, time.perf_counter() - t0
+
+    cores = all_threads()
+    with omp_threads(cores):
+        r, dt = run(n)
+    with omp_threads(1):
+        r1, dt1 = run(n1)
+    toks, toks1 = int(r["meta"][:, 0].sum()), int(r1["meta"][:, 0].sum())
+    rep = []
+    sub_gpu = {k: v[:n] for k, v in gpu.items()}
+    compare_verify(sub_gpu, r, K=K, D=D, report=rep, label=f"verify workload, first {n} windows")
+    base = {"value": toks / dt, "unit": "image tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n} of {B} windows (step 1000), {dt:.1f} s on {cores} threads ({cpu_model()}); "
+                      f"full {B}-window step extrapolated: {dt * B / n:.1f} s",
+            "one_thread": {"value": toks1 / dt1, "unit": "image tokens/s", "cores": 1,
+                           "sample": f"first {n1} windows, {dt1:.1f} s"},
+            "bytes_per_s": 2.0 * n * L * V * 4 / dt}
+    return base, rep[0]
 
 
+# ---------------------------------------------------------------------------- decoder step
 def step_bytes(cfg, n_mean, B=1, streams=None):
-    """Algorithmic HBM bytes of one step: every weight streamed once (bf16),
-    the LM head rows of the sampled range only, the cached keys and values
-    read once (hi/lo bf16 planes, 4 bytes per element), the window's K/V
-    written, and the logits written and read back by the verification; B
-    images share the weight stream, each has its own cache and logits
-    (n_mean: mean cached rows per image); a guided step has two streams
-    (two caches) and one image's logits."""
+    """Algorithmic HBM bytes of one step (the per-unit figures of the
+    method's byte model): every weight streamed once (bf16), the LM head
+    rows of the sampled range only; the cached keys and values read once in
+    bf16, 2 * layers * Hkv * hd * 2 bytes per cached row at the mean fill;
+    the logits written once and read once as current rows and once as draft
+    rows (3 * L * V * 4 bytes). B images share the weight stream, each with
+    its own cache and logits; a guided step has two streams (two caches) and
+    one image's logits. Returns (total, weights, kv, logits, kv_hilo): kv_hilo
+    is what the cache actually moves, two bf16 planes per element (the
+    precision design), reported beside the algorithmic figure."""
     d, H, Hkv, hd, F, V, L = (cfg[k] for k in ("d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim", "V", "L"))
     per_layer = (H * hd * d + 2 * Hkv * hd * d + d * H * hd + 3 * F * d) * 2
     weights = cfg["n_layers"] * per_layer + V * d * 2
-    kv = (streams or B) * cfg["n_layers"] * 2 * Hkv * hd * 4 * (n_mean + L)
-    logits = B * 2 * L * V * 4 * 2  # written once, current + draft rows read once
-    return weights + kv + logits, weights, kv
+    kv_row = cfg["n_layers"] * 2 * Hkv * hd * 2
+    kv = (streams or B) * kv_row * n_mean
+    logits = B * 3 * L * V * 4
+    return weights + kv + logits, weights, kv, logits, 2 * kv
 
 
-def bench_step(args):
-    import numpy as np
+def decoder_inputs(cfg, B, context, guided, device="cuda"):
     import torch
 
-    from paper_2603_18599_amd.sjd import Engine, SjdError
-    from synth_inputs import image_history, model_config, model_weights, prompt_tokens
+    from synth_inputs import image_history, prompt_tokens
+    prompts = []
+    for b in range(B):  # image b: its own prompt (and image so far)
+        p = prompt_tokens(cfg, 2 + 10 * b)
+        if context == "mid":
+            p = torch.cat([p, image_history(cfg, cfg["n_gen"] // 2, 3 + 10 * b)])
+        prompts.append(p.to(device))
+    uncond = None
+    if guided:  # the unconditional stream: its own prompt ids, the same image so far
+        u = prompt_tokens(cfg, 77)
+        if context == "mid":
+            u = torch.cat([u, image_history(cfg, cfg["n_gen"] // 2, 3)])
+        uncond = u.to(device)
+    return prompts, uncond
 
+
+def workload_config(args, workload=None):
+    from synth_inputs import model_config
     over = {"flags": {"sjd-pac": 3, "sjd": 0, "ac": 1, "pd": 2}[args.mode] | (4 if args.eager else 0)
             | (16 if getattr(args, "tune", False) else 0)}
     if args.L > 0:
@@ -377,29 +479,28 @@ def bench_step(args):
         over["D"] = args.D
     if args.mode in ("sjd", "ac") and args.K <= 0:
         over["K"], over["D"] = 1, 0  # no drafting tree without PD
-    B = args.batch
-    over["batch"] = B
-    guided = args.cfg_w != 0.0
-    if guided:
-        if B != 1:
+    over["batch"] = args.batch
+    if args.cfg_w != 0.0:
+        if args.batch != 1:
             raise SystemExit("guidance runs one image per step (--batch 1)")
         over["cfg_w"] = args.cfg_w
-    cfg = model_config(args.workload, **over)
+    return model_config(workload or args.workload, **over)
+
+
+def bench_step(args, cpu=True):
+    import numpy as np
+    import torch
+
+    from paper_2603_18599_amd.sjd import Engine, SjdError
+    from synth_inputs import model_weights
+
+    cfg = workload_config(args)
+    B = args.batch
+    guided = args.cfg_w != 0.0
     seed = 11
     w = model_weights(cfg, 1, device="cuda")
-    prompts = []
-    for b in range(B):  # image b: its own prompt (and image so far)
-        p = prompt_tokens(cfg, 2 + 10 * b)
-        if args.context == "mid":
-            p = torch.cat([p, image_history(cfg, cfg["n_gen"] // 2, 3 + 10 * b)])
-        prompts.append(p.cuda())
+    prompts, uncond = decoder_inputs(cfg, B, args.context, guided)
     prompt = prompts[0]
-    uncond = None
-    if guided:  # the unconditional stream: its own prompt ids, the same image so far
-        u = prompt_tokens(cfg, 77)
-        if args.context == "mid":
-            u = torch.cat([u, image_history(cfg, cfg["n_gen"] // 2, 3)])
-        uncond = u.cuda()
     eng = Engine(cfg, w)
     stream = torch.cuda.current_stream()
     K, W = args.steps, args.warmup
@@ -415,7 +516,7 @@ def bench_step(args):
     if not args.calibrate_copy:  # (counter runs: one prefill only, each dispatch is slow there)
         prefill_all(seed)
     torch.cuda.synchronize()
-    progress(f"model ready; prefill of {B} x {prompt.numel()} tokens")
+    progress(f"{args.workload}: model ready; prefill of {B} x {prompt.numel()} tokens")
     t_pre = time.perf_counter()
     prefill_all(seed)
     torch.cuda.synchronize()
@@ -433,11 +534,10 @@ def bench_step(args):
             prefill_all(seed + restarts)
             eng.step(cfg["temperature"], cfg["top_k"], seed, t, out_meta=metas[t], stream=stream)
 
-    progress("prefill done")
     for t in range(W):
         one(t)
     torch.cuda.synchronize()
-    progress("warmup done")
+    progress(f"{args.workload}: warmup done")
     if args.calibrate_copy:
         profiler_region(True)
         calibration_copy()
@@ -460,8 +560,9 @@ def bench_step(args):
     step_ms = [a.elapsed_time(b) for a, b in evs]
     avg_ms = float(np.mean(step_ms))
     n_mean = float(np.mean(ns - ncs))
-    total, weights, kv = step_bytes(cfg, n_mean, B, streams=2 if guided else None)
+    total, weights, kv, logit_b, kv_hilo = step_bytes(cfg, n_mean, B, streams=2 if guided else None)
     achieved = total / (avg_ms * 1e-3) / 1e9
+    moved = total - kv + kv_hilo
     res = dict(metric="image tokens/sec on 1 MI355X; mean accept length/step; verify HBM GB/s",
                value=float(ncs.sum()) / wall, unit="image tokens/s", n_gpus=1, steps=K, warmup=W,
                ms_per_step=wall * 1e3 / K, higher_is_better=True, scaling="weak", vs_baseline=None, dtype="bf16",
@@ -476,7 +577,7 @@ def bench_step(args):
                                    f"{cfg['n_prompt']}-token prompt, {cfg['n_gen']}-token image, "
                                    f"steps timed from KV length {prompt.numel() - 1}",
                        "global_batch": B, "seq_len": cfg["L"]},
-               mean_accept_length=float(ncs.mean()), step_latency_ms=avg_ms,
+               mean_accept_length=float(ncs.mean()), nc_hist=nc_histogram(ncs, cfg["L"]), step_latency_ms=avg_ms,
                step_latency_p50_ms=float(np.percentile(step_ms, 50)),
                step_latency_p99_ms=float(np.percentile(step_ms, 99)),
                prefill_ms=prefill_ms, kv_rows_mean=n_mean, image_restarts=restarts,
@@ -485,52 +586,173 @@ def bench_step(args):
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic(args.workload),
                          "kernel": "sjd_step (window forward + verification + KV commit)",
                          "bytes_per_launch": total, "weight_bytes": weights, "kv_bytes": kv,
-                         "avg_launch_ms": avg_ms,
-                         "mfma_tflops": 2.0 * weights / 2 * cfg["L"] * B / (avg_ms * 1e-3) / 1e12})
+                         "logit_bytes": logit_b, "avg_launch_ms": avg_ms,
+                         "bytes_moved_hilo_kv": moved,
+                         "frac_hilo_kv": moved / (avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                         "mfma_tflops": 2.0 * weights / 2 * cfg["L"] * B / (avg_ms * 1e-3) / 1e12,
+                         "mfma_frac": 2.0 * weights / 2 * cfg["L"] * B / (avg_ms * 1e-3) / 2.5e15})
     eng.close()
     del w
     torch.cuda.empty_cache()
-    if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline_step(args, cfg, seed)
+    if cpu and not args.no_cpu_baseline and B == 1 and not guided:
+        res["cpu_baseline"] = cpu_baseline_step(args, cfg, seed, n_mean, prompt)
     return res
 
 
-def cpu_baseline_step(args, cfg, seed):
-    """The oracle (plain C, fp64 accumulation, OpenMP) on one SJD-PAC step of
-    the same model at the same start: weights regenerated from the same seed,
-    prompt prefilled untimed, then the first window's forward + verification
-    timed. Scaled to committed tokens per second."""
+def cpu_baseline_step(args, cfg, seed, n_target, gpu_prompt):
+    """The oracle (plain C, fp64 accumulation, OpenMP over output rows and
+    heads) on the same model (weights regenerated from the same seed) and
+    the same kind of step (window forward + verification of the context's
+    window), on all host cores, plus a one-thread figure.
+
+    Small models (tiny, mid): the GPU line's context is prefilled (untimed)
+    and a few steps are timed at its cache length. Large models (7b, 8b): a
+    full prefill of the GPU line's ~1240 or ~4160 tokens would take minutes,
+    so one step is timed after a 64-token prefill and scaled by the step's
+    flop count to the GPU line's mean fill (only the attention grows with
+    it: +5% at 1240 rows on the 7B shape); labelled as extrapolated.
+    One thread: a one-layer slice (same shapes, same LM head) is timed on
+    one thread and on all threads; the ratio scales the all-thread step."""
     import numpy as np
     import torch
 
-    sys.path.insert(0, os.path.join(ROOT, "tests"))
-    from model_util import oracle_model, oracle_prefill, placeholders, weights_numpy
     from oracle import oracle as orc
-    from synth_inputs import model_weights, prompt_tokens
+    from oracle.harness import causal, oracle_model, oracle_prefill, placeholders, weights_numpy
+    from synth_inputs import model_weights
 
-    w = model_weights(cfg, 1, device="cuda")
+    w = model_weights(cfg, 1, device="cuda" if torch.cuda.is_available() else "cpu")
     w = dict(embed=w["embed"].cpu(), final_norm=w["final_norm"].cpu(), lm_head=w["lm_head"].cpu(),
              layers=[{k: v.cpu() for k, v in l.items()} for l in w["layers"]])
-    prompt = prompt_tokens(cfg, 2).numpy().astype(np.int32)
-    m = oracle_model(orc, cfg, weights_numpy(w))
-    n = oracle_prefill(m, prompt)
+    if torch.cuda.is_available():
+        torch.cuda.empty_cache()
+    w_np = weights_numpy(w)
     L, V = cfg["L"], cfg["V"]
     spine = placeholders(orc, cfg, seed)
-    t0 = time.perf_counter()
-    logits = m.forward(n, [int(prompt[-1])] + spine[:L - 1], [n + i for i in range(L)],
-                       [(1 << (a + 1)) - 1 for a in range(L)])
-    meta = np.array([[0, 0, 0, 0]], np.int32)
-    r = orc.verify(logits[None], logits[None], np.array([spine], np.int32), meta, K=cfg["K"], D=cfg["D"],
-                   top_k=cfg["top_k"], T=cfg["temperature"], flags=cfg.get("flags", 3), seed=seed, step=0,
-                   vis_lo=cfg["vis_lo"],
-                   eol_id=cfg["eol_id"], row_len=cfg["row_len"])
-    dt = time.perf_counter() - t0
-    m.close()
-    n_c = int(r["meta"][0, 0])
-    return {"value": n_c / dt, "unit": "image tokens/s", "cores": int(os.environ.get("OMP_NUM_THREADS", cpu_cores())),
-            "kind": "oracle",
-            "sample": f"first SJD-PAC step after a {cfg['n_prompt']}-token prefill (prefill untimed): "
-                      f"{L}-slot window forward + verification, {dt:.1f} s, n_c={n_c}"}
+    cores = all_threads()
+    large = cfg["d_model"] >= 4096
+
+    def one_step(m, n, pending):
+        t0 = time.perf_counter()
+        logits = m.forward(n, [int(pending)] + spine[:L - 1], [n + i for i in range(L)], causal(L))
+        meta = np.array([[0, 0, 0, 0]], np.int32)
+        r = orc.verify(logits[None], logits[None], np.array([spine], np.int32), meta, K=cfg["K"], D=cfg["D"],
+                       top_k=cfg["top_k"], T=cfg["temperature"], flags=cfg.get("flags", 3) & 3, seed=seed,
+                       step=0, vis_lo=cfg["vis_lo"], eol_id=cfg["eol_id"], row_len=cfg["row_len"])
+        return time.perf_counter() - t0, int(r["meta"][0, 0])
+
+    prompt = gpu_prompt.cpu().numpy().astype(np.int32)
+    with omp_threads(cores):
+        if large:
+            m = oracle_model(orc, cfg, w_np, max_seq=160)
+            n = oracle_prefill(m, prompt[:65])
+            t1, nc = one_step(m, n, prompt[n])
+            m.close()
+            nc = float(nc)
+
+            def flops(rows):
+                # GEMMs (every weight once per slot) + attention over the
+                # cached rows and the window
+                d, H, Hkv, hd, F = (cfg[k] for k in ("d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim"))
+                params = cfg["n_layers"] * (2 * H * hd * d + 2 * Hkv * hd * d + 3 * F * d) + V * d
+                return 2.0 * params * L + 4.0 * cfg["n_layers"] * H * hd * L * (rows + L / 2)
+
+            t_step = t1 * flops(n_target) / flops(n)
+            how = (f"one SJD-PAC step (32-slot window forward + verification) timed after a {n}-token prefill: "
+                   f"{t1:.1f} s on {cores} threads ({cpu_model()}); scaled by the step's flop count to the GPU "
+                   f"line's mean cache of {n_target:.0f} rows (only the attention grows with it): "
+                   f"{t_step:.1f} s per step (extrapolated)")
+        else:
+            m = oracle_model(orc, cfg, w_np)
+            n = oracle_prefill(m, prompt)
+            reps = 3 if cfg["d_model"] >= 1024 else 8
+            dts, ncs = [], []
+            for _ in range(reps):
+                dt, c = one_step(m, n, prompt[n])
+                dts.append(dt)
+                ncs.append(c)
+            m.close()
+            t_step = float(np.mean(dts))
+            nc = float(np.mean(ncs))
+            how = (f"{reps} SJD-PAC steps (window forward + verification) at the GPU line's cache of {n} rows, "
+                   f"{t_step:.2f} s per step on {cores} threads ({cpu_model()})")
+    # one thread: a one-layer slice of the same shapes (and the same LM
+    # head) over a 4-slot window, on one thread and on all of them
+    one = dict(cfg, n_layers=1)
+    w1 = dict(w_np, layers=w_np["layers"][:1])
+    times = {}
+    for th in (cores, 1):
+        with omp_threads(th):
+            m = oracle_model(orc, one, w1, max_seq=128)
+            oracle_prefill(m, prompt[:65])
+            t0 = time.perf_counter()
+            m.forward(64, [int(prompt[64])] + spine[:3], [64 + i for i in range(4)], causal(4))
+            times[th] = time.perf_counter() - t0
+            m.close()
+    ratio = times[1] / times[cores]
+    return {"value": nc / t_step, "unit": "image tokens/s", "cores": cores, "kind": "oracle", "sample": how,
+            "step_s": t_step,
+            "one_thread": {"value": nc / (t_step * ratio), "unit": "image tokens/s", "cores": 1,
+                           "sample": f"one-layer slice, 4-slot window forward: {times[1]:.2f} s on 1 thread vs "
+                                     f"{times[cores]:.2f} s on {cores}; the all-thread step scaled by that ratio "
+                                     f"({ratio:.1f}x, extrapolated)"}}
+
+
+# ---------------------------------------------------------------------------- sweep (ablation, K/D/L grid)
+def run_sweep(args):
+    """Ablation modes and the drafting tree / window grid (Tabs. 2-3 of the
+    paper) on a small model where random-init weights still accept tokens:
+    whole generations of the workload's image from its prompt, per
+    configuration: mean committed tokens per step, the n_c histogram and the
+    step time. One JSON line per configuration."""
+    import numpy as np
+    import torch
+
+    from paper_2603_18599_amd.sjd import Engine
+    from synth_inputs import model_config, model_weights, prompt_tokens
+
+    grid = []
+    for mode in ("sjd", "ac", "pd", "sjd-pac"):
+        grid.append((mode, 32, 4, 3))
+    for L in (32, 64):
+        for K in (2, 3, 4, 5):
+            for D in (2, 3, 4):
+                grid.append(("sjd-pac", L, K, D))
+    base = model_config(args.workload)
+    w = model_weights(base, 1, device="cuda")
+    prompt = prompt_tokens(base, 2).cuda()
+    for mode, L, K, D in grid:
+        flags = {"sjd-pac": 3, "sjd": 0, "ac": 1, "pd": 2}[mode]
+        if mode in ("sjd", "ac"):
+            K, D = 1, 0
+        if K * D > L:
+            continue
+        cfg = model_config(args.workload, L=L, K=K, D=D, flags=flags)
+        eng = Engine(cfg, w)
+        meta = torch.zeros(8, dtype=torch.int32, device="cuda")
+        ncs, ms = [], []
+        for img in range(args.sweep_images):
+            eng.prefill(prompt, 100 + img)
+            gen, t = 0, 0
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            while gen < cfg["n_gen"]:
+                ev0.record()
+                eng.step(cfg["temperature"], cfg["top_k"], 100 + img, t, out_meta=meta)
+                ev1.record()
+                torch.cuda.synchronize()
+                n_c = int(meta[0])
+                ncs.append(n_c)
+                ms.append(ev0.elapsed_time(ev1))
+                gen += n_c
+                t += 1
+        eng.close()
+        print(json.dumps({"workload": args.workload, "mode": mode, "L": L, "K": K, "D": D,
+                          "images": args.sweep_images, "steps": len(ncs), "mean_accept_length": float(np.mean(ncs)),
+                          "nc_hist": nc_histogram(ncs, L), "step_ms": float(np.median(ms))}), flush=True)
+
+
+def section(res, keys=("value", "unit", "ms_per_step", "mean_accept_length", "nc_hist", "step_latency_ms",
+                       "kv_rows_mean", "config", "roofline", "cpu_baseline")):
+    return {k: res[k] for k in keys if k in res}
 
 
 def main():
@@ -539,30 +761,37 @@ def main():
         traffic_from(args)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "this build runs on one GPU only (one process, one device); "
+                                   "--gpus must be 1"}))
         sys.exit(2)
+    if args.sweep:
+        run_sweep(args)
+        return
     if args.workload == "verify":
         res = bench_verify(args)
     else:
         res = bench_step(args)
+        quick = argparse.Namespace(**dict(vars(args), steps=10, warmup=2))
         if not args.no_verify:
-            v = bench_verify(argparse.Namespace(steps=10, warmup=2, no_cpu_baseline=True, cpu_sample=0,
-                                                calibrate_copy=False))
-            res["verify"] = {k: v[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length",
-                                               "expected_accept_length", "expected_accept_length_over_drafts",
-                                               "verify_GBps", "roofline", "config")}
+            v = bench_verify(quick, cpu=not args.no_cpu_baseline)
+            res["verify"] = section(v, ("value", "unit", "ms_per_step", "mean_accept_length", "nc_hist",
+                                        "expected_accept_length", "expected_accept_length_over_drafts",
+                                        "verify_GBps", "roofline", "config", "cpu_baseline", "parity_sample"))
+        if args.workload == "7b" and args.batch == 1 and args.cfg_w == 0.0 and not args.no_configs \
+                and not args.calibrate_copy:
+            # the other decoder shapes of the byte model, each with its own
+            # oracle baseline
+            for wl in ("tiny", "mid", "8b"):
+                r = bench_step(argparse.Namespace(**dict(vars(args), workload=wl)))
+                res[wl] = section(r)
         if args.batch == 1 and not args.no_batch2 and not args.calibrate_copy:
             # the same workload with two images per step (serving several requests)
-            b2 = bench_step(argparse.Namespace(**dict(vars(args), batch=2, no_cpu_baseline=True)))
-            res["batch2"] = {k: b2[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length",
-                                                "step_latency_ms", "config")}
-            res["batch2"]["roofline_frac"] = b2["roofline"]["frac"]
+            b2 = bench_step(argparse.Namespace(**dict(vars(args), batch=2)), cpu=False)
+            res["batch2"] = section(b2)
         if args.batch == 1 and args.cfg_w == 0.0 and not args.no_guided and not args.calibrate_copy:
             # the paper's sampling setting: guidance weight 3 (Sec. 5.1), both streams in one forward
-            gd = bench_step(argparse.Namespace(**dict(vars(args), cfg_w=3.0, no_cpu_baseline=True)))
-            res["guided"] = {k: gd[k] for k in ("value", "unit", "ms_per_step", "mean_accept_length",
-                                                "step_latency_ms", "config")}
-            res["guided"]["roofline_frac"] = gd["roofline"]["frac"]
+            gd = bench_step(argparse.Namespace(**dict(vars(args), cfg_w=3.0)), cpu=False)
+            res["guided"] = section(gd)
     print(json.dumps(res), flush=True)
 
 

@@ -1,4 +1,6 @@
-"""Comparison of sjd_verify (HIP) outputs with the oracle's, with the near-tie
+"""Comparison of sjd_verify (HIP) outputs with the oracle's (test
+infrastructure: used by the GPU tests, the smoke check and the benchmark's
+CPU-baseline leg), with the near-tie
 classes of the parity bar:
   (i)   accept near-tie   |u - ratio| < 1e-6,
   (ii)  race near-tie     relative gap of the two smallest keys < 1e-6,

@@ -25,7 +25,7 @@ def pytest_terminal_summary(terminalreporter, exitstatus, config):
     (the parity bar excludes decisions within 1e-6 of a tie; they are
     counted and printed here)."""
     try:
-        import parity
+        from oracle import parity
     except ImportError:
         return
     lines = parity.summary()

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from parity import compare_verify
+from oracle.parity import compare_verify
 from synth_inputs import CONFIGS, verify_inputs
 
 pytestmark = pytest.mark.gpu
