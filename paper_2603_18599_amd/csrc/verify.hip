@@ -887,6 +887,102 @@ SJD_DEV int race_compact(const VSh<BLOCK, NC>& shc, VSh<BLOCK, NC>& sh, int nk, 
   return best == kNoKey ? -1 : (int)(uint32_t)best;
 }
 
+// Drafting candidates of one row (proactive drafting, Sec. 4.1): the Km1
+// smallest race keys of p over the kept list (sp_x / sp_p, nk entries)
+// without token excl, in ascending key order (K - 1 draws without
+// replacement), from stream (tag 5, stage 0, row j); out[t] = -1 past the
+// tokens found.
+template <int BLOCK, int NC>
+SJD_DEV void draft_candidates(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int nk, int excl, int j, int b, int Km1,
+                              int (&out)[7]) {
+  constexpr int W = BLOCK / kWave;
+  const int tid = threadIdx.x;
+  const Stream rs(a.seed, kTagPd, 0, (uint32_t)j, (uint32_t)b, a.step);
+  // this thread's keys: Philox blocks tid, tid + BLOCK, ... of the compact
+  // list (keys carry the token, so they are distinct)
+  constexpr int KB = (kKcap / 4 + BLOCK - 1) / BLOCK;
+  uint64_t key[4 * KB];
+#pragma unroll
+  for (int q = 0; q < KB; ++q) {
+    const int jj = tid + q * BLOCK;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) key[4 * q + e] = kNoKey;
+    if (4 * jj < nk) {
+      const uint4 wd = rs.block((uint32_t)jj);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int ent = 4 * jj + e;
+        if (ent < nk) {
+          const int x = (int)sh.sp_x[ent];
+          const float pw = sh.sp_p[ent];
+          if (pw > 0.0f && x != excl) key[4 * q + e] = pack_key(exp1(compu(wd, e)) / pw, x);
+        }
+      }
+    }
+  }
+  // each wave's Km1 smallest keys in order, then the Km1 smallest of
+  // those W lists
+  const int lane = tid & (kWave - 1), w = tid / kWave;
+  uint64_t mine = kNoKey;
+#pragma unroll
+  for (int t = 0; t < 7; ++t) {
+    if (t < Km1) {
+      uint64_t lm = key[0];
+#pragma unroll
+      for (int q = 1; q < 4 * KB; ++q) lm = key[q] < lm ? key[q] : lm;
+      const uint64_t m = wave_min_u64_dpp(lm);
+      if (m != kNoKey) {
+#pragma unroll
+        for (int q = 0; q < 4 * KB; ++q) key[q] = key[q] == m ? kNoKey : key[q];
+      }
+      if (lane == t) mine = m;
+    }
+  }
+  if (lane < 8) sh.pd_w[w * 8 + lane] = mine;
+  __syncthreads();
+  if (w == 0) {
+    uint64_t c0 = kNoKey, c1 = kNoKey;
+    if (lane < W * 8) c0 = sh.pd_w[lane];
+    if (lane + kWave < W * 8) c1 = sh.pd_w[lane + kWave];
+#pragma unroll
+    for (int t = 0; t < 7; ++t) {
+      if (t < Km1) {
+        const uint64_t m = wave_min_u64_dpp(c0 < c1 ? c0 : c1);
+        if (m != kNoKey) {
+          if (c0 == m) c0 = kNoKey;
+          if (c1 == m) c1 = kNoKey;
+        }
+        if (lane == 0) sh.pd_o[t] = m == kNoKey ? -1 : (int)(uint32_t)m;
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < 7; ++t) out[t] = t < Km1 ? sh.pd_o[t] : -1;
+}
+
+// A row's target statistics in its record (words 10..15), for the rows
+// k_verify_pd drafts at.
+SJD_DEV void put_stats(int32_t* rec, const RowStats& st) {
+  rec[10] = __float_as_int(st.tau_v);
+  rec[11] = st.tau_x;
+  rec[12] = __float_as_int(st.m);
+  const uint64_t z = (uint64_t)__double_as_longlong(st.invZ);
+  rec[13] = (int32_t)(uint32_t)z;
+  rec[14] = (int32_t)(uint32_t)(z >> 32);
+  rec[15] = st.all ? 1 : 0;
+}
+SJD_DEV RowStats get_stats(const int32_t* rec, float T) {
+  RowStats st{};
+  st.tau_v = __int_as_float(rec[10]);
+  st.tau_x = rec[11];
+  st.m = __int_as_float(rec[12]);
+  st.invZ = __longlong_as_double((long long)(((uint64_t)(uint32_t)rec[14] << 32) | (uint32_t)rec[13]));
+  st.all = rec[15] != 0;
+  st.T = T;
+  return st;
+}
+
 // ------------------------------------------------------------ row kernel
 // What a row needs from memory (uniform over the workgroup).
 struct RowLoad {
@@ -1277,81 +1373,22 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
     fresh = race_compact<BLOCK, NC>(sh, sh, nk, rs, prow);
   }
 
-  // proactive drafting: K-1 draws without replacement from p, excluding the
-  // token this row carries into the next window
-  int pds[7] = {-1, -1, -1, -1, -1, -1, -1};
-  if (pd) {
-    const int excl = ac ? out_tok : fresh;
-    const Stream rs(a.seed, kTagPd, 0, (uint32_t)j, (uint32_t)b, a.step);
-    // this thread's keys: Philox blocks tid, tid + BLOCK, ... of the compact
-    // list (keys carry the token, so they are distinct)
-    constexpr int KB = (kKcap / 4 + BLOCK - 1) / BLOCK;
-    uint64_t key[4 * KB];
-#pragma unroll
-    for (int q = 0; q < KB; ++q) {
-      const int jj = tid + q * BLOCK;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) key[4 * q + e] = kNoKey;
-      if (4 * jj < nk) {
-        const uint4 wd = rs.block((uint32_t)jj);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int ent = 4 * jj + e;
-          if (ent < nk) {
-            const int x = (int)sh.sp_x[ent];
-            const float pw = sh.sp_p[ent];
-            if (pw > 0.0f && x != excl) key[4 * q + e] = pack_key(exp1(compu(wd, e)) / pw, x);
-          }
-        }
-      }
-    }
-    // each wave's Km1 smallest keys in order, then the Km1 smallest of
-    // those W lists
-    const int lane = tid & (kWave - 1), w = tid / kWave;
-    uint64_t mine = kNoKey;
-#pragma unroll
-    for (int t = 0; t < 7; ++t) {
-      if (t < Km1) {
-        uint64_t lm = key[0];
-#pragma unroll
-        for (int q = 1; q < 4 * KB; ++q) lm = key[q] < lm ? key[q] : lm;
-        const uint64_t m = wave_min_u64_dpp(lm);
-        if (m != kNoKey) {
-#pragma unroll
-          for (int q = 0; q < 4 * KB; ++q) key[q] = key[q] == m ? kNoKey : key[q];
-        }
-        if (lane == t) mine = m;
-      }
-    }
-    if (lane < 8) sh.pd_w[w * 8 + lane] = mine;
-    __syncthreads();
-    if (w == 0) {
-      uint64_t c0 = kNoKey, c1 = kNoKey;
-      if (lane < W * 8) c0 = sh.pd_w[lane];
-      if (lane + kWave < W * 8) c1 = sh.pd_w[lane + kWave];
-#pragma unroll
-      for (int t = 0; t < 7; ++t) {
-        if (t < Km1) {
-          const uint64_t m = wave_min_u64_dpp(c0 < c1 ? c0 : c1);
-          if (m != kNoKey) {
-            if (c0 == m) c0 = kNoKey;
-            if (c1 == m) c1 = kNoKey;
-          }
-          if (lane == 0) sh.pd_o[t] = m == kNoKey ? -1 : (int)(uint32_t)m;
-        }
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int t = 0; t < 7; ++t)
-      if (t < Km1) pds[t] = sh.pd_o[t];
-  }
-
+  // proactive drafting: a small launch (every row resident at once) draws
+  // each row's candidates here; otherwise k_verify_pd draws them for the
+  // rows the next window drafts at, from the statistics this row leaves
+  const bool inl = pd && (a.flags & kFlagPDInline);
+  int pds[7];
+  if (inl) draft_candidates<BLOCK, NC>(a, sh, nk, ac ? out_tok : fresh, j, b, Km1, pds);
   if (tid == 0) {
     rec[0] = out_tok;
     rec[1] = out_stage;
-    for (int t = 0; t < 7; ++t) rec[2 + t] = pds[t];
     rec[9] = fresh;
+    put_stats(rec, ps);
+    if (inl) {
+#pragma unroll
+      for (int t = 0; t < 7; ++t)
+        if (t < Km1) rec[2 + t] = pds[t];
+    }
     if (a.out_rows) {
       int32_t* o = a.out_rows + ((size_t)b * L + j) * 2;
       o[0] = out_tok < 0 ? -1 : out_tok + a.vis_lo;
@@ -1462,11 +1499,14 @@ __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, Finaliz
     }
     onext[lane] = t;
   }
+  // the drafting candidates of depths d < Dn: drawn by the rows themselves
+  // (small launches) or afterwards by k_verify_pd
+  const bool inl = (a.flags & kFlagPDInline) != 0;
   int32_t* osib = o.out_sib + (size_t)b * o.sib_stride;
   for (int i = lane; i < D * Km1; i += kWave) {
     const int d = i / Km1, k = i % Km1;
     int t = -1;
-    if (d < Dn) {
+    if (inl && d < Dn) {
       const int jj = n_c + d;
       if (rec[jj * kRecInts + 1] != -1) {
         const int y = rec[jj * kRecInts + 2 + k];
@@ -1479,6 +1519,69 @@ __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, Finaliz
     int32_t* om = o.out_meta + (size_t)b * o.meta_stride;
     om[0] = n_c; om[1] = r; om[2] = Dn; om[3] = n_s2; om[4] = n_q2; om[5] = acc_k;
     om[6] = (int32_t)(g0 + n_c); om[7] = 0;
+  }
+}
+
+// ------------------------------------------------------------ drafting
+// One workgroup per (trial, depth d): after finalize, the next window's
+// siblings at depth d < D' come from row n_c + d of this step (proactive
+// drafting, Sec. 4.1; Alg. 1 drafts only after a rejection). The row's kept
+// set is rebuilt from its logits and the statistics its row kernel left in
+// its record (the same threshold, maximum and normaliser, so the same
+// probabilities and ranks), and the K - 1 candidates are drawn without
+// replacement excluding the token the row carries forward. Only the rows
+// the next window drafts at pay for the draws.
+template <int BLOCK, int NC>
+__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 512 ? 4 : 1))) void k_verify_pd(
+    VerifyArgs a, FinalizeOut o) {
+  __shared__ VSh<BLOCK, NC> sh;
+  constexpr int W = BLOCK / kWave;
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x / a.D, d = blockIdx.x % a.D;
+  const int L = a.L, Km1 = a.K - 1;
+  const int32_t* om = o.out_meta + (size_t)b * o.meta_stride;
+  const int n_c = om[0], Dn = om[2];
+  if (n_c < 0 || d >= Dn) return;  // (invalid trial, or no drafting at this depth)
+  const int jj = n_c + d;
+  const int32_t* rec = a.rec + ((size_t)b * L + jj) * kRecInts;
+  if (rec[1] == -1) return;  // row end: no siblings
+  const int excl = (a.flags & kFlagAC) ? rec[0] : rec[9];
+  const RowStats st = get_stats(rec, a.T);
+  float4 v[NC];
+  load_row<BLOCK, NC>(v, row_logits(a, b * L + jj), a.V);
+  bitmap_from_tau<BLOCK, NC>(v, a.V, st, sh.bm);
+  __syncthreads();
+  constexpr int NW = VSh<BLOCK, NC>::NW;
+  constexpr int WPT = NW / BLOCK > 0 ? NW / BLOCK : 1;
+  int cnt[WPT];
+  int s0 = 0;
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int wi = tid * WPT + i;
+    cnt[i] = wi < NW ? __popc(sh.bm[wi]) : 0;
+    s0 += cnt[i];
+  }
+  int run = block_excl_scan<W>(s0, sh.red_i);
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int wi = tid * WPT + i;
+    if (wi < NW) sh.pre[wi] = run;
+    run += cnt[i];
+  }
+  if (tid == BLOCK - 1) sh.ncand[0] = run;
+  __syncthreads();
+  const int nk = sh.ncand[0];
+  compact_row<BLOCK, NC>(v, a.V, sh.bm, sh.pre, sh.sp_x, sh.sp_p);
+  __syncthreads();
+  for (int i = tid; i < nk; i += BLOCK) sh.sp_p[i] = (float)((double)expf(over_T(sh.sp_p[i] - st.m, a.T)) * st.invZ);
+  __syncthreads();
+  int pds[7];
+  draft_candidates<BLOCK, NC>(a, sh, nk, excl, jj, b, Km1, pds);
+  if (tid < Km1) {
+    int y = -1;
+#pragma unroll
+    for (int t = 0; t < 7; ++t) y = t == tid ? pds[t] : y;
+    o.out_sib[(size_t)b * o.sib_stride + (size_t)d * Km1 + tid] = y < 0 ? -1 : y + a.vis_lo;
   }
 }
 
@@ -1509,9 +1612,15 @@ hipError_t noalloc_scratch(int32_t** out) {
 }
 
 // ------------------------------------------------------------ launch
-hipError_t launch_verify(const VerifyArgs& a, const FinalizeOut& o, hipStream_t s) {
-  const long rows = (long)a.B * a.L;
+hipError_t launch_verify(const VerifyArgs& a0, const FinalizeOut& o, hipStream_t s) {
+  const long rows = (long)a0.B * a0.L;
   if (rows < 1 || rows > 0x7FFFFFFFL) return hipErrorInvalidValue;
+  // a launch whose rows are all resident at once (two workgroups per compute
+  // unit) draws the drafting candidates in the row kernel: a second kernel
+  // would only add its latency
+  VerifyArgs a = a0;
+  const bool pd = (a.flags & kFlagPD) && a.K >= 2 && a.D >= 1;
+  if (pd && rows <= kPdInlineRows) a.flags |= kFlagPDInline;
   const dim3 grid((unsigned)rows);
   if (a.V <= 4096) hipLaunchKernelGGL((k_verify_rows<256, 4, true>), grid, dim3(256), 0, s, a);
   else if (a.V <= 16384) hipLaunchKernelGGL((k_verify_rows<512, 8, true>), grid, dim3(512), 0, s, a);
@@ -1521,6 +1630,13 @@ hipError_t launch_verify(const VerifyArgs& a, const FinalizeOut& o, hipStream_t 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_verify_finalize, dim3(a.B), dim3(kWave), 0, s, a, o);
+  e = hipGetLastError();
+  if (e != hipSuccess || !pd || (a.flags & kFlagPDInline)) return e;
+  const dim3 gpd((unsigned)((long)a.B * a.D));
+  if (a.V <= 4096) hipLaunchKernelGGL((k_verify_pd<256, 4>), gpd, dim3(256), 0, s, a, o);
+  else if (a.V <= 16384) hipLaunchKernelGGL((k_verify_pd<512, 8>), gpd, dim3(512), 0, s, a, o);
+  else if (a.V <= 32768) hipLaunchKernelGGL((k_verify_pd<1024, 8>), gpd, dim3(1024), 0, s, a, o);
+  else hipLaunchKernelGGL((k_verify_pd<1024, 16>), gpd, dim3(1024), 0, s, a, o);
   return hipGetLastError();
 }
 

@@ -93,6 +93,20 @@ def test_verify_tree_rows_with_siblings(orc):
     assert (ref["rows"][:, :3, 1] != 1).any()
 
 
+@pytest.mark.parametrize("V,top_k", [(4096, 300), (16384, 2000), (32768, 1000), (65536, 2000)])
+@pytest.mark.parametrize("B", [8, 17])
+def test_verify_drafting_in_row_kernel_and_after_finalize(orc, B, V, top_k):
+    # launches of at most 512 rows draw the drafting candidates in the row
+    # kernel, larger ones in a kernel of their own after finalize (from the
+    # statistics the rows leave): both must match the oracle, at every
+    # vocabulary tier
+    L, K, D = 32, 4, 3
+    inp = verify_inputs(B, L, V, top_k=top_k, seed=B * 7 + V, K=K, D=D, D_in=3, draft_noise=1.2)
+    gpu, ref = run_both(orc, inp, K=K, D=D, top_k=top_k, seed=17, step=4, want_p=False)
+    check(gpu, ref, K, D, want_p=False)
+    assert (ref["sib"] >= 0).any()
+
+
 def test_verify_placeholders_and_row_ends(orc):
     B, L, V = 6, 16, 2048
     inp = verify_inputs(B, L, V, top_k=100, seed=5, n_q=9)
