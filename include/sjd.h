@@ -88,6 +88,13 @@ typedef enum {
  * changed, if one is found. sjd_verify: in sjd_verify_params.flags;
  * decoder contexts: in sjd_config.flags. */
 #define SJD_CHECK_FINITE 32u
+/* sjd_verify only, the reference mode of the top-k selection: every row
+ * selects its kept set by histograms over the whole row instead of by the
+ * candidates at or above a threshold estimated from a sample of the row. The
+ * kept sets and thresholds are the same; the normalisers are summed in a
+ * different order (fp64), so a decision within a few fp64 ulps of a tie can
+ * differ. For tests and profiling. */
+#define SJD_FULL_SELECT 64u
 
 /* Rows (B * L) sjd_verify_noalloc can take: its record scratch is a static
  * device array of this many 64-byte records (8 MiB per device). */
@@ -132,7 +139,8 @@ typedef struct {
   int32_t top_k;      /* >= 0; the kept set (top_k, or V when top_k is 0 or >= V)
                          may hold at most 2048 tokens (SJD_ENOTSUP otherwise)    */
   float temperature;  /* > 0                                                      */
-  uint32_t flags;     /* SJD_AC | SJD_PD, optionally | SJD_CHECK_FINITE             */
+  uint32_t flags;     /* SJD_AC | SJD_PD, optionally | SJD_CHECK_FINITE,
+                         SJD_FULL_SELECT                                           */
   uint64_t seed;
   uint32_t step;      /* counter word 3 of every random stream                   */
   int32_t vis_lo;     /* token id of logits entry 0                               */

@@ -76,7 +76,7 @@ int check_verify_params(const sjd_verify_params* p) {
     return SJD_EINVAL;
   if (p->K < 1 || p->K > 8 || p->D < 0 || (long)p->K * p->D > p->L) return SJD_EINVAL;
   if (p->top_k < 0 || !(p->temperature > 0.0f)) return SJD_EINVAL;
-  if (p->flags & ~(SJD_AC | SJD_PD | SJD_CHECK_FINITE)) return SJD_EINVAL;
+  if (p->flags & ~(SJD_AC | SJD_PD | SJD_CHECK_FINITE | SJD_FULL_SELECT)) return SJD_EINVAL;
   return check_verify_limits(p->V, p->top_k);
 }
 }  // namespace sjd
@@ -99,6 +99,7 @@ int enqueue_verify(const sjd_verify_params* p, const sjd_verify_io* io, int32_t*
   sjd::VerifyArgs a{};
   a.B = p->B; a.L = p->L; a.V = p->V; a.K = p->K; a.D = p->D; a.top_k = p->top_k;
   a.T = p->temperature; a.flags = p->flags & (SJD_AC | SJD_PD); a.seed = p->seed; a.step = p->step;
+  if (p->flags & SJD_FULL_SELECT) a.flags |= sjd::kFlagFullSelect;
   a.vis_lo = p->vis_lo; a.eol = p->eol_id; a.row_len = p->row_len;
   a.cur = io->d_cur; a.draft = io->d_draft; a.draft_bstride = (long long)p->L * p->V; a.q_off = nullptr;
   a.draft_tok = io->d_draft_tok; a.sib = io->d_sib; a.in_meta = io->d_in_meta;

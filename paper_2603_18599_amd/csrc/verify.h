@@ -9,6 +9,7 @@ constexpr uint32_t kFlagAC = 1u;
 constexpr uint32_t kFlagPD = 2u;
 constexpr uint32_t kFlagPDInline = 1u << 30;  // (internal) rows draw their own drafting candidates
 constexpr long kPdInlineRows = 512;           // launches of at most this many rows do
+constexpr uint32_t kFlagFullSelect = 1u << 29;  // (internal) every row takes the full-row selection
 constexpr int kRecInts = 16;  // per-row record: tok, stage, 7 drafting candidates, fresh, pad
 constexpr int kVerifyMaxV = 65536;  // logits per row held on chip
 constexpr int kVerifyMaxK = 2048;   // kept (top-k) tokens per row when V > kVerifyMaxK

@@ -48,35 +48,69 @@ constexpr int kKcap = kVerifyMaxK;   // kept tokens per row held on chip
 constexpr int kCandCap = 256;        // threshold-bin entries ranked exactly
 constexpr int kBins = 2048;
 
+constexpr int kFastBins = 1024;  // candidate-path threshold histogram (bins over [lo, max])
+constexpr int kSampBins = 512;   // candidate-path sample histogram (bins over the sample range)
+
+// Compact list of a row's kept tokens, by rank (index order).
+struct SpList {
+  uint16_t x[kKcap];  // token index,
+  float p[kKcap];     //   target probability,
+  float q[kKcap];     //   draft probability
+};
+
 template <int BLOCK, int NC>
 struct VSh {
   static constexpr int W = BLOCK / kWave;
   static constexpr int NW = BLOCK * NC / 8;  // bitmap words (32 entries each)
+  // candidate path: entries of a row at or above its estimated threshold,
+  // CAPW per wave
+  static constexpr int CAP = BLOCK >= 1024 ? 4096 : 3072;
+  static constexpr int CAPW = CAP / W;
   static_assert(W <= 16, "the drafting merge holds 8 keys of each wave in two registers per lane");
+  // scratch of the full-row selection (the fallback path)
+  struct OldSel {
+    uint32_t bmq[NW];   // kept set of the draft row
+    int32_t preq[NW];   // its per-word prefix popcounts
+    union {
+      uint32_t hist[kBins];
+      float qc[kKcap];  // draft row's kept weights (its normaliser)
+    };
+    uint32_t hist_q[kBins];  // the draft row's histogram when both rows are selected together
+    // per selected row (target, draft): threshold-bin entries, then sentinels
+    // that outrank nothing (-inf, INT_MAX)
+    float cand_v[2][kCandCap + 8];
+    int cand_x[2][kCandCap + 8];
+  };
+  // scratch of the candidate path
+  struct FastSel {
+    float cv[CAP];    // target candidates: logit (after the normaliser: weight, or -1 if not kept)
+    float cq[CAP];    //   the draft logit of the same token
+    int32_t cx[CAP];  //   token index
+    uint32_t hist[2][kFastBins];
+    float tb_v[2][kCandCap + 8];  // threshold-bin entries, then sentinels
+    int tb_x[2][kCandCap + 8];
+    int tb_s[1][kCandCap + 8];  // the target's threshold-bin entries' candidate slots
+  };
   uint32_t bm[NW];    // kept set of the target row
   int32_t pre[NW];    // its per-word prefix popcounts
-  uint32_t bmq[NW];   // kept set of the draft row
-  int32_t preq[NW];
-  uint16_t sp_x[kKcap];  // compact list: token index,
-  float sp_p[kKcap];     //   target probability,
-  float sp_q[kKcap];     //   draft probability
   union {
-    uint32_t hist[kBins];
-    float qc[kKcap];  // draft row's kept weights (its normaliser)
+    SpList sp;        // compact list of the target row's kept tokens
+    float dv[CAP];    // candidate path: the draft row's candidates (dead before the list is built)
+  } u;
+  union {
+    OldSel o;
+    FastSel f;
   };
-  uint32_t hist_q[kBins];  // the draft row's histogram when both rows are selected together
-  // per selected row (target, draft): threshold-bin entries, then sentinels
-  // that outrank nothing (-inf, INT_MAX)
-  float cand_v[2][kCandCap + 8];
-  int cand_x[2][kCandCap + 8];
   uint64_t pd_w[W * 8];  // per-wave drafting keys
   int pd_o[8];            // the drafting draws
   double red_d[2 * W];
   uint64_t red_u[W];
-  float red_f[4 * W];
+  alignas(16) float red_f[8 * W];
   int red_i[2 * W];
   float tau_v[2];
   int tau_x[2], bin[2], above[2], ncand[2];
+  int wcnt[2][W];  // candidate path: candidates per wave (-1: overflow)
+  int fflag;       // candidate path: a row needs the full selection
 };
 static_assert(kBins == kKcap, "the draft weights reuse the histogram");
 
@@ -196,7 +230,7 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
   for (int pass = 0; pass < 3; ++pass) {
     const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
     const int nb = pass == 2 ? 1024 : 2048;
-    for (int b = tid; b < nb; b += BLOCK) sh.hist[b] = 0;
+    for (int b = tid; b < nb; b += BLOCK) sh.o.hist[b] = 0;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
@@ -205,7 +239,7 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const uint32_t key = okey(comp(v[i], e));
-          if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & (uint32_t)(nb - 1)], 1u);
+          if ((key & pmask) == prefix) atomicAdd(&sh.o.hist[(key >> shift) & (uint32_t)(nb - 1)], 1u);
         }
       }
     }
@@ -216,7 +250,7 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int bi = tid * per + i;
-      cnts[i] = (i < per && bi < nb) ? (int)sh.hist[nb - 1 - bi] : 0;
+      cnts[i] = (i < per && bi < nb) ? (int)sh.o.hist[nb - 1 - bi] : 0;
       s += cnts[i];
     }
     int run = block_excl_scan<W>(s, sh.red_i);
@@ -235,7 +269,7 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
     rem -= sh.above[0];
     __syncthreads();
   }
-  const int eq = (int)sh.hist[last_bin];
+  const int eq = (int)sh.o.hist[last_bin];
   __syncthreads();
   tau_v = 0.0f;
   // value of the threshold key (any entry with that key)
@@ -250,7 +284,7 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
   uint32_t ipre = 0, imask = 0;
   for (int pass = 0; pass < 2; ++pass) {
     const int shift = pass == 0 ? 11 : 0;
-    for (int b = tid; b < 2048; b += BLOCK) sh.hist[b] = 0;
+    for (int b = tid; b < 2048; b += BLOCK) sh.o.hist[b] = 0;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
@@ -259,7 +293,7 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const uint32_t x = (uint32_t)(4 * c + e);
-          if (okey(comp(v[i], e)) == prefix && (x & imask) == ipre) atomicAdd(&sh.hist[(x >> shift) & 2047u], 1u);
+          if (okey(comp(v[i], e)) == prefix && (x & imask) == ipre) atomicAdd(&sh.o.hist[(x >> shift) & 2047u], 1u);
         }
       }
     }
@@ -269,7 +303,7 @@ SJD_DEV void radix_topk(const float4 (&v)[NC], int V, int k, VSh<BLOCK, NC>& sh,
     int cnts[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      cnts[i] = i < per ? (int)sh.hist[tid * per + i] : 0;
+      cnts[i] = i < per ? (int)sh.o.hist[tid * per + i] : 0;
       s += cnts[i];
     }
     int run = block_excl_scan<W>(s, sh.red_i);
@@ -361,10 +395,10 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
     const float scale = fast ? (float)kBins / (mx - mn) : 0.0f;
     fast = fast && (scale < INFINITY) && (scale > 0.0f);
     if (fast) {
-      for (int b = tid; b < kBins; b += BLOCK) sh.hist[b] = 0;
+      for (int b = tid; b < kBins; b += BLOCK) sh.o.hist[b] = 0;
       for (int b = tid; b < kCandCap + 8; b += BLOCK) {
-        sh.cand_v[0][b] = -INFINITY;
-        sh.cand_x[0][b] = 0x7FFFFFFF;
+        sh.o.cand_v[0][b] = -INFINITY;
+        sh.o.cand_x[0][b] = 0x7FFFFFFF;
       }
       if (tid == 0) sh.ncand[0] = 0;
       __syncthreads();
@@ -381,7 +415,7 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
         const int c = tid + i * BLOCK;
         if (c < nchunk) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) atomicAdd(&sh.hist[binof(comp(v[i], e))], 1u);
+          for (int e = 0; e < 4; ++e) atomicAdd(&sh.o.hist[binof(comp(v[i], e))], 1u);
         }
       }
       __syncthreads();
@@ -391,7 +425,7 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
       int s = 0;
 #pragma unroll
       for (int i = 0; i < per; ++i) {
-        cnts[i] = (int)sh.hist[kBins - 1 - (tid * per + i)];
+        cnts[i] = (int)sh.o.hist[kBins - 1 - (tid * per + i)];
         s += cnts[i];
       }
       int run = block_excl_scan<W>(s, sh.red_i);
@@ -404,7 +438,7 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
         run += cnts[i];
       }
       __syncthreads();
-      const int bstar = sh.bin[0], rem = k - sh.above[0], c = (int)sh.hist[bstar];
+      const int bstar = sh.bin[0], rem = k - sh.above[0], c = (int)sh.o.hist[bstar];
       if (c <= kCandCap) {
         // entries of higher bins are kept; the threshold bin's are collected
 #pragma unroll
@@ -424,8 +458,8 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
             for (int e = 0; e < 4; ++e) {
               if ((hit >> e) & 1u) {
                 const int p = atomicAdd(&sh.ncand[0], 1);
-                sh.cand_v[0][p] = comp(v[i], e);
-                sh.cand_x[0][p] = 4 * ch + e;
+                sh.o.cand_v[0][p] = comp(v[i], e);
+                sh.o.cand_x[0][p] = 4 * ch + e;
               }
             }
           }
@@ -439,14 +473,14 @@ SJD_DEV int select_kept(const float4 (&v)[NC], int V, int top_k, float mx, float
         // of eight whose loads issue together)
         const int cpad = (c + 7) & ~7;
         for (int i = tid; i < c; i += BLOCK) {
-          const float vi = sh.cand_v[0][i];
-          const int xi = sh.cand_x[0][i];
+          const float vi = sh.o.cand_v[0][i];
+          const int xi = sh.o.cand_x[0][i];
           int r = 0;
           for (int j0 = 0; j0 < cpad; j0 += 8) {
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-              const float vj = sh.cand_v[0][j0 + u];
-              r += (vj > vi) || (vj == vi && sh.cand_x[0][j0 + u] < xi);
+              const float vj = sh.o.cand_v[0][j0 + u];
+              r += (vj > vi) || (vj == vi && sh.o.cand_x[0][j0 + u] < xi);
             }
           }
           if (r < rem) atomicOr(&bm[xi >> 5], 1u << (xi & 31));
@@ -657,14 +691,14 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
   }
   if (!fast) return false;
   for (int b = tid; b < kBins; b += BLOCK) {
-    sh.hist[b] = 0;
-    sh.hist_q[b] = 0;
+    sh.o.hist[b] = 0;
+    sh.o.hist_q[b] = 0;
   }
   for (int b = tid; b < kCandCap + 8; b += BLOCK) {
-    sh.cand_v[0][b] = -INFINITY;
-    sh.cand_x[0][b] = 0x7FFFFFFF;
-    sh.cand_v[1][b] = -INFINITY;
-    sh.cand_x[1][b] = 0x7FFFFFFF;
+    sh.o.cand_v[0][b] = -INFINITY;
+    sh.o.cand_x[0][b] = 0x7FFFFFFF;
+    sh.o.cand_v[1][b] = -INFINITY;
+    sh.o.cand_x[1][b] = 0x7FFFFFFF;
   }
   if (tid == 0) {
     sh.ncand[0] = 0;
@@ -680,8 +714,8 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
     if (c < nchunk) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        atomicAdd(&sh.hist[binof(comp(v[i], e), 0)], 1u);
-        atomicAdd(&sh.hist_q[binof(comp(u[i], e), 1)], 1u);
+        atomicAdd(&sh.o.hist[binof(comp(v[i], e), 0)], 1u);
+        atomicAdd(&sh.o.hist_q[binof(comp(u[i], e), 1)], 1u);
       }
     }
   }
@@ -691,8 +725,8 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
   int sp = 0, sq = 0;
 #pragma unroll
   for (int i = 0; i < per; ++i) {
-    cp[i] = (int)sh.hist[kBins - 1 - (tid * per + i)];
-    cq[i] = (int)sh.hist_q[kBins - 1 - (tid * per + i)];
+    cp[i] = (int)sh.o.hist[kBins - 1 - (tid * per + i)];
+    cq[i] = (int)sh.o.hist_q[kBins - 1 - (tid * per + i)];
     sp += cp[i];
     sq += cq[i];
   }
@@ -713,7 +747,7 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
   __syncthreads();
   const int bs0 = sh.bin[0], bs1 = sh.bin[1];
   const int rem0 = k - sh.above[0], rem1 = k - sh.above[1];
-  const int c0 = (int)sh.hist[bs0], c1 = (int)sh.hist_q[bs1];
+  const int c0 = (int)sh.o.hist[bs0], c1 = (int)sh.o.hist_q[bs1];
   if (c0 > kCandCap || c1 > kCandCap) return false;
   // entries of higher bins are kept; the threshold bins' are collected
 #pragma unroll
@@ -735,13 +769,13 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
       for (int e = 0; e < 4; ++e) {
         if ((hp >> e) & 1u) {
           const int p = atomicAdd(&sh.ncand[0], 1);
-          sh.cand_v[0][p] = comp(v[i], e);
-          sh.cand_x[0][p] = 4 * ch + e;
+          sh.o.cand_v[0][p] = comp(v[i], e);
+          sh.o.cand_x[0][p] = 4 * ch + e;
         }
         if ((hq >> e) & 1u) {
           const int p = atomicAdd(&sh.ncand[1], 1);
-          sh.cand_v[1][p] = comp(u[i], e);
-          sh.cand_x[1][p] = 4 * ch + e;
+          sh.o.cand_v[1][p] = comp(u[i], e);
+          sh.o.cand_x[1][p] = 4 * ch + e;
         }
       }
     }
@@ -751,7 +785,7 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
     bq = or8_dpp(bq);
     if ((tid & 7) == 0) {
       sh.bm[(tid >> 3) + i * (BLOCK / 8)] = bp;
-      sh.bmq[(tid >> 3) + i * (BLOCK / 8)] = bq;
+      sh.o.bmq[(tid >> 3) + i * (BLOCK / 8)] = bq;
     }
   }
   __syncthreads();
@@ -760,18 +794,18 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
     const int r = t < c0 ? 0 : 1;
     const int i = t - (r ? c0 : 0);
     const int c = r ? c1 : c0;
-    const float vi = sh.cand_v[r][i];
-    const int xi = sh.cand_x[r][i];
+    const float vi = sh.o.cand_v[r][i];
+    const int xi = sh.o.cand_x[r][i];
     int rank = 0;
     for (int j0 = 0; j0 < c; j0 += 8) {
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        const float vj = sh.cand_v[r][j0 + q];
-        rank += (vj > vi) || (vj == vi && sh.cand_x[r][j0 + q] < xi);
+        const float vj = sh.o.cand_v[r][j0 + q];
+        rank += (vj > vi) || (vj == vi && sh.o.cand_x[r][j0 + q] < xi);
       }
     }
     const int rem = r ? rem1 : rem0;
-    if (rank < rem) atomicOr(r ? &sh.bmq[xi >> 5] : &sh.bm[xi >> 5], 1u << (xi & 31));
+    if (rank < rem) atomicOr(r ? &sh.o.bmq[xi >> 5] : &sh.bm[xi >> 5], 1u << (xi & 31));
     if (rank == rem - 1) {
       sh.tau_v[r] = vi;
       sh.tau_x[r] = xi;
@@ -791,7 +825,7 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
   for (int i = 0; i < WPT; ++i) {
     const int wi = tid * WPT + i;
     np[i] = wi < NW ? __popc(sh.bm[wi]) : 0;
-    nqw[i] = wi < NW ? __popc(sh.bmq[wi]) : 0;
+    nqw[i] = wi < NW ? __popc(sh.o.bmq[wi]) : 0;
     rp += np[i];
     rq += nqw[i];
   }
@@ -801,7 +835,7 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
     const int wi = tid * WPT + i;
     if (wi < NW) {
       sh.pre[wi] = rp;
-      sh.preq[wi] = rq;
+      sh.o.preq[wi] = rq;
     }
     rp += np[i];
     rq += nqw[i];
@@ -815,6 +849,411 @@ SJD_DEV bool select_kept2(const float4 (&v)[NC], const float4 (&u)[NC], int V, i
   nq = sh.ncand[1];
   __syncthreads();
   return true;
+}
+
+// ------------------------------------------------------ candidate path
+// Top-k selection that touches each logit once. A sample of the row (every
+// fourth entry of half the register slots) gives a value lo that about
+// k + 3 sigma of the row's entries reach; one pass over the row in registers
+// appends every entry >= lo to its wave's region of LDS (per-wave append by
+// ballot and mbcnt). The exact threshold (value desc, index asc) is then
+// found among those candidates alone: a histogram over [lo, max], the
+// threshold bin's entries ranked exactly. The kept set, its normaliser and
+// the threshold are those of the full selection; only the order of the fp64
+// normaliser sum differs. The compact list (index order) is built from the
+// candidates when a row draws from it (fast_build_list). Any case the
+// candidates cannot decide (a row with -inf, NaN or +inf entries, too few or
+// too many candidates, a crowded threshold bin, tied draft values split by
+// the threshold) returns false with nothing decided; the caller then runs
+// the full selection.
+
+// Wave max that propagates NaN (no quieting copy per step).
+SJD_DEV float wave_vmax_dpp(float v) {
+  return wave_reduce32(v, [](float a, float b) { return __builtin_elementwise_maximum(a, b); });
+}
+
+// Block-wide max of four values; every thread gets the four results.
+template <int W>
+SJD_DEV void block_max4(float (&a)[4], float* red) {
+  const int w = threadIdx.x / kWave;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] = wave_vmax_dpp(a[i]);
+  if ((threadIdx.x & (kWave - 1)) == 0) *(float4*)&red[4 * w] = make_float4(a[0], a[1], a[2], a[3]);
+  __syncthreads();
+  float4 m = *(const float4*)&red[0];
+#pragma unroll 2
+  for (int t = 1; t < W; ++t) {
+    const float4 o = *(const float4*)&red[4 * t];
+    m.x = __builtin_elementwise_maximum(m.x, o.x);
+    m.y = __builtin_elementwise_maximum(m.y, o.y);
+    m.z = __builtin_elementwise_maximum(m.z, o.z);
+    m.w = __builtin_elementwise_maximum(m.w, o.w);
+  }
+  a[0] = m.x; a[1] = m.y; a[2] = m.z; a[3] = m.w;
+  __syncthreads();
+}
+
+// One wave: the bin of hist[0..NB) (counted from the top) that holds the
+// target-th entry, and the number of entries above it, into *bin / *above.
+template <int NB>
+SJD_DEV void wave_find_from_top(const uint32_t* hist, int target, int* bin, int* above) {
+  constexpr int PER = NB / kWave;
+  static_assert(PER % 4 == 0, "bins are read four at a time");
+  const int lane = threadIdx.x & (kWave - 1);
+  // lane l owns bins [NB - (l + 1) * PER, NB - l * PER), read from the top
+  uint32_t c[PER];
+#pragma unroll
+  for (int i = 0; i < PER; i += 4) {
+    const uint4 q = *(const uint4*)&hist[NB - (lane + 1) * PER + i];
+    c[PER - 1 - i] = q.x; c[PER - 2 - i] = q.y; c[PER - 3 - i] = q.z; c[PER - 4 - i] = q.w;
+  }
+  int s = 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) s += (int)c[i];
+  int run = wave_incl_scan_dpp(s) - s;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    if (run < target && run + (int)c[i] >= target) {
+      *bin = NB - 1 - (lane * PER + i);
+      *above = run;
+    }
+    run += (int)c[i];
+  }
+}
+
+template <int BLOCK, int NC, bool TWO>
+SJD_DEV bool fast_select(const float4 (&v)[NC], const float4 (&u)[NC], int V, int top_k, float T,
+                         VSh<BLOCK, NC>& sh, RowStats& ps, RowStats& qs) {
+  using Sh = VSh<BLOCK, NC>;
+  constexpr int W = BLOCK / kWave;
+  constexpr int CAPW = Sh::CAPW;
+  constexpr int R = TWO ? 2 : 1;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int nchunk = V >> 2;
+  const int k = (top_k <= 0 || top_k >= V) ? V : top_k;
+  if (k >= V) return false;
+
+  // 1. row maxima, and the smallest sampled value (entry 4c of the even
+  //    slots); the samples are binned over [sample min, row max]
+  float st[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    st[0] = vmax(st[0], vmax(vmax(v[i].x, v[i].y), vmax(v[i].z, v[i].w)));
+    if (TWO) st[2] = vmax(st[2], vmax(vmax(u[i].x, u[i].y), vmax(u[i].z, u[i].w)));
+    if ((i & 1) == 0 && tid + i * BLOCK < nchunk) {
+      st[1] = vmax(st[1], -v[i].x);
+      if (TWO) st[3] = vmax(st[3], -u[i].x);
+    }
+  }
+  block_max4<W>(st, sh.red_f);
+  // samples per row
+  int S = 0;
+#pragma unroll
+  for (int i = 0; i < NC; i += 2) {
+    const int n = nchunk - i * BLOCK;
+    S += n <= 0 ? 0 : (n >= BLOCK ? BLOCK : n);
+  }
+  // rank (from the top) of the sample that sets lo: k's share of the
+  // samples plus three standard deviations (scales and ranks here only steer
+  // the selection, so approximate reciprocals do)
+  const float kf = (float)k, rV = __builtin_amdgcn_rcpf((float)V);
+  const float kSV = kf * (float)S * rV;
+  const int rstar = (int)ceilf(kSV + 3.0f * __builtin_amdgcn_sqrtf(kSV * (1.0f - kf * rV)) + 1.0f);
+  if (rstar > S) return false;
+  float sscale[2], soff[2], smn[2], srng[2];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const float mx = st[2 * r];
+    smn[r] = -st[2 * r + 1];
+    // finite range (a -inf, +inf or NaN sample or maximum sends the row to
+    // the full selection)
+    if (!(mx > smn[r]) || !(mx < INFINITY) || !(smn[r] > -INFINITY)) return false;
+    srng[r] = mx - smn[r];
+    sscale[r] = (float)kSampBins * __builtin_amdgcn_rcpf(srng[r]);
+    if (!(sscale[r] < INFINITY) || !(sscale[r] > 0.0f)) return false;
+    soff[r] = -smn[r] * sscale[r];
+  }
+
+  // 2. sample histograms; lo = one bin below the bin that holds sample rstar
+  //    from the top
+  for (int b = tid; b < R * kFastBins; b += BLOCK) (&sh.f.hist[0][0])[b] = 0;
+  __syncthreads();
+  auto sbin = [&](float l, int r) -> int {
+    return (int)__builtin_amdgcn_fmed3f(__builtin_fmaf(l, sscale[r], soff[r]), 0.0f, (float)(kSampBins - 1));
+  };
+#pragma unroll
+  for (int i = 0; i < NC; i += 2) {
+    if (tid + i * BLOCK < nchunk) {
+      atomicAdd(&sh.f.hist[0][sbin(v[i].x, 0)], 1u);
+      if (TWO) atomicAdd(&sh.f.hist[1][sbin(u[i].x, 1)], 1u);
+    }
+  }
+  __syncthreads();
+  if (w < R) wave_find_from_top<kSampBins>(sh.f.hist[w], rstar, &sh.bin[w], &sh.above[w]);
+  __syncthreads();
+  float lo[2];
+#pragma unroll
+  for (int r = 0; r < R; ++r) lo[r] = smn[r] + ((float)sh.bin[r] - 1.0f) * srng[r] * (1.0f / kSampBins);
+
+  // 3. candidates: every entry >= lo, appended to the wave's region
+  //    [w * CAPW, w * CAPW + count); a region that would overflow stops
+  //    taking entries and marks the row
+  int cnt[2] = {0, 0};
+  bool ovf[2] = {false, false};
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int xb = 4 * (tid + i * BLOCK);  // padding chunks hold -inf and are never taken
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const float4 x4 = r == 0 ? v[i] : u[i];
+      const bool s0 = x4.x >= lo[r], s1 = x4.y >= lo[r], s2 = x4.z >= lo[r], s3 = x4.w >= lo[r];
+      const uint64_t m0 = __ballot(s0), m1 = __ballot(s1), m2 = __ballot(s2), m3 = __ballot(s3);
+      const int t0 = __popcll(m0), t1 = __popcll(m1), t2 = __popcll(m2), t3 = __popcll(m3);
+      const int tot = t0 + t1 + t2 + t3;
+      if (cnt[r] + tot <= CAPW) {
+        int base = w * CAPW + cnt[r];
+        auto put = [&](bool s, uint64_t m, float l, int e) {
+          if (s) {
+            const int p = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, (uint32_t)base));
+            if (r == 0) {
+              sh.f.cv[p] = l;
+              sh.f.cx[p] = xb + e;
+              if (TWO) sh.f.cq[p] = comp(u[i], e);
+            } else {
+              sh.u.dv[p] = l;
+            }
+          }
+        };
+        put(s0, m0, x4.x, 0);
+        base += t0;
+        put(s1, m1, x4.y, 1);
+        base += t1;
+        put(s2, m2, x4.z, 2);
+        base += t2;
+        put(s3, m3, x4.w, 3);
+      } else {
+        ovf[r] = true;
+      }
+      cnt[r] += tot;
+    }
+  }
+  if (lane == 0) {
+    sh.wcnt[0][w] = ovf[0] ? -1 : cnt[0];
+    if (TWO) sh.wcnt[1][w] = ovf[1] ? -1 : cnt[1];
+  }
+  __syncthreads();
+  int tot[2] = {0, 0};
+  bool bad = false;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+#pragma unroll
+    for (int t = 0; t < W; ++t) {
+      const int c = sh.wcnt[r][t];
+      bad |= c < 0;
+      tot[r] += c;
+    }
+    bad |= tot[r] < k;
+  }
+  if (bad) {
+    __syncthreads();
+    return false;
+  }
+
+  // 4. histogram of the candidates over [lo, max]
+  float scale[2], off[2];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const float mx = st[2 * r];
+    scale[r] = (float)kFastBins * __builtin_amdgcn_rcpf(mx - lo[r]);
+    if (!(scale[r] < INFINITY) || !(scale[r] > 0.0f)) bad = true;
+    off[r] = -lo[r] * scale[r];
+  }
+  if (bad) {
+    __syncthreads();
+    return false;
+  }
+  auto fbin = [&](float l, int r) -> int {
+    return (int)__builtin_amdgcn_fmed3f(__builtin_fmaf(l, scale[r], off[r]), 0.0f, (float)(kFastBins - 1));
+  };
+  for (int b = tid; b < R * kFastBins; b += BLOCK) (&sh.f.hist[0][0])[b] = 0;
+  for (int b = tid; b < R * (kCandCap + 8); b += BLOCK) {
+    (&sh.f.tb_v[0][0])[b] = -INFINITY;
+    (&sh.f.tb_x[0][0])[b] = 0x7FFFFFFF;
+  }
+  if (tid == 0) {
+    sh.ncand[0] = 0;
+    sh.ncand[1] = 0;
+    sh.fflag = 0;
+  }
+  __syncthreads();
+  for (int i = lane; i < cnt[0]; i += kWave) atomicAdd(&sh.f.hist[0][fbin(sh.f.cv[w * CAPW + i], 0)], 1u);
+  if (TWO)
+    for (int i = lane; i < cnt[1]; i += kWave) atomicAdd(&sh.f.hist[1][fbin(sh.u.dv[w * CAPW + i], 1)], 1u);
+  __syncthreads();
+  if (w < R) wave_find_from_top<kFastBins>(sh.f.hist[w], k, &sh.bin[w], &sh.above[w]);
+  __syncthreads();
+  int bs[2], rem[2], cb[2];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    bs[r] = sh.bin[r];
+    rem[r] = k - sh.above[r];
+    cb[r] = (int)sh.f.hist[r][bs[r]];
+    bad |= cb[r] > kCandCap;
+  }
+  if (bad) {
+    __syncthreads();
+    return false;
+  }
+
+  // 5. one pass over the candidates: entries of bins above the threshold bin
+  //    are kept (weight into the normaliser; a target candidate's slot keeps
+  //    its weight), entries below it are not (slot -1), the threshold bin's
+  //    entries are collected with their slot
+  const float mp = st[0], mq = st[2];
+  double zp = 0.0, zq = 0.0;
+  for (int i = lane; i < cnt[0]; i += kWave) {
+    const int s = w * CAPW + i;
+    const float l = sh.f.cv[s];
+    const int bn = fbin(l, 0);
+    float e = -1.0f;
+    if (bn > bs[0]) {
+      e = expf(over_T(l - mp, T));
+      zp += (double)e;
+    } else if (bn == bs[0]) {
+      const int p = atomicAdd(&sh.ncand[0], 1);
+      sh.f.tb_v[0][p] = l;
+      sh.f.tb_x[0][p] = sh.f.cx[s];
+      sh.f.tb_s[0][p] = s;
+    }
+    sh.f.cv[s] = e;
+  }
+  if (TWO) {
+    for (int i = lane; i < cnt[1]; i += kWave) {
+      const int s = w * CAPW + i;
+      const float l = sh.u.dv[s];
+      const int bn = fbin(l, 1);
+      if (bn > bs[1]) {
+        zq += (double)expf(over_T(l - mq, T));
+      } else if (bn == bs[1]) {
+        const int p = atomicAdd(&sh.ncand[1], 1);
+        sh.f.tb_v[1][p] = l;
+        sh.f.tb_x[1][p] = s;
+      }
+    }
+  }
+  __syncthreads();
+  // 6. exact rank inside each threshold bin: the first rem join the kept set
+  //    (and the normaliser), entry rem - 1 is the threshold
+  const int c0 = cb[0], c1 = TWO ? cb[1] : 0;
+  for (int t = tid; t < c0 + c1; t += BLOCK) {
+    const int r = t < c0 ? 0 : 1;
+    const int i = t - (r ? c0 : 0);
+    const int c = r ? c1 : c0;
+    const float vi = sh.f.tb_v[r][i];
+    const int xi = sh.f.tb_x[r][i];
+    int rank = 0, later_tie = 0;
+    for (int j0 = 0; j0 < c; j0 += 8) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float vj = sh.f.tb_v[r][j0 + q];
+        const int xj = sh.f.tb_x[r][j0 + q];
+        rank += (vj > vi) || (vj == vi && xj < xi);
+        later_tie += (vj == vi && xj > xi);
+      }
+    }
+    const bool keep = rank < rem[r];
+    const float e = keep ? expf(over_T(vi - (r ? mq : mp), T)) : -1.0f;
+    if (r == 0) {
+      sh.f.cv[sh.f.tb_s[0][i]] = e;
+      if (keep) zp += (double)e;
+    } else if (keep) {
+      zq += (double)e;
+    }
+    if (rank == rem[r] - 1) {
+      sh.tau_v[r] = vi;
+      sh.tau_x[r] = r == 0 ? xi : 0x7FFFFFFF;
+      // a draft value tied across the threshold needs token indices
+      if (r == 1 && later_tie > 0) sh.fflag = 1;
+    }
+  }
+  block_sum_d2<W>(zp, zq, sh.red_d);  // (its barriers publish tau and fflag)
+  if (sh.fflag) {
+    __syncthreads();
+    return false;
+  }
+  ps.m = mp;
+  ps.T = T;
+  ps.all = false;
+  ps.tau_v = sh.tau_v[0];
+  ps.tau_x = sh.tau_x[0];
+  ps.invZ = 1.0 / zp;
+  if (TWO) {
+    qs.m = mq;
+    qs.T = T;
+    qs.all = false;
+    qs.tau_v = sh.tau_v[1];
+    qs.tau_x = sh.tau_x[1];
+    qs.invZ = 1.0 / zq;
+  }
+  return true;
+}
+
+// Compact list (index order) of the kept target candidates: bitmap of the
+// kept set, per-word prefix popcounts, then each kept token at its rank with
+// its probability and, if want_q, its draft probability (from the draft
+// logits stored beside it, or read from draft_row).
+template <int BLOCK, int NC>
+SJD_DEV void fast_build_list(VSh<BLOCK, NC>& sh, const RowStats& ps, const RowStats& qs, bool want_q, bool two,
+                             const float* draft_row) {
+  using Sh = VSh<BLOCK, NC>;
+  constexpr int W = BLOCK / kWave;
+  constexpr int NW = Sh::NW;
+  constexpr int CAPW = Sh::CAPW;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int cnt = sh.wcnt[0][w];
+  for (int i = tid; i < NW; i += BLOCK) sh.bm[i] = 0;
+  __syncthreads();
+  for (int i = lane; i < cnt; i += kWave) {
+    const int s = w * CAPW + i;
+    if (sh.f.cv[s] >= 0.0f) {
+      const int x = sh.f.cx[s];
+      atomicOr(&sh.bm[x >> 5], 1u << (x & 31));
+    }
+  }
+  __syncthreads();
+  constexpr int WPT = NW / BLOCK > 0 ? NW / BLOCK : 1;
+  int wc[WPT];
+  int s0 = 0;
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int wi = tid * WPT + i;
+    wc[i] = wi < NW ? __popc(sh.bm[wi]) : 0;
+    s0 += wc[i];
+  }
+  int run = block_excl_scan<W>(s0, sh.red_i);
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int wi = tid * WPT + i;
+    if (wi < NW) sh.pre[wi] = run;
+    run += wc[i];
+  }
+  __syncthreads();
+  for (int i = lane; i < cnt; i += kWave) {
+    const int s = w * CAPW + i;
+    const float e = sh.f.cv[s];
+    if (e >= 0.0f) {
+      const int x = sh.f.cx[s];
+      const int r = sh.pre[x >> 5] + __popc(sh.bm[x >> 5] & ((1u << (x & 31)) - 1u));
+      sh.u.sp.x[r] = (uint16_t)x;
+      sh.u.sp.p[r] = (float)((double)e * ps.invZ);
+      if (want_q) {
+        const float l = two ? sh.f.cq[s] : draft_row[x];
+        sh.u.sp.q[r] = qs.in_set(l, x) ? (float)((double)expf(over_T(l - qs.m, qs.T)) * qs.invZ) : 0.0f;
+      }
+    }
+  }
+  __syncthreads();
 }
 
 // Softmax weights over a compact list of logits: w[i] = expf((w[i] - m) / T)
@@ -877,7 +1316,7 @@ SJD_DEV int race_compact(const VSh<BLOCK, NC>& shc, VSh<BLOCK, NC>& sh, int nk, 
       if (ent < nk) {
         const float w = wfn(ent);
         if (w > 0.0f) {
-          const uint64_t pk = pack_key(exp1(compu(wd, e)) / w, (int)shc.sp_x[ent]);
+          const uint64_t pk = pack_key(exp1(compu(wd, e)) / w, (int)shc.u.sp.x[ent]);
           best = pk < best ? pk : best;
         }
       }
@@ -913,8 +1352,8 @@ SJD_DEV void draft_candidates(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int nk, i
       for (int e = 0; e < 4; ++e) {
         const int ent = 4 * jj + e;
         if (ent < nk) {
-          const int x = (int)sh.sp_x[ent];
-          const float pw = sh.sp_p[ent];
+          const int x = (int)sh.u.sp.x[ent];
+          const float pw = sh.u.sp.p[ent];
           if (pw > 0.0f && x != excl) key[4 * q + e] = pack_key(exp1(compu(wd, e)) / pw, x);
         }
       }
@@ -1096,19 +1535,29 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
     }
   }
 
-  // draft logits at the candidates, loaded now so that the accept loop
-  // does not wait for them
-  float qcl[8];
-#pragma unroll
-  for (int t = 0; t < 8; ++t) qcl[t] = t < ncand ? ld.draft[stg.cand[t]] : 0.0f;
+  // the draft and target logits at the first candidate, loaded now so that
+  // the first accept test does not wait for them (later candidates are read
+  // when their stage comes)
+  const float qcl0 = ncand > 0 ? ld.draft[stg.cand[0]] : 0.0f;
+  const float pcl0 = ncand > 0 ? ld.cur[stg.cand[0]] : 0.0f;
 
   RowStats ps{}, qs{};
   int nk = 0;
   bool q_ready = false;  // the draft distribution at the target's kept entries is in sp_q
+  // candidate path: the compact list (and sp_q) is built when a draw needs it
+  bool lazy = false;
+  const bool two = ld.need_q && !ld.q_cached;
   if (ld.need_p) {
     if (!PF) load_row<BLOCK, NC>(v, ld.cur, V);
     if constexpr (PF) {
-      if (ld.need_q && !ld.q_cached) {
+      if (!(a.flags & kFlagFullSelect)) {
+        if (two) lazy = fast_select<BLOCK, NC, true>(v, vq, V, a.top_k, a.T, sh, ps, qs);
+        else lazy = fast_select<BLOCK, NC, false>(v, v, V, a.top_k, a.T, sh, ps, qs);
+      }
+      if (lazy) {
+        nk = (a.top_k <= 0 || a.top_k >= V) ? V : a.top_k;
+        q_ready = two;
+      } else if (two) {
         // target and draft rows together
         float mx2[2], mn2[2];
         row_maxmin2<BLOCK, NC>(v, vq, sh, mx2, mn2);
@@ -1124,20 +1573,20 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
             const int c = tid + i * BLOCK;
             if (c < nchunk) {
               const int sh4 = 4 * (c & 7);
-              const uint32_t wp = sh.bm[c >> 3], wq = sh.bmq[c >> 3];
+              const uint32_t wp = sh.bm[c >> 3], wq = sh.o.bmq[c >> 3];
               const uint32_t np = (wp >> sh4) & 15u, nqb = (wq >> sh4) & 15u;
               if (np | nqb) {
                 int rp = sh.pre[c >> 3] + __popc(wp & ((1u << sh4) - 1u));
-                int rq = sh.preq[c >> 3] + __popc(wq & ((1u << sh4) - 1u));
+                int rq = sh.o.preq[c >> 3] + __popc(wq & ((1u << sh4) - 1u));
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                   if ((np >> e) & 1u) {
-                    sh.sp_x[rp] = (uint16_t)(4 * c + e);
-                    sh.sp_p[rp] = comp(v[i], e);
-                    sh.sp_q[rp] = comp(vq[i], e);
+                    sh.u.sp.x[rp] = (uint16_t)(4 * c + e);
+                    sh.u.sp.p[rp] = comp(v[i], e);
+                    sh.u.sp.q[rp] = comp(vq[i], e);
                     ++rp;
                   }
-                  if ((nqb >> e) & 1u) sh.qc[rq++] = comp(vq[i], e);
+                  if ((nqb >> e) & 1u) sh.o.qc[rq++] = comp(vq[i], e);
                 }
               }
             }
@@ -1147,35 +1596,35 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
           const int nmax = nk > nq ? nk : nq;
           for (int i = tid; i < nmax; i += BLOCK) {
             if (i < nk) {
-              const float e = expf(over_T(sh.sp_p[i] - ps.m, a.T));
-              sh.sp_p[i] = e;
+              const float e = expf(over_T(sh.u.sp.p[i] - ps.m, a.T));
+              sh.u.sp.p[i] = e;
               zp += (double)e;
             }
-            if (i < nq) zq += (double)expf(over_T(sh.qc[i] - qs.m, a.T));
+            if (i < nq) zq += (double)expf(over_T(sh.o.qc[i] - qs.m, a.T));
           }
           block_sum_d2<W>(zp, zq, sh.red_d);
           ps.invZ = 1.0 / zp;
           qs.invZ = 1.0 / zq;
           for (int i = tid; i < nk; i += BLOCK) {
-            sh.sp_p[i] = (float)((double)sh.sp_p[i] * ps.invZ);
-            const int x = (int)sh.sp_x[i];
-            const bool in_q = (sh.bmq[x >> 5] >> (x & 31)) & 1u;
-            sh.sp_q[i] = in_q ? (float)((double)expf(over_T(sh.sp_q[i] - qs.m, a.T)) * qs.invZ) : 0.0f;
+            sh.u.sp.p[i] = (float)((double)sh.u.sp.p[i] * ps.invZ);
+            const int x = (int)sh.u.sp.x[i];
+            const bool in_q = (sh.o.bmq[x >> 5] >> (x & 31)) & 1u;
+            sh.u.sp.q[i] = in_q ? (float)((double)expf(over_T(sh.u.sp.q[i] - qs.m, a.T)) * qs.invZ) : 0.0f;
           }
           q_ready = true;
         }
       }
     }
-    if (!q_ready) {
+    if (!q_ready && !lazy) {
       float mx, mn;
       row_maxmin<BLOCK, NC>(v, sh, mx, mn);
       ps.m = mx;
       ps.T = a.T;
       nk = select_kept<BLOCK, NC>(v, V, a.top_k, mx, mn, sh, sh.bm, sh.pre, ps);
-      compact_row<BLOCK, NC>(v, V, sh.bm, sh.pre, sh.sp_x, sh.sp_p);
+      compact_row<BLOCK, NC>(v, V, sh.bm, sh.pre, sh.u.sp.x, sh.u.sp.p);
       __syncthreads();
-      ps.invZ = softmax_weights<BLOCK, NC>(sh.sp_p, nk, ps.m, a.T, sh);
-      for (int i = tid; i < nk; i += BLOCK) sh.sp_p[i] = (float)((double)sh.sp_p[i] * ps.invZ);
+      ps.invZ = softmax_weights<BLOCK, NC>(sh.u.sp.p, nk, ps.m, a.T, sh);
+      for (int i = tid; i < nk; i += BLOCK) sh.u.sp.p[i] = (float)((double)sh.u.sp.p[i] * ps.invZ);
     }
     if (a.stats_out && tid == 0) {
       RowStatsCache c;
@@ -1200,7 +1649,15 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
     }
     __syncthreads();
   }
-  auto prow = [&](int ent) -> float { return sh.sp_p[ent]; };
+  auto prow = [&](int ent) -> float { return sh.u.sp.p[ent]; };
+  // the compact list for the draws that need it (candidate path: built here,
+  // with the draft probabilities when the row has candidates)
+  auto need_list = [&]() {
+    if (lazy) {
+      fast_build_list<BLOCK, NC>(sh, ps, qs, ncand > 0, two, ld.draft);
+      lazy = false;
+    }
+  };
 
   // ---- sibling rows: bonus draw from the sibling's own output row
   if (!spine) {
@@ -1213,6 +1670,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       tok = -1; stage = -1;
     } else {
       const Stream rs(a.seed, kTagBonus, 0, (uint32_t)j, (uint32_t)b, a.step);
+      need_list();
       tok = race_compact<BLOCK, NC>(sh, sh, nk, rs, prow);
     }
     if (tid == 0) {
@@ -1264,12 +1722,14 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       // and the draft logits at the target's kept entries (gathered)
       const RowStatsCache c = *ld.q_cached;
       qs.m = c.m; qs.T = c.T; qs.tau_v = c.tau_v; qs.tau_x = c.tau_x; qs.all = c.all != 0; qs.invZ = c.invZ;
-      for (int i = tid; i < nk; i += BLOCK) {
-        const int x = (int)sh.sp_x[i];
-        const float l = draft_row[x];
-        sh.sp_q[i] = qs.in_set(l, x) ? (float)((double)expf(over_T(l - qs.m, a.T)) * qs.invZ) : 0.0f;
+      if (!lazy) {
+        for (int i = tid; i < nk; i += BLOCK) {
+          const int x = (int)sh.u.sp.x[i];
+          const float l = draft_row[x];
+          sh.u.sp.q[i] = qs.in_set(l, x) ? (float)((double)expf(over_T(l - qs.m, a.T)) * qs.invZ) : 0.0f;
+        }
+        __syncthreads();
       }
-      __syncthreads();
     } else {
     // draft row: selection, then its logits at the kept entries
     if (!PF) load_row<BLOCK, NC>(vq, draft_row, V);
@@ -1277,7 +1737,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
     row_maxmin<BLOCK, NC>(vq, sh, qmx, qmn);
     qs.m = qmx;
     qs.T = a.T;
-    const int nq = select_kept<BLOCK, NC>(vq, V, a.top_k, qmx, qmn, sh, sh.bmq, sh.preq, qs);
+    const int nq = select_kept<BLOCK, NC>(vq, V, a.top_k, qmx, qmn, sh, sh.o.bmq, sh.o.preq, qs);
     // draft logits at the target's kept entries (by target rank) and at its
     // own kept entries (by draft rank, for its normaliser)
 #pragma unroll
@@ -1285,43 +1745,41 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       const int c = tid + i * BLOCK;
       if (c < nchunk) {
         const int sh4 = 4 * (c & 7);
-        const uint32_t wp = sh.bm[c >> 3], wq = sh.bmq[c >> 3];
+        const uint32_t wp = sh.bm[c >> 3], wq = sh.o.bmq[c >> 3];
         const uint32_t np = (wp >> sh4) & 15u, nqb = (wq >> sh4) & 15u;
         if (np | nqb) {
           int rp = sh.pre[c >> 3] + __popc(wp & ((1u << sh4) - 1u));
-          int rq = sh.preq[c >> 3] + __popc(wq & ((1u << sh4) - 1u));
+          int rq = sh.o.preq[c >> 3] + __popc(wq & ((1u << sh4) - 1u));
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const float l = comp(vq[i], e);
-            if ((np >> e) & 1u) sh.sp_q[rp++] = l;
-            if ((nqb >> e) & 1u) sh.qc[rq++] = l;
+            if ((np >> e) & 1u) sh.u.sp.q[rp++] = l;
+            if ((nqb >> e) & 1u) sh.o.qc[rq++] = l;
           }
         }
       }
     }
     __syncthreads();
-    qs.invZ = softmax_weights<BLOCK, NC>(sh.qc, nq, qs.m, a.T, sh);
+    qs.invZ = softmax_weights<BLOCK, NC>(sh.o.qc, nq, qs.m, a.T, sh);
     for (int i = tid; i < nk; i += BLOCK) {
-      const int x = (int)sh.sp_x[i];
-      const bool in_q = (sh.bmq[x >> 5] >> (x & 31)) & 1u;
-      sh.sp_q[i] = in_q ? (float)((double)expf(over_T(sh.sp_q[i] - qs.m, a.T)) * qs.invZ) : 0.0f;
+      const int x = (int)sh.u.sp.x[i];
+      const bool in_q = (sh.o.bmq[x >> 5] >> (x & 31)) & 1u;
+      sh.u.sp.q[i] = in_q ? (float)((double)expf(over_T(sh.u.sp.q[i] - qs.m, a.T)) * qs.invZ) : 0.0f;
     }
     __syncthreads();
     }
-    auto qrow_c = [&](int ent) -> float { return sh.sp_q[ent]; };
+    auto qrow_c = [&](int ent) -> float { return sh.u.sp.q[ent]; };
 
     float Qsum = 0.0f;
     float Nf = 1.0f;
     for (int k = 1; k <= ncand; ++k) {
       int x = stg.cand[0];
-      float lq = qcl[0];
 #pragma unroll
-      for (int t = 1; t < 8; ++t) {
-        x = (t == k - 1) ? stg.cand[t] : x;
-        lq = (t == k - 1) ? qcl[t] : lq;
-      }
+      for (int t = 1; t < 8; ++t) x = (t == k - 1) ? stg.cand[t] : x;
+      const float lq = k == 1 ? qcl0 : draft_row[x];
+      const float lp = k == 1 ? pcl0 : ld.cur[x];
       const float den = 1.0f - Qsum;
-      const float px = kept(sh, x) ? sh.sp_p[rank_of(sh, x)] : 0.0f;
+      const float px = ps.prob(lp, x);
       const float qx = qs.prob(lq, x);
       const float pk = stg.rho(px, qx, x) / Nf;
       const float qk = den > 0.0f ? qx / den : 0.0f;
@@ -1338,9 +1796,10 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       for (int t = 0; t < 8; ++t)
         if (t == stg.n) { stg.Nf[t] = Nf; stg.den[t] = den; }
       stg.n += 1;
+      need_list();
       double nd = 0.0;
       for (int ent = tid; ent < nk; ent += BLOCK)
-        nd += (double)stg.rho(sh.sp_p[ent], sh.sp_q[ent], (int)sh.sp_x[ent]);
+        nd += (double)stg.rho(sh.u.sp.p[ent], sh.u.sp.q[ent], (int)sh.u.sp.x[ent]);
       nd = block_sum_d<W>(nd, sh.red_d);
       Qsum = Qsum + qx;
       if (!(nd > 0.0)) {
@@ -1354,14 +1813,16 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       // zero-mass exit, in which case that stage was tried too
       const int tried = stg.n + (stg.n < ncand ? 1 : 0);
       const Stream rs(a.seed, kTagRes, (uint32_t)tried, (uint32_t)j, (uint32_t)b, a.step);
+      need_list();
       out_tok = race_compact<BLOCK, NC>(sh, sh, nk, rs, [&](int ent) -> float {
-        return stg.rho(sh.sp_p[ent], qrow_c(ent), (int)sh.sp_x[ent]);
+        return stg.rho(sh.u.sp.p[ent], qrow_c(ent), (int)sh.u.sp.x[ent]);
       });
     }
   } else {
     // no draft distribution (appended placeholder) or no valid candidate:
     // a plain draw from p, counted as a rejection
     const Stream rs(a.seed, kTagRes, 0, (uint32_t)j, (uint32_t)b, a.step);
+    need_list();
     out_tok = race_compact<BLOCK, NC>(sh, sh, nk, rs, prow);
     out_stage = 0;
   }
@@ -1370,6 +1831,7 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   int fresh = out_tok;
   if (!ac) {
     const Stream rs(a.seed, kTagFresh, 0, (uint32_t)j, (uint32_t)b, a.step);
+    need_list();
     fresh = race_compact<BLOCK, NC>(sh, sh, nk, rs, prow);
   }
 
@@ -1378,7 +1840,10 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   // rows the next window drafts at, from the statistics this row leaves
   const bool inl = pd && (a.flags & kFlagPDInline);
   int pds[7];
-  if (inl) draft_candidates<BLOCK, NC>(a, sh, nk, ac ? out_tok : fresh, j, b, Km1, pds);
+  if (inl) {
+    need_list();
+    draft_candidates<BLOCK, NC>(a, sh, nk, ac ? out_tok : fresh, j, b, Km1, pds);
+  }
   if (tid == 0) {
     rec[0] = out_tok;
     rec[1] = out_stage;
@@ -1571,9 +2036,9 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 
   if (tid == BLOCK - 1) sh.ncand[0] = run;
   __syncthreads();
   const int nk = sh.ncand[0];
-  compact_row<BLOCK, NC>(v, a.V, sh.bm, sh.pre, sh.sp_x, sh.sp_p);
+  compact_row<BLOCK, NC>(v, a.V, sh.bm, sh.pre, sh.u.sp.x, sh.u.sp.p);
   __syncthreads();
-  for (int i = tid; i < nk; i += BLOCK) sh.sp_p[i] = (float)((double)expf(over_T(sh.sp_p[i] - st.m, a.T)) * st.invZ);
+  for (int i = tid; i < nk; i += BLOCK) sh.u.sp.p[i] = (float)((double)expf(over_T(sh.u.sp.p[i] - st.m, a.T)) * st.invZ);
   __syncthreads();
   int pds[7];
   draft_candidates<BLOCK, NC>(a, sh, nk, excl, jj, b, Km1, pds);

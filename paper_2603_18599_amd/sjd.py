@@ -17,6 +17,7 @@ SJD_EAGER = 4
 SJD_NO_TUNE = 8
 SJD_TUNE = 16
 SJD_CHECK_FINITE = 32
+SJD_FULL_SELECT = 64
 SJD_VERIFY_NOALLOC_MAX_ROWS = 131072
 
 _STATUS = {0: "SJD_OK", -1: "SJD_EINVAL", -2: "SJD_ENOMEM", -3: "SJD_EHIP", -4: "SJD_ESTATE", -5: "SJD_ENOTSUP",

@@ -13,7 +13,7 @@ pytestmark = pytest.mark.gpu
 
 
 def run_both(orc, inp, *, K, D, top_k, T=1.0, flags=3, seed=1, step=0, vis_lo=0, eol=-1, row_len=0,
-             want_p=True, oracle_trials=None):
+             want_p=True, oracle_trials=None, gpu_flags=0):
     import paper_2603_18599_amd as sjd
     from paper_2603_18599_amd.sjd import verify_outputs
     dev = {k: (v.cuda() if v is not None else None) for k, v in inp.items()}
@@ -22,7 +22,8 @@ def run_both(orc, inp, *, K, D, top_k, T=1.0, flags=3, seed=1, step=0, vis_lo=0,
     rows = torch.zeros(B, L, 2, dtype=torch.int32, device="cuda")
     dbg = torch.zeros(B, L, V, dtype=torch.float32, device="cuda") if want_p else None
     sjd.sjd_verify(dev["cur"], dev["draft"], dev["draft_tok"], dev["meta"], out, K=K, D=D, top_k=top_k,
-                   temperature=T, flags=flags, seed=seed, step=step, sib=dev["sib"], vis_lo=vis_lo, eol_id=eol,
+                   temperature=T, flags=flags | gpu_flags, seed=seed, step=step, sib=dev["sib"], vis_lo=vis_lo,
+                   eol_id=eol,
                    row_len=row_len, out_rows=rows, dbg_p=dbg)
     torch.cuda.synchronize()
     idx = np.arange(B) if oracle_trials is None else np.asarray(oracle_trials)
@@ -82,6 +83,62 @@ def test_verify_temperature_matches_oracle(orc, V, top_k, T):
     inp = verify_inputs(B, L, V, top_k=top_k, seed=V + 17, K=K, D=D, D_in=2, draft_noise=1.0, temperature=T)
     gpu, ref = run_both(orc, inp, K=K, D=D, top_k=top_k, T=T, seed=13, step=2)
     check(gpu, ref, K, D)
+
+
+@pytest.mark.parametrize("V,top_k", [(4096, 200), (16384, 2000), (32768, 2048)])
+def test_verify_full_select_mode_matches_oracle(orc, V, top_k):
+    """SJD_FULL_SELECT, the reference mode of the top-k selection (histograms
+    over every row instead of the candidates at or above a sampled
+    threshold), against the oracle: tree rows, drafting, residual draws."""
+    from paper_2603_18599_amd.sjd import SJD_FULL_SELECT
+    B, L, K, D = 6, 32, 4, 3
+    inp = verify_inputs(B, L, V, top_k=top_k, seed=V + 5, K=K, D=D, D_in=2, draft_noise=1.0)
+    gpu, ref = run_both(orc, inp, K=K, D=D, top_k=top_k, seed=21, step=1, gpu_flags=SJD_FULL_SELECT)
+    check(gpu, ref, K, D)
+
+
+def test_verify_selection_edge_rows(orc):
+    """Rows whose top-k set the sampled threshold estimate handles badly or
+    not at all, against the oracle (whichever selection the kernel takes):
+    -inf entries (a few, or a third of the row); the kept set concentrated in
+    one stripe of the row (every 2048 entries, the first 256 lifted by 4);
+    logits on a coarse grid (long runs of equal values at the threshold, in
+    the target and the draft row); a kept set of half and of nearly all of
+    the row."""
+    B, L, K, D = 8, 32, 4, 3
+    V, top_k = 16384, 2000
+    inp = verify_inputs(B, L, V, top_k=top_k, seed=77, K=K, D=D, D_in=2, draft_noise=1.0)
+    g = torch.Generator().manual_seed(78)
+    cur, dr = inp["cur"], inp["draft"]
+    idx = torch.arange(V)
+    for j in range(0, L, 4):
+        few = torch.randint(0, V, (3,), generator=g)
+        cur[0, j, few] = -float("inf")
+        dr[1, j, few] = -float("inf")
+    third = torch.rand(L, V, generator=g) < 0.33
+    cur[2][third] = -float("inf")
+    dr[2][torch.roll(third, 1, 1)] = -float("inf")
+    stripe = (idx // 256) % 8 == 0
+    cur[3][:, stripe] += 4.0
+    dr[3][:, stripe] += 4.0
+    cur[4] = torch.round(cur[4] * 2) / 2
+    dr[4] = torch.round(dr[4] * 2) / 2
+    cur[5] = torch.round(cur[5] * 8) / 8
+    dr[5] = cur[5] + torch.round(torch.randn(L, V, generator=g) * 4) / 8
+    # drafts must stay inside each draft row's kept set for the comparison to
+    # exercise acceptances: redraw the spine drafts of the edited trials
+    for b in range(6):
+        vals, ix = torch.topk(dr[b], top_k, dim=1)
+        pick = torch.multinomial(torch.softmax(vals.double(), 1), K, replacement=False, generator=g)
+        toks = torch.gather(ix, 1, pick).to(torch.int32)
+        inp["draft_tok"][b] = toks[:, 0]
+        inp["sib"][b, :2] = toks[:2, 1:]
+    gpu, ref = run_both(orc, inp, K=K, D=D, top_k=top_k, seed=5, step=2)
+    check(gpu, ref, K, D)
+    for V2, k2 in [(4096, 2048), (2048, 2000)]:
+        inp2 = verify_inputs(4, L, V2, top_k=k2, seed=V2 + k2, K=K, D=D, D_in=1, draft_noise=1.0)
+        gpu, ref = run_both(orc, inp2, K=K, D=D, top_k=k2, seed=6, step=3)
+        check(gpu, ref, K, D)
 
 
 def test_verify_tree_rows_with_siblings(orc):
