@@ -10,9 +10,10 @@ Prints ONE JSON line. Workloads (synthetic, seeded; see synth_inputs.py):
            row-end tokens after a 64-token random prompt; top-2000, T = 1,
            K = 4, D = 3. value = committed image tokens per second. The same
            line carries the other workloads under "verify", "tiny", "mid" and
-           "8b" (each with its roofline fraction and oracle baseline), and
-           the 7B step with two images per step ("batch2") and with guidance
-           weight 3 ("guided").
+           "8b" (each with its roofline fraction and oracle baseline), the
+           7B step with two and four images per step ("batch2", "batch4"),
+           with guidance weight 3 ("guided") and with two guided images per
+           step ("guided_batch2", four streams in one forward).
   8b, mid, tiny: the other decoder shapes.
   --sweep: ablation modes and the K/D/L grid on a small model (one JSON line
            per configuration).
@@ -54,9 +55,11 @@ def parse():
     ap.add_argument("--L", type=int, default=0, help="window slots (0 = the workload's)")
     ap.add_argument("--K", type=int, default=0, help="drafting candidates per tree row (0 = the workload's)")
     ap.add_argument("--D", type=int, default=-1, help="tree depth (-1 = the workload's)")
-    ap.add_argument("--batch", type=int, default=1, choices=[1, 2],
-                    help="images per step (2: both windows in one forward, one pass over the weights)")
-    ap.add_argument("--no-batch2", action="store_true", help="skip the two-images-per-step section")
+    ap.add_argument("--batch", type=int, default=1, choices=[1, 2, 3, 4],
+                    help="images per step (all windows in one forward, one pass over the weights; "
+                         "at most 2 with --cfg-w)")
+    ap.add_argument("--no-batch2", action="store_true",
+                    help="skip the batched sections (2 and 4 images per step, 2 guided images per step)")
     ap.add_argument("--cfg-w", type=float, default=0.0,
                     help="classifier-free guidance weight (Sec. 5.1 samples with 3): a text-prompt and an "
                          "unconditional stream in one window forward; 0 = unguided")
@@ -452,18 +455,17 @@ def decoder_inputs(cfg, B, context, guided, device="cuda"):
     import torch
 
     from synth_inputs import image_history, prompt_tokens
-    prompts = []
+    prompts, uncond = [], []
     for b in range(B):  # image b: its own prompt (and image so far)
         p = prompt_tokens(cfg, 2 + 10 * b)
         if context == "mid":
             p = torch.cat([p, image_history(cfg, cfg["n_gen"] // 2, 3 + 10 * b)])
         prompts.append(p.to(device))
-    uncond = None
-    if guided:  # the unconditional stream: its own prompt ids, the same image so far
-        u = prompt_tokens(cfg, 77)
-        if context == "mid":
-            u = torch.cat([u, image_history(cfg, cfg["n_gen"] // 2, 3)])
-        uncond = u.to(device)
+        if guided:  # the unconditional stream: its own prompt ids, the same image so far
+            u = prompt_tokens(cfg, 77 + 10 * b)
+            if context == "mid":
+                u = torch.cat([u, image_history(cfg, cfg["n_gen"] // 2, 3 + 10 * b)])
+            uncond.append(u.to(device))
     return prompts, uncond
 
 
@@ -481,8 +483,8 @@ def workload_config(args, workload=None):
         over["K"], over["D"] = 1, 0  # no drafting tree without PD
     over["batch"] = args.batch
     if args.cfg_w != 0.0:
-        if args.batch != 1:
-            raise SystemExit("guidance runs one image per step (--batch 1)")
+        if args.batch > 2:
+            raise SystemExit("guidance runs at most two images per step (four streams)")
         over["cfg_w"] = args.cfg_w
     return model_config(workload or args.workload, **over)
 
@@ -507,11 +509,11 @@ def bench_step(args, cpu=True):
     metas = torch.zeros(W + K, B, 8, dtype=torch.int32, device="cuda")
 
     def prefill_all(sd):
-        if guided:
-            eng.prefill_cfg(prompts[0], uncond, sd, stream=stream)
-            return
         for b in range(B):
-            eng.prefill_image(b, prompts[b], sd + 1000 * b, stream=stream)
+            if guided:
+                eng.prefill_cfg(prompts[b], uncond[b], sd + 1000 * b, stream=stream, image=b)
+            else:
+                eng.prefill_image(b, prompts[b], sd + 1000 * b, stream=stream)
 
     if not args.calibrate_copy:  # (counter runs: one prefill only, each dispatch is slow there)
         prefill_all(seed)
@@ -560,7 +562,7 @@ def bench_step(args, cpu=True):
     step_ms = [a.elapsed_time(b) for a, b in evs]
     avg_ms = float(np.mean(step_ms))
     n_mean = float(np.mean(ns - ncs))
-    total, weights, kv, logit_b, kv_hilo = step_bytes(cfg, n_mean, B, streams=2 if guided else None)
+    total, weights, kv, logit_b, kv_hilo = step_bytes(cfg, n_mean, B, streams=2 * B if guided else None)
     achieved = total / (avg_ms * 1e-3) / 1e9
     moved = total - kv + kv_hilo
     res = dict(metric="image tokens/sec on 1 MI355X; mean accept length/step; verify HBM GB/s",
@@ -572,7 +574,8 @@ def bench_step(args, cpu=True):
                                    f"SwiGLU {cfg['ffn_dim']}, vocab {cfg['vocab_size']} (sampled {cfg['V']}), "
                                    f"L={cfg['L']} K={cfg['K']} D={cfg['D']}, mode {args.mode}, "
                                    + (f"{B} images per step, " if B > 1 else "") +
-                                   (f"CFG weight {args.cfg_w:g} (text + unconditional stream), " if guided else "") +
+                                   (f"CFG weight {args.cfg_w:g} (text + unconditional stream per image), "
+                                    if guided else "") +
                                    f"top-{cfg['top_k']}, T=1, "
                                    f"{cfg['n_prompt']}-token prompt, {cfg['n_gen']}-token image, "
                                    f"steps timed from KV length {prompt.numel() - 1}",
@@ -785,13 +788,19 @@ def main():
                 r = bench_step(argparse.Namespace(**dict(vars(args), workload=wl)))
                 res[wl] = section(r)
         if args.batch == 1 and not args.no_batch2 and not args.calibrate_copy:
-            # the same workload with two images per step (serving several requests)
-            b2 = bench_step(argparse.Namespace(**dict(vars(args), batch=2)), cpu=False)
-            res["batch2"] = section(b2)
+            # the same workload with two and four images per step (serving
+            # several requests per weight pass)
+            for nb in (2, 4):
+                bn = bench_step(argparse.Namespace(**dict(vars(args), batch=nb)), cpu=False)
+                res[f"batch{nb}"] = section(bn)
         if args.batch == 1 and args.cfg_w == 0.0 and not args.no_guided and not args.calibrate_copy:
             # the paper's sampling setting: guidance weight 3 (Sec. 5.1), both streams in one forward
             gd = bench_step(argparse.Namespace(**dict(vars(args), cfg_w=3.0)), cpu=False)
             res["guided"] = section(gd)
+            if not args.no_batch2:
+                # two guided images per step (four streams in one forward)
+                gd2 = bench_step(argparse.Namespace(**dict(vars(args), cfg_w=3.0, batch=2)), cpu=False)
+                res["guided_batch2"] = section(gd2)
     print(json.dumps(res), flush=True)
 
 

@@ -213,16 +213,18 @@ typedef struct {
   int32_t eol_id, row_len;
   int32_t weights_f32;   /* 1: weights are fp32, 0: bf16                                */
   float cfg_w;           /* classifier-free guidance weight w (Sec. 5.1 uses 3); 0 = off.
-                            On: the context keeps a second (unconditional) stream,
-                            prefilled by sjd_prefill_cfg, and every step samples from
-                            l_u + w (l_c - l_u); needs L <= 32 (SJD_ENOTSUP otherwise) */
-  int32_t batch;         /* images generated together, 1 (0 reads as 1) or 2. With 2,
-                            every step runs both images' windows in one forward (one
-                            pass over the weights), each image with its own cache,
-                            state and prompt (sjd_prefill_image), drawing from Philox
-                            trial b; needs L <= 32 and cfg_w = 0 (SJD_ENOTSUP). The
-                            paper decodes one image at a time; batching serves
-                            several requests per weight pass. */
+                            On: every image keeps a second (unconditional) stream,
+                            prefilled by sjd_prefill_cfg / sjd_prefill_image_cfg, and
+                            every step samples from l_u + w (l_c - l_u); needs L <= 32
+                            (SJD_ENOTSUP otherwise) */
+  int32_t batch;         /* images generated together, 1 (0 reads as 1) to 4, or to 2
+                            with guidance (four streams at most; SJD_ENOTSUP beyond).
+                            With more than one, every step runs all images' windows in
+                            one forward (one pass over the weights; stream z in rows
+                            [32 z, 32 z + L)), each image with its own cache, state and
+                            prompt (sjd_prefill_image), drawing from Philox trial b;
+                            needs L <= 32. The paper decodes one image at a time;
+                            batching serves several requests per weight pass. */
 } sjd_config;
 
 /* Device pointers, row-major [out][in] (a Linear layer's layout), bf16 or
@@ -266,11 +268,18 @@ SJD_API int sjd_prefill_image(sjd_ctx* ctx, int32_t image, const int32_t* d_prom
 /* sjd_prefill for a guided context (cfg_w != 0; SJD_EINVAL otherwise, and
  * sjd_prefill is SJD_EINVAL on a guided context): d_prompt[0..n) is the
  * text prompt, d_uncond[0..n_u) the unconditional prompt, prefilled into the
- * second stream's cache. Both streams then receive the same window tokens
- * (the second stream's first pending token is d_uncond[n_u-1]) at their own
- * positions. n, n_u >= 1; n + L <= max_seq and n_u + L <= max_seq. */
+ * image's unconditional stream's cache. Both streams then receive the same
+ * window tokens (the unconditional stream's first pending token is
+ * d_uncond[n_u-1]) at their own positions. n, n_u >= 1; n + L <= max_seq and
+ * n_u + L <= max_seq. sjd_prefill_cfg is sjd_prefill_image_cfg for image 0. */
 SJD_API int sjd_prefill_cfg(sjd_ctx* ctx, const int32_t* d_prompt, int32_t n, const int32_t* d_uncond,
                             int32_t n_u, uint64_t seed, void* stream);
+
+/* sjd_prefill_cfg for image `image` (0 .. batch-1) of a guided batched
+ * context (Sec. 5.1's guided sampling, several images per weight pass); the
+ * other images' generations are left as they are. */
+SJD_API int sjd_prefill_image_cfg(sjd_ctx* ctx, int32_t image, const int32_t* d_prompt, int32_t n,
+                                  const int32_t* d_uncond, int32_t n_u, uint64_t seed, void* stream);
 
 /* One SJD-PAC iteration (Alg. 1): takes the drafts X^{t-1} and their draft
  * distributions P^{t-1}, runs the window forward, verification, drafting and
@@ -324,14 +333,15 @@ SJD_API int sjd_set_drafts(sjd_ctx* ctx, int32_t image, const int32_t* d_draft_t
 
 /* Window forward only (no verification): logits of the current window into
  * d_logits[L][V] (a guided context: the guided logits; a batched context:
- * d_logits[32 + L][V], image b's rows from row 32 b). For parity tests. */
+ * d_logits[32 (batch - 1) + L][V], image b's rows from row 32 b). For parity
+ * tests. */
 SJD_API int sjd_forward_window(sjd_ctx* ctx, float* d_logits, void* stream);
 
 /* The context's GEMM plan, written to splits[0 .. min(n, 20)): for windows
  * of up to 32 rows, [0..5) how many workgroups share the K range of the
  * QKV, O, gate|up, down and LM-head projections and [5..10) how many 32-column
  * blocks each workgroup takes (4 or 8); [10..20) the same for windows of
- * more rows (two streams, L > 32, prefill). Chosen at sjd_init: the closed
+ * more rows (several streams, L > 32, prefill). Chosen at sjd_init: the closed
  * form, the process-wide timed plan (the first context of a process that
  * meets a projection shape and row class times GEMM + consumer pairs;
  * SJD_NO_TUNE skips this), or the environment variable

@@ -51,11 +51,11 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   static_assert(kAttnChunk == 4 * 32, "one 32-key block per wave");
   __shared__ AttnSmem<HD> sm;
   const int h = blockIdx.x, sp = blockIdx.y;
-  // two-stream windows: slot half z is stream z (its own cache and
+  // multi-stream windows: slot block z is stream z (its own cache and
   // positions, L slots each); otherwise the M slots are one stream
   const bool two = a.st.mode != kStreamsOne;
-  const bool second = two && blockIdx.z == 1;
-  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, second);
+  const int z = blockIdx.z;
+  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, z);
   const int Ms = two ? a.st.L : a.M, nk = n + Ms;
   const int kbeg = sp * kAttnChunk;
   if (kbeg >= nk) return;
@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   const int slot = r32;            // local slot (MFMA column)
   const int gslot = zs + slot;
   const bool slot_ok = two ? slot < Ms : gslot < Ms;
-  const size_t so = second ? a.sstride : 0;
+  const size_t so = two ? (size_t)z * a.sstride : 0;
   const uint16_t* kc = a.kc + so;
   const uint16_t* kc_lo = a.kc_lo + so;
   const uint16_t* vt = a.vt + so;
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
     f[w] = mx == -INFINITY ? 0.0f : exp2f(sm.m[w][sl] - mx);
     ls += sm.l[w][sl] * f[w];
   }
-  float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * 64 + zs + sl) * HD + d0;
+  float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * kWinRows + zs + sl) * HD + d0;
 #pragma unroll
   for (int i = 0; i < DPT; i += 4) {
     float4 v;
@@ -235,7 +235,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
     *(float4*)(wo + i) = v;
   }
   if ((threadIdx.x & 7) == 0) {
-    float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 64 * 2 + (size_t)(zs + sl) * 2;
+    float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * kWinRows * 2 + (size_t)(zs + sl) * 2;
     wml[0] = mx;
     wml[1] = ls;
   }
@@ -266,8 +266,8 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
   const int kvh = blockIdx.x, sp = blockIdx.y;
   const int G = a.H / a.Hkv;  // query heads sharing this key/value head
   const bool two = a.st.mode != kStreamsOne;
-  const bool second = two && blockIdx.z == 1;
-  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, second);
+  const int z = blockIdx.z;
+  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, z);
   const int Ms = two ? a.st.L : a.M, nk = n + Ms;
   const int kbeg = sp * kAttnChunk;
   if (kbeg >= nk) return;
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
   const int slot = lane & 31;
   const int gslot = zs + slot;
   const bool slot_ok = two ? slot < Ms : gslot < Ms;
-  const size_t hbase = (size_t)kvh * a.cap * HD + (second ? a.sstride : 0);
+  const size_t hbase = (size_t)kvh * a.cap * HD + (two ? (size_t)z * a.sstride : 0);
   const int kb = kbeg + wave * 32;  // this wave's key block
   const bool has = kb < nk;
 
@@ -431,12 +431,12 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
       for (int r = 0; r < 16; ++r) o[r] += f * t[r];
     }
     // register r of lane (slot, half): dim 32 wave + 8(r/4) + 4 half + r%4
-    float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * 64 + zs + slot) * HD + wave * 32 + 4 * half;
+    float* wo = a.ws_o + (((size_t)h * a.nsplit_max + sp) * kWinRows + zs + slot) * HD + wave * 32 + 4 * half;
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4)
       *(float4*)(wo + 8 * q4) = make_float4(o[4 * q4], o[4 * q4 + 1], o[4 * q4 + 2], o[4 * q4 + 3]);
     if (wave == 0 && half == 0) {
-      float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * 64 * 2 + (size_t)(zs + slot) * 2;
+      float* wml = a.ws_ml + ((size_t)h * a.nsplit_max + sp) * kWinRows * 2 + (size_t)(zs + slot) * 2;
       wml[0] = mx;
       wml[1] = ls;
     }
@@ -456,16 +456,16 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   if (slot >= a.M) return;
   const size_t oo = (size_t)slot * a.ldo + (size_t)h * HD + dim0;
   const bool two = a.st.mode != kStreamsOne;
-  if (two && (slot & 31) >= a.st.L) {  // padding row of a two-stream window: finite zeros
+  if (two && (slot & 31) >= a.st.L) {  // padding row of a multi-stream window: finite zeros
     *(ushort4*)(a.out + oo) = make_ushort4(0, 0, 0, 0);
     *(ushort4*)(a.out_lo + oo) = make_ushort4(0, 0, 0, 0);
     return;
   }
-  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, two && slot >= 32);
+  const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, slot >> 5);
   const int nk = n + (two ? a.st.L : a.M);
   const int ns = (nk + kAttnChunk - 1) / kAttnChunk;
-  const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * 128 + slot * 2;
-  const float* wo = a.ws_o + ((size_t)h * a.nsplit_max * 64 + slot) * HD + dim0;
+  const float* wml = a.ws_ml + (size_t)h * a.nsplit_max * kWinRows * 2 + slot * 2;
+  const float* wo = a.ws_o + ((size_t)h * a.nsplit_max * kWinRows + slot) * HD + dim0;
   float mx = -INFINITY, ls = 0.0f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int s0 = 0; s0 < ns; s0 += kCombGroup) {
@@ -474,8 +474,8 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < kCombGroup; ++i) {
       const int sx = s0 + i < ns ? s0 + i : ns - 1;
-      ml[i] = *(const float2*)(wml + (size_t)sx * 128);
-      v[i] = *(const float4*)(wo + (size_t)sx * 64 * HD);
+      ml[i] = *(const float2*)(wml + (size_t)sx * kWinRows * 2);
+      v[i] = *(const float4*)(wo + (size_t)sx * kWinRows * HD);
     }
     float gm = mx;
 #pragma unroll
@@ -511,8 +511,8 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
 }
 
 hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s) {
-  if (a.M < 1 || a.M > 64) return hipErrorInvalidValue;
-  const unsigned zh = (unsigned)(a.M + 31) / 32;  // 32-slot halves
+  if (a.M < 1 || a.M > (a.st.mode == kStreamsOne ? 64 : 32 * kMaxStreams)) return hipErrorInvalidValue;
+  const unsigned zh = (unsigned)(a.M + 31) / 32;  // 32-slot blocks
   const dim3 g1(a.H, a.nsplit_max, zh), g2(a.H, hd / 32, zh);
   if (hd == 128) {
     // one workgroup per key / value head: its tiles are read once for the

@@ -111,7 +111,7 @@ __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* w
   const int m = blockIdx.y, hh = blockIdx.x, i = threadIdx.x;
   const int half = hd / 2;
   const bool two = sm.mode != kStreamsOne;
-  const bool second = two && m >= 32;
+  const int z = two ? m >> 5 : 0;
   const int loc = two ? (m & 31) : m;
   if (two && loc >= sm.L) {
     if (hh < H) {
@@ -120,13 +120,13 @@ __global__ void k_rope_kv(const float* qkv, int S, size_t plane, const Window* w
     }
     return;
   }
-  const int n = stream_rows(sm, n_dev ? *n_dev : n_host, second);
+  const int n = stream_rows(sm, n_dev ? *n_dev : n_host, z);
   const int row = n + loc;
-  if (second) {
-    o.kc += o.sstride;
-    o.kc_lo += o.sstride;
-    o.vt += o.sstride;
-    o.vt_lo += o.sstride;
+  if (z) {
+    o.kc += z * o.sstride;
+    o.kc_lo += z * o.sstride;
+    o.vt += z * o.sstride;
+    o.vt_lo += z * o.sstride;
   }
   const int ld = (H + 2 * Hkv) * hd;
   const float* src = qkv + (size_t)m * ld + (size_t)hh * hd;

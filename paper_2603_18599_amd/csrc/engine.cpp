@@ -29,7 +29,8 @@ struct Ctx {
   sjd_config c{};
   int cap = 0;      // KV rows
   int cap_pad = 0;  // row stride of the caches (multiple of the attention chunk)
-  int Mpad = 64;  // activation rows (window slots <= 64; prefill windows of 64 tokens)
+  int Mpad = 64;  // activation rows (window rows: one stream of <= 64, or up to four streams of 32)
+  static constexpr int kPrefillRows = 64;  // prefill windows (one stream)
   // library-owned weights: embedding and norm gains as bf16 rows, matrices
   // in the GEMM tile layout; lw[l] = {attn_norm, wqkv, -, -, wo, ffn_norm, wgu, -, wd}
   const uint16_t* embed = nullptr;
@@ -47,15 +48,16 @@ struct Ctx {
   uint16_t *hbuf = nullptr, *hbuf_lo = nullptr;
   uint16_t *kc = nullptr, *kc_lo = nullptr;
   uint16_t *vt = nullptr, *vt_lo = nullptr;
-  // streams: 1, or 2 for a guided context (text prompt + unconditional
-  // stream) or a batch of two images; stream z's caches start z * kv_elems
-  // elements into kc.. (the guided stream's positions are the text stream's
-  // plus delta = n_uncond - n_prompt)
+  // streams: one per image of a batch (up to four), two per image for a
+  // guided context (text prompt + unconditional stream; up to two images);
+  // stream z's caches start z * kv_elems elements into kc.. (an
+  // unconditional stream's positions are its text stream's plus the image's
+  // delta = n_uncond - n_prompt, kept in the image's device state)
   bool guided = false;
   int B = 1;         // images per step
   int nstreams = 1;
   size_t kv_elems = 0;
-  int delta = 0;
+  int delta[sjd::kMaxStreams] = {0, 0, 0, 0};  // per image (host copy, for the cache-fill bound)
   float2* rope = nullptr;
   float* logits[2] = {nullptr, nullptr};
   // target-row statistics of the step that wrote logits[i] ([B][L]); the
@@ -92,9 +94,9 @@ struct Ctx {
   int32_t* h_n_dev = nullptr;  // its device-side address
   hipEvent_t ev[kRing];
   long long ev_step[kRing];
-  long long known_step[2] = {-1, -1};  // step after which known_n holds
-  long long img_step0[2] = {0, 0};     // first step of the image's current generation
-  int known_n[2] = {0, 0};
+  long long known_step[sjd::kMaxStreams] = {-1, -1, -1, -1};  // step after which known_n holds
+  long long img_step0[sjd::kMaxStreams] = {0, 0, 0, 0};      // first step of the image's current generation
+  int known_n[sjd::kMaxStreams] = {0, 0, 0, 0};
   int n_events = 0;
 };
 
@@ -107,9 +109,9 @@ int dalloc(Ctx& x, T** p, size_t count) {
   return SJD_OK;
 }
 
-// rows of a step's logits buffer: the window rows that carry logits (two
-// batched images: rows [0, L) and [32, 32 + L))
-int logit_rows(const Ctx& x) { return x.B == 2 ? 32 + x.c.L : x.c.L; }
+// rows of a step's logits buffer: image b's rows at [32 b, 32 b + L) (a
+// guided head writes each image's guided rows there)
+int logit_rows(const Ctx& x) { return 32 * (x.B - 1) + x.c.L; }
 
 int check_config(const sjd_config* c) {
   if (!c) return SJD_EINVAL;
@@ -127,10 +129,10 @@ int check_config(const sjd_config* c) {
   if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return SJD_EINVAL;
   if (!std::isfinite(c->cfg_w)) return SJD_EINVAL;
   if (c->batch < 0) return SJD_EINVAL;
-  if (c->batch > 2) return SJD_ENOTSUP;
-  const bool two = c->cfg_w != 0.0f || c->batch == 2;
-  if (c->cfg_w != 0.0f && c->batch == 2) return SJD_ENOTSUP;  // four streams
-  if (two && c->L > 32) return SJD_ENOTSUP;                   // two streams of L rows in 64
+  const int B = c->batch > 1 ? c->batch : 1;
+  const int nz = B * (c->cfg_w != 0.0f ? 2 : 1);
+  if (nz > sjd::kMaxStreams) return SJD_ENOTSUP;  // streams of 32 rows in 128
+  if (nz > 1 && c->L > 32) return SJD_ENOTSUP;
   return SJD_OK;
 }
 
@@ -203,7 +205,7 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
     g.A = x.xn; g.A_lo = x.xn_lo; g.lda = x.ld_d; g.M = M; g.W = x.head; g.N = c.V; g.K = d; g.S = 1;
     g.wide = 1;  // measured faster at 32 and 64 rows
     g.out = logits; g.plane = 0; g.ldo = c.V;
-    if (sm.mode == sjd::kStreamsGuided) {  // rows [0, L) of the output: guided logits
+    if (sm.mode == sjd::kStreamsMulti && sm.guided) {  // rows [32 b, 32 b + L): image b's guided logits
       g.cfg_rows = sm.L;
       g.cfg_w = c.cfg_w;
     }
@@ -289,7 +291,7 @@ Ctx::Plan tune_projection(Ctx& x, int proj, const std::vector<Ctx::Plan>& cand, 
   const int Nq = H * hd, Nkv = Hkv * hd, Nqkv = Nq + 2 * Nkv;
   const Ctx::Plan fail{0, 0};
   const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d, guplane = (size_t)x.Mpad * 2 * F;
-  const sjd::Streams one{sjd::kStreamsOne, 0, 0, nullptr};
+  const sjd::Streams one{sjd::kStreamsOne, 0, 0, 0, nullptr};
   auto pair = [&](const Ctx::Plan& pl, int rep) -> hipError_t {
     const auto& w = x.lw[rep % c.n_layers];
     const int S = pl.S;
@@ -366,8 +368,8 @@ Ctx::Plan tune_projection(Ctx& x, int proj, const std::vector<Ctx::Plan>& cand, 
 // Refreshes the cache-fill bound of every image from completed steps;
 // blocks only when the bound says the next window might not fit.
 int cache_check(Ctx& x) {
-  const int ahead = x.delta > 0 ? x.delta : 0;  // the unconditional stream runs ahead by delta
   for (int b = 0; b < x.B; ++b) {
+    const int ahead = x.delta[b] > 0 ? x.delta[b] : 0;  // an unconditional stream runs ahead by delta
     auto refresh = [&](bool wait) -> int {
       for (int i = 0; i < kRing; ++i) {
         if (x.ev_step[i] <= x.known_step[b] || x.ev_step[i] < x.img_step0[b]) continue;
@@ -409,8 +411,9 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   const sjd_config& c = x.c;
   x.guided = c.cfg_w != 0.0f;
   x.use_graph = !(c.flags & SJD_EAGER);
-  x.B = c.batch == 2 ? 2 : 1;
-  x.nstreams = x.guided || x.B == 2 ? 2 : 1;
+  x.B = c.batch > 1 ? c.batch : 1;
+  x.nstreams = x.B * (x.guided ? 2 : 1);
+  x.Mpad = x.nstreams > 2 ? 32 * x.nstreams : 64;
   auto fail = [&](int rc) {
     sjd_destroy(h);
     return rc;
@@ -496,8 +499,8 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       (rc = dalloc(x, &x.logits[0], (size_t)logit_rows(x) * c.V)) ||
       (rc = dalloc(x, &x.logits[1], (size_t)logit_rows(x) * c.V)) ||
       (rc = dalloc(x, &x.stats[0], (size_t)x.B * c.L)) || (rc = dalloc(x, &x.stats[1], (size_t)x.B * c.L)) ||
-      (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * 64 * hd)) ||
-      (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * 128)) || (rc = dalloc(x, &x.st, x.B)) ||
+      (rc = dalloc(x, &x.attn_o, (size_t)H * x.nsplit_max * sjd::kWinRows * hd)) ||
+      (rc = dalloc(x, &x.attn_ml, (size_t)H * x.nsplit_max * sjd::kWinRows * 2)) || (rc = dalloc(x, &x.st, x.B)) ||
       (rc = dalloc(x, &x.win, 1)) || (rc = dalloc(x, &x.rec, (size_t)x.B * c.L * sjd::kRecInts)) ||
       (rc = dalloc(x, &x.nonfinite, 16)))
     return fail(rc);
@@ -517,7 +520,7 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
   // timed only for contexts whose steps run them, else the closed form, which
   // serves their 64-row prefill windows)
   const int kind_N[4] = {Nqkv, d, 2 * F, d}, kind_K[4] = {d, Nq, d, F};
-  const bool step64 = x.nstreams == 2 || c.L > 32;
+  const bool step64 = x.nstreams > 1 || c.L > 32;
   struct Proj { int kind, N, K, cls; Ctx::Plan closed; std::vector<Ctx::Plan> cand; bool tune; };
   std::vector<Proj> projs;
   for (int cls = 0; cls < 2; ++cls)
@@ -656,33 +659,26 @@ namespace {
 // Caches the first n - 1 prompt tokens (windows of Mpad rows) into the caches
 // of stream `cache`.
 int prefill_stream(Ctx& x, const int32_t* d_prompt, int n, int cache, hipStream_t s) {
-  const sjd::Streams one{sjd::kStreamsOne, 0, 0, nullptr};
-  for (int start = 0; start < n - 1; start += x.Mpad) {
-    const int M = (n - 1 - start) < x.Mpad ? (n - 1 - start) : x.Mpad;
+  const sjd::Streams one{sjd::kStreamsOne, 0, 0, 0, nullptr};
+  const int P = Ctx::kPrefillRows;
+  for (int start = 0; start < n - 1; start += P) {
+    const int M = (n - 1 - start) < P ? (n - 1 - start) : P;
     HIPTRY(sjd::launch_build_prefill(d_prompt, start, M, x.win, s));
     TRY(forward(x, M, nullptr, start, nullptr, one, cache, s));
   }
   return SJD_OK;
 }
 
-// image b (its caches: stream b) with prompt d_prompt; a guided context also
-// prefills the unconditional prompt into stream 1
+// image b with prompt d_prompt into its caches (stream b; guided: stream 2b,
+// and the unconditional prompt into stream 2b + 1)
 int prefill(Ctx& x, int b, const int32_t* d_prompt, int n, const int32_t* d_uncond, int n_u, uint64_t seed,
             hipStream_t s) {
   x.prefilled &= ~(1u << b);
-  TRY(prefill_stream(x, d_prompt, n, b, s));
-  if (d_uncond) TRY(prefill_stream(x, d_uncond, n_u, 1, s));
+  TRY(prefill_stream(x, d_prompt, n, x.guided ? 2 * b : b, s));
+  if (d_uncond) TRY(prefill_stream(x, d_uncond, n_u, 2 * b + 1, s));
   HIPTRY(sjd::launch_state_init(x.st + b, d_prompt, n, d_uncond, n_u, x.c.L, x.c.V, x.c.vis_lo, x.c.eol_id,
                                 x.c.row_len, seed, s));
-  if (d_uncond && n_u - n != x.delta) {
-    // the captured forwards carry delta as an argument: capture again
-    for (hipGraphExec_t& e : x.fwd_exec)
-      if (e) {
-        (void)hipGraphExecDestroy(e);
-        e = nullptr;
-      }
-    x.delta = n_u - n;
-  }
+  x.delta[b] = d_uncond ? n_u - n : 0;
   x.prefilled |= 1u << b;
   // the image's cache-fill bound restarts; steps before this one say nothing about it
   x.img_step0[b] = x.steps;
@@ -694,13 +690,12 @@ int prefill(Ctx& x, int b, const int32_t* d_prompt, int n, const int32_t* d_unco
 bool all_prefilled(const Ctx& x) { return x.prefilled == (1u << x.B) - 1u; }
 
 sjd::Streams window_streams(Ctx& x) {
-  if (x.guided) return sjd::Streams{sjd::kStreamsGuided, x.c.L, x.delta, nullptr};
-  if (x.B == 2) return sjd::Streams{sjd::kStreamsBatch, x.c.L, 0, &x.st[1].n};
-  return sjd::Streams{sjd::kStreamsOne, 0, 0, nullptr};
+  if (x.nstreams > 1) return sjd::Streams{sjd::kStreamsMulti, x.c.L, x.nstreams, x.guided ? 1 : 0, x.st};
+  return sjd::Streams{sjd::kStreamsOne, 0, 0, 0, nullptr};
 }
 
-// window rows: one stream of L, or two streams in rows [0, L) and [32, 32 + L)
-int window_rows(const Ctx& x) { return x.nstreams == 2 ? 32 + x.c.L : x.c.L; }
+// window rows: one stream of L, or stream z in rows [32 z, 32 z + L)
+int window_rows(const Ctx& x) { return 32 * (x.nstreams - 1) + x.c.L; }
 
 // A step's window build and forward into logits buffer `buf`: replayed from
 // a graph captured on the first step that uses the buffer (the kernels read
@@ -747,13 +742,18 @@ extern "C" int sjd_prefill_image(sjd_ctx* h, int32_t image, const int32_t* d_pro
   return prefill(x, image, d_prompt, n, nullptr, 0, seed, (hipStream_t)stream);
 }
 
-extern "C" int sjd_prefill_cfg(sjd_ctx* h, const int32_t* d_prompt, int32_t n, const int32_t* d_uncond,
-                               int32_t n_u, uint64_t seed, void* stream) {
+extern "C" int sjd_prefill_image_cfg(sjd_ctx* h, int32_t image, const int32_t* d_prompt, int32_t n,
+                                     const int32_t* d_uncond, int32_t n_u, uint64_t seed, void* stream) {
   if (!h || !d_prompt || n < 1 || !d_uncond || n_u < 1) return SJD_EINVAL;
   Ctx& x = h->x;
-  if (!x.guided) return SJD_EINVAL;
+  if (!x.guided || image < 0 || image >= x.B) return SJD_EINVAL;
   if (n + x.c.L > x.cap || n_u + x.c.L > x.cap) return SJD_ESTATE;
-  return prefill(x, 0, d_prompt, n, d_uncond, n_u, seed, (hipStream_t)stream);
+  return prefill(x, image, d_prompt, n, d_uncond, n_u, seed, (hipStream_t)stream);
+}
+
+extern "C" int sjd_prefill_cfg(sjd_ctx* h, const int32_t* d_prompt, int32_t n, const int32_t* d_uncond,
+                               int32_t n_u, uint64_t seed, void* stream) {
+  return sjd_prefill_image_cfg(h, 0, d_prompt, n, d_uncond, n_u, seed, stream);
 }
 
 namespace sjd {
@@ -821,9 +821,9 @@ extern "C" int sjd_step(sjd_ctx* h, const int32_t* d_draft_tok, const float* d_d
     TRY(check_finite(x, cur, (size_t)logit_rows(x) * c.V, &bad, s));
     if (bad) return SJD_ENONFINITE;
   }
-  // image b: logits rows from 32 b (batch), decoder state x.st[b], Philox trial b
+  // image b: logits rows from 32 b, decoder state x.st[b], Philox trial b
   const int sstate = (int)(sizeof(sjd::DevState) / sizeof(int32_t));
-  const long long lstride = x.B == 2 ? 32LL * c.V : 0;
+  const long long lstride = x.B > 1 ? 32LL * c.V : 0;
   sjd::VerifyArgs a{};
   a.B = x.B; a.L = c.L; a.V = c.V; a.K = c.K; a.D = c.D; a.top_k = top_k; a.T = temperature;
   a.flags = c.flags & (SJD_AC | SJD_PD);
@@ -841,8 +841,8 @@ extern "C" int sjd_step(sjd_ctx* h, const int32_t* d_draft_tok, const float* d_d
   o.out_next = x.st->spine; o.next_stride = sstate; o.out_sib = x.st->sib; o.sib_stride = sstate;
   HIPTRY(sjd::launch_verify(a, o, s));
   const sjd::KvPlanes all{nullptr, nullptr, x.kc, x.kc_lo, x.vt, x.vt_lo, x.kv_elems};
-  HIPTRY(sjd::launch_kv_move(x.st, all, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, x.nstreams,
-                             x.B == 2 ? 1 : 0, x.guided ? x.delta : 0, s));
+  HIPTRY(sjd::launch_kv_move(x.st, all, c.n_layers, c.n_kv_heads, c.head_dim, x.cap_pad, c.K, x.nstreams, x.guided,
+                             s));
   const int slot = (int)(x.steps % kRing);
   HIPTRY(sjd::launch_state_update(x.st, d_out_meta, d_out_tok, d_out_next, c.L, x.B, x.h_n_dev + slot * x.B, s));
   HIPTRY(hipEventRecord(x.ev[slot], s));

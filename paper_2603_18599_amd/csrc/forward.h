@@ -18,9 +18,9 @@ constexpr int kGemmMaxSplits = 32;
 // tiled as row blocks of one [N][K].
 struct GemmArgs {
   const uint16_t* A;     // activations as two bf16 planes (A = hi + lo), 32 rows
-  const uint16_t* A_lo;  // (64 if M > 32; rows >= M finite), row stride lda
+  const uint16_t* A_lo;  // per started 32 (rows >= M finite), row stride lda
   int lda;
-  int M;               // 1..64
+  int M;               // 1..128
   const uint16_t* W;   // tiled weights [N][K]
   int N, K;            // N multiple of 32, K multiple of 64
   int S;               // workgroups along K = fp32 partial planes (1..kGemmMaxSplits)
@@ -32,8 +32,9 @@ struct GemmArgs {
   const float* ss;
   int ss_n;
   float inv_d, eps;
-  // guided head (M > 32 only): rows m < cfg_rows of the output are
-  // u + cfg_w (c - u) with c = product row m, u = product row 32 + m
+  // guided head (M > 32 only): for each image b (product rows [64 b, 64 b +
+  // 64)), output row 32 b + m (m < cfg_rows) is u + cfg_w (c - u) with c =
+  // product row 64 b + m, u = product row 64 b + 32 + m
   int cfg_rows;
   float cfg_w;
   // 8 column blocks per workgroup (else 4): half the activation loads per
@@ -52,10 +53,13 @@ hipError_t launch_tile_weights(const void* src, int is_f32, size_t row0, int N, 
                                int nblk_total, int nb0, hipStream_t s);
 
 // Window description in device memory (written by the window builder).
+// Row a's ancestors: bit i = row base + i of its own stream (base 0 for
+// one stream, 32 z for stream z), a row itself included.
+constexpr int kWinRows = 128;
 struct Window {
-  int32_t tok[64];
-  int32_t pos[64];
-  uint64_t anc[64];
+  int32_t tok[kWinRows];
+  int32_t pos[kWinRows];
+  uint64_t anc[kWinRows];
 };
 
 // Device-resident decoding state of one context.
@@ -68,29 +72,35 @@ struct DevState {
   int32_t meta[8];  // last step's outcome
   int32_t tok[64];  // last step's committed tokens
   int32_t pending_u;  // guided contexts: pending token of the unconditional stream
-  int32_t pad2[3];
+  int32_t delta_u;    // guided contexts: unconditional-stream position minus text-stream position
+  int32_t pad2[2];
 };
 
-// A window forward runs one stream (rows [0, M)) or two: rows [0, L) are
-// stream 0, rows [32, 32 + L) stream 1, the other rows padding (never
-// cached, never read). Each stream has its own key/value cache (stream 1's
-// at the stream-0 cache + sstride) and its own positions:
-//  - guided (classifier-free guidance): stream 1 is the unconditional
-//    stream: same window tokens (its own first pending token), positions
-//    shifted by delta;
-//  - batched: stream 1 is a second image with its own decoder state.
-enum { kStreamsOne = 0, kStreamsGuided = 1, kStreamsBatch = 2 };
+// A window forward runs one stream (rows [0, M)) or nz <= 4 streams of L <=
+// 32 rows each: stream z at rows [32 z, 32 z + L), the other rows padding
+// (never cached, never read). Each stream has its own key/value cache
+// (stream z's at the stream-0 cache + z * sstride) and its own positions:
+//  - batched: stream z is image z, with its own decoder state;
+//  - guided (classifier-free guidance): streams come in pairs per image,
+//    2b the text stream and 2b + 1 the unconditional stream, which is fed
+//    the same window tokens (its own first pending token) at positions
+//    shifted by the image's delta_u.
+enum { kStreamsOne = 0, kStreamsMulti = 1 };
+constexpr int kMaxStreams = 4;
 struct Streams {
-  int mode;           // kStreams*
-  int L;              // window rows per stream (two-stream modes)
-  int delta;          // guided: stream-1 position = stream-0 position + delta
-  const int32_t* n2;  // batched: stream 1's cached rows (device scalar)
+  int mode;            // kStreams*
+  int L;               // window rows per stream (multi)
+  int nz;              // streams (multi)
+  int guided;          // multi: (text, unconditional) stream pairs
+  const DevState* st;  // multi: decoder state of image 0 (image b at st + b)
 };
-
-// cached rows before the window of the stream that row-half `second` is
-__device__ inline int stream_rows(const Streams& sm, int n0, bool second) {
-  if (!second) return n0;
-  return sm.mode == kStreamsBatch ? *sm.n2 : n0 + sm.delta;
+__device__ inline int stream_image(const Streams& sm, int z) { return sm.guided ? z >> 1 : z; }
+__device__ inline bool stream_uncond(const Streams& sm, int z) { return sm.guided && (z & 1); }
+// cached rows before the window of stream z (one stream: n0)
+__device__ inline int stream_rows(const Streams& sm, int n0, int z) {
+  if (sm.mode == kStreamsOne) return n0;
+  const DevState& d = sm.st[stream_image(sm, z)];
+  return d.n + (stream_uncond(sm, z) ? d.delta_u : 0);
 }
 
 // Key / value cache layout. Per layer and kv head, positions are grouped in
@@ -122,15 +132,15 @@ struct AttnArgs {
   const uint16_t* kc_lo;
   const uint16_t* vt;    // [Hkv][cap * hd] value cache of this layer (tiled)
   const uint16_t* vt_lo;
-  size_t sstride;        // two-stream modes: stream 1's caches are these + sstride
+  size_t sstride;        // multi-stream windows: stream z's caches are these + z * sstride
   Streams st;
   const Window* win;
   const int32_t* n_dev;  // cached rows before the window (device scalar), or NULL -> n_host
   int n_host;
   int M, H, Hkv, cap;
   float scale;
-  float* ws_o;           // [H][nsplit_max][64][hd] partial outputs (per query slot)
-  float* ws_ml;          // [H][nsplit_max][64][2]  partial max (log2 domain) and sum
+  float* ws_o;           // [H][nsplit_max][128][hd] partial outputs (per query slot)
+  float* ws_ml;          // [H][nsplit_max][128][2]  partial max (log2 domain) and sum
   int nsplit_max;
   uint16_t* out;         // [Mpad][ldo]
   uint16_t* out_lo;
@@ -153,7 +163,7 @@ hipError_t launch_resid_norm(float* x, const float* part, int S, size_t plane, c
 // rotary embedding of q and k, key row and transposed value column into the caches
 struct KvPlanes {
   uint16_t *q, *q_lo, *kc, *kc_lo, *vt, *vt_lo;
-  size_t sstride;  // two-stream modes: stream 1's caches are kc.. + sstride
+  size_t sstride;  // multi-stream windows: stream z's caches are kc.. + z * sstride
 };
 // qkv: S fp32 partial planes [S][plane] summed in order
 hipError_t launch_rope_kv(const float* qkv, int S, size_t plane, const Window* win, const int32_t* n_dev, int n_host,

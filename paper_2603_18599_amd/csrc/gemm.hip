@@ -1,5 +1,6 @@
 // Skinny bf16 GEMM for the window forward: C[M x N] = A[M x K] . W[N x K]^T
-// with M <= 64 window slots, on gfx950 MFMA (v_mfma_f32_32x32x16_bf16).
+// with M <= 128 window slots (up to four streams of 32), on gfx950 MFMA
+// (v_mfma_f32_32x32x16_bf16).
 //
 // The window forward is bound by streaming the weights from HBM (2 flop per
 // weight byte per slot: 64 flop/B at M = 32, far below the MFMA ridge), so
@@ -27,7 +28,7 @@
 // fp32-class product at no HBM cost (the MFMA units are otherwise idle).
 // Epilogue: optional per-row RMS scale (the normalisation of a preceding
 // RMSNorm, whose gain is already folded into A), then store fp32 to plane sp;
-// for a guided head, the guidance combine of row pairs (m, 32 + m).
+// for a guided head, the guidance combine of row pairs (64b + m, 64b + 32 + m).
 #include "device.h"
 #include "forward.h"
 
@@ -185,13 +186,17 @@ __global__ __launch_bounds__(NW * kWave) void k_gemm(GemmArgs g) {
   // accumulator register r of lane l holds row 8(r/4) + 4(l/32) + r%4 of
   // its row tile, column l%32
   float* out = g.out + (size_t)sp * g.plane + (size_t)nb * 32 + r32;
-  if (MT == 2 && g.cfg_rows > 0) {  // guided head: rows m and 32 + m share lane and register
+  if ((MT & 1) == 0 && g.cfg_rows > 0) {
+    // guided head: image b's text row 64b + m and unconditional row 64b +
+    // 32 + m share lane and register; the guided row goes to row 32b + m
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = 8 * (r / 4) + 4 * half + (r % 4);
-      const float c = acc[0][r] * sm.inv[m], u = acc[MT - 1][r] * sm.inv[32 + m];
-      if (m < g.cfg_rows) out[(size_t)m * g.ldo] = u + g.cfg_w * (c - u);
-    }
+    for (int b = 0; b < MT / 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = 8 * (r / 4) + 4 * half + (r % 4);
+        const float c = acc[2 * b][r] * sm.inv[64 * b + m], u = acc[2 * b + 1][r] * sm.inv[64 * b + 32 + m];
+        if (m < g.cfg_rows) out[(size_t)(32 * b + m) * g.ldo] = u + g.cfg_w * (c - u);
+      }
     return;
   }
 #pragma unroll
@@ -234,21 +239,31 @@ int gemm_splits(int N, int K, int target_wgs, bool wide) {
 }
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
-  if (g.M < 1 || g.M > 64 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
-  if (g.cfg_rows < 0 || g.cfg_rows > 32 || (g.cfg_rows > 0 && g.M < 32 + g.cfg_rows)) return hipErrorInvalidValue;
+  if (g.M < 1 || g.M > 128 || g.N % 32 || g.K % 64 || g.S < 1 || g.S > kGemmMaxSplits) return hipErrorInvalidValue;
+  const int MT = (g.M + 31) / 32;
+  if (g.cfg_rows < 0 || g.cfg_rows > 32 || (g.cfg_rows > 0 && (MT & 1))) return hipErrorInvalidValue;
   const int nw = g.wide ? kGWavesWide : kGWaves;
   const dim3 grid((unsigned)(((g.N / 32 + nw - 1) / nw) * g.S)), block((unsigned)(nw * kWave));
   // at one workgroup per compute unit or fewer nothing else hides a
   // workgroup's load latency: keep more weight tiles in flight
   const bool lone = grid.x <= 256;
   if (g.wide) {
-    if (g.M <= 32) hipLaunchKernelGGL((k_gemm<kRingDepth, 1, kGWavesWide>), grid, block, 0, s, g);
-    else hipLaunchKernelGGL((k_gemm<kRingDepth, 2, kGWavesWide>), grid, block, 0, s, g);
-  } else if (g.M <= 32) {
-    if (lone) hipLaunchKernelGGL((k_gemm<kRingDeep, 1, kGWaves>), grid, block, 0, s, g);
-    else hipLaunchKernelGGL((k_gemm<kRingDepth, 1, kGWaves>), grid, block, 0, s, g);
+    switch (MT) {
+      case 1: hipLaunchKernelGGL((k_gemm<kRingDepth, 1, kGWavesWide>), grid, block, 0, s, g); break;
+      case 2: hipLaunchKernelGGL((k_gemm<kRingDepth, 2, kGWavesWide>), grid, block, 0, s, g); break;
+      case 3: hipLaunchKernelGGL((k_gemm<kRingDepth, 3, kGWavesWide>), grid, block, 0, s, g); break;
+      default: hipLaunchKernelGGL((k_gemm<kRingDepth, 4, kGWavesWide>), grid, block, 0, s, g); break;
+    }
   } else {
-    hipLaunchKernelGGL((k_gemm<kRingDepth, 2, kGWaves>), grid, block, 0, s, g);
+    switch (MT) {
+      case 1:
+        if (lone) hipLaunchKernelGGL((k_gemm<kRingDeep, 1, kGWaves>), grid, block, 0, s, g);
+        else hipLaunchKernelGGL((k_gemm<kRingDepth, 1, kGWaves>), grid, block, 0, s, g);
+        break;
+      case 2: hipLaunchKernelGGL((k_gemm<kRingDepth, 2, kGWaves>), grid, block, 0, s, g); break;
+      case 3: hipLaunchKernelGGL((k_gemm<kRingDepth, 3, kGWaves>), grid, block, 0, s, g); break;
+      default: hipLaunchKernelGGL((k_gemm<kRingDepth, 4, kGWaves>), grid, block, 0, s, g); break;
+    }
   }
   return hipGetLastError();
 }

@@ -19,10 +19,11 @@ hipError_t launch_set_drafts(DevState* st, const int32_t* tok, int L, bool has_q
 hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, const int32_t* uncond, int n_u, int L,
                              int V, int vis_lo, int eol, int row_len, uint64_t seed, hipStream_t s);
 // c.kc / c.vt hold the whole caches ([layers][Hkv][...]); q planes unused.
-// ncache caches (1 or 2): cache z at c + z * c.sstride, driven by state
-// st + z * st_step (0: one shared state), positions shifted by z ? off1 : 0
+// ncache caches: cache z at c + z * c.sstride, driven by image z's state, or
+// (guided) caches 2b, 2b + 1 by image b's, the second at positions shifted by
+// its delta_u
 hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K,
-                          int ncache, int st_step, int off1, hipStream_t s);
+                          int ncache, bool guided, hipStream_t s);
 // B images (states st[0..B), outputs [B][8], [B][L], [B][L]); host_n[B]:
 // pinned host memory that receives each image's cached rows (or NULL)
 hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L, int B,

@@ -17,24 +17,25 @@ namespace sjd {
 
 __global__ void k_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, Streams sm) {
   const int a = threadIdx.x;
-  const bool two = sm.mode != kStreamsOne;
-  const int loc = two ? (a & 31) : a;  // window row within its stream
-  const bool second = two && a >= 32;
-  if (loc >= L) {  // padding row of a two-stream window: never read, never cached
-    if (two && a < 64) {
+  const bool multi = sm.mode != kStreamsOne;
+  const int z = multi ? a >> 5 : 0;      // stream of this row
+  const int loc = multi ? (a & 31) : a;  // window row within its stream
+  if (loc >= L) {  // padding row of a multi-stream window: never read, never cached
+    if (multi) {
       w->tok[a] = vis_lo;
       w->pos[a] = st->n;
       w->anc[a] = 0ull;
     }
     return;
   }
-  // batched: the second stream is the next image, with its own state
-  const DevState* d = second && sm.mode == kStreamsBatch ? st + 1 : st;
+  // batched: stream z is image z; guided: streams 2b, 2b + 1 are image b
+  const DevState* d = multi ? st + stream_image(sm, z) : st;
+  const bool unc = multi && stream_uncond(sm, z);
   const int n = d->n, n_s = d->n_s;
   int tok, pos;
   uint64_t anc;
   if (loc < n_s) {
-    tok = loc == 0 ? (second && sm.mode == kStreamsGuided ? d->pending_u : d->pending) : d->spine[loc - 1];
+    tok = loc == 0 ? (unc ? d->pending_u : d->pending) : d->spine[loc - 1];
     pos = n + loc;
     anc = loc == 63 ? ~0ull : ((1ull << (loc + 1)) - 1ull);
   } else {
@@ -45,7 +46,7 @@ __global__ void k_build_window(const DevState* st, Window* w, int L, int K, int 
     anc = ((1ull << (dd + 1)) - 1ull) | (1ull << loc);
   }
   w->tok[a] = tok;
-  w->pos[a] = second && sm.mode == kStreamsGuided ? pos + sm.delta : pos;
+  w->pos[a] = unc ? pos + d->delta_u : pos;
   w->anc[a] = anc;
 }
 
@@ -67,7 +68,8 @@ __global__ void k_state_init(DevState* st, const int32_t* prompt, int n_p, const
     st->n = n_p - 1;
     st->pending = prompt[n_p - 1];
     st->pending_u = uncond ? uncond[n_u - 1] : prompt[n_p - 1];
-    st->pad2[0] = st->pad2[1] = st->pad2[2] = 0;
+    st->delta_u = uncond ? n_u - n_p : 0;
+    st->pad2[0] = st->pad2[1] = 0;
     st->n_s = L;
     st->D_in = 0;
     st->n_q = 0;
@@ -95,12 +97,14 @@ __global__ void k_state_init(DevState* st, const int32_t* prompt, int n_p, const
 
 // Accepted sibling (meta[5] = k >= 2 at first rejected row r): its key and
 // value move from cache position n + n_s + r(K-1) + k-2 to n + r + 1.
-// grid (layers, Hkv, caches), block hd: cache z is the one at c + z * sstride,
-// driven by state st + z * st_step, its positions shifted by z ? off1 : 0.
-__global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int cap, int K, int st_step, int off1) {
+// grid (layers, Hkv, caches), block hd: cache z is the one at c + z *
+// sstride; without guidance it is image z's, with guidance caches 2b and
+// 2b + 1 are image b's text and unconditional streams (the latter's
+// positions shifted by the image's delta_u).
+__global__ void k_kv_move(const DevState* st, KvPlanes c, int Hkv, int hd, int cap, int K, int guided) {
   const int z = blockIdx.z;
-  st += z * st_step;
-  const int off = z ? off1 : 0;
+  st += guided ? z >> 1 : z;
+  const int off = guided && (z & 1) ? st->delta_u : 0;
   c.kc += z * c.sstride;
   c.kc_lo += z * c.sstride;
   c.vt += z * c.sstride;
@@ -198,7 +202,9 @@ hipError_t launch_set_drafts(DevState* st, const int32_t* tok, int L, bool has_q
 
 hipError_t launch_build_window(const DevState* st, Window* w, int L, int K, int vis_lo, const Streams& sm,
                                hipStream_t s) {
-  hipLaunchKernelGGL(k_build_window, dim3(1), dim3(64), 0, s, st, w, L, K, vis_lo, sm);
+  const bool multi = sm.mode != kStreamsOne;
+  if (multi && (sm.nz < 1 || sm.nz > kMaxStreams || L > 32)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_build_window, dim3(1), dim3(multi ? 32 * sm.nz : 64), 0, s, st, w, L, K, vis_lo, sm);
   return hipGetLastError();
 }
 hipError_t launch_build_prefill(const int32_t* prompt, int start, int M, Window* w, hipStream_t s) {
@@ -212,8 +218,8 @@ hipError_t launch_state_init(DevState* st, const int32_t* prompt, int n_p, const
   return hipGetLastError();
 }
 hipError_t launch_kv_move(const DevState* st, const KvPlanes& c, int layers, int Hkv, int hd, int cap, int K,
-                          int ncache, int st_step, int off1, hipStream_t s) {
-  hipLaunchKernelGGL(k_kv_move, dim3(layers, Hkv, ncache), dim3(hd), 0, s, st, c, Hkv, hd, cap, K, st_step, off1);
+                          int ncache, bool guided, hipStream_t s) {
+  hipLaunchKernelGGL(k_kv_move, dim3(layers, Hkv, ncache), dim3(hd), 0, s, st, c, Hkv, hd, cap, K, guided ? 1 : 0);
   return hipGetLastError();
 }
 hipError_t launch_state_update(DevState* st, int32_t* out_meta, int32_t* out_tok, int32_t* out_next, int L, int B,

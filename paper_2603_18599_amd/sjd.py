@@ -58,8 +58,9 @@ class Weights(C.Structure):
                 ("d_lm_head", C.c_void_p)]
 
 
-EXPORTS = ["sjd_status_str", "sjd_verify", "sjd_verify_noalloc", "sjd_init", "sjd_prefill", "sjd_prefill_image", "sjd_prefill_cfg",
-           "sjd_set_drafts", "sjd_step", "sjd_forward_window", "sjd_get_plan", "sjd_destroy"]
+EXPORTS = ["sjd_status_str", "sjd_verify", "sjd_verify_noalloc", "sjd_init", "sjd_prefill", "sjd_prefill_image",
+           "sjd_prefill_cfg", "sjd_prefill_image_cfg", "sjd_set_drafts", "sjd_step", "sjd_forward_window",
+           "sjd_get_plan", "sjd_destroy"]
 
 _lib = None
 
@@ -98,6 +99,9 @@ def load_library():
     lib.sjd_prefill_cfg.restype = C.c_int
     lib.sjd_prefill_cfg.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_uint64,
                                     C.c_void_p]
+    lib.sjd_prefill_image_cfg.restype = C.c_int
+    lib.sjd_prefill_image_cfg.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32,
+                                          C.c_uint64, C.c_void_p]
     lib.sjd_step.restype = C.c_int
     lib.sjd_step.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_float, C.c_int32,
                              C.c_uint64, C.c_uint32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
@@ -202,10 +206,17 @@ class Engine:
         _check("sjd_prefill_image", load_library().sjd_prefill_image(self.h, image, _ptr(prompt), prompt.numel(), seed,
                                                                       _stream(stream)))
 
-    def prefill_cfg(self, prompt, uncond, seed, stream=None):
-        """Guided contexts (cfg_w != 0): text prompt and unconditional prompt."""
-        _check("sjd_prefill_cfg", load_library().sjd_prefill_cfg(self.h, _ptr(prompt), prompt.numel(), _ptr(uncond),
-                                                                  uncond.numel(), seed, _stream(stream)))
+    def prefill_cfg(self, prompt, uncond, seed, stream=None, image=None):
+        """Guided contexts (cfg_w != 0): text prompt and unconditional prompt
+        (of image `image` of a guided batch; None: sjd_prefill_cfg)."""
+        lib = load_library()
+        if image is None:
+            _check("sjd_prefill_cfg", lib.sjd_prefill_cfg(self.h, _ptr(prompt), prompt.numel(), _ptr(uncond),
+                                                          uncond.numel(), seed, _stream(stream)))
+        else:
+            _check("sjd_prefill_image_cfg", lib.sjd_prefill_image_cfg(self.h, image, _ptr(prompt), prompt.numel(),
+                                                                      _ptr(uncond), uncond.numel(), seed,
+                                                                      _stream(stream)))
 
     def set_drafts(self, draft_tok, draft_logits=None, image=0, stream=None):
         """The next step verifies draft_tok (int32 [L], vocabulary ids) against
