@@ -28,6 +28,7 @@
 // precision); contraction into FMA is off in this file so each operation
 // rounds as IEEE specifies.
 #include <mutex>
+#include <type_traits>
 #include <vector>
 
 #include "device.h"
@@ -182,6 +183,16 @@ SJD_DEV float vmin(float a, float b) { return __builtin_elementwise_minimum(a, b
 // d / T with the division skipped at T = 1, where IEEE division returns d
 // exactly
 SJD_DEV float over_T(float d, float T) { return T == 1.0f ? d : d / T; }
+// The same with T = 1 decided at compile time: in a loop, over_T's division
+// is computed and then discarded by a select; loops run once per case
+// through with_unit_T instead.
+template <bool UT>
+SJD_DEV float div_T(float d, float T) { return UT ? d : d / T; }
+template <class F>
+SJD_DEV void with_unit_T(float T, F&& f) {
+  if (T == 1.0f) f(std::true_type{});
+  else f(std::false_type{});
+}
 
 SJD_DEV float comp(const float4& v, int e) { return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w; }
 SJD_DEV uint32_t compu(const uint4& v, int e) { return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w; }
@@ -1112,36 +1123,39 @@ SJD_DEV bool fast_select(const float4 (&v)[NC], const float4 (&u)[NC], int V, in
   //    entries are collected with their slot
   const float mp = st[0], mq = st[2];
   double zp = 0.0, zq = 0.0;
-  for (int i = lane; i < cnt[0]; i += kWave) {
-    const int s = w * CAPW + i;
-    const float l = sh.f.cv[s];
-    const int bn = fbin(l, 0);
-    float e = -1.0f;
-    if (bn > bs[0]) {
-      e = expf(over_T(l - mp, T));
-      zp += (double)e;
-    } else if (bn == bs[0]) {
-      const int p = atomicAdd(&sh.ncand[0], 1);
-      sh.f.tb_v[0][p] = l;
-      sh.f.tb_x[0][p] = sh.f.cx[s];
-      sh.f.tb_s[0][p] = s;
-    }
-    sh.f.cv[s] = e;
-  }
-  if (TWO) {
-    for (int i = lane; i < cnt[1]; i += kWave) {
+  with_unit_T(T, [&](auto ut) {
+    constexpr bool UT = decltype(ut)::value;
+    for (int i = lane; i < cnt[0]; i += kWave) {
       const int s = w * CAPW + i;
-      const float l = sh.u.dv[s];
-      const int bn = fbin(l, 1);
-      if (bn > bs[1]) {
-        zq += (double)expf(over_T(l - mq, T));
-      } else if (bn == bs[1]) {
-        const int p = atomicAdd(&sh.ncand[1], 1);
-        sh.f.tb_v[1][p] = l;
-        sh.f.tb_x[1][p] = s;
+      const float l = sh.f.cv[s];
+      const int bn = fbin(l, 0);
+      float e = -1.0f;
+      if (bn > bs[0]) {
+        e = expf(div_T<UT>(l - mp, T));
+        zp += (double)e;
+      } else if (bn == bs[0]) {
+        const int p = atomicAdd(&sh.ncand[0], 1);
+        sh.f.tb_v[0][p] = l;
+        sh.f.tb_x[0][p] = sh.f.cx[s];
+        sh.f.tb_s[0][p] = s;
+      }
+      sh.f.cv[s] = e;
+    }
+    if (TWO) {
+      for (int i = lane; i < cnt[1]; i += kWave) {
+        const int s = w * CAPW + i;
+        const float l = sh.u.dv[s];
+        const int bn = fbin(l, 1);
+        if (bn > bs[1]) {
+          zq += (double)expf(div_T<UT>(l - mq, T));
+        } else if (bn == bs[1]) {
+          const int p = atomicAdd(&sh.ncand[1], 1);
+          sh.f.tb_v[1][p] = l;
+          sh.f.tb_x[1][p] = s;
+        }
       }
     }
-  }
+  });
   __syncthreads();
   // 6. exact rank inside each threshold bin: the first rem join the kept set
   //    (and the normaliser), entry rem - 1 is the threshold
@@ -1239,20 +1253,23 @@ SJD_DEV void fast_build_list(VSh<BLOCK, NC>& sh, const RowStats& ps, const RowSt
     run += wc[i];
   }
   __syncthreads();
-  for (int i = lane; i < cnt; i += kWave) {
-    const int s = w * CAPW + i;
-    const float e = sh.f.cv[s];
-    if (e >= 0.0f) {
-      const int x = sh.f.cx[s];
-      const int r = sh.pre[x >> 5] + __popc(sh.bm[x >> 5] & ((1u << (x & 31)) - 1u));
-      sh.u.sp.x[r] = (uint16_t)x;
-      sh.u.sp.p[r] = (float)((double)e * ps.invZ);
-      if (want_q) {
-        const float l = two ? sh.f.cq[s] : draft_row[x];
-        sh.u.sp.q[r] = qs.in_set(l, x) ? (float)((double)expf(over_T(l - qs.m, qs.T)) * qs.invZ) : 0.0f;
+  with_unit_T(qs.T, [&](auto ut) {
+    constexpr bool UT = decltype(ut)::value;
+    for (int i = lane; i < cnt; i += kWave) {
+      const int s = w * CAPW + i;
+      const float e = sh.f.cv[s];
+      if (e >= 0.0f) {
+        const int x = sh.f.cx[s];
+        const int r = sh.pre[x >> 5] + __popc(sh.bm[x >> 5] & ((1u << (x & 31)) - 1u));
+        sh.u.sp.x[r] = (uint16_t)x;
+        sh.u.sp.p[r] = (float)((double)e * ps.invZ);
+        if (want_q) {
+          const float l = two ? sh.f.cq[s] : draft_row[x];
+          sh.u.sp.q[r] = qs.in_set(l, x) ? (float)((double)expf(div_T<UT>(l - qs.m, qs.T)) * qs.invZ) : 0.0f;
+        }
       }
     }
-  }
+  });
   __syncthreads();
 }
 
@@ -1797,11 +1814,15 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
         if (t == stg.n) { stg.Nf[t] = Nf; stg.den[t] = den; }
       stg.n += 1;
       need_list();
+      Qsum = Qsum + qx;
+      // the last candidate's residual needs no normaliser (the draw below
+      // races its unnormalised weights); it has mass iff one weight is
+      // positive, which the draw itself finds out
+      if (k == ncand) break;
       double nd = 0.0;
       for (int ent = tid; ent < nk; ent += BLOCK)
         nd += (double)stg.rho(sh.u.sp.p[ent], sh.u.sp.q[ent], (int)sh.u.sp.x[ent]);
       nd = block_sum_d<W>(nd, sh.red_d);
-      Qsum = Qsum + qx;
       if (!(nd > 0.0)) {
         stg.n -= 1;  // no residual mass: draw from p^(k) itself
         break;
@@ -1814,9 +1835,18 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       const int tried = stg.n + (stg.n < ncand ? 1 : 0);
       const Stream rs(a.seed, kTagRes, (uint32_t)tried, (uint32_t)j, (uint32_t)b, a.step);
       need_list();
-      out_tok = race_compact<BLOCK, NC>(sh, sh, nk, rs, [&](int ent) -> float {
-        return stg.rho(sh.u.sp.p[ent], qrow_c(ent), (int)sh.u.sp.x[ent]);
-      });
+      auto draw = [&]() {
+        return race_compact<BLOCK, NC>(sh, sh, nk, rs, [&](int ent) -> float {
+          return stg.rho(sh.u.sp.p[ent], qrow_c(ent), (int)sh.u.sp.x[ent]);
+        });
+      };
+      out_tok = draw();
+      if (out_tok < 0 && stg.n == ncand) {
+        // the last residual has no mass (a rounding artefact): draw from
+        // p^(ncand) itself, from the same stream
+        stg.n -= 1;
+        out_tok = draw();
+      }
     }
   } else {
     // no draft distribution (appended placeholder) or no valid candidate:
