@@ -80,6 +80,11 @@ struct Ctx {
     int S = 1, wide = 0;
   };
   Plan plan[2][4];
+  // windows of more than 64 rows (three or four streams): the 64-row plan
+  // with each projection's splits cut to fit one workgroup per compute unit
+  // (a 96- or 128-row workgroup holds three or four accumulator tiles and
+  // only one fits a compute unit; a larger grid runs in two rounds)
+  Plan plan_wide[4];
   long long steps = 0;
   unsigned prefilled = 0;  // bit b: image b prefilled
   // the step's window forward (window build + ~10 kernels per layer + head),
@@ -158,7 +163,7 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
   HIPTRY(sjd::launch_embed(x.embed, x.win, M, d, c.vocab_size, c.vis_lo, x.x, s));
   const size_t qplane = (size_t)x.Mpad * Nqkv, rplane = (size_t)x.Mpad * d, guplane = (size_t)x.Mpad * 2 * F;
   int pend = 0;  // partial planes of the last residual projection not yet added into x
-  const Ctx::Plan* P = x.plan[M > 32 ? 1 : 0];
+  const Ctx::Plan* P = M > 64 ? x.plan_wide : x.plan[M > 32 ? 1 : 0];
   sjd::GemmArgs normed{};  // GEMM arguments that apply the RMSNorm row scale
   normed.ss = x.ss;
   normed.ss_n = sjd::norm_chunks(d);
@@ -628,6 +633,13 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       tuned = true;
     }
     x.plan[p.cls][p.kind] = it->second;
+  }
+  for (int k = 0; k < 4; ++k) {
+    Ctx::Plan pw = x.plan[1][k];
+    const int groups = (kind_N[k] / 32 + (pw.wide ? 7 : 3)) / (pw.wide ? 8 : 4);
+    const int smax_one = ncu / groups > 0 ? ncu / groups : 1;
+    if (pw.S > smax_one) pw.S = smax_one;
+    x.plan_wide[k] = pw;
   }
   if (tuned) {
     bool okz = hipMemsetAsync(x.x, 0, (size_t)Mp * d * sizeof(float), s) == hipSuccess;
