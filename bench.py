@@ -64,6 +64,7 @@ def parse():
                     help="classifier-free guidance weight (Sec. 5.1 samples with 3): a text-prompt and an "
                          "unconditional stream in one window forward; 0 = unguided")
     ap.add_argument("--no-guided", action="store_true", help="skip the guided (CFG weight 3) section")
+    ap.add_argument("--top-k", type=int, default=-1, help="sampler top-k (-1 = the workload's; 1 = greedy)")
     ap.add_argument("--eager", action="store_true", help="enqueue every kernel directly (no captured graph)")
     ap.add_argument("--tune", action="store_true",
                     help="time candidate GEMM plans at init (SJD_TUNE) instead of the recorded / closed-form plan")
@@ -481,6 +482,8 @@ def workload_config(args, workload=None):
         over["D"] = args.D
     if args.mode in ("sjd", "ac") and args.K <= 0:
         over["K"], over["D"] = 1, 0  # no drafting tree without PD
+    if getattr(args, "top_k", -1) >= 0:
+        over["top_k"] = args.top_k
     over["batch"] = args.batch
     if args.cfg_w != 0.0:
         if args.batch > 2:
@@ -801,6 +804,7 @@ def main():
                 # two guided images per step (four streams in one forward)
                 gd2 = bench_step(argparse.Namespace(**dict(vars(args), cfg_w=3.0, batch=2)), cpu=False)
                 res["guided_batch2"] = section(gd2)
+
     print(json.dumps(res), flush=True)
 
 
