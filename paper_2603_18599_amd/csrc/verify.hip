@@ -934,7 +934,8 @@ SJD_DEV void wave_find_from_top(const uint32_t* hist, int target, int* bin, int*
 
 template <int BLOCK, int NC, bool TWO>
 SJD_DEV bool fast_select(const float4 (&v)[NC], const float4 (&u)[NC], int V, int top_k, float T,
-                         VSh<BLOCK, NC>& sh, RowStats& ps, RowStats& qs) {
+                         VSh<BLOCK, NC>& sh, RowStats& ps, RowStats& qs, float lp0, float lq0, float& ep0,
+                         float& eq0) {
   using Sh = VSh<BLOCK, NC>;
   constexpr int W = BLOCK / kWave;
   constexpr int CAPW = Sh::CAPW;
@@ -957,6 +958,10 @@ SJD_DEV bool fast_select(const float4 (&v)[NC], const float4 (&u)[NC], int V, in
     }
   }
   block_max4<W>(st, sh.red_f);
+  // the first candidate's weights under both rows' maxima, computed here so
+  // that the accept test after the selection only scales them
+  ep0 = expf(over_T(lp0 - st[0], T));
+  if (TWO) eq0 = expf(over_T(lq0 - st[2], T));
   // samples per row
   int S = 0;
 #pragma unroll
@@ -1557,23 +1562,30 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
   // when their stage comes)
   const float qcl0 = ncand > 0 ? ld.draft[stg.cand[0]] : 0.0f;
   const float pcl0 = ncand > 0 ? ld.cur[stg.cand[0]] : 0.0f;
+  // the first accept draw (uniform over the workgroup), ahead of the selection
+  const float u0 = u01(Stream(a.seed, kTagAcc, 0u, (uint32_t)j, (uint32_t)b, a.step).word(0));
+  // candidate path: the first candidate's weights exp((l - max) / T) under
+  // each row's maximum (computed once the maxima are known)
+  float ep0 = 0.0f, eq0 = 0.0f;
 
   RowStats ps{}, qs{};
   int nk = 0;
   bool q_ready = false;  // the draft distribution at the target's kept entries is in sp_q
   // candidate path: the compact list (and sp_q) is built when a draw needs it
   bool lazy = false;
+  bool fast_first = false;  // ep0 / eq0 hold the first candidate's weights
   const bool two = ld.need_q && !ld.q_cached;
   if (ld.need_p) {
     if (!PF) load_row<BLOCK, NC>(v, ld.cur, V);
     if constexpr (PF) {
       if (!(a.flags & kFlagFullSelect)) {
-        if (two) lazy = fast_select<BLOCK, NC, true>(v, vq, V, a.top_k, a.T, sh, ps, qs);
-        else lazy = fast_select<BLOCK, NC, false>(v, v, V, a.top_k, a.T, sh, ps, qs);
+        if (two) lazy = fast_select<BLOCK, NC, true>(v, vq, V, a.top_k, a.T, sh, ps, qs, pcl0, qcl0, ep0, eq0);
+        else lazy = fast_select<BLOCK, NC, false>(v, v, V, a.top_k, a.T, sh, ps, qs, pcl0, qcl0, ep0, eq0);
       }
       if (lazy) {
         nk = (a.top_k <= 0 || a.top_k >= V) ? V : a.top_k;
         q_ready = two;
+        fast_first = true;
       } else if (two) {
         // target and draft rows together
         float mx2[2], mn2[2];
@@ -1796,12 +1808,16 @@ SJD_DEV void verify_row(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int row, const 
       const float lq = k == 1 ? qcl0 : draft_row[x];
       const float lp = k == 1 ? pcl0 : ld.cur[x];
       const float den = 1.0f - Qsum;
-      const float px = ps.prob(lp, x);
-      const float qx = qs.prob(lq, x);
-      const float pk = stg.rho(px, qx, x) / Nf;
-      const float qk = den > 0.0f ? qx / den : 0.0f;
-      const Stream us(a.seed, kTagAcc, (uint32_t)(k - 1), (uint32_t)j, (uint32_t)b, a.step);
-      const float u = u01(us.word(0));
+      // at stage 1 the normaliser and the remaining draft mass are 1, so
+      // p^(1) and q^(1) are p and q exactly; the weights of the first
+      // candidate are those exp((l - max) / T) the selection computed
+      const bool first_fast = k == 1 && fast_first;
+      const float px = first_fast ? (ps.in_set(lp, x) ? (float)((double)ep0 * ps.invZ) : 0.0f) : ps.prob(lp, x);
+      const float qx = (first_fast && two) ? (qs.in_set(lq, x) ? (float)((double)eq0 * qs.invZ) : 0.0f)
+                                           : qs.prob(lq, x);
+      const float pk = k == 1 ? px : stg.rho(px, qx, x) / Nf;
+      const float qk = k == 1 ? qx : (den > 0.0f ? qx / den : 0.0f);
+      const float u = k == 1 ? u0 : u01(Stream(a.seed, kTagAcc, (uint32_t)(k - 1), (uint32_t)j, (uint32_t)b, a.step).word(0));
       const bool acc = qk > 0.0f ? (u < pk / qk) : (pk > 0.0f);
       if (acc) {
         out_tok = x;
