@@ -138,6 +138,45 @@ def profiler_region(on):
         return
 
 
+_HBM_REF = None
+
+
+def hbm_reference():
+    """This device's measured copy rate, for a fraction beside the one of the
+    published 8 TB/s peak: a 2 GiB device-to-device copy through the HIP
+    runtime, read + write bytes, best of five, measured once per run outside
+    every timed region (a yardstick, not the measured path; a plain
+    streaming-read kernel reaches more, about 6.6-7.0 TB/s on 100-540 MB)."""
+    global _HBM_REF
+    if _HBM_REF is not None:
+        return _HBM_REF
+    import torch
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    a = torch.empty(1 << 29, dtype=torch.float32, device="cuda").fill_(1.0)  # 2 GiB
+    b = torch.empty_like(a)
+    b.copy_(a)
+    t = []
+    for _ in range(5):
+        ev[0].record()
+        b.copy_(a)
+        ev[1].record()
+        torch.cuda.synchronize()
+        t.append(ev[0].elapsed_time(ev[1]))
+    del a, b
+    torch.cuda.empty_cache()
+    _HBM_REF = {"copy_GBps": 2.0 * (1 << 29) * 4 / (min(t) * 1e-3) / 1e9}
+    return _HBM_REF
+
+
+def with_measured(roof):
+    """roofline dict + the achieved rate over this device's measured copy rate"""
+    ref = hbm_reference()
+    roof["measured_copy_GBps"] = ref["copy_GBps"]
+    roof["frac_of_copy"] = roof["achieved"] / ref["copy_GBps"]
+    return roof
+
+
 def calibration_copy():
     import torch
     a = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
@@ -343,6 +382,8 @@ def bench_verify(args, cpu=True):
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic("verify"),
                          "kernel": "k_verify_rows + k_verify_finalize", "bytes_per_launch": bytes_per_launch,
                          "avg_launch_ms": avg_ms})
+    if not getattr(args, "calibrate_copy", False):
+        with_measured(res["roofline"])
     res["expected_accept_length"], res["expected_accept_length_over_drafts"] = chain_expected_nc(
         inp["cur"], inp["draft"], inp["draft_tok"], top_k, c["temperature"])
     if cpu and not args.no_cpu_baseline:
@@ -600,6 +641,8 @@ def bench_step(args, cpu=True):
     eng.close()
     del w
     torch.cuda.empty_cache()
+    if not getattr(args, "calibrate_copy", False):
+        with_measured(res["roofline"])
     if cpu and not args.no_cpu_baseline and B == 1 and not guided:
         res["cpu_baseline"] = cpu_baseline_step(args, cfg, seed, n_mean, prompt)
     return res
