@@ -2,7 +2,8 @@
 oracle's fp64-accumulated forward on the same weights, prompt and window:
 logits within 3e-2 max-abs. Shapes: the tiny and mid models, slices (few
 layers) of the 7B-shaped and 8B GQA large-vocabulary models at their full
-widths, the full 32-layer 7B-shaped model (the benchmark's model), and
+widths (also at the benchmarked cache lengths), the full 32-layer 7B-shaped
+and 8B GQA models (the benchmarked models, after a short prompt), and
 narrow models with 128-dim heads over caches of 700-2100 rows (the
 split-KV attention with many chunks)."""
 import numpy as np
@@ -24,6 +25,12 @@ CASES = [
     ("tiny", {"L": 7, "K": 2, "D": 3, "n_prompt": 1}),
     ("mid", {}),
     ("7b", {"n_prompt": 16}),
+    ("8b", {"n_prompt": 16}),
+    # the benchmarked widths at the benchmarked cache lengths: a 7B slice
+    # after 1239 cached rows (ten 128-key chunks per head) and an 8B GQA
+    # slice after 4158 (33 chunks per key/value head)
+    ("7b", {"n_layers": 2, "n_prompt": 1240}),
+    ("8b", {"n_layers": 1, "n_prompt": 4159}),
     # windows of up to 64 slots: two 32-row GEMM tiles, two attention slot
     # halves; prompts longer than one 64-token prefill window
     ("tiny", {"L": 64, "n_prompt": 100}),
