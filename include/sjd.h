@@ -341,12 +341,17 @@ SJD_API int sjd_forward_window(sjd_ctx* ctx, float* d_logits, void* stream);
  * of up to 32 rows, [0..5) how many workgroups share the K range of the
  * QKV, O, gate|up, down and LM-head projections and [5..10) how many 32-column
  * blocks each workgroup takes (4 or 8); [10..20) the same for windows of
- * more rows (several streams, L > 32, prefill). Chosen at sjd_init: the closed
- * form, the process-wide timed plan (the first context of a process that
- * meets a projection shape and row class times GEMM + consumer pairs;
- * SJD_NO_TUNE skips this), or the environment variable
- * SJD_SPLITS="qkv,o,gu,down" (each entry S or S:blocks) for windows of up
- * to 32 rows when set. */
+ * more rows (several streams, L > 32, prefill). Chosen at sjd_init (see
+ * SJD_TUNE): the plan recorded for the shape, else the closed form; with
+ * SJD_TUNE the process-wide timed plan; and, when the environment variable
+ * SJD_SPLITS="qkv,o,gu,down" is set (each entry S or S:blocks), that plan for
+ * windows of up to 32 rows (a malformed value fails sjd_init with
+ * SJD_EINVAL). The environment variable SJD_QPARTS=p likewise sets how many
+ * attention workgroups share one key / value head's query heads (default:
+ * one per query head; p must divide n_heads / n_kv_heads, else sjd_init
+ * fails with SJD_EINVAL); it leaves every result bitwise unchanged (each
+ * query head's arithmetic is the same in any workgroup), whereas a plan
+ * changes the logits' rounding. */
 SJD_API int sjd_get_plan(const sjd_ctx* ctx, int32_t* splits, int32_t n);
 
 SJD_API void sjd_destroy(sjd_ctx* ctx);

@@ -259,12 +259,19 @@ struct AttnPxSmem {
   float l[4][32];
 };
 
+// MULTI: each workgroup takes several query heads of its key / value head
+// (grouped-query attention), one after another. The query heads of a key /
+// value head are split over PARTS workgroups (blockIdx.x = kv head + Hkv *
+// part); with Hkv a multiple of the XCD count the parts of a head run on one
+// XCD, so only the first reads its key and value tiles from HBM.
+template <bool MULTI>
 __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
   constexpr int HD = 128, NQ = HD / 16;
   static_assert(kAttnChunk == 4 * 32, "one 32-key block per wave");
   __shared__ AttnPxSmem sm;
-  const int kvh = blockIdx.x, sp = blockIdx.y;
-  const int G = a.H / a.Hkv;  // query heads sharing this key/value head
+  const int kvh = (int)blockIdx.x % a.Hkv, part = (int)blockIdx.x / a.Hkv, sp = blockIdx.y;
+  const int G = a.H / a.Hkv / a.qparts;  // query heads of this workgroup
+  const int g0 = part * G;               // the first of them, within the key / value head's group
   const bool two = a.st.mode != kStreamsOne;
   const int z = blockIdx.z;
   const int n = stream_rows(a.st, a.n_dev ? *a.n_dev : a.n_host, z);
@@ -295,8 +302,9 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
       qr[1][i] = slot_ok ? qpl[t] : make_uint4(0, 0, 0, 0);
     }
   };
+  const int hq0 = kvh * (a.H / a.Hkv) + g0;  // this workgroup's first query head
   uint4 qs[2][2];
-  load_q(kvh * G, qs);
+  load_q(hq0, qs);
   uint4 kh[NQ], kl[NQ], vh[4][2], vl[4][2];
   if (has) {
     const uint4* kp = (const uint4*)(a.kc + hbase + (size_t)kb * HD + (size_t)lane * 8);
@@ -332,14 +340,17 @@ __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
   }
 
   for (int g = 0; g < G; ++g) {
-    const int h = kvh * G + g;
-    if (g > 0) load_q(h, qs);
+    const int h = hq0 + g;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       sm.q[0][wave + 4 * i][lane] = qs[0][i];
       sm.q[1][wave + 4 * i][lane] = qs[1][i];
     }
     __syncthreads();  // (also: every wave is done with the previous head's P)
+    // several heads: the next head's q is read while this one computes (the
+    // last re-reads its own: an unconditional load keeps the wait counts
+    // exact)
+    if constexpr (MULTI) load_q(g + 1 < G ? h + 1 : h, qs);
 
     float m_w = -INFINITY, l_w = 0.0f;
     uint4 pb[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)}, pbl[2] = {pb[0], pb[1]};
@@ -517,7 +528,11 @@ hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s) {
   if (hd == 128) {
     // one workgroup per key / value head: its tiles are read once for the
     // whole group of query heads that share them
-    hipLaunchKernelGGL(k_attn_partial_px, dim3(a.Hkv, a.nsplit_max, zh), dim3(256), 0, s, a);
+    const int G = a.H / a.Hkv;
+    if (a.qparts < 1 || G % a.qparts) return hipErrorInvalidValue;
+    const dim3 gp((unsigned)(a.Hkv * a.qparts), a.nsplit_max, zh);
+    if (G / a.qparts > 1) hipLaunchKernelGGL(k_attn_partial_px<true>, gp, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_attn_partial_px<false>, gp, dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_attn_combine<128>, g2, dim3(256), 0, s, a);
   } else if (hd == 64) {
     hipLaunchKernelGGL(k_attn_partial<64>, g1, dim3(256), 0, s, a);

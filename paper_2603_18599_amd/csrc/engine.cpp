@@ -87,6 +87,9 @@ struct Ctx {
   Plan plan_wide[4];
   long long steps = 0;
   unsigned prefilled = 0;  // bit b: image b prefilled
+  // attention workgroups per key / value head (its grouped query heads split
+  // over them)
+  int qparts = 1;
   // the step's window forward (window build + ~10 kernels per layer + head),
   // captured once per logits buffer on cap_stream and replayed on the
   // caller's stream: its kernels and arguments never change for a context
@@ -186,7 +189,7 @@ int forward(Ctx& x, int M, const int32_t* n_dev, int n_host, float* logits, cons
     a.n_dev = n_dev; a.n_host = n_host; a.M = M; a.H = H; a.Hkv = Hkv; a.cap = x.cap_pad;
     a.scale = (float)(1.4426950408889634 / std::sqrt((double)hd));
     a.ws_o = x.attn_o; a.ws_ml = x.attn_ml; a.nsplit_max = x.nsplit_max; a.out = x.att; a.out_lo = x.att_lo;
-    a.ldo = x.ld_q;
+    a.ldo = x.ld_q; a.qparts = x.qparts;
     HIPTRY(sjd::launch_attention(a, hd, s));
     g = sjd::GemmArgs{};
     g.A = x.att; g.A_lo = x.att_lo; g.lda = x.ld_q; g.M = M; g.W = w[4]; g.N = d; g.K = Nq; g.S = P[kProjO].S;
@@ -520,6 +523,22 @@ extern "C" int sjd_init(const sjd_config* cfg, const sjd_weights* w, void* strea
       ncu = prop.multiProcessorCount;
   }
   const int target = 5 * ncu / 2;
+  // grouped-query attention: one attention workgroup per query head by
+  // default (the parts of a key / value head share an XCD and its L2, so the
+  // head's tiles still come from HBM once); SJD_QPARTS=p takes G / p query
+  // heads per workgroup (p must divide G)
+  {
+    const int G = H / Hkv;
+    const char* e = std::getenv("SJD_QPARTS");
+    int qp = G;
+    if (e && *e) {
+      char* end = nullptr;
+      const long v = std::strtol(e, &end, 10);
+      if (*end != '\0' || v < 1 || G % v) return fail(SJD_EINVAL);
+      qp = (int)v;
+    }
+    x.qparts = qp;
+  }
   const int Nqkv = Nq + 2 * Nkv;
   // one plan per projection and row class (windows of <= 32 rows; of more:
   // timed only for contexts whose steps run them, else the closed form, which

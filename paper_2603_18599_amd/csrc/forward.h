@@ -145,6 +145,7 @@ struct AttnArgs {
   uint16_t* out;         // [Mpad][ldo]
   uint16_t* out_lo;
   int ldo;
+  int qparts;            // workgroups per key / value head, each taking H / Hkv / qparts query heads
 };
 constexpr int kAttnChunk = 128;  // keys per workgroup (4 waves x 32)
 hipError_t launch_attention(const AttnArgs& a, int hd, hipStream_t s);

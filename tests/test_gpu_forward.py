@@ -129,3 +129,36 @@ def test_malformed_plan_pins_are_rejected(monkeypatch, plan):
     with pytest.raises(SjdError) as e:
         make_engine(cfg, weights_device(w))
     assert e.value.code == -1
+
+
+def test_window_forward_query_head_split_is_bitwise_neutral(orc, monkeypatch):
+    """Grouped-query attention splits a key / value head's query heads over
+    SJD_QPARTS workgroups (default one per query head): 1, 2 and 4 query
+    heads per workgroup (4 query heads per key / value head, 128-dim heads,
+    a cache of 700 rows: many 128-key chunks) give bitwise identical logits,
+    which match the oracle; a part count that does not divide the group
+    fails sjd_init."""
+    cfg = model_config("tiny", n_layers=2, d_model=512, n_heads=8, n_kv_heads=2, head_dim=128, ffn_dim=1024,
+                       n_prompt=700, weights_f32=False)
+    w, prompt = setup(cfg, wseed=21, pseed=22, device="cuda")
+    outs = {}
+    for qp in ("1", "2", "4", ""):
+        monkeypatch.setenv("SJD_QPARTS", qp)
+        eng = make_engine(cfg, weights_device(w))
+        eng.prefill(prompt.cuda(), 5)
+        logits = torch.empty(cfg["L"], cfg["V"], dtype=torch.float32, device="cuda")
+        eng.forward_window(logits)
+        torch.cuda.synchronize()
+        outs[qp] = logits.cpu().numpy()
+        eng.close()
+    for qp in ("2", "4", ""):
+        assert np.array_equal(outs[qp], outs["1"]), qp
+    ref = oracle_first_window(orc, cfg, weights_numpy(w), prompt.numpy().astype(np.int32), 5)
+    err = np.abs(outs[""] - ref).max()
+    print(f"query-head split: max |logit error| = {err:.3e}", flush=True)
+    assert err <= TOL, err
+    from paper_2603_18599_amd.sjd import SjdError
+    monkeypatch.setenv("SJD_QPARTS", "3")
+    with pytest.raises(SjdError) as e:
+        make_engine(cfg, weights_device(w))
+    assert e.value.code == -1
