@@ -123,6 +123,16 @@ def recorded_traffic(workload):
         return None
 
 
+def default_step_config(args):
+    """True for the step configuration the traffic records measure (one
+    image, no guidance, the workload's window, tree, mode, sampler and
+    cache point; graph replay, recorded plan): a record does not apply to
+    any other."""
+    return (args.batch == 1 and args.cfg_w == 0.0 and args.L == 0 and args.K == 0 and args.D == -1
+            and args.mode == "sjd-pac" and args.top_k == -1 and args.context == "mid" and not args.eager
+            and not args.tune)
+
+
 def profiler_region(on):
     """Resume (on) or pause the profiler's collection (rocprofv3
     --selected-regions); a no-op when the ROCtx library is absent."""
@@ -630,7 +640,8 @@ def bench_step(args, cpu=True):
                prefill_ms=prefill_ms, kv_rows_mean=n_mean, image_restarts=restarts,
                host_enqueue_ms_per_step=host_s * 1e3 / K, split_plan=eng.plan(), split_pin=eng.plan_pin(),
                roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                         "frac": achieved / HBM_PEAK_GBPS, "traffic": recorded_traffic(args.workload),
+                         "frac": achieved / HBM_PEAK_GBPS,
+                         "traffic": recorded_traffic(args.workload) if default_step_config(args) else None,
                          "kernel": "sjd_step (window forward + verification + KV commit)",
                          "bytes_per_launch": total, "weight_bytes": weights, "kv_bytes": kv,
                          "logit_bytes": logit_b, "avg_launch_ms": avg_ms,
