@@ -259,11 +259,13 @@ struct AttnPxSmem {
   float l[4][32];
 };
 
-// MULTI: each workgroup takes several query heads of its key / value head
-// (grouped-query attention), one after another. The query heads of a key /
-// value head are split over PARTS workgroups (blockIdx.x = kv head + Hkv *
-// part); with Hkv a multiple of the XCD count the parts of a head run on one
-// XCD, so only the first reads its key and value tiles from HBM.
+// The query heads of a key / value head (grouped-query attention) are dealt
+// to a.qparts workgroups, blockIdx.x = kv head + Hkv * part. Workgroups go to
+// the XCDs round-robin by launch index, so with Hkv a multiple of the XCD
+// count every part of a head (and every chunk of it) runs on one XCD: the
+// head's key and value tiles come from HBM once and from that XCD's L2 for
+// the other parts. MULTI: a workgroup takes several query heads, one after
+// another, the next head's q read while the current one computes.
 template <bool MULTI>
 __global__ __launch_bounds__(256) void k_attn_partial_px(AttnArgs a) {
   constexpr int HD = 128, NQ = HD / 16;
