@@ -241,8 +241,8 @@ const RecordedPlan kRecordedPlans[] = {
     // {projection (0 QKV, 1 O, 2 gate|up, 3 down), N, K, row class (0: windows
     //  of <= 32 rows, 1: more), splits, 8 column blocks per workgroup}
     // 7B shape (d 4096, 32 x 128 heads, FFN 11008)
-    {0, 12288, 4096, 0, 5, 1}, {1, 4096, 4096, 0, 8, 0}, {2, 22016, 4096, 0, 5, 1}, {3, 4096, 11008, 0, 8, 0},
-    {0, 12288, 4096, 1, 5, 1}, {1, 4096, 4096, 1, 8, 0}, {2, 22016, 4096, 1, 5, 1}, {3, 4096, 11008, 1, 15, 1},
+    {0, 12288, 4096, 0, 5, 1}, {1, 4096, 4096, 0, 8, 0}, {2, 22016, 4096, 0, 2, 1}, {3, 4096, 11008, 0, 8, 0},
+    {0, 12288, 4096, 1, 5, 1}, {1, 4096, 4096, 1, 8, 0}, {2, 22016, 4096, 1, 2, 1}, {3, 4096, 11008, 1, 15, 1},
     // 8B GQA shape (d 4096, 32 / 8 x 128 heads, FFN 14336); its O projection is the 7B one
     {0, 6144, 4096, 0, 5, 0}, {2, 28672, 4096, 0, 2, 1}, {3, 4096, 14336, 0, 8, 0},
     {0, 6144, 4096, 1, 5, 0}, {2, 28672, 4096, 1, 2, 1}, {3, 4096, 14336, 1, 16, 1},
@@ -264,11 +264,13 @@ std::mutex g_plan_mu;
 // (projection, N, K, row class) -> plan
 std::map<std::tuple<int, int, int, int>, Ctx::Plan> g_plan;
 
-// candidate plans: 4 and 8 column blocks per workgroup, three quarters to
+// candidate plans: 4 and 8 column blocks per workgroup, half a workgroup to
 // three workgroups per compute unit (a grid just short of one per unit
 // leaves a few idle but none doubled up: the 7B QKV projection ran fastest
-// at 5 splits of 48 eight-block groups, 240 workgroups), at least two
-// k-steps per workgroup, plus the closed-form choice
+// at 5 splits of 48 eight-block groups, 240 workgroups; fewer splits mean
+// fewer partial planes for the consumer to sum, which can outweigh a
+// slower GEMM), at least two k-steps per workgroup, plus the closed-form
+// choice
 std::vector<Ctx::Plan> plan_candidates(int N, int K, int ncu, Ctx::Plan fallback) {
   const int T = K / 64;
   std::vector<Ctx::Plan> out;
@@ -278,7 +280,7 @@ std::vector<Ctx::Plan> plan_candidates(int N, int K, int ncu, Ctx::Plan fallback
     for (int S = 1; S <= sjd::kGemmMaxSplits; ++S) {
       if (S > 1 && T / S < 2) break;
       const long wg = (long)groups * S;
-      if (4 * wg >= 3L * ncu && wg <= 3L * ncu) out.push_back(Ctx::Plan{S, wide});
+      if (2 * wg >= (long)ncu && wg <= 3L * ncu) out.push_back(Ctx::Plan{S, wide});
     }
   }
   bool has = false;
