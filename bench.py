@@ -844,13 +844,16 @@ def main():
             for wl in ("tiny", "mid", "8b"):
                 r = bench_step(argparse.Namespace(**dict(vars(args), workload=wl)))
                 res[wl] = section(r)
-        if args.batch == 1 and not args.no_batch2 and not args.calibrate_copy:
+        # several streams per forward (images, or guided pairs) take windows
+        # of at most 32 slots; a longer window skips those sections
+        multi = args.L <= 32
+        if args.batch == 1 and not args.no_batch2 and not args.calibrate_copy and multi:
             # the same workload with two and four images per step (serving
             # several requests per weight pass)
             for nb in (2, 4):
                 bn = bench_step(argparse.Namespace(**dict(vars(args), batch=nb)), cpu=False)
                 res[f"batch{nb}"] = section(bn)
-        if args.batch == 1 and args.cfg_w == 0.0 and not args.no_guided and not args.calibrate_copy:
+        if args.batch == 1 and args.cfg_w == 0.0 and not args.no_guided and not args.calibrate_copy and multi:
             # the paper's sampling setting: guidance weight 3 (Sec. 5.1), both streams in one forward
             gd = bench_step(argparse.Namespace(**dict(vars(args), cfg_w=3.0)), cpu=False)
             res["guided"] = section(gd)
