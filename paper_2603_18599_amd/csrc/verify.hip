@@ -1353,8 +1353,8 @@ SJD_DEV int race_compact(const VSh<BLOCK, NC>& shc, VSh<BLOCK, NC>& sh, int nk, 
 // without token excl, in ascending key order (K - 1 draws without
 // replacement), from stream (tag 5, stage 0, row j); out[t] = -1 past the
 // tokens found.
-template <int BLOCK, int NC>
-SJD_DEV void draft_candidates(const VerifyArgs& a, VSh<BLOCK, NC>& sh, int nk, int excl, int j, int b, int Km1,
+template <int BLOCK, int NC, class Sh>
+SJD_DEV void draft_candidates(const VerifyArgs& a, Sh& sh, int nk, int excl, int j, int b, int Km1,
                               int (&out)[7]) {
   constexpr int W = BLOCK / kWave;
   const int tid = threadIdx.x;
@@ -2042,10 +2042,32 @@ __global__ __launch_bounds__(kWave) void k_verify_finalize(VerifyArgs a, Finaliz
 // probabilities and ranks), and the K - 1 candidates are drawn without
 // replacement excluding the token the row carries forward. Only the rows
 // the next window drafts at pay for the draws.
+// Shared memory of the drafting kernel: the kept set, its prefix counts and
+// the compact list (tokens and probabilities) only, about a quarter of the
+// row kernel's, so four workgroups share a compute unit instead of two.
+template <int BLOCK, int NC>
+struct PdSh {
+  static constexpr int W = BLOCK / kWave;
+  static constexpr int NW = BLOCK * NC / 8;  // bitmap words (32 entries each)
+  struct List {
+    uint16_t x[kKcap];
+    float p[kKcap];
+  };
+  uint32_t bm[NW];
+  int32_t pre[NW];
+  union {
+    List sp;
+  } u;
+  uint64_t pd_w[W * 8];
+  int pd_o[8];
+  int red_i[2 * W];
+  int ncand[2];
+};
+
 template <int BLOCK, int NC>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 512 ? 4 : 1))) void k_verify_pd(
     VerifyArgs a, FinalizeOut o) {
-  __shared__ VSh<BLOCK, NC> sh;
+  __shared__ PdSh<BLOCK, NC> sh;
   constexpr int W = BLOCK / kWave;
   const int tid = threadIdx.x;
   const int b = blockIdx.x / a.D, d = blockIdx.x % a.D;
@@ -2062,7 +2084,7 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 
   load_row<BLOCK, NC>(v, row_logits(a, b * L + jj), a.V);
   bitmap_from_tau<BLOCK, NC>(v, a.V, st, sh.bm);
   __syncthreads();
-  constexpr int NW = VSh<BLOCK, NC>::NW;
+  constexpr int NW = PdSh<BLOCK, NC>::NW;
   constexpr int WPT = NW / BLOCK > 0 ? NW / BLOCK : 1;
   int cnt[WPT];
   int s0 = 0;
